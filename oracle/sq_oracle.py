@@ -1,0 +1,309 @@
+"""CPU oracle for the fused low-bit linear of a world-action DiT (SteerQuant /
+Rudder, arXiv 2609.39056).  TEST INFRASTRUCTURE ONLY: the tests, the smoke
+check and the benchmark's CPU-baseline leg may call it; the product path never
+does.
+
+Plain, slow and step-by-step.  Every floating-point step is an IEEE binary32
+operation with round-to-nearest-even, evaluated in exactly the order written
+(numpy float32 arrays: one rounding per operation, no fused multiply-add).  The
+integer GEMM is exact.  Nothing here is shared with the HIP implementation.
+
+What is computed, following the paper:
+
+* Symmetric k-bit quantizer, Sec. 3.1 Eq. (1): Q = clip(round(X / Delta),
+  -q_max, q_max) with Delta = c / q_max and q_max = 2^(k-1) - 1.
+* Channel scaling, Sec. 4.2 Eq. (6): the input is X D^-1 and the weight is
+  Q(D W); one D per layer, shared by all streams and steps.
+* Stream-specific modulation, Sec. 4.3 Eq. (8): gamma^-1 Q(gamma X D^-1; c) W^.
+* Rudder's two kernels, Sec. 4.4: the first applies D^-1 and the stream gain
+  while quantizing and emits integer activations plus row scales
+  r_i = Delta_X / gamma_s(i); the second accumulates Q_X Q_W in INT32 and
+  applies Eq. (10): Y = cast[(FP32(C_ij) r_i) Delta_W,j + b_j].
+* Effective ranges, App. C.1: stream s sees threshold c / gamma_s.
+
+Readings where the paper leaves a choice (each is listed in the design doc):
+
+* Two range modes.  STATIC: c is the per-step table value c_tau (the paper's
+  static activation scale, App. D).  DYNAMIC: c is the absolute maximum of
+  X D^-1 over the row (A8) or over a 64-wide group of the row (A4), taken
+  before the gain, so the gain still moves the effective threshold to c/gamma.
+* Quantizing divides by multiplying with a reciprocal:
+  Delta = c / q_max, inv = 1 / Delta, t = (x~ * g) * inv.  If 1 / Delta is
+  infinite (Delta = 0 or tiny), inv = 0 and the codes are 0.
+* Rounding is round-half-to-even; clamping happens in float before rounding.
+* A4 steps are rounded to fp16 before use (Delta <- fp16(Delta)), so the
+  stored fp16 group scale is exactly the quantization step, and the gain
+  compensation gamma^-1 (kappa) is applied per row in the epilogue.
+* Weights may carry one fp16 scale per output channel (group = K, as in the
+  paper) or per 128-wide group of K.  The epilogue then sums, over K-blocks in
+  ascending order, (FP32(C_block) * s) * Delta_W; with a single block this is
+  Eq. (10) exactly.
+* int4 packing (both weights and A4 activations): for every 8 consecutive
+  codes k = 8g..8g+7 the four bytes 4g..4g+3 hold code 8g+b in the low nibble
+  and code 8g+b+4 in the high nibble of byte 4g+b.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+RANGE_DYNAMIC = 0
+RANGE_STATIC = 1
+A4_GROUP = 64
+Q_MAX = {8: 127, 4: 7}
+W_QMAX = 7
+
+F32 = np.float32
+
+
+# --------------------------------------------------------------------------
+# Number formats
+# --------------------------------------------------------------------------
+def bf16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    """Exact widening of bf16 bit patterns to fp32."""
+    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(F32)
+
+
+def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 with round-to-nearest-even (finite inputs)."""
+    u = np.ascontiguousarray(x, dtype=F32).view(np.uint32).astype(np.uint64)
+    lsb = (u >> np.uint64(16)) & np.uint64(1)
+    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
+    return (r & np.uint64(0xFFFF)).astype(np.uint16)
+
+
+def f16_bits_to_f32(bits: np.ndarray) -> np.ndarray:
+    return np.asarray(bits, dtype=np.uint16).view(np.float16).astype(F32)
+
+
+def f32_to_f16_bits(x: np.ndarray) -> np.ndarray:
+    """fp32 -> fp16 with round-to-nearest-even (numpy's IEEE conversion)."""
+    with np.errstate(over="ignore"):
+        return np.asarray(x, dtype=F32).astype(np.float16).view(np.uint16)
+
+
+def pack_int4(codes: np.ndarray) -> np.ndarray:
+    """Pack int codes in [-8, 7], shape [R, K] (K % 8 == 0), to bytes [R, K/2].
+
+    Byte 4g+b holds code 8g+b (low nibble) and code 8g+b+4 (high nibble)."""
+    c = np.asarray(codes).astype(np.int64)
+    R, K = c.shape
+    assert K % 8 == 0
+    nib = (c & 0xF).astype(np.uint8).reshape(R, K // 8, 2, 4)
+    lo, hi = nib[:, :, 0, :], nib[:, :, 1, :]
+    return (lo | (hi << np.uint8(4))).reshape(R, K // 2)
+
+
+def unpack_int4(packed: np.ndarray) -> np.ndarray:
+    """Inverse of pack_int4: bytes [R, K/2] -> int8 codes [R, K] (two's
+    complement nibbles, -8..7)."""
+    p = np.asarray(packed, dtype=np.uint8)
+    R, H = p.shape
+    g = p.reshape(R, H // 4, 4)
+    lo = (g & np.uint8(0xF)).astype(np.int16)
+    hi = (g >> np.uint8(4)).astype(np.int16)
+    both = np.stack([lo, hi], axis=2)                    # [R, H/4, 2, 4]
+    signed = np.where(both >= 8, both - 16, both)
+    return signed.reshape(R, H * 2).astype(np.int8)
+
+
+# --------------------------------------------------------------------------
+# First kernel: channel scaling, stream gain, quantization (Sec. 4.4, first
+# kernel; Eq. (1) applied to gamma X D^-1 as in Eq. (8))
+# --------------------------------------------------------------------------
+def _reciprocal_or_zero(delta: np.ndarray) -> np.ndarray:
+    with np.errstate(divide="ignore", over="ignore"):
+        inv = F32(1.0) / delta
+    return np.where(np.isinf(inv), F32(0.0), inv).astype(F32)
+
+
+def quantize_act(x_bits, tok2stream, gamma, step, dinv=None, clip=None,
+                 range_mode=RANGE_DYNAMIC, act_bits=8):
+    """Quantize bf16 activations [M, K] for one layer at denoising step `step`.
+
+    Returns a dict with
+      codes  int8 [M, K]          the integer activations Q_X
+      qx     A8: int8 [M, K]; A4: uint8 [M, K/2] packed (the stored form)
+      scale  A8: fp32 r [M]  (r_i = Delta_i / gamma_s(i), Sec. 4.4)
+             A4: fp16 bit patterns sigma [M, K/64] (the fp16 step per group)
+      kappa  fp32 [M], 1 / gamma_s(i) (the output compensation of Eq. (8))
+      delta  fp32 [M, groups] the quantization step per row / group
+      xt     fp32 [M, K] the channel-scaled activation X D^-1
+      g      fp32 [M] the row's gain
+    """
+    x_bits = np.asarray(x_bits, dtype=np.uint16)
+    M, K = x_bits.shape
+    qa = Q_MAX[act_bits]
+    gamma = np.asarray(gamma, dtype=F32)
+    S = gamma.shape[1]
+    t2s = np.asarray(tok2stream, dtype=np.int64)
+    assert t2s.shape == (M,)
+    assert np.all((t2s >= 0) & (t2s < S)), "stream id out of range"
+    assert 0 <= step < gamma.shape[0]
+
+    # Row gain gamma_{tau, s(i)} (Sec. 4.3; the token-wise diagonal of Fig. 2).
+    g = gamma[step, t2s].astype(F32)
+
+    # Channel scaling X D^-1 (Eq. 6), one fp32 multiply per element.
+    x = bf16_bits_to_f32(x_bits)
+    xt = x if dinv is None else (x * np.asarray(dinv, dtype=F32)[None, :]).astype(F32)
+
+    group = K if act_bits == 8 else A4_GROUP
+    assert K % group == 0
+    ng = K // group
+    xg = xt.reshape(M, ng, group)
+
+    # Reference range c: the per-step table value, or the group's amax of
+    # X D^-1 before the gain.
+    if range_mode == RANGE_STATIC:
+        assert clip is not None
+        c = np.full((M, ng), np.asarray(clip, dtype=F32)[step], dtype=F32)
+    else:
+        c = np.max(np.abs(xg), axis=2).astype(F32)
+
+    # Step Delta = c / q_max (Eq. 1).  A4 steps are fp16 values.
+    delta = (c / F32(qa)).astype(F32)
+    if act_bits == 4:
+        delta = f16_bits_to_f32(f32_to_f16_bits(delta))
+    inv = _reciprocal_or_zero(delta)
+
+    # t = (x~ * gamma) * (1 / Delta); clamp to [-q_max, q_max]; round to even.
+    t = ((xg * g[:, None, None]).astype(F32) * inv[:, :, None]).astype(F32)
+    t = np.minimum(np.maximum(t, F32(-qa)), F32(qa))
+    codes = np.rint(t).astype(np.int8).reshape(M, K)
+
+    kappa = (F32(1.0) / g).astype(F32)
+    if act_bits == 8:
+        r = (delta[:, 0] / g).astype(F32)          # r_i = Delta_X / gamma_s(i)
+        return dict(codes=codes, qx=codes.copy(), scale=r, kappa=kappa,
+                    delta=delta, xt=xt, g=g)
+    sigma = f32_to_f16_bits(delta)
+    return dict(codes=codes, qx=pack_int4(codes), scale=sigma, kappa=kappa,
+                delta=delta, xt=xt, g=g)
+
+
+# --------------------------------------------------------------------------
+# Offline weight preparation: fold D, quantize per group to int4, pack
+# (Sec. 4.2, "we fold D* into the weights ... stored as packed integers")
+# --------------------------------------------------------------------------
+def pack_weights(w, d=None, w_group=128):
+    """w: fp32 [N, K] (W^T), d: fp32 [K] or None.
+
+    Returns codes int8 [N, K] in [-7, 7], qw uint8 [N, K/2] (packed), and
+    w_scale fp16 bit patterns [N, K / w_group]."""
+    w = np.asarray(w, dtype=F32)
+    N, K = w.shape
+    assert K % w_group == 0
+    wf = w if d is None else (w * np.asarray(d, dtype=F32)[None, :]).astype(F32)
+    nb = K // w_group
+    wg = wf.reshape(N, nb, w_group)
+    amax = np.max(np.abs(wg), axis=2).astype(F32)
+    scale_bits = f32_to_f16_bits((amax / F32(W_QMAX)).astype(F32))
+    inv = _reciprocal_or_zero(f16_bits_to_f32(scale_bits))
+    t = (wg * inv[:, :, None]).astype(F32)
+    t = np.minimum(np.maximum(t, F32(-W_QMAX)), F32(W_QMAX))
+    codes = np.rint(t).astype(np.int8).reshape(N, K)
+    return dict(codes=codes, qw=pack_int4(codes), w_scale=scale_bits)
+
+
+# --------------------------------------------------------------------------
+# Second kernel: INT32 accumulation and the dequantization epilogue
+# (Sec. 4.4, Eq. (10), generalized to K-blocks)
+# --------------------------------------------------------------------------
+def block_size(act_bits: int, K: int, w_group: int) -> int:
+    """K-block over which one int32 accumulator runs: the smaller of the
+    activation group (K for A8, 64 for A4) and the weight group."""
+    return min(K if act_bits == 8 else A4_GROUP, w_group)
+
+
+def block_acc(codes_x, codes_w, G):
+    """C^beta_ij = sum_{k in block beta} q_ik w_jk, exactly.
+
+    codes_x int [M, K], codes_w int [N, K] -> int64 [K/G, M, N].  The float64
+    matmul is exact: every partial sum is an integer below 2^53."""
+    qx = np.asarray(codes_x, dtype=np.float64)
+    qw = np.asarray(codes_w, dtype=np.float64)
+    M, K = qx.shape
+    assert K % G == 0
+    out = np.empty((K // G, M, qw.shape[0]), dtype=np.int64)
+    for b in range(K // G):
+        sl = slice(b * G, (b + 1) * G)
+        blk = qx[:, sl] @ qw[:, sl].T
+        out[b] = blk.astype(np.int64)
+    assert np.abs(out).max(initial=0) < 2**31, "int32 accumulator overflow"
+    return out
+
+
+def epilogue(C, act_bits, scale, kappa, w_scale_bits, w_group, bias_bits=None):
+    """Dequantize block accumulators C [nb, M, N] (int64) into fp32 y.
+
+    A8: y = sum_beta (f32(C^beta) * r_i) * Delta_W[j, beta]        (+ b_j)
+    A4: y = (sum_beta (f32(C^beta) * sigma_i,beta) * Delta_W[j, b(beta)]) * kappa_i  (+ b_j)
+
+    Also returns y64 (the same sum in fp64) and A (sum of the magnitudes of
+    the terms, the scale of the rounding error)."""
+    nb, M, N = C.shape
+    K = None
+    ws = f16_bits_to_f32(w_scale_bits)                       # [N, K/w_group]
+    n_wg = ws.shape[1]
+    K = n_wg * w_group
+    G = K // nb
+    y = np.zeros((M, N), dtype=F32)
+    y64 = np.zeros((M, N), dtype=np.float64)
+    A = np.zeros((M, N), dtype=np.float64)
+    if act_bits == 8:
+        s_all = np.asarray(scale, dtype=F32)[:, None]         # r_i, [M, 1]
+    else:
+        sig = f16_bits_to_f32(scale)                          # [M, K/64]
+    for b in range(nb):
+        wb = (b * G) // w_group
+        dw = ws[:, wb][None, :]                               # [1, N]
+        s = s_all if act_bits == 8 else sig[:, b][:, None]
+        term = ((C[b].astype(F32) * s).astype(F32) * dw).astype(F32)
+        y = (y + term).astype(F32)
+        t64 = C[b].astype(np.float64) * s.astype(np.float64) * dw.astype(np.float64)
+        y64 += t64
+        A += np.abs(t64)
+    if act_bits == 4:
+        k = np.asarray(kappa, dtype=F32)[:, None]
+        y = (y * k).astype(F32)
+        y64 *= k.astype(np.float64)
+        A *= k.astype(np.float64)
+    if bias_bits is not None:
+        b32 = bf16_bits_to_f32(bias_bits)[None, :]
+        y = (y + b32).astype(F32)
+        y64 += b32.astype(np.float64)
+        A += np.abs(b32.astype(np.float64))
+    return y, y64, A
+
+
+def cast_output(y, out_dtype):
+    """'f32' -> fp32 values; 'bf16' / 'f16' -> bit patterns (uint16)."""
+    if out_dtype == "f32":
+        return np.asarray(y, dtype=F32)
+    if out_dtype == "bf16":
+        return f32_to_bf16_bits(y)
+    if out_dtype == "f16":
+        return f32_to_f16_bits(y)
+    raise ValueError(out_dtype)
+
+
+def linear(x_bits, tok2stream, gamma, step, qw_codes, w_scale_bits, w_group,
+           dinv=None, clip=None, bias_bits=None, range_mode=RANGE_DYNAMIC, act_bits=8):
+    """The whole fused linear: quantize (first kernel), block accumulate and
+    epilogue (second kernel).  Returns the quantize dict plus C, y, y64, A."""
+    qa = quantize_act(x_bits, tok2stream, gamma, step, dinv=dinv, clip=clip,
+                      range_mode=range_mode, act_bits=act_bits)
+    K = qa["codes"].shape[1]
+    G = block_size(act_bits, K, w_group)
+    C = block_acc(qa["codes"], qw_codes, G)
+    y, y64, A = epilogue(C, act_bits, qa["scale"], qa["kappa"], w_scale_bits, w_group, bias_bits)
+    qa.update(C=C, y=y, y64=y64, A=A, G=G)
+    return qa
+
+
+def full_precision_linear(x_bits, w, bias_bits=None):
+    """Y = X W (+ b) in fp64 with unquantized operands (the target of Eq. 2)."""
+    y = bf16_bits_to_f32(x_bits).astype(np.float64) @ np.asarray(w, np.float64).T
+    if bias_bits is not None:
+        y = y + bf16_bits_to_f32(bias_bits).astype(np.float64)[None, :]
+    return y
