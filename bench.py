@@ -1,0 +1,245 @@
+"""Benchmark of the fused W4A8 linear on one MI355X.
+
+Workload: the 2B-class world-action DiT MLP pair at W4A8, hidden 2048 -> 8192
+-> 2048, 4096 video + 32 proprio + 64 action tokens (M = 4192), per-step
+per-stream gain tables for 10 denoising steps, int4 weights with fp16 steps
+per 128-wide group.  One step = one pass of the hot path over the batch: for
+the up and the down projection, the first kernel (channel scaling, stream
+gain, per-token int8 quantization) and the second (int8-MFMA GEMM against the
+int4 weight with the dequantization / compensation / bias epilogue), bf16
+output.  The denoising step index tau cycles through the table.
+
+Prints one JSON line.  Besides the contract fields it carries the roofline of
+the dominant kernel (the GEMM, against the int8 MFMA peak), the unfused
+variant and the W4A4 variant on the same layers, and the CPU oracle timed on a
+bounded row sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POP/s
+PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+TOKENS = (4096, 32, 64)
+LINEARS = (("up", 2048, 8192), ("down", 8192, 2048))
+T_STEPS = 10
+W_GROUP = 128
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=200)
+    p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--cpu-rows", type=int, default=1536, help="rows of each layer the oracle times")
+    return p.parse_args()
+
+
+def make_layers(torch, B, synth, dev):
+    layers = []
+    for li, (name, K, N) in enumerate(LINEARS):
+        L = synth.make_layer(K=K, N=N, stream_counts=TOKENS, T=T_STEPS, seed=[0, 2, li])
+        x = torch.from_numpy(L.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        W = B.prepare_weight(torch.from_numpy(L.w).to(dev), torch.from_numpy(L.d).to(dev), W_GROUP,
+                             bias=torch.from_numpy(L.bias_bits.view(np.int16)).view(torch.bfloat16).to(dev))
+        acts = {}
+        for bits in (8, 4):
+            acts[bits] = B.ActParams(tok2stream=torch.from_numpy(L.tok2stream).to(dev),
+                                     gamma=torch.from_numpy(L.gamma).to(dev), step=0, act_bits=bits,
+                                     dinv=torch.from_numpy(L.dinv).to(dev))
+        layers.append(dict(name=name, K=K, N=N, L=L, x=x, W=W, acts=acts))
+    return layers
+
+
+def cpu_baseline(layers, rows_per_layer):
+    """The oracle, as it stands, on a row sample of each layer (all the same
+    arithmetic per row as the full layer); throughput scaled to TOPS."""
+    from oracle import sq_oracle as O
+
+    rng = np.random.default_rng(0)
+    prepared = []
+    for ly in layers:  # offline weight preparation: not part of the timed sample
+        L = ly["L"]
+        prepared.append((L, O.pack_weights(L.w, L.d, W_GROUP),
+                         np.sort(rng.choice(L.M, size=rows_per_layer, replace=False))))
+    ops = 0
+    t0 = time.perf_counter()
+    for L, pw, rows in prepared:
+        O.linear(L.x_bits[rows], L.tok2stream[rows], L.gamma, 3, pw["codes"], pw["w_scale"], W_GROUP,
+                 dinv=L.dinv, bias_bits=L.bias_bits, act_bits=8)
+        ops += 2 * rows_per_layer * L.K * L.N
+    dt = time.perf_counter() - t0
+    try:
+        cores = len(os.sched_getaffinity(0))
+    except AttributeError:
+        cores = os.cpu_count()
+    threads = int(os.environ.get("OMP_NUM_THREADS", cores))
+    return dict(value=ops / dt / 1e12, unit="TOPS", cores=min(cores, threads), kind="oracle",
+                seconds=round(dt, 3),
+                sample=f"{rows_per_layer} random rows of each of the up (2048->8192) and down (8192->2048) "
+                       f"W4A8 layers (quantize, exact block accumulation, fp32 epilogue); weights packed "
+                       f"beforehand; TOPS = 2*rows*K*N / time")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
+              f"(the layer is row-parallel; see DESIGN.md for how it would shard)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_39056_amd import binding as B
+    from paper_2609_39056_amd import synth
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    B.lib()
+    M = sum(TOKENS)
+    layers = make_layers(torch, B, synth, dev)
+    stream = torch.cuda.current_stream()
+
+    # per-layer buffers
+    for ly in layers:
+        ly["qx8"], ly["r8"] = B.act_buffers(M, ly["K"], 8, dev)
+        ly["y"] = torch.empty((M, ly["N"]), dtype=torch.bfloat16, device=dev)
+        ly["ws_unf"] = {b: B.alloc_workspace(B.SQ_VARIANT_UNFUSED, M, ly["K"], ly["N"], b, dev) for b in (8, 4)}
+        ly["ws_fused"] = {b: B.alloc_workspace(B.SQ_VARIANT_FUSED, M, ly["K"], ly["N"], b, dev) for b in (8, 4)}
+
+    def fused_step(tau, events=None):
+        for i, ly in enumerate(layers):
+            act = ly["acts"][8]
+            act.step = tau
+            if events is not None:
+                events[2 * i].record(stream)
+            B.sq_quantize_act(ly["x"], act, ly["qx8"], ly["r8"], stream)
+            if events is not None:
+                events[2 * i + 1].record(stream)
+            B.sq_gemm_w4a8(ly["qx8"], ly["r8"], ly["W"], ly["y"], B.SQ_OUT_BF16, stream)
+        if events is not None:
+            events[4].record(stream)
+
+    def variant_step(tau, fn, bits, ws_key):
+        for ly in layers:
+            act = ly["acts"][bits]
+            act.step = tau
+            fn(ly["x"], act, ly["W"], ly["y"], B.SQ_OUT_BF16, ly[ws_key][bits], stream)
+
+    # ---- main timed region: fused W4A8, events around every kernel
+    for s in range(args.warmup):
+        fused_step(s % T_STEPS)
+    torch.cuda.synchronize()
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        fused_step(s % T_STEPS, evs[s])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_per_step = wall * 1e3 / args.steps
+
+    k1 = np.zeros(2)
+    k2 = np.zeros(2)
+    for e in evs:
+        for i in range(2):
+            k1[i] += e[2 * i].elapsed_time(e[2 * i + 1])
+            k2[i] += e[2 * i + 1].elapsed_time(e[2 * i + 2])
+    k1 /= args.steps
+    k2 /= args.steps  # ms per launch, per layer
+
+    ops = [2.0 * M * ly["K"] * ly["N"] for ly in layers]
+    ops_step = sum(ops)
+    value = ops_step / (ms_per_step * 1e-3) / 1e12
+    gemm_tops = sum(ops) / (k2.sum() * 1e-3) / 1e12
+    # algorithmic bytes of the first kernel: bf16 X in, int8 Q_X + fp32 r out
+    k1_bytes = [M * ly["K"] * 2 + M * ly["K"] + 4 * M for ly in layers]
+    k1_gbs = sum(k1_bytes) / (k1.sum() * 1e-3) / 1e9
+    # algorithmic bytes of the whole layer (bf16 X, int4 W, fp16 steps, bf16 Y, stream map)
+    alg_bytes = [M * ly["K"] * 2 + ly["N"] * ly["K"] // 2 + ly["N"] * ly["K"] // W_GROUP * 2 + M * ly["N"] * 2
+                 + 4 * M for ly in layers]
+    serial = [b1 / (PEAK_HBM_GBS * 1e9) + max(o / (PEAK_INT8_TOPS * 1e12), 0.0)
+              for b1, o in zip(k1_bytes, ops)]
+    per_layer = {
+        ly["name"]: dict(
+            us_quant=round(k1[i] * 1e3, 2), us_gemm=round(k2[i] * 1e3, 2),
+            us_layer=round((k1[i] + k2[i]) * 1e3, 2),
+            tops_layer=round(ops[i] / ((k1[i] + k2[i]) * 1e-3) / 1e12, 1),
+            frac_layer_int8=round(ops[i] / ((k1[i] + k2[i]) * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4),
+            frac_gemm_int8=round(ops[i] / (k2[i] * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4),
+            frac_quant_hbm=round(k1_bytes[i] / (k1[i] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            frac_serial_roofline=round(serial[i] / ((k1[i] + k2[i]) * 1e-3), 4),
+            alg_mb=round(alg_bytes[i] / 1e6, 2))
+        for i, ly in enumerate(layers)}
+
+    # ---- unfused W4A8 and fused W4A4 on the same layers (context)
+    def time_variant(fn, bits, ws_key, steps):
+        for s in range(max(3, args.warmup // 4)):
+            variant_step(s % T_STEPS, fn, bits, ws_key)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        for s in range(steps):
+            variant_step(s % T_STEPS, fn, bits, ws_key)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t) * 1e3 / steps
+
+    vsteps = max(10, args.steps // 4)
+    ms_unfused = time_variant(B.sq_linear_unfused, 8, "ws_unf", vsteps)
+    ms_w4a4 = time_variant(B.sq_linear_w4a4, 4, "ws_fused", vsteps)
+    ms_w4a8_api = time_variant(B.sq_linear_w4a8, 8, "ws_fused", vsteps)
+
+    out = {
+        "metric": "fused W4A8/W4A4 linear TOPS + % int8-MFMA (or HBM) roofline per layer",
+        "value": round(value, 2),
+        "unit": "TOPS",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8",
+        "data": "synthetic",
+        "config": {
+            "workload": "2B-class WAM DiT MLP pair, W4A8: up 2048->8192 and down 8192->2048, "
+                        "M=4192 tokens (4096 video + 32 proprio + 64 action), 10-step gain tables, "
+                        "int4 weight groups of 128 (fp16 steps), per-token int8 activations (DYNAMIC), bf16 out",
+            "M": M, "linears": [[ly["name"], ly["K"], ly["N"]] for ly in layers],
+            "act_bits": 8, "w_group": W_GROUP,
+        },
+        "roofline": {
+            "bound": "mfma", "kernel": "gemm_w4_kernel<8,0> (sq_gemm_w4a8)",
+            "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",
+            "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": None,
+        },
+        "per_layer": per_layer,
+        "quant_kernel_gbs": round(k1_gbs, 1),
+        "unfused_w4a8": {"ms_per_step": round(ms_unfused, 5),
+                         "tops": round(ops_step / (ms_unfused * 1e-3) / 1e12, 2),
+                         "fused_speedup": round(ms_unfused / ms_per_step, 3)},
+        "fused_w4a8_api": {"ms_per_step": round(ms_w4a8_api, 5)},
+        "fused_w4a4": {"ms_per_step": round(ms_w4a4, 5),
+                       "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2)},
+    }
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(layers, args.cpu_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,188 @@
+/*
+ * sq.h -- C ABI of the fused low-bit linear layer of a world-action diffusion
+ * Transformer (SteerQuant / Rudder, arXiv 2609.39056), for AMD MI355X (gfx950).
+ *
+ * The layer computes, for one linear at denoising step tau
+ * (Sec. 4.3 Eq. 8 with the channel scaling of Sec. 4.2 Eq. 6):
+ *
+ *     Y = gamma_{tau,s}^-1 Q(gamma_{tau,s} X D^-1 ; c) Q(D W) + b
+ *
+ * in two kernels (Sec. 4.4): the first applies D^-1 and the stream gain while
+ * quantizing and writes integer activations Q_X plus row scales
+ * r_i = Delta_X / gamma_s(i); the second accumulates Q_X Q_W in int32 and
+ * applies the epilogue of Eq. 10, Y_ij = cast[(fp32(C_ij) r_i) Delta_W,j + b_j].
+ *
+ * Conventions shared by every entry point
+ * --------------------------------------
+ * - Pointers named in the structs and arguments are DEVICE pointers unless
+ *   stated otherwise; the structs themselves live in host memory and are
+ *   read before the call returns.
+ * - The caller owns every buffer.  The library allocates nothing, frees
+ *   nothing, keeps no pointer after returning and never synchronizes: all work
+ *   is enqueued on `stream` (a hipStream_t; NULL = the null stream).
+ * - Arguments are validated on the host before anything is enqueued; a
+ *   failing check returns a negative sq_status and launches nothing.  A launch
+ *   failure returns SQ_ERR_HIP.  Stream ids in tok2stream are device data and
+ *   are not checked: each must lie in [0, num_streams).
+ * - Matrices are row-major.  X is [M, K] bf16 (K contiguous).  W is stored
+ *   transposed, [N, K] (K contiguous), as packed int4.  Y is [M, N].
+ * - Shapes: 1 <= M <= 2^24; K % 128 == 0 and 128 <= K <= 32768; N % 64 == 0
+ *   and 64 <= N <= 2^20.
+ * - Alignment: x, qx, qw, y and workspace 16 bytes; every other pointer 4
+ *   bytes (2 for bf16/fp16 arrays).
+ * - Inputs must be finite; X D^-1 gamma must stay finite in fp32.
+ *
+ * Packed int4 layout (weights and A4 activations)
+ * -----------------------------------------------
+ * Codes are two's-complement nibbles.  Per row, each group of 8 consecutive
+ * codes k = 8g .. 8g+7 occupies bytes 4g .. 4g+3; byte 4g+b holds code 8g+b
+ * in its low nibble and code 8g+b+4 in its high nibble.
+ *
+ * Quantization arithmetic (both range modes; q_max = 127 for 8-bit, 7 for
+ * 4-bit activations; every step is one IEEE fp32 operation, round to nearest
+ * even, no contraction):
+ *     x~    = fp32(x) * dinv[k]                            (Eq. 6)
+ *     c     = clip[tau]  (STATIC)  |  max |x~| over the row (8-bit) or over the
+ *             64-wide group (4-bit), before the gain       (DYNAMIC)
+ *     Delta = c / q_max;  4-bit: Delta = fp32(fp16(Delta))  (Eq. 1)
+ *     inv   = 1 / Delta, or 0 where that is infinite
+ *     q     = rint(clamp((x~ * g) * inv, -q_max, q_max)),   g = gamma[tau][s(i)]
+ *     8-bit: r_i = Delta / g  (fp32)                        (Sec. 4.4)
+ *     4-bit: sigma_{i,a} = fp16(Delta) per 64-group; the compensation
+ *            1/g is applied to the row in the GEMM epilogue (Eq. 8).
+ */
+#ifndef SQ_H_
+#define SQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SQ_OK = 0,
+  SQ_ERR_NULL = -1,        /* a required pointer is NULL */
+  SQ_ERR_SHAPE = -2,       /* a size, step index or stream count is out of range */
+  SQ_ERR_ALIGN = -3,       /* a pointer is not aligned as required */
+  SQ_ERR_UNSUPPORTED = -4, /* bits, group size, range mode or dtype not supported */
+  SQ_ERR_WORKSPACE = -5,   /* workspace smaller than sq_workspace_bytes() */
+  SQ_ERR_HIP = -6          /* a kernel launch failed */
+} sq_status;
+
+typedef enum {
+  SQ_RANGE_DYNAMIC = 0, /* c = per-token (8-bit) or per-64-group (4-bit) amax of X D^-1 */
+  SQ_RANGE_STATIC = 1   /* c = clip[tau], the per-step threshold of Sec. 4.3 */
+} sq_range_mode;
+
+typedef enum { SQ_OUT_F32 = 0, SQ_OUT_BF16 = 1, SQ_OUT_F16 = 2 } sq_out_dtype;
+
+typedef enum { SQ_VARIANT_FUSED = 0, SQ_VARIANT_UNFUSED = 1 } sq_variant;
+
+/* Per-layer activation-side parameters (Sec. 4.3: gains and threshold stored
+ * in a layer-step lookup table; Sec. 4.2: one channel scaling per layer). */
+typedef struct sq_act_params {
+  const int32_t* tok2stream; /* [M] stream id s(i) of every row, in [0, num_streams) */
+  const float* gamma;        /* [num_steps][num_streams] gains, finite and > 0 */
+  const float* clip;         /* [num_steps] thresholds > 0; required for STATIC, else may be NULL */
+  const float* dinv;         /* [K] D^-1 (positive), or NULL for D = I */
+  int32_t num_streams;       /* S >= 1 */
+  int32_t num_steps;         /* T >= 1 */
+  int32_t step;              /* tau, 0 <= tau < T */
+  int32_t range_mode;        /* sq_range_mode */
+  int32_t act_bits;          /* 8 (per-token steps) or 4 (per-64-group fp16 steps) */
+} sq_act_params;
+
+/* A prepared weight: Q(D W) with fp16 steps (Sec. 4.2, fold then pack). */
+typedef struct sq_weight {
+  const uint8_t* qw;        /* [N][K/2] packed int4 codes (layout above) */
+  const uint16_t* w_scale;  /* [N][K/w_group] fp16 steps Delta_W */
+  const uint16_t* bias;     /* [N] bf16 bias b, or NULL */
+  int32_t N, K;
+  int32_t w_group;          /* 128, or K (one step per output channel, as in the paper) */
+} sq_weight;
+
+/* Human-readable name of a status code (static storage). */
+const char* sq_status_string(int32_t status);
+
+/* Bytes of device workspace that sq_linear_w4a8 / sq_linear_w4a4
+ * (variant SQ_VARIANT_FUSED) or sq_linear_unfused (SQ_VARIANT_UNFUSED) need
+ * for this shape; 0 for invalid arguments.  Host-only. */
+size_t sq_workspace_bytes(int32_t variant, int32_t M, int32_t K, int32_t N, int32_t act_bits);
+
+/* Offline weight preparation (Sec. 4.2: fold D* into W, quantize to int4 with
+ * symmetric steps, store packed integers with their scales).
+ *   w        [N][K] fp32, the transposed weight W^T
+ *   d        [K] fp32 positive channel scaling D, or NULL for D = I
+ *   qw       out [N][K/2] packed int4 codes in [-7, 7]
+ *   w_scale  out [N][K/w_group] fp16 steps
+ * Per (row j, group): w' = w * d[k]; Delta_W = fp16(amax|w'| / 7);
+ * inv = 1 / fp32(Delta_W) (0 where infinite); code = rint(clamp(w' * inv, -7, 7)).
+ * Requires amax / 7 <= 65504 in every group. */
+sq_status sq_pack_weights(const float* w, const float* d, int32_t N, int32_t K, int32_t w_group,
+                          uint8_t* qw, uint16_t* w_scale, hipStream_t stream);
+
+/* The first kernel (Sec. 4.4): channel scaling, stream gain and quantization
+ * of X [M][K] bf16 in one pass.
+ *   act->act_bits == 8: qx = int8 [M][K]; act_scale = fp32 r [M]
+ *   act->act_bits == 4: qx = packed int4 [M][K/2]; act_scale = fp16 sigma [M][K/64]
+ * qx and act_scale must not overlap x. */
+sq_status sq_quantize_act(const uint16_t* x, int32_t M, int32_t K, const sq_act_params* act,
+                          void* qx, void* act_scale, hipStream_t stream);
+
+/* The second kernel for 8-bit activations (Sec. 4.4, Eq. 10, with one int32
+ * accumulator per K-block of w_group): C^b = Q_X Q_W over the block, then
+ * Y_ij = r_i * sum_b fp32(C^b_ij) Delta_W[j][b] + b_j, cast to out_dtype.
+ *   qx int8 [M][K], row_scale fp32 [M] (as written by sq_quantize_act),
+ *   y  [M][N] of out_dtype. */
+sq_status sq_gemm_w4a8(const int8_t* qx, const float* row_scale, int32_t M, const sq_weight* w,
+                       void* y, int32_t out_dtype, hipStream_t stream);
+
+/* The second kernel for 4-bit activations: one int32 accumulator per 64-wide
+ * K-block, Y_ij = kappa_i * sum_b (fp32(C^b_ij) sigma_{i,b}) Delta_W[j][b(k)] + b_j
+ * with kappa_i = 1 / gamma[tau][s(i)] (the inverse-gain compensation of Eq. 8,
+ * taken from act->tok2stream, act->gamma and act->step).
+ *   qx packed int4 [M][K/2], group_scale fp16 [M][K/64]. */
+sq_status sq_gemm_w4a4(const uint8_t* qx, const uint16_t* group_scale, int32_t M,
+                       const sq_act_params* act, const sq_weight* w, void* y, int32_t out_dtype,
+                       hipStream_t stream);
+
+/* The fused linear with 8-bit activations: sq_quantize_act then sq_gemm_w4a8,
+ * Q_X and r living in `workspace` (>= sq_workspace_bytes(SQ_VARIANT_FUSED, ...)).
+ * Requires act->act_bits == 8 and w->K == K of x. */
+sq_status sq_linear_w4a8(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                         void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
+                         hipStream_t stream);
+
+/* The fused linear with 4-bit activations (act->act_bits == 4). */
+sq_status sq_linear_w4a4(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                         void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
+                         hipStream_t stream);
+
+/* The same layer without fusion, as the execution that Sec. 4.4 replaces:
+ * channel scaling, gain, quantization, GEMM, dequantization, inverse-gain
+ * compensation and bias each run as their own kernel, passing fp32 (or
+ * int32) intermediates through `workspace`
+ * (>= sq_workspace_bytes(SQ_VARIANT_UNFUSED, ...)).  act->act_bits 8 or 4.
+ * Codes and accumulators equal the fused path's; outputs differ only in
+ * fp32 rounding order. */
+sq_status sq_linear_unfused(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                            void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Test hook: runs the fused GEMM main loop on already-quantized activations
+ * and writes every int32 block accumulator instead of the epilogue:
+ * acc_out[b][i][j] = sum over K-block b of q_ik * w_jk, with blocks of
+ * w_group (8-bit) or 64 (4-bit).  qx as for sq_gemm_w4a8 / sq_gemm_w4a4.
+ * acc_out is int32 [K/block][M][N]. */
+sq_status sq_debug_block_acc_i32(const void* qx, int32_t M, int32_t act_bits, const sq_weight* w,
+                                 int32_t* acc_out, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SQ_H_ */

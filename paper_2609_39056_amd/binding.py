@@ -1,0 +1,250 @@
+"""ctypes binding of libsq (include/sq.h).  Argument marshalling only: every
+step of the linear runs in the HIP kernels of the library.
+
+The functions carry the C names.  Device buffers are torch tensors on the GPU
+(torch supplies the memory and the stream); shapes are read from them.  A
+non-zero status raises SqError.  If the library has not been built, loading
+fails loudly: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "lib", "libsq.so")
+
+SQ_OK = 0
+SQ_RANGE_DYNAMIC = 0
+SQ_RANGE_STATIC = 1
+SQ_OUT_F32 = 0
+SQ_OUT_BF16 = 1
+SQ_OUT_F16 = 2
+SQ_VARIANT_FUSED = 0
+SQ_VARIANT_UNFUSED = 1
+A4_GROUP = 64
+
+OUT_DTYPES = {SQ_OUT_F32: torch.float32, SQ_OUT_BF16: torch.bfloat16, SQ_OUT_F16: torch.float16}
+
+
+class SqError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {status_string(status)} ({status})")
+        self.status = status
+
+
+class sq_act_params(ctypes.Structure):
+    _fields_ = [
+        ("tok2stream", ctypes.c_void_p),
+        ("gamma", ctypes.c_void_p),
+        ("clip", ctypes.c_void_p),
+        ("dinv", ctypes.c_void_p),
+        ("num_streams", ctypes.c_int32),
+        ("num_steps", ctypes.c_int32),
+        ("step", ctypes.c_int32),
+        ("range_mode", ctypes.c_int32),
+        ("act_bits", ctypes.c_int32),
+    ]
+
+
+class sq_weight(ctypes.Structure):
+    _fields_ = [
+        ("qw", ctypes.c_void_p),
+        ("w_scale", ctypes.c_void_p),
+        ("bias", ctypes.c_void_p),
+        ("N", ctypes.c_int32),
+        ("K", ctypes.c_int32),
+        ("w_group", ctypes.c_int32),
+    ]
+
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+_S = ctypes.c_size_t
+_SIGS = {
+    "sq_status_string": (ctypes.c_char_p, [_I]),
+    "sq_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
+    "sq_pack_weights": (_I, [_P, _P, _I, _I, _I, _P, _P, _P]),
+    "sq_quantize_act": (_I, [_P, _I, _I, ctypes.POINTER(sq_act_params), _P, _P, _P]),
+    "sq_gemm_w4a8": (_I, [_P, _P, _I, ctypes.POINTER(sq_weight), _P, _I, _P]),
+    "sq_gemm_w4a4": (_I, [_P, _P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P]),
+    "sq_linear_w4a8": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
+    "sq_linear_w4a4": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
+    "sq_linear_unfused": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
+    "sq_debug_block_acc_i32": (_I, [_P, _I, _I, ctypes.POINTER(sq_weight), _P, _P]),
+}
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libsq.so (built by paper_2609_39056_amd._build) and declare its
+    signatures.  Raises if the library is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} not found: build it first (python -m paper_2609_39056_amd._build)")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().sq_status_string(int(status)).decode()
+
+
+def _check(status: int, what: str) -> None:
+    if status != SQ_OK:
+        raise SqError(status, what)
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("libsq takes device tensors")
+    if not t.is_contiguous():
+        raise ValueError("libsq takes contiguous tensors")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+@dataclass
+class ActParams:
+    """Device tensors of the activation-side table for one layer."""
+
+    tok2stream: torch.Tensor           # int32 [M]
+    gamma: torch.Tensor                # fp32 [T, S]
+    step: int
+    act_bits: int = 8
+    range_mode: int = SQ_RANGE_DYNAMIC
+    clip: Optional[torch.Tensor] = None  # fp32 [T]
+    dinv: Optional[torch.Tensor] = None  # fp32 [K]
+
+    def struct(self) -> sq_act_params:
+        T, S = self.gamma.shape
+        return sq_act_params(_ptr(self.tok2stream), _ptr(self.gamma), _ptr(self.clip), _ptr(self.dinv),
+                             S, T, self.step, self.range_mode, self.act_bits)
+
+
+@dataclass
+class Weight:
+    """A prepared int4 weight on the device."""
+
+    qw: torch.Tensor                   # uint8 [N, K/2]
+    w_scale: torch.Tensor              # fp16 [N, K/w_group] (or int16 bit patterns)
+    w_group: int
+    bias: Optional[torch.Tensor] = None  # bf16 [N]
+
+    @property
+    def N(self) -> int:
+        return int(self.qw.shape[0])
+
+    @property
+    def K(self) -> int:
+        return int(self.qw.shape[1]) * 2
+
+    def struct(self) -> sq_weight:
+        return sq_weight(_ptr(self.qw), _ptr(self.w_scale), _ptr(self.bias), self.N, self.K, self.w_group)
+
+
+def sq_workspace_bytes(variant: int, M: int, K: int, N: int, act_bits: int) -> int:
+    return int(lib().sq_workspace_bytes(variant, M, K, N, act_bits))
+
+
+def sq_pack_weights(w: torch.Tensor, d: Optional[torch.Tensor], w_group: int, qw: torch.Tensor,
+                    w_scale: torch.Tensor, stream=None) -> None:
+    N, K = w.shape
+    _check(lib().sq_pack_weights(_ptr(w), _ptr(d), N, K, w_group, _ptr(qw), _ptr(w_scale), _stream(stream)),
+           "sq_pack_weights")
+
+
+def sq_quantize_act(x: torch.Tensor, act: ActParams, qx: torch.Tensor, act_scale: torch.Tensor,
+                    stream=None) -> None:
+    M, K = x.shape
+    s = act.struct()
+    _check(lib().sq_quantize_act(_ptr(x), M, K, ctypes.byref(s), _ptr(qx), _ptr(act_scale), _stream(stream)),
+           "sq_quantize_act")
+
+
+def sq_gemm_w4a8(qx: torch.Tensor, row_scale: torch.Tensor, w: Weight, y: torch.Tensor, out_dtype: int,
+                 stream=None) -> None:
+    M = qx.shape[0]
+    ws = w.struct()
+    _check(lib().sq_gemm_w4a8(_ptr(qx), _ptr(row_scale), M, ctypes.byref(ws), _ptr(y), out_dtype,
+                              _stream(stream)), "sq_gemm_w4a8")
+
+
+def sq_gemm_w4a4(qx: torch.Tensor, group_scale: torch.Tensor, act: ActParams, w: Weight, y: torch.Tensor,
+                 out_dtype: int, stream=None) -> None:
+    M = qx.shape[0]
+    s, ws = act.struct(), w.struct()
+    _check(lib().sq_gemm_w4a4(_ptr(qx), _ptr(group_scale), M, ctypes.byref(s), ctypes.byref(ws), _ptr(y),
+                              out_dtype, _stream(stream)), "sq_gemm_w4a4")
+
+
+def _linear(fn: str, x, act, w, y, out_dtype, workspace, stream):
+    M = x.shape[0]
+    s, ws = act.struct(), w.struct()
+    st = getattr(lib(), fn)(_ptr(x), M, ctypes.byref(s), ctypes.byref(ws), _ptr(y), out_dtype,
+                            _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+    _check(st, fn)
+
+
+def sq_linear_w4a8(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, stream=None) -> None:
+    _linear("sq_linear_w4a8", x, act, w, y, out_dtype, workspace, stream)
+
+
+def sq_linear_w4a4(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, stream=None) -> None:
+    _linear("sq_linear_w4a4", x, act, w, y, out_dtype, workspace, stream)
+
+
+def sq_linear_unfused(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, stream=None) -> None:
+    _linear("sq_linear_unfused", x, act, w, y, out_dtype, workspace, stream)
+
+
+def sq_debug_block_acc_i32(qx: torch.Tensor, act_bits: int, w: Weight, acc_out: torch.Tensor,
+                           stream=None) -> None:
+    M = qx.shape[0]
+    ws = w.struct()
+    _check(lib().sq_debug_block_acc_i32(_ptr(qx), M, act_bits, ctypes.byref(ws), _ptr(acc_out),
+                                        _stream(stream)), "sq_debug_block_acc_i32")
+
+
+# ------------------------------------------------------------------ helpers
+def alloc_workspace(variant: int, M: int, K: int, N: int, act_bits: int, device="cuda") -> torch.Tensor:
+    n = sq_workspace_bytes(variant, M, K, N, act_bits)
+    if n == 0:
+        raise ValueError("invalid shape for workspace")
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def prepare_weight(w: torch.Tensor, d: Optional[torch.Tensor], w_group: int,
+                   bias: Optional[torch.Tensor] = None, stream=None) -> Weight:
+    """Fold, quantize and pack a device fp32 weight [N, K] with sq_pack_weights."""
+    N, K = w.shape
+    qw = torch.empty((N, K // 2), dtype=torch.uint8, device=w.device)
+    ws = torch.empty((N, K // w_group), dtype=torch.float16, device=w.device)
+    sq_pack_weights(w, d, w_group, qw, ws, stream)
+    return Weight(qw=qw, w_scale=ws, w_group=w_group, bias=bias)
+
+
+def act_buffers(M: int, K: int, act_bits: int, device="cuda"):
+    """Allocate Q_X and its scales for sq_quantize_act."""
+    if act_bits == 8:
+        return (torch.empty((M, K), dtype=torch.int8, device=device),
+                torch.empty((M,), dtype=torch.float32, device=device))
+    return (torch.empty((M, K // 2), dtype=torch.uint8, device=device),
+            torch.empty((M, K // A4_GROUP), dtype=torch.float16, device=device))

@@ -1,0 +1,292 @@
+// Host side of the C ABI declared in sq.h: argument validation, workspace
+// layout and kernel dispatch.  Nothing here allocates, frees or synchronizes.
+#include <stdint.h>
+
+#include "sq_internal.h"
+
+using namespace sq;
+
+namespace {
+
+constexpr int32_t kMaxM = 1 << 24;
+constexpr int32_t kMaxN = 1 << 20;
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+sq_status hip_status(hipError_t e) { return e == hipSuccess ? SQ_OK : SQ_ERR_HIP; }
+
+bool valid_m(int32_t M) { return M >= 1 && M <= kMaxM; }
+bool valid_k(int32_t K) { return K >= kKTile && K <= kMaxK && K % kKTile == 0; }
+bool valid_n(int32_t N) { return N >= 64 && N <= kMaxN && N % 64 == 0; }
+
+sq_status check_act(const sq_act_params* act, int32_t K) {
+  if (act == nullptr || act->tok2stream == nullptr || act->gamma == nullptr) return SQ_ERR_NULL;
+  if (act->act_bits != 8 && act->act_bits != 4) return SQ_ERR_UNSUPPORTED;
+  if (act->range_mode != SQ_RANGE_DYNAMIC && act->range_mode != SQ_RANGE_STATIC) return SQ_ERR_UNSUPPORTED;
+  if (act->range_mode == SQ_RANGE_STATIC && act->clip == nullptr) return SQ_ERR_NULL;
+  if (act->num_streams < 1 || act->num_steps < 1) return SQ_ERR_SHAPE;
+  if (act->step < 0 || act->step >= act->num_steps) return SQ_ERR_SHAPE;
+  if (!valid_k(K)) return SQ_ERR_SHAPE;
+  if (!aligned(act->tok2stream, 4) || !aligned(act->gamma, 4)) return SQ_ERR_ALIGN;
+  if (act->clip != nullptr && !aligned(act->clip, 4)) return SQ_ERR_ALIGN;
+  if (act->dinv != nullptr && !aligned(act->dinv, 16)) return SQ_ERR_ALIGN;
+  return SQ_OK;
+}
+
+sq_status check_weight(const sq_weight* w) {
+  if (w == nullptr || w->qw == nullptr || w->w_scale == nullptr) return SQ_ERR_NULL;
+  if (!valid_k(w->K) || !valid_n(w->N)) return SQ_ERR_SHAPE;
+  if (w->w_group < kKTile || w->w_group % kKTile != 0 || w->K % w->w_group != 0) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(w->qw, 16) || !aligned(w->w_scale, 2)) return SQ_ERR_ALIGN;
+  if (w->bias != nullptr && !aligned(w->bias, 2)) return SQ_ERR_ALIGN;
+  return SQ_OK;
+}
+
+bool valid_out(int32_t d) { return d == SQ_OUT_F32 || d == SQ_OUT_BF16 || d == SQ_OUT_F16; }
+
+size_t qx_bytes(int32_t M, int32_t K, int32_t bits) {
+  return bits == 8 ? static_cast<size_t>(M) * K : static_cast<size_t>(M) * K / 2;
+}
+size_t act_scale_bytes(int32_t M, int32_t K, int32_t bits) {
+  return bits == 8 ? static_cast<size_t>(M) * 4 : static_cast<size_t>(M) * (K / kA4Group) * 2;
+}
+
+struct FusedWs {
+  void* qx;
+  void* scale;
+};
+FusedWs fused_ws(void* ws, int32_t M, int32_t K, int32_t bits) {
+  uint8_t* p = static_cast<uint8_t*>(ws);
+  FusedWs f;
+  f.qx = p;
+  f.scale = p + round_up(qx_bytes(M, K, bits));
+  return f;
+}
+
+size_t fused_ws_bytes(int32_t M, int32_t K, int32_t bits) {
+  return round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits));
+}
+
+size_t unfused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
+  const size_t mk4 = round_up(static_cast<size_t>(M) * K * 4);
+  const size_t mn4 = round_up(static_cast<size_t>(M) * N * 4);
+  const size_t groups = bits == 8 ? 1 : K / kA4Group;
+  return 2 * mk4 + round_up(static_cast<size_t>(M) * groups * 4) + round_up(qx_bytes(M, K, bits)) +
+         round_up(act_scale_bytes(M, K, bits)) + 3 * mn4;
+}
+
+sq_status quantize(const uint16_t* x, int32_t M, int32_t K, const sq_act_params* act, void* qx,
+                   void* scale, hipStream_t stream) {
+  QuantArgs q;
+  q.x = x;
+  q.tok2stream = act->tok2stream;
+  q.gamma = act->gamma;
+  q.clip = act->clip;
+  q.dinv = act->dinv;
+  q.qx = qx;
+  q.scale = scale;
+  q.M = M;
+  q.K = K;
+  q.S = act->num_streams;
+  q.step = act->step;
+  q.range_mode = act->range_mode;
+  return hip_status(launch_quantize_act(act->act_bits, q, stream));
+}
+
+GemmArgs gemm_args(const void* qx, const void* scale, int32_t M, const sq_act_params* act,
+                   const sq_weight* w, void* out, int32_t out_dtype) {
+  GemmArgs g{};
+  g.qx = qx;
+  g.act_scale = scale;
+  if (act != nullptr) {
+    g.tok2stream = act->tok2stream;
+    g.gamma = act->gamma;
+    g.S = act->num_streams;
+    g.step = act->step;
+  }
+  g.qw = w->qw;
+  g.w_scale = w->w_scale;
+  g.bias = w->bias;
+  g.out = out;
+  g.M = M;
+  g.N = w->N;
+  g.K = w->K;
+  g.w_group = w->w_group;
+  g.out_dtype = out_dtype;
+  return g;
+}
+
+sq_status linear_fused(int32_t bits, const uint16_t* x, int32_t M, const sq_act_params* act,
+                       const sq_weight* w, void* y, int32_t out_dtype, void* ws, size_t ws_bytes,
+                       hipStream_t stream) {
+  if (x == nullptr || y == nullptr || ws == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  st = check_act(act, w->K);
+  if (st != SQ_OK) return st;
+  if (act->act_bits != bits) return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 16)) return SQ_ERR_ALIGN;
+  if (ws_bytes < fused_ws_bytes(M, w->K, bits)) return SQ_ERR_WORKSPACE;
+  FusedWs f = fused_ws(ws, M, w->K, bits);
+  st = quantize(x, M, w->K, act, f.qx, f.scale, stream);
+  if (st != SQ_OK) return st;
+  return hip_status(launch_gemm(bits, kEpiOut, gemm_args(f.qx, f.scale, M, act, w, y, out_dtype), stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* sq_status_string(int32_t status) {
+  switch (status) {
+    case SQ_OK: return "SQ_OK";
+    case SQ_ERR_NULL: return "SQ_ERR_NULL: a required pointer is NULL";
+    case SQ_ERR_SHAPE: return "SQ_ERR_SHAPE: a size, step index or stream count is out of range";
+    case SQ_ERR_ALIGN: return "SQ_ERR_ALIGN: a pointer is not aligned as required";
+    case SQ_ERR_UNSUPPORTED: return "SQ_ERR_UNSUPPORTED: bits, group size, range mode or dtype not supported";
+    case SQ_ERR_WORKSPACE: return "SQ_ERR_WORKSPACE: workspace too small";
+    case SQ_ERR_HIP: return "SQ_ERR_HIP: a kernel launch failed";
+    default: return "unknown sq_status";
+  }
+}
+
+size_t sq_workspace_bytes(int32_t variant, int32_t M, int32_t K, int32_t N, int32_t act_bits) {
+  if (!valid_m(M) || !valid_k(K) || !valid_n(N) || (act_bits != 8 && act_bits != 4)) return 0;
+  if (variant == SQ_VARIANT_FUSED) return fused_ws_bytes(M, K, act_bits);
+  if (variant == SQ_VARIANT_UNFUSED) return unfused_ws_bytes(M, K, N, act_bits);
+  return 0;
+}
+
+sq_status sq_pack_weights(const float* w, const float* d, int32_t N, int32_t K, int32_t w_group,
+                          uint8_t* qw, uint16_t* w_scale, hipStream_t stream) {
+  if (w == nullptr || qw == nullptr || w_scale == nullptr) return SQ_ERR_NULL;
+  if (!valid_k(K) || !valid_n(N)) return SQ_ERR_SHAPE;
+  if (w_group < kKTile || w_group % kKTile != 0 || K % w_group != 0) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(w, 16) || !aligned(qw, 16) || !aligned(w_scale, 2)) return SQ_ERR_ALIGN;
+  if (d != nullptr && !aligned(d, 16)) return SQ_ERR_ALIGN;
+  PackArgs p{w, d, qw, w_scale, N, K, w_group};
+  return hip_status(launch_pack_weights(p, stream));
+}
+
+sq_status sq_quantize_act(const uint16_t* x, int32_t M, int32_t K, const sq_act_params* act,
+                          void* qx, void* act_scale, hipStream_t stream) {
+  if (x == nullptr || qx == nullptr || act_scale == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_act(act, K);
+  if (st != SQ_OK) return st;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(qx, 16)) return SQ_ERR_ALIGN;
+  if (!aligned(act_scale, act->act_bits == 8 ? 4 : 2)) return SQ_ERR_ALIGN;
+  return quantize(x, M, K, act, qx, act_scale, stream);
+}
+
+sq_status sq_gemm_w4a8(const int8_t* qx, const float* row_scale, int32_t M, const sq_weight* w,
+                       void* y, int32_t out_dtype, hipStream_t stream) {
+  if (qx == nullptr || row_scale == nullptr || y == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(qx, 16) || !aligned(y, 16) || !aligned(row_scale, 4)) return SQ_ERR_ALIGN;
+  return hip_status(launch_gemm(8, kEpiOut, gemm_args(qx, row_scale, M, nullptr, w, y, out_dtype), stream));
+}
+
+sq_status sq_gemm_w4a4(const uint8_t* qx, const uint16_t* group_scale, int32_t M,
+                       const sq_act_params* act, const sq_weight* w, void* y, int32_t out_dtype,
+                       hipStream_t stream) {
+  if (qx == nullptr || group_scale == nullptr || y == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  st = check_act(act, w->K);
+  if (st != SQ_OK) return st;
+  if (act->act_bits != 4) return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(qx, 16) || !aligned(y, 16) || !aligned(group_scale, 4)) return SQ_ERR_ALIGN;
+  return hip_status(launch_gemm(4, kEpiOut, gemm_args(qx, group_scale, M, act, w, y, out_dtype), stream));
+}
+
+sq_status sq_linear_w4a8(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                         void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
+                         hipStream_t stream) {
+  return linear_fused(8, x, M, act, w, y, out_dtype, workspace, ws_bytes, stream);
+}
+
+sq_status sq_linear_w4a4(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                         void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
+                         hipStream_t stream) {
+  return linear_fused(4, x, M, act, w, y, out_dtype, workspace, ws_bytes, stream);
+}
+
+sq_status sq_linear_unfused(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                            void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
+                            hipStream_t stream) {
+  if (x == nullptr || y == nullptr || workspace == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  st = check_act(act, w->K);
+  if (st != SQ_OK) return st;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(y, 16) || !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  const int32_t K = w->K, N = w->N, bits = act->act_bits;
+  if (ws_bytes < unfused_ws_bytes(M, K, N, bits)) return SQ_ERR_WORKSPACE;
+
+  uint8_t* p = static_cast<uint8_t*>(workspace);
+  UnfusedArgs u{};
+  u.x = x;
+  u.tok2stream = act->tok2stream;
+  u.gamma = act->gamma;
+  u.clip = act->clip;
+  u.dinv = act->dinv;
+  u.qw = w->qw;
+  u.w_scale = w->w_scale;
+  u.bias = w->bias;
+  u.M = M;
+  u.K = K;
+  u.N = N;
+  u.S = act->num_streams;
+  u.step = act->step;
+  u.range_mode = act->range_mode;
+  u.act_bits = bits;
+  u.w_group = w->w_group;
+  u.out_dtype = out_dtype;
+  const size_t mk4 = round_up(static_cast<size_t>(M) * K * 4);
+  const size_t mn4 = round_up(static_cast<size_t>(M) * N * 4);
+  const size_t groups = bits == 8 ? 1 : K / kA4Group;
+  u.xt = reinterpret_cast<float*>(p);
+  p += mk4;
+  u.xh = reinterpret_cast<float*>(p);
+  p += mk4;
+  u.gmax = reinterpret_cast<float*>(p);
+  p += round_up(static_cast<size_t>(M) * groups * 4);
+  u.qx = p;
+  p += round_up(qx_bytes(M, K, bits));
+  u.qscale = p;
+  p += round_up(act_scale_bytes(M, K, bits));
+  u.gemm_out = p;
+  p += mn4;
+  u.y1 = reinterpret_cast<float*>(p);
+  p += mn4;
+  u.y2 = reinterpret_cast<float*>(p);
+  u.y = y;
+  return hip_status(launch_unfused(u, stream));
+}
+
+sq_status sq_debug_block_acc_i32(const void* qx, int32_t M, int32_t act_bits, const sq_weight* w,
+                                 int32_t* acc_out, hipStream_t stream) {
+  if (qx == nullptr || acc_out == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  if (act_bits != 8 && act_bits != 4) return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!aligned(qx, 16) || !aligned(acc_out, 4)) return SQ_ERR_ALIGN;
+  GemmArgs g = gemm_args(qx, nullptr, M, nullptr, w, acc_out, SQ_OUT_F32);
+  return hip_status(launch_gemm(act_bits, kEpiDump, g, stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,117 @@
+// Internal declarations shared by the HIP translation units of libsq.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "sq.h"
+
+namespace sq {
+
+constexpr int kA4Group = 64;      // activation group of 4-bit codes along K
+constexpr int kKTile = 128;       // K extent of one GEMM pipeline stage
+constexpr int kMaxK = 32768;
+
+// ---------------------------------------------------------------- number formats
+__device__ __forceinline__ float bf16_to_f32(uint32_t bits16) {
+  return __uint_as_float(bits16 << 16);
+}
+
+// fp32 -> bf16, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// fp32 -> fp16 bits with the hardware conversion (round to nearest even).
+__device__ __forceinline__ uint32_t f32_to_f16(float f) {
+  _Float16 h = static_cast<_Float16>(f);
+  return static_cast<uint32_t>(__builtin_bit_cast(uint16_t, h));
+}
+
+__device__ __forceinline__ float f16_to_f32(uint32_t bits16) {
+  return static_cast<float>(__builtin_bit_cast(_Float16, static_cast<uint16_t>(bits16)));
+}
+
+// Two's-complement nibbles of one packed dword (codes k0..k7 with k_b in the
+// low and k_{b+4} in the high nibble of byte b) -> two dwords of int8 bytes
+// holding 16 * code: lo = (16k0, 16k1, 16k2, 16k3), hi = (16k4, .., 16k7).
+// Placing a nibble in the top half of a byte multiplies its signed value by 16
+// without any sign extension.
+__device__ __forceinline__ void unpack_int4x8_times16(uint32_t p, uint32_t& lo, uint32_t& hi) {
+  lo = (p << 4) & 0xF0F0F0F0u;
+  hi = p & 0xF0F0F0F0u;
+}
+
+// ---------------------------------------------------------------- launch arguments
+struct QuantArgs {
+  const uint16_t* x;
+  const int32_t* tok2stream;
+  const float* gamma;
+  const float* clip;
+  const float* dinv;
+  void* qx;
+  void* scale;
+  int32_t M, K, S, step, range_mode;
+};
+
+enum EpiMode : int {
+  kEpiOut = 0,      // full epilogue: row factor, bias, cast, store y
+  kEpiPartial = 1,  // fp32 sum_b fp32(C^b) * s_b * Delta_W (no row factor / bias)
+  kEpiInt32 = 2,    // int32 C (one block spanning K)
+  kEpiDump = 3,     // int32 C^b of every block to acc_out[b][i][j]
+};
+
+struct GemmArgs {
+  const void* qx;           // int8 [M][K] or packed int4 [M][K/2]
+  const void* act_scale;    // fp32 r [M] (8-bit) or fp16 sigma [M][K/64] (4-bit); may be NULL in partial modes
+  const int32_t* tok2stream;  // 4-bit kappa: s(i)
+  const float* gamma;       // 4-bit kappa: gamma table
+  int32_t S, step;
+  const uint8_t* qw;
+  const uint16_t* w_scale;
+  const uint16_t* bias;
+  void* out;                // y, partial sums, int32 C or block dump
+  int32_t M, N, K, w_group;
+  int32_t out_dtype;
+};
+
+struct PackArgs {
+  const float* w;
+  const float* d;
+  uint8_t* qw;
+  uint16_t* w_scale;
+  int32_t N, K, w_group;
+};
+
+// ---------------------------------------------------------------- launchers (return hipError_t)
+hipError_t launch_quantize_act(int act_bits, const QuantArgs& a, hipStream_t s);
+hipError_t launch_pack_weights(const PackArgs& a, hipStream_t s);
+hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s);
+
+// unfused stages
+struct UnfusedArgs {
+  const uint16_t* x;
+  const int32_t* tok2stream;
+  const float* gamma;
+  const float* clip;
+  const float* dinv;
+  const uint8_t* qw;
+  const uint16_t* w_scale;
+  const uint16_t* bias;
+  int32_t M, K, N, S, step, range_mode, act_bits, w_group, out_dtype;
+  // workspace views
+  float* xt;        // [M][K] X D^-1
+  float* gmax;      // [M][groups] amax of X D^-1
+  float* xh;        // [M][K] X D^-1 gamma
+  void* qx;         // codes
+  void* qscale;     // 8-bit: fp32 Delta [M]; 4-bit: fp16 sigma [M][K/64]
+  void* gemm_out;   // fp32 partial [M][N] or int32 C [M][N]
+  float* y1;        // [M][N] after the activation step
+  float* y2;        // [M][N] after the inverse-gain compensation
+  void* y;          // final output
+};
+hipError_t launch_unfused(const UnfusedArgs& a, hipStream_t s);
+
+}  // namespace sq

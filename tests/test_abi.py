@@ -1,0 +1,143 @@
+"""The C ABI on the host (no GPU): the library loads, exports every entry point
+include/sq.h declares, and rejects invalid arguments before launching
+anything.  Every call below fails validation, so no kernel is enqueued and the
+HIP runtime is never asked for a device."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_39056_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "sq.h")
+
+OK, NULL, SHAPE, ALIGN, UNSUP, WS = 0, -1, -2, -3, -4, -5
+A = 0x10000  # a fake, suitably aligned device address (never dereferenced)
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB_PATH):
+        from paper_2609_39056_amd import _build
+        _build.build()
+    return B.lib()
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(sq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(L):
+    syms = declared_symbols()
+    assert "sq_linear_w4a8" in syms and "sq_linear_w4a4" in syms and "sq_linear_unfused" in syms
+    assert "sq_quantize_act" in syms
+    for s in syms:
+        assert hasattr(L, s), s
+    assert set(syms) == set(B._SIGS), "binding and header disagree"
+
+
+def test_status_strings(L):
+    for code in (OK, NULL, SHAPE, ALIGN, UNSUP, WS, -6):
+        assert B.status_string(code).startswith("SQ_")
+    assert "unknown" in B.status_string(42)
+
+
+def test_workspace_bytes(L):
+    M, K, N = 4192, 2048, 8192
+    fused8 = B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, K, N, 8)
+    fused4 = B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, K, N, 4)
+    assert fused8 >= M * K + 4 * M and fused8 % 256 == 0
+    assert fused4 >= M * K // 2 + 2 * M * (K // 64)
+    unf = B.sq_workspace_bytes(B.SQ_VARIANT_UNFUSED, M, K, N, 8)
+    assert unf >= 8 * M * K + 12 * M * N
+    assert B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, 0, K, N, 8) == 0
+    assert B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, 100, N, 8) == 0
+    assert B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, K, 100, 8) == 0
+    assert B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, K, N, 5) == 0
+    assert B.sq_workspace_bytes(7, M, K, N, 8) == 0
+
+
+def act(**kw):
+    d = dict(tok2stream=A, gamma=A, clip=A, dinv=None, num_streams=3, num_steps=2, step=0,
+             range_mode=0, act_bits=8)
+    d.update(kw)
+    return B.sq_act_params(**d)
+
+
+def wt(**kw):
+    d = dict(qw=A, w_scale=A, bias=None, N=256, K=256, w_group=128)
+    d.update(kw)
+    return B.sq_weight(**d)
+
+
+def quant(L, x=A, M=88, K=256, a=None, qx=A, sc=A):
+    a = act() if a is None else a
+    return L.sq_quantize_act(x, M, K, ctypes.byref(a) if a is not False else None, qx, sc, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(x=None), NULL), (dict(qx=None), NULL), (dict(sc=None), NULL), (dict(a=False), NULL),
+    (dict(M=0), SHAPE), (dict(M=1 << 25), SHAPE), (dict(K=100), SHAPE), (dict(K=64), SHAPE),
+    (dict(K=65536), SHAPE), (dict(x=A + 2), ALIGN), (dict(qx=A + 8), ALIGN), (dict(sc=A + 2), ALIGN),
+])
+def test_quantize_rejects(L, kw, code):
+    assert quant(L, **kw) == code
+
+
+@pytest.mark.parametrize("akw,code", [
+    (dict(tok2stream=None), NULL), (dict(gamma=None), NULL), (dict(act_bits=5), UNSUP),
+    (dict(range_mode=2), UNSUP), (dict(range_mode=1, clip=None), NULL), (dict(step=2), SHAPE),
+    (dict(step=-1), SHAPE), (dict(num_streams=0), SHAPE), (dict(num_steps=0), SHAPE),
+    (dict(dinv=A + 4), ALIGN), (dict(gamma=A + 1), ALIGN),
+])
+def test_act_params_rejected(L, akw, code):
+    assert quant(L, a=act(**akw)) == code
+
+
+def lin(L, fn="sq_linear_w4a8", x=A, M=88, a=None, w=None, y=A, out=0, ws=A, nbytes=1 << 30):
+    a = act() if a is None else a
+    w = wt() if w is None else w
+    return getattr(L, fn)(x, M, ctypes.byref(a), ctypes.byref(w), y, out, ws, nbytes, None)
+
+
+@pytest.mark.parametrize("fn", ["sq_linear_w4a8", "sq_linear_w4a4", "sq_linear_unfused"])
+@pytest.mark.parametrize("kw,code", [
+    (dict(x=None), NULL), (dict(y=None), NULL), (dict(ws=None), NULL), (dict(M=0), SHAPE),
+    (dict(out=3), UNSUP), (dict(y=A + 4), ALIGN), (dict(ws=A + 8), ALIGN), (dict(nbytes=16), WS),
+    (dict(w=wt(N=100)), SHAPE), (dict(w=wt(K=200)), SHAPE), (dict(w=wt(w_group=64)), UNSUP),
+    (dict(w=wt(K=384, w_group=256)), UNSUP), (dict(w=wt(qw=None)), NULL), (dict(w=wt(w_scale=None)), NULL),
+    (dict(w=wt(qw=A + 4)), ALIGN),
+])
+def test_linear_rejects(L, fn, kw, code):
+    if fn == "sq_linear_w4a4":
+        kw = dict(kw)
+        kw.setdefault("a", act(act_bits=4))
+    assert lin(L, fn=fn, **kw) == code
+
+
+def test_linear_bits_mismatch(L):
+    assert lin(L, "sq_linear_w4a8", a=act(act_bits=4)) == UNSUP
+    assert lin(L, "sq_linear_w4a4", a=act(act_bits=8)) == UNSUP
+
+
+def test_gemm_and_pack_reject(L):
+    w = wt()
+    assert L.sq_gemm_w4a8(None, A, 88, ctypes.byref(w), A, 0, None) == NULL
+    assert L.sq_gemm_w4a8(A, A, 0, ctypes.byref(w), A, 0, None) == SHAPE
+    a4 = act(act_bits=4)
+    assert L.sq_gemm_w4a4(A, A, 88, ctypes.byref(act()), ctypes.byref(w), A, 0, None) == UNSUP
+    assert L.sq_gemm_w4a4(A, A + 2, 88, ctypes.byref(a4), ctypes.byref(w), A, 0, None) == ALIGN
+    assert L.sq_pack_weights(A, None, 256, 256, 96, A, A, None) == UNSUP
+    assert L.sq_pack_weights(A, None, 100, 256, 128, A, A, None) == SHAPE
+    assert L.sq_pack_weights(None, None, 256, 256, 128, A, A, None) == NULL
+    assert L.sq_pack_weights(A + 4, None, 256, 256, 128, A, A, None) == ALIGN
+    assert L.sq_debug_block_acc_i32(A, 88, 6, ctypes.byref(w), A, None) == UNSUP
+    assert L.sq_debug_block_acc_i32(None, 88, 8, ctypes.byref(w), A, None) == NULL
+
+
+def test_binding_loads_only_the_built_library():
+    assert B.LIB_PATH.endswith(os.path.join("paper_2609_39056_amd", "lib", "libsq.so"))

@@ -1,0 +1,252 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Integers (codes, packed bytes, int32 block accumulators) and stored scales
+must match bit-exactly; fp32 outputs within 1e-5 of the summation scale
+(and 1e-5 relative where the sum does not cancel); bf16 / fp16 outputs within
+1 ulp of the oracle's value cast the same way."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import (act_params, bits16, check_output, f32_to_dev, i32_to_dev, oracle_weight,
+                      u16_to_dev, u8_to_dev)
+from oracle import sq_oracle as O
+from paper_2609_39056_amd import binding as B
+from paper_2609_39056_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+F32, BF16, F16 = B.SQ_OUT_F32, B.SQ_OUT_BF16, B.SQ_OUT_F16
+TORCH_OUT = {F32: torch.float32, BF16: torch.bfloat16, F16: torch.float16}
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+def split(M):
+    a = max(M // 6, 0)
+    p = max(M // 10, 0)
+    return (M - a - p, p, a)
+
+
+def layer(M, K, N, seed, T=3, permute=True, **kw):
+    return synth.make_layer(K=K, N=N, stream_counts=split(M), T=T, seed=seed, permute=permute, **kw)
+
+
+def xdev(L, rows=None):
+    xb = L.x_bits if rows is None else L.x_bits[rows]
+    return u16_to_dev(xb, torch.bfloat16)
+
+
+# ------------------------------------------------------------------ first kernel
+@pytest.mark.parametrize("bits,mode", [(8, 0), (8, 1), (4, 0), (4, 1)])
+@pytest.mark.parametrize("K,M", [(128, 5), (256, 88), (2048, 67), (5120, 33), (8192, 40), (13824, 9)])
+def test_quantize_bitexact(bits, mode, K, M):
+    L = layer(M, K, 64, seed=[1, K, M])
+    x = xdev(L)
+    for step in (0, 2):
+        for use_dinv in (True, False):
+            act = act_params(L, step, bits, mode, use_dinv=use_dinv)
+            qx, sc = B.act_buffers(M, K, bits)
+            B.sq_quantize_act(x, act, qx, sc)
+            ref = O.quantize_act(L.x_bits, L.tok2stream, L.gamma, step, dinv=L.dinv if use_dinv else None,
+                                 clip=L.clip, range_mode=mode, act_bits=bits)
+            assert np.array_equal(qx.cpu().numpy().view(np.uint8), ref["qx"].view(np.uint8))
+            if bits == 8:
+                assert np.array_equal(sc.cpu().numpy().view(np.uint32), ref["scale"].view(np.uint32))
+            else:
+                assert np.array_equal(bits16(sc), ref["scale"])
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_quantize_degenerate_rows(bits):
+    """All-zero rows, a single non-zero element, bf16 subnormal magnitudes (the
+    step underflows into fp32 subnormals and its reciprocal overflows), huge
+    values, and STATIC thresholds below every element."""
+    K = 256
+    rows = []
+    rows.append(np.zeros(K))
+    r = np.zeros(K); r[17] = -3.5; rows.append(r)
+    rows.append(np.full(K, 2.0**-130) * np.sign(np.arange(K) - 100.5))
+    rows.append(np.linspace(-1e30, 1e30, K))
+    rows.append(np.random.default_rng(0).standard_normal(K) * 1e-3)
+    x = np.stack(rows).astype(np.float32)
+    xb = O.f32_to_bf16_bits(x)
+    M = xb.shape[0]
+    t2s = np.array([0, 1, 2, 0, 1], np.int32)
+    gamma = np.array([[1.0, 0.5, 3.0], [1.25, 1.0, 0.75]], np.float32)
+    clip = np.array([1e-6, 2.0], np.float32)
+    for mode in (0, 1):
+        for step in (0, 1):
+            act = B.ActParams(tok2stream=i32_to_dev(t2s), gamma=f32_to_dev(gamma), step=step, act_bits=bits,
+                              range_mode=mode, clip=f32_to_dev(clip), dinv=None)
+            qx, sc = B.act_buffers(M, K, bits)
+            B.sq_quantize_act(u16_to_dev(xb, torch.bfloat16), act, qx, sc)
+            ref = O.quantize_act(xb, t2s, gamma, step, clip=clip, range_mode=mode, act_bits=bits)
+            assert np.array_equal(qx.cpu().numpy().view(np.uint8), ref["qx"].view(np.uint8)), (mode, step)
+            if bits == 8:
+                assert np.array_equal(sc.cpu().numpy().view(np.uint32), ref["scale"].view(np.uint32))
+            else:
+                assert np.array_equal(bits16(sc), ref["scale"])
+
+
+# ------------------------------------------------------------------ weight preparation
+@pytest.mark.parametrize("K,N,G", [(256, 256, 128), (256, 256, 256), (2048, 512, 128), (5120, 192, 128),
+                                   (13824, 64, 13824), (384, 64, 384)])
+def test_pack_weights_bitexact(K, N, G):
+    L = layer(16, K, N, seed=[2, K, N])
+    for use_d in (True, False):
+        d = L.d if use_d else None
+        ref = O.pack_weights(L.w, d, G)
+        W = B.prepare_weight(f32_to_dev(L.w), f32_to_dev(L.d) if use_d else None, G)
+        assert np.array_equal(W.qw.cpu().numpy(), ref["qw"])
+        assert np.array_equal(bits16(W.w_scale), ref["w_scale"])
+
+
+# ------------------------------------------------------------------ int32 accumulators
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("M,K,N,G", [(88, 256, 256, 128), (1, 256, 64, 128), (63, 384, 192, 128),
+                                     (130, 512, 320, 256), (200, 1024, 128, 1024), (257, 2048, 256, 128)])
+def test_block_acc_bitexact(bits, M, K, N, G):
+    """The fused main loop's int32 block accumulators, on random codes over the
+    full two's-complement ranges (including -128 and -8)."""
+    rng = np.random.default_rng([3, M, K, N, G, bits])
+    if bits == 8:
+        cx = rng.integers(-128, 128, size=(M, K)).astype(np.int8)
+        qx = torch.from_numpy(cx).cuda()
+    else:
+        cx = rng.integers(-8, 8, size=(M, K)).astype(np.int8)
+        qx = u8_to_dev(O.pack_int4(cx))
+    cw = rng.integers(-8, 8, size=(N, K)).astype(np.int8)
+    W = B.Weight(qw=u8_to_dev(O.pack_int4(cw)), w_scale=torch.ones((N, K // G), dtype=torch.float16, device="cuda"),
+                 w_group=G)
+    blk = G if bits == 8 else 64
+    acc = torch.full((K // blk, M, N), 0x7EADBEEF, dtype=torch.int32, device="cuda")
+    B.sq_debug_block_acc_i32(qx, bits, W, acc)
+    ref = O.block_acc(cx, cw, blk)
+    assert np.array_equal(acc.cpu().numpy().astype(np.int64), ref)
+
+
+# ------------------------------------------------------------------ whole linear
+def run_linear(fn, L, act, W, out, M=None, rows=None):
+    M = L.M if M is None else M
+    variant = B.SQ_VARIANT_UNFUSED if fn is B.sq_linear_unfused else B.SQ_VARIANT_FUSED
+    ws = B.alloc_workspace(variant, M, W.K, W.N, act.act_bits)
+    y = torch.full((M, W.N), float("nan"), dtype=TORCH_OUT[out], device="cuda")
+    fn(xdev(L, rows), act, W, y, out, ws)
+    return y, ws
+
+
+def oracle_linear(L, step, bits, mode, pw, G, with_bias=True, rows=None):
+    xb = L.x_bits if rows is None else L.x_bits[rows]
+    t2s = L.tok2stream if rows is None else L.tok2stream[rows]
+    return O.linear(xb, t2s, L.gamma, step, pw["codes"], pw["w_scale"], G, dinv=L.dinv, clip=L.clip,
+                    bias_bits=L.bias_bits if with_bias else None, range_mode=mode, act_bits=bits)
+
+
+FUSED = {8: B.sq_linear_w4a8, 4: B.sq_linear_w4a4}
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("mode", [0, 1])
+@pytest.mark.parametrize("out", [F32, BF16, F16])
+@pytest.mark.parametrize("G", [128, 256])
+def test_linear_cfg1(bits, mode, out, G):
+    """The 88-token 256 x 256 layer (64 video, 8 proprio, 16 action tokens,
+    2 denoising steps), fused and unfused."""
+    L = synth.make_layer(K=256, N=256, stream_counts=(64, 8, 16), T=2, seed=0)
+    pw, W = oracle_weight(L, G)
+    for step in (0, 1):
+        act = act_params(L, step, bits, mode)
+        res = oracle_linear(L, step, bits, mode, pw, G)
+        for fn in (FUSED[bits], B.sq_linear_unfused):
+            y, ws = run_linear(fn, L, act, W, out)
+            check_output(y, res, out)
+            if fn is not B.sq_linear_unfused:  # the workspace holds Q_X first
+                n = L.M * L.K if bits == 8 else L.M * L.K // 2
+                assert np.array_equal(ws[:n].cpu().numpy(), res["qx"].reshape(-1).view(np.uint8))
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("M,K,N,G,bias", [(1, 256, 64, 128, True), (63, 384, 192, 384, True),
+                                          (130, 2048, 320, 128, False), (200, 1024, 128, 1024, True),
+                                          (97, 13824, 64, 128, True)])
+def test_linear_shapes(bits, M, K, N, G, bias):
+    """Ragged M and N tiles, a weight step per output channel (G = K, the
+    paper's granularity), no bias, the largest K."""
+    L = layer(M, K, N, seed=[4, M, K, N])
+    pw, W = oracle_weight(L, G, with_bias=bias)
+    act = act_params(L, 1, bits, 0)
+    res = oracle_linear(L, 1, bits, 0, pw, G, with_bias=bias)
+    for fn in (FUSED[bits], B.sq_linear_unfused):
+        y, _ = run_linear(fn, L, act, W, F32)
+        check_output(y, res, F32)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_gemm_entry_points(bits):
+    """The second kernel alone, fed the oracle's codes and scales."""
+    L = layer(150, 512, 192, seed=5)
+    pw, W = oracle_weight(L, 128)
+    res = oracle_linear(L, 2, bits, 0, pw, 128)
+    y = torch.empty((L.M, L.N), dtype=torch.float32, device="cuda")
+    if bits == 8:
+        B.sq_gemm_w4a8(torch.from_numpy(res["qx"]).cuda(), f32_to_dev(res["scale"]), W, y, F32)
+    else:
+        B.sq_gemm_w4a4(u8_to_dev(res["qx"]), u16_to_dev(res["scale"], torch.float16), act_params(L, 2, 4, 0), W,
+                       y, F32)
+    check_output(y, res, F32)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_gpu_prepared_weights_chain(bits):
+    """Weights folded and packed on the GPU (sq_pack_weights), then the fused
+    linear: equals the oracle's chain from the fp32 weight."""
+    L = layer(100, 1024, 256, seed=6)
+    W = B.prepare_weight(f32_to_dev(L.w), f32_to_dev(L.d), 128, bias=u16_to_dev(L.bias_bits, torch.bfloat16))
+    pw = O.pack_weights(L.w, L.d, 128)
+    act = act_params(L, 0, bits, 0)
+    y, _ = run_linear(FUSED[bits], L, act, W, BF16)
+    check_output(y, oracle_linear(L, 0, bits, 0, pw, 128), BF16)
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_deterministic(bits):
+    L = layer(300, 2048, 512, seed=7)
+    _, W = oracle_weight(L, 128)
+    act = act_params(L, 1, bits, 0)
+    y1, _ = run_linear(FUSED[bits], L, act, W, F32)
+    y2, _ = run_linear(FUSED[bits], L, act, W, F32)
+    assert torch.equal(y1.view(torch.int32), y2.view(torch.int32))
+
+
+# ------------------------------------------------------------------ full-size layers, sampled rows
+FULL = [
+    ("2B up W4A8", 8, synth.TOKENS_2B, 2048, 8192, 0.02),
+    ("2B down W4A8", 8, synth.TOKENS_2B, 8192, 2048, 0.02),
+    ("2B qkv W4A4", 4, synth.TOKENS_2B, 2048, 6144, (0.01, 0.02, 0.05)),
+    ("2B down W4A4", 4, synth.TOKENS_2B, 8192, 2048, (0.01, 0.02, 0.05)),
+    ("14B out W4A8", 8, synth.TOKENS_14B, 5120, 5120, 0.02),
+]
+
+
+@pytest.mark.parametrize("name,bits,tokens,K,N,outl", FULL, ids=[f[0] for f in FULL])
+def test_full_size_sampled_rows(name, bits, tokens, K, N, outl):
+    """Full-size layers in the launch configuration the benchmark times; the
+    oracle checks every proprio / action row and 256 random video rows."""
+    L = synth.make_layer(K=K, N=N, stream_counts=tokens, T=10, seed=[8, K, N], outlier_frac=outl)
+    pw, W = oracle_weight(L, 128)
+    step = 7
+    act = act_params(L, step, bits, 0)
+    y, ws = run_linear(FUSED[bits], L, act, W, BF16)
+    rows = synth.stratified_rows(L.tok2stream, 256, seed=0)
+    res = oracle_linear(L, step, bits, 0, pw, 128, rows=rows)
+    check_output(y, res, BF16, rows=rows)
+    # codes of the sampled rows, read back from the workspace
+    rb = L.K if bits == 8 else L.K // 2
+    q = ws[: L.M * rb].view(L.M, rb)[torch.as_tensor(rows, device="cuda")]
+    assert np.array_equal(q.cpu().numpy(), res["qx"].view(np.uint8).reshape(len(rows), rb))
