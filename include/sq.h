@@ -99,7 +99,8 @@ typedef struct sq_act_params {
 /* A prepared weight: Q(D W) with fp16 steps (Sec. 4.2, fold then pack). */
 typedef struct sq_weight {
   const uint8_t* qw;        /* [N][K/2] packed int4 codes (layout above) */
-  const uint16_t* w_scale;  /* [N][K/w_group] fp16 steps Delta_W */
+  const uint16_t* w_scale;  /* [K/w_group][N] fp16 steps Delta_W, group-major: the steps of
+                               one input-channel group are contiguous over output channels */
   const uint16_t* bias;     /* [N] bf16 bias b, or NULL */
   int32_t N, K;
   int32_t w_group;          /* 128, or K (one step per output channel, as in the paper) */
@@ -118,7 +119,7 @@ size_t sq_workspace_bytes(int32_t variant, int32_t M, int32_t K, int32_t N, int3
  *   w        [N][K] fp32, the transposed weight W^T
  *   d        [K] fp32 positive channel scaling D, or NULL for D = I
  *   qw       out [N][K/2] packed int4 codes in [-7, 7]
- *   w_scale  out [N][K/w_group] fp16 steps
+ *   w_scale  out [K/w_group][N] fp16 steps (group-major)
  * Per (row j, group): w' = w * d[k]; Delta_W = fp16(amax|w'| / 7);
  * inv = 1 / fp32(Delta_W) (0 where infinite); code = rint(clamp(w' * inv, -7, 7)).
  * Requires amax / 7 <= 65504 in every group. */

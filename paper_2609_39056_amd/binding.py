@@ -144,7 +144,7 @@ class Weight:
     """A prepared int4 weight on the device."""
 
     qw: torch.Tensor                   # uint8 [N, K/2]
-    w_scale: torch.Tensor              # fp16 [N, K/w_group] (or int16 bit patterns)
+    w_scale: torch.Tensor              # fp16 [K/w_group, N], group-major
     w_group: int
     bias: Optional[torch.Tensor] = None  # bf16 [N]
 
@@ -236,7 +236,7 @@ def prepare_weight(w: torch.Tensor, d: Optional[torch.Tensor], w_group: int,
     """Fold, quantize and pack a device fp32 weight [N, K] with sq_pack_weights."""
     N, K = w.shape
     qw = torch.empty((N, K // 2), dtype=torch.uint8, device=w.device)
-    ws = torch.empty((N, K // w_group), dtype=torch.float16, device=w.device)
+    ws = torch.empty((K // w_group, N), dtype=torch.float16, device=w.device)
     sq_pack_weights(w, d, w_group, qw, ws, stream)
     return Weight(qw=qw, w_scale=ws, w_group=w_group, bias=bias)
 

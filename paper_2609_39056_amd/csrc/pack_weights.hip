@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(PackArgs a) {
     }
     *reinterpret_cast<uint32_t*>(qr + c * 4) = word;
   }
-  if (lane == 0) a.w_scale[static_cast<size_t>(j) * ng + b] = static_cast<uint16_t>(sbits);
+  if (lane == 0) a.w_scale[static_cast<size_t>(b) * a.N + j] = static_cast<uint16_t>(sbits);  // group-major
 }
 
 }  // namespace

@@ -143,6 +143,7 @@ __global__ __launch_bounds__(256) void u5_dequant_kernel(UnfusedArgs a) {
     const float dx = static_cast<const float*>(a.qscale)[row];
     float v;
     if (int_c) {
+      // one weight group spanning K: the group-major steps are w_scale[col]
       v = (static_cast<float>(static_cast<const int32_t*>(a.gemm_out)[i]) * dx) * f16_to_f32(a.w_scale[col]);
     } else {
       v = static_cast<const float*>(a.gemm_out)[i] * dx;

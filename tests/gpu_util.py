@@ -41,7 +41,8 @@ def act_params(L, step, act_bits=8, range_mode=B.SQ_RANGE_DYNAMIC, use_dinv=True
 def oracle_weight(L, w_group, with_bias=True):
     """Weights prepared by the oracle, as device tensors (inputs to the HIP path)."""
     pw = O.pack_weights(L.w, L.d, w_group)
-    dev = B.Weight(qw=u8_to_dev(pw["qw"]), w_scale=u16_to_dev(pw["w_scale"], torch.float16),
+    # the C ABI stores weight steps group-major: [K/w_group][N]
+    dev = B.Weight(qw=u8_to_dev(pw["qw"]), w_scale=u16_to_dev(pw["w_scale"].T, torch.float16),
                    w_group=w_group,
                    bias=u16_to_dev(L.bias_bits, torch.bfloat16) if with_bias else None)
     return pw, dev

@@ -104,7 +104,7 @@ def test_pack_weights_bitexact(K, N, G):
         ref = O.pack_weights(L.w, d, G)
         W = B.prepare_weight(f32_to_dev(L.w), f32_to_dev(L.d) if use_d else None, G)
         assert np.array_equal(W.qw.cpu().numpy(), ref["qw"])
-        assert np.array_equal(bits16(W.w_scale), ref["w_scale"])
+        assert np.array_equal(bits16(W.w_scale), ref["w_scale"].T)  # group-major
 
 
 # ------------------------------------------------------------------ int32 accumulators
@@ -122,7 +122,7 @@ def test_block_acc_bitexact(bits, M, K, N, G):
         cx = rng.integers(-8, 8, size=(M, K)).astype(np.int8)
         qx = u8_to_dev(O.pack_int4(cx))
     cw = rng.integers(-8, 8, size=(N, K)).astype(np.int8)
-    W = B.Weight(qw=u8_to_dev(O.pack_int4(cw)), w_scale=torch.ones((N, K // G), dtype=torch.float16, device="cuda"),
+    W = B.Weight(qw=u8_to_dev(O.pack_int4(cw)), w_scale=torch.ones((K // G, N), dtype=torch.float16, device="cuda"),
                  w_group=G)
     blk = G if bits == 8 else 64
     acc = torch.full((K // blk, M, N), 0x7EADBEEF, dtype=torch.int32, device="cuda")
