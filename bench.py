@@ -17,8 +17,10 @@ bounded row sample.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -30,6 +32,9 @@ if ROOT not in sys.path:
 
 PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
+COPY_MIB = 512               # plain device copy run after the timed region (counter calibration)
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_w4a8_2B_mlp_M4192_hbm_traffic.md")
+GEMM_SOURCES = ("paper_2609_39056_amd/csrc/gemm_w4.hip", "paper_2609_39056_amd/csrc/sq_internal.h")
 TOKENS = (4096, 32, 64)
 LINEARS = (("up", 2048, 8192), ("down", 8192, 2048))
 T_STEPS = 10
@@ -42,7 +47,8 @@ def parse():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    p.add_argument("--cpu-rows", type=int, default=1536, help="rows of each layer the oracle times")
+    p.add_argument("--cpu-rows", type=int, default=0,
+                   help="rows of each layer the oracle times (0 = all: one whole step)")
     return p.parse_args()
 
 
@@ -62,6 +68,29 @@ def make_layers(torch, B, synth, dev):
     return layers
 
 
+def gemm_source_sha256():
+    h = hashlib.sha256()
+    for rel in GEMM_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per GEMM launch from the committed counter summary, or None
+    when there is none or it was taken on a different GEMM source."""
+    try:
+        with open(TRAFFIC_SUMMARY) as f:
+            text = f.read()
+    except OSError:
+        return None
+    sha = re.search(r"^source_sha256:\s*([0-9a-f]{64})\s*$", text, re.M)
+    val = re.search(r"^traffic_bytes_per_launch:\s*([0-9]+)\s*$", text, re.M)
+    if not sha or not val or sha.group(1) != gemm_source_sha256():
+        return None
+    return int(val.group(1))
+
+
 def cpu_baseline(layers, rows_per_layer):
     """The oracle, as it stands, on a row sample of each layer (all the same
     arithmetic per row as the full layer); throughput scaled to TOPS."""
@@ -71,14 +100,15 @@ def cpu_baseline(layers, rows_per_layer):
     prepared = []
     for ly in layers:  # offline weight preparation: not part of the timed sample
         L = ly["L"]
+        n = L.M if rows_per_layer <= 0 else min(rows_per_layer, L.M)
         prepared.append((L, O.pack_weights(L.w, L.d, W_GROUP),
-                         np.sort(rng.choice(L.M, size=rows_per_layer, replace=False))))
+                         np.sort(rng.choice(L.M, size=n, replace=False))))
     ops = 0
     t0 = time.perf_counter()
     for L, pw, rows in prepared:
         O.linear(L.x_bits[rows], L.tok2stream[rows], L.gamma, 3, pw["codes"], pw["w_scale"], W_GROUP,
                  dinv=L.dinv, bias_bits=L.bias_bits, act_bits=8)
-        ops += 2 * rows_per_layer * L.K * L.N
+        ops += 2 * len(rows) * L.K * L.N
     dt = time.perf_counter() - t0
     try:
         cores = len(os.sched_getaffinity(0))
@@ -87,16 +117,16 @@ def cpu_baseline(layers, rows_per_layer):
     threads = int(os.environ.get("OMP_NUM_THREADS", cores))
     return dict(value=ops / dt / 1e12, unit="TOPS", cores=min(cores, threads), kind="oracle",
                 seconds=round(dt, 3),
-                sample=f"{rows_per_layer} random rows of each of the up (2048->8192) and down (8192->2048) "
-                       f"W4A8 layers (quantize, exact block accumulation, fp32 epilogue); weights packed "
-                       f"beforehand; TOPS = 2*rows*K*N / time")
+                sample=f"{len(prepared[0][2])} of {prepared[0][0].M} rows of each of the up (2048->8192) and "
+                       f"down (8192->2048) W4A8 layers, one step at tau=3 (quantize, exact block "
+                       f"accumulation, fp32 epilogue); weights packed beforehand; TOPS = 2*rows*K*N / time")
 
 
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              f"(the layer is row-parallel; see DESIGN.md for how it would shard)", file=sys.stderr)
+              f"(the layer is row-parallel: each GPU would take its own slice of the tokens)", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -202,6 +232,19 @@ def main():
     ms_w4a4 = time_variant(B.sq_linear_w4a4, 4, "ws_fused", vsteps)
     ms_w4a8_api = time_variant(B.sq_linear_w4a8, 8, "ws_fused", vsteps)
 
+    # ---- a plain device copy of known size: the reference for the HBM byte
+    # counters (FETCH_SIZE / WRITE_SIZE) of the profiled GEMM launches
+    src = torch.empty(COPY_MIB << 20, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    copy_us = c0.elapsed_time(c1) * 1e3
+    del src, dst
+
     out = {
         "metric": "fused W4A8/W4A4 linear TOPS + % int8-MFMA (or HBM) roofline per layer",
         "value": round(value, 2),
@@ -225,7 +268,7 @@ def main():
         "roofline": {
             "bound": "mfma", "kernel": "gemm_w4_kernel<8,0> (sq_gemm_w4a8)",
             "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",
-            "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": None,
+            "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": measured_traffic(),
         },
         "per_layer": per_layer,
         "quant_kernel_gbs": round(k1_gbs, 1),
@@ -235,6 +278,8 @@ def main():
         "fused_w4a8_api": {"ms_per_step": round(ms_w4a8_api, 5)},
         "fused_w4a4": {"ms_per_step": round(ms_w4a4, 5),
                        "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2)},
+        "hbm_copy": {"bytes": 2 * (COPY_MIB << 20), "us": round(copy_us, 1),
+                     "gbs": round(2 * (COPY_MIB << 20) / (copy_us * 1e-6) / 1e9, 1)},
     }
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(layers, args.cpu_rows)

@@ -21,7 +21,7 @@ What is computed, following the paper:
   applies Eq. (10): Y = cast[(FP32(C_ij) r_i) Delta_W,j + b_j].
 * Effective ranges, App. C.1: stream s sees threshold c / gamma_s.
 
-Readings where the paper leaves a choice (each is listed in the design doc):
+Readings where the paper leaves a choice:
 
 * Two range modes.  STATIC: c is the per-step table value c_tau (the paper's
   static activation scale, App. D).  DYNAMIC: c is the absolute maximum of
