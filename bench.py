@@ -150,6 +150,7 @@ def main():
         ly["y"] = torch.empty((M, ly["N"]), dtype=torch.bfloat16, device=dev)
         ly["ws_unf"] = {b: B.alloc_workspace(B.SQ_VARIANT_UNFUSED, M, ly["K"], ly["N"], b, dev) for b in (8, 4)}
         ly["ws_fused"] = {b: B.alloc_workspace(B.SQ_VARIANT_FUSED, M, ly["K"], ly["N"], b, dev) for b in (8, 4)}
+        ly["ws_gemm"] = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, ly["K"], ly["N"], 8, dev)
 
     def fused_step(tau, events=None):
         for i, ly in enumerate(layers):
@@ -160,7 +161,8 @@ def main():
             B.sq_quantize_act(ly["x"], act, ly["qx8"], ly["r8"], stream)
             if events is not None:
                 events[2 * i + 1].record(stream)
-            B.sq_gemm_w4a8(ly["qx8"], ly["r8"], ly["W"], ly["y"], B.SQ_OUT_BF16, stream)
+            B.sq_gemm_w4a8(ly["qx8"], ly["r8"], ly["W"], ly["y"], B.SQ_OUT_BF16, workspace=ly["ws_gemm"],
+                           stream=stream)
         if events is not None:
             events[4].record(stream)
 

@@ -80,7 +80,11 @@ typedef enum {
 
 typedef enum { SQ_OUT_F32 = 0, SQ_OUT_BF16 = 1, SQ_OUT_F16 = 2 } sq_out_dtype;
 
-typedef enum { SQ_VARIANT_FUSED = 0, SQ_VARIANT_UNFUSED = 1 } sq_variant;
+typedef enum {
+  SQ_VARIANT_FUSED = 0,   /* sq_linear_w4a8 / sq_linear_w4a4 */
+  SQ_VARIANT_UNFUSED = 1, /* sq_linear_unfused */
+  SQ_VARIANT_GEMM = 2     /* sq_gemm_w4a8 / sq_gemm_w4a4 (optional workspace) */
+} sq_variant;
 
 /* Per-layer activation-side parameters (Sec. 4.3: gains and threshold stored
  * in a layer-step lookup table; Sec. 4.2: one channel scaling per layer). */
@@ -110,8 +114,15 @@ typedef struct sq_weight {
 const char* sq_status_string(int32_t status);
 
 /* Bytes of device workspace that sq_linear_w4a8 / sq_linear_w4a4
- * (variant SQ_VARIANT_FUSED) or sq_linear_unfused (SQ_VARIANT_UNFUSED) need
- * for this shape; 0 for invalid arguments.  Host-only. */
+ * (variant SQ_VARIANT_FUSED), sq_linear_unfused (SQ_VARIANT_UNFUSED) or
+ * sq_gemm_w4a8 / sq_gemm_w4a4 (SQ_VARIANT_GEMM) use for this shape on the
+ * current device (at least 256); 0 for invalid arguments.  Host-only.
+ *
+ * The GEMM part of a workspace holds fp32 partial sums: when the output tiles
+ * do not fill whole rounds of the device's workgroup slots, the tiles left
+ * over are split along K over the idle slots and a second kernel adds the
+ * partial sums (in a fixed order: results are deterministic).  Its contents
+ * need no initialization and are garbage after a call. */
 size_t sq_workspace_bytes(int32_t variant, int32_t M, int32_t K, int32_t N, int32_t act_bits);
 
 /* Offline weight preparation (Sec. 4.2: fold D* into W, quantize to int4 with
@@ -138,21 +149,26 @@ sq_status sq_quantize_act(const uint16_t* x, int32_t M, int32_t K, const sq_act_
  * accumulator per K-block of w_group): C^b = Q_X Q_W over the block, then
  * Y_ij = r_i * sum_b fp32(C^b_ij) Delta_W[j][b] + b_j, cast to out_dtype.
  *   qx int8 [M][K], row_scale fp32 [M] (as written by sq_quantize_act),
- *   y  [M][N] of out_dtype. */
+ *   y  [M][N] of out_dtype.
+ *   workspace: NULL (every output tile is computed whole) or a device buffer
+ *   of ws_bytes (16-byte aligned; sq_workspace_bytes(SQ_VARIANT_GEMM, ...)
+ *   enables the split-K tail) that must not overlap the other buffers. */
 sq_status sq_gemm_w4a8(const int8_t* qx, const float* row_scale, int32_t M, const sq_weight* w,
-                       void* y, int32_t out_dtype, hipStream_t stream);
+                       void* y, int32_t out_dtype, void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /* The second kernel for 4-bit activations: one int32 accumulator per 64-wide
  * K-block, Y_ij = kappa_i * sum_b (fp32(C^b_ij) sigma_{i,b}) Delta_W[j][b(k)] + b_j
  * with kappa_i = 1 / gamma[tau][s(i)] (the inverse-gain compensation of Eq. 8,
  * taken from act->tok2stream, act->gamma and act->step).
- *   qx packed int4 [M][K/2], group_scale fp16 [M][K/64]. */
+ *   qx packed int4 [M][K/2], group_scale fp16 [M][K/64]; workspace as for
+ *   sq_gemm_w4a8. */
 sq_status sq_gemm_w4a4(const uint8_t* qx, const uint16_t* group_scale, int32_t M,
                        const sq_act_params* act, const sq_weight* w, void* y, int32_t out_dtype,
-                       hipStream_t stream);
+                       void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /* The fused linear with 8-bit activations: sq_quantize_act then sq_gemm_w4a8,
- * Q_X and r living in `workspace` (>= sq_workspace_bytes(SQ_VARIANT_FUSED, ...)).
+ * Q_X, r and the GEMM's partial sums living in `workspace`
+ * (>= sq_workspace_bytes(SQ_VARIANT_FUSED, ...)).
  * Requires act->act_bits == 8 and w->K == K of x. */
 sq_status sq_linear_w4a8(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                          void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,

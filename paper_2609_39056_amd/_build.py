@@ -4,6 +4,7 @@ from __future__ import annotations
 
 import concurrent.futures as cf
 import os
+import re
 import subprocess
 import sys
 
@@ -37,13 +38,31 @@ FLAGS = [
 SOURCES = ["sq_api.cpp", "quant_act.hip", "pack_weights.hip", "gemm_w4.hip", "unfused.hip"]
 
 
+_REMARK = re.compile(r"remark: Function Name: (\S+)|remark:\s+(ScratchSize \[bytes/lane\]|VGPRs Spill|SGPRs Spill): (\d+)")
+
+
+def _check_resources(src: str, stderr: str) -> None:
+    """Every kernel must keep its working set in registers and LDS: any
+    scratch (private memory) use or register spill fails the build."""
+    kernel, bad = None, []
+    for m in _REMARK.finditer(stderr):
+        if m.group(1):
+            kernel = m.group(1)
+        elif int(m.group(3)) != 0:
+            bad.append(f"{kernel}: {m.group(2)} = {m.group(3)}")
+    if bad:
+        raise RuntimeError(f"{src}: kernels use scratch memory or spill registers:\n  " + "\n  ".join(bad))
+
+
 def _compile(src: str) -> str:
     path = os.path.join(CSRC, src)
     obj = os.path.join(OBJDIR, os.path.splitext(src)[0] + ".o")
-    cmd = [HIPCC, *FLAGS, "-x", "hip", "-c", path, "-o", obj]
+    cmd = [HIPCC, *FLAGS, "-Rpass-analysis=kernel-resource-usage", "-x", "hip", "-c", path, "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed for {src}:\n{' '.join(cmd)}\n{r.stdout}\n{r.stderr}")
+    if src.endswith(".hip"):
+        _check_resources(src, r.stderr)
     return obj
 
 

@@ -25,6 +25,7 @@ SQ_OUT_BF16 = 1
 SQ_OUT_F16 = 2
 SQ_VARIANT_FUSED = 0
 SQ_VARIANT_UNFUSED = 1
+SQ_VARIANT_GEMM = 2
 A4_GROUP = 64
 
 OUT_DTYPES = {SQ_OUT_F32: torch.float32, SQ_OUT_BF16: torch.bfloat16, SQ_OUT_F16: torch.float16}
@@ -69,8 +70,9 @@ _SIGS = {
     "sq_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
     "sq_pack_weights": (_I, [_P, _P, _I, _I, _I, _P, _P, _P]),
     "sq_quantize_act": (_I, [_P, _I, _I, ctypes.POINTER(sq_act_params), _P, _P, _P]),
-    "sq_gemm_w4a8": (_I, [_P, _P, _I, ctypes.POINTER(sq_weight), _P, _I, _P]),
-    "sq_gemm_w4a4": (_I, [_P, _P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P]),
+    "sq_gemm_w4a8": (_I, [_P, _P, _I, ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
+    "sq_gemm_w4a4": (_I, [_P, _P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S,
+                          _P]),
     "sq_linear_w4a8": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_w4a4": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_unfused": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
@@ -179,20 +181,28 @@ def sq_quantize_act(x: torch.Tensor, act: ActParams, qx: torch.Tensor, act_scale
            "sq_quantize_act")
 
 
+def _ws(workspace: Optional[torch.Tensor]):
+    if workspace is None:
+        return None, 0
+    return _ptr(workspace), workspace.numel() * workspace.element_size()
+
+
 def sq_gemm_w4a8(qx: torch.Tensor, row_scale: torch.Tensor, w: Weight, y: torch.Tensor, out_dtype: int,
-                 stream=None) -> None:
+                 workspace: Optional[torch.Tensor] = None, stream=None) -> None:
     M = qx.shape[0]
     ws = w.struct()
-    _check(lib().sq_gemm_w4a8(_ptr(qx), _ptr(row_scale), M, ctypes.byref(ws), _ptr(y), out_dtype,
+    wp, wb = _ws(workspace)
+    _check(lib().sq_gemm_w4a8(_ptr(qx), _ptr(row_scale), M, ctypes.byref(ws), _ptr(y), out_dtype, wp, wb,
                               _stream(stream)), "sq_gemm_w4a8")
 
 
 def sq_gemm_w4a4(qx: torch.Tensor, group_scale: torch.Tensor, act: ActParams, w: Weight, y: torch.Tensor,
-                 out_dtype: int, stream=None) -> None:
+                 out_dtype: int, workspace: Optional[torch.Tensor] = None, stream=None) -> None:
     M = qx.shape[0]
     s, ws = act.struct(), w.struct()
+    wp, wb = _ws(workspace)
     _check(lib().sq_gemm_w4a4(_ptr(qx), _ptr(group_scale), M, ctypes.byref(s), ctypes.byref(ws), _ptr(y),
-                              out_dtype, _stream(stream)), "sq_gemm_w4a4")
+                              out_dtype, wp, wb, _stream(stream)), "sq_gemm_w4a4")
 
 
 def _linear(fn: str, x, act, w, y, out_dtype, workspace, stream):

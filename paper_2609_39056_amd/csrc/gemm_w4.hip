@@ -27,6 +27,8 @@
 // y += (fp32(C) * sigma_i) * Delta_W (4-bit).  The epilogue multiplies by r_i (8-bit) or by
 // kappa_i = 1/gamma_s(i) (4-bit, the compensation of Eq. 8), adds the bias and
 // casts.
+#include <algorithm>
+#include <atomic>
 #include <type_traits>
 
 #include "sq_internal.h"
@@ -71,15 +73,17 @@ __device__ __forceinline__ v4i unpack_frag(uint32_t p0, uint32_t p1) {
 }
 
 // Workgroup -> output tile.  Workgroups are dealt to the 8 XCDs round-robin;
-// renumber them so each XCD runs a contiguous range of logical tiles, then walk
-// the logical range in supertiles of GROUP_M m-tiles so that tiles running at
-// the same time on one XCD share activation rows and weight columns in its L2.
-__device__ __forceinline__ void tile_of(int ntm, int ntn, int& tm, int& tn) {
-  const int nblk = gridDim.x;
-  const int bid = blockIdx.x;
-  const int q = nblk / 8, r = nblk % 8;
+// xcd_order renumbers the first n of them so that each XCD runs a contiguous
+// range of logical tiles, and supertile walks the logical range in supertiles
+// of GROUP_M m-tiles, so that tiles running at the same time on one XCD share
+// activation rows and weight columns in its L2.
+__device__ __forceinline__ int xcd_order(int bid, int n) {
+  const int q = n / 8, r = n % 8;
   const int xcd = bid % 8, i = bid / 8;
-  const int lid = xcd * q + min(xcd, r) + i;
+  return xcd * q + min(xcd, r) + i;
+}
+
+__device__ __forceinline__ void supertile(int lid, int ntm, int ntn, int& tm, int& tn) {
   const int per_group = GROUP_M * ntn;
   const int group = lid / per_group;
   const int first_m = group * GROUP_M;
@@ -181,6 +185,88 @@ __device__ __forceinline__ void dump_block(const GemmArgs& a, const v16i (&acc)[
     }
 }
 
+// Epilogue of one 128 x 128 output tile: row factor, bias, cast, then store
+// through LDS so that every lane writes 16 contiguous bytes (whole 128-byte
+// lines).  Each wave stages 64 rows x 128 bytes (both 32-column tiles for
+// 16-bit outputs, one for fp32) in its own region of `smem` (>= 4 x 9 KB, not
+// in use by any wave of the workgroup).  Loads of bias and row factors come
+// before the stores (as far as the compiler knows the output may alias them).
+template <int ABITS, int EPI>
+__device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN][16], int m0, int n0, int wm,
+                                           int wn, int wave, int lane, uint8_t* smem) {
+  const int M = a.M, N = a.N;
+  constexpr int EP_PITCH = 144;  // bytes per staged row (16-byte aligned, spreads banks)
+  uint8_t* ep = smem + wave * 64 * EP_PITCH;
+  const bool cols_ok = n0 + wn * 64 < N;  // N % 64 == 0: a wave's 64 columns are all in or all out
+  float bcol[TN];
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    const int n = min(n0 + wn * 64 + tn * 32 + (lane & 31), N - 1);
+    bcol[tn] = (EPI == kEpiOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
+  }
+  const int esz = (EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32) ? 4 : 2;
+  const int npass = esz == 4 ? 2 : 1;  // fp32: one 32-column tile per pass
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    float rowf[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = min(m0 + wm * 64 + tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3), M - 1);
+      rowf[r] = 1.0f;
+      if constexpr (EPI == kEpiOut) {
+        if constexpr (ABITS == 8) {
+          rowf[r] = static_cast<const float*>(a.act_scale)[m];
+        } else {
+          rowf[r] = 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const float v = EPI == kEpiPartial ? y[tm][tn][r] : __builtin_fmaf(y[tm][tn][r], rowf[r], bcol[tn]);
+        y[tm][tn][r] = v;
+      }
+  }
+  // constant trip count: `pass` indexes y, which must stay in registers
+#pragma unroll
+  for (int pass = 0; pass < 2; ++pass) {
+    if (pass >= npass) break;
+    // stage: row (within the wave's 64) = tm*32 + (r>>2)*8 + (lane>>5)*4 + (r&3)
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        uint8_t* rp = ep + row * EP_PITCH;
+        if (esz == 4) {
+          reinterpret_cast<float*>(rp)[lane & 31] = y[tm][pass][r];
+        } else {
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn) {
+            const float v = y[tm][tn][r];
+            const uint32_t b = a.out_dtype == SQ_OUT_BF16 ? f32_to_bf16(v) : f32_to_f16(v);
+            reinterpret_cast<uint16_t*>(rp)[tn * 32 + (lane & 31)] = static_cast<uint16_t>(b);
+          }
+        }
+      }
+    // read back 16-byte chunks (8 rows of 128 bytes per instruction) and store
+    if (cols_ok) {
+      const size_t row_bytes = static_cast<size_t>(N) * esz;
+      uint8_t* gbase = static_cast<uint8_t*>(a.out) + static_cast<size_t>(n0 + wn * 64 + pass * 32) * esz;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int row = i * 8 + (lane >> 3);
+        const int m = m0 + wm * 64 + row;
+        const uint4 v = *reinterpret_cast<const uint4*>(ep + row * EP_PITCH + (lane & 7) * 16);
+        if (m < M) *reinterpret_cast<uint4*>(gbase + static_cast<size_t>(m) * row_bytes + (lane & 7) * 16) = v;
+      }
+    }
+  }
+}
+
+
 // ABITS: 8 or 4.  EPI: EpiMode.  W128: 8-bit activations with one weight step
 // per 128 input channels (one K-block per pipeline stage).
 // PIPE (full or partial epilogue, and either 4-bit activations or W128): the
@@ -207,11 +293,22 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
 
   const int ntm = (M + BM - 1) / BM;
   const int ntn = (N + BN - 1) / BN;
+  const int nkt = K / KT;
+  // whole tile, or one K range [kt_begin, kt_end) of a split tail tile
+  int lid, kt_begin = 0, kt_end = nkt, unit = -1;
+  if (static_cast<int>(blockIdx.x) < a.ndp) {
+    lid = xcd_order(blockIdx.x, a.ndp);
+  } else {
+    unit = blockIdx.x - a.ndp;
+    lid = a.ndp + unit / a.split;
+    const int sl = unit % a.split;
+    kt_begin = sl * nkt / a.split;
+    kt_end = (sl + 1) * nkt / a.split;
+  }
   int tile_m, tile_n;
-  tile_of(ntm, ntn, tile_m, tile_n);
+  supertile(lid, ntm, ntn, tile_m, tile_n);
   const int m0 = tile_m * BM;
   const int n0 = tile_n * BN;
-  const int nkt = K / KT;
   const uint8_t* qx = static_cast<const uint8_t*>(a.qx);
   const uint32_t smem_lds = lds_offset(smem);
 
@@ -254,14 +351,14 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
   // (c even; N is even, so the pair is clamped inside the row)
   const uint32_t wcol2 = static_cast<uint32_t>(min(n0 + wn * 64 + 2 * (lane & 31), N - 2));
 
-  // Loads stage kt into ring slot kt % STAGES.  Past the last stage the
-  // source is clamped to the last stage: the slot written is free (its stage
-  // was consumed before the previous barrier) and is never read again, and the
-  // loop body stays free of branches, so its MFMAs and VALU work can be
-  // interleaved.
+  // Loads stage kt into ring slot kt % STAGES.  Past the last stage of the
+  // range the source is clamped to that stage: the slot written is free (its
+  // stage was consumed before the previous barrier) and is never read again,
+  // and the loop body stays free of branches, so its MFMAs and VALU work can
+  // be interleaved.
   auto issue_stage = [&](int kt_slot) {
     const uint32_t st = smem_lds + (kt_slot % STAGES) * LY::STAGE;
-    const int kt = min(kt_slot, nkt - 1);
+    const int kt = min(kt_slot, kt_end - 1);
     const uint8_t* bA = baseA + kt * (ABITS == 8 ? KT : KT / 2);
     const uint8_t* bB = baseB + kt * (KT / 2);
 #pragma unroll
@@ -362,8 +459,8 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
     }
   };
 
-  issue_stage(0);
-  issue_stage(1);
+  issue_stage(kt_begin);
+  issue_stage(kt_begin + 1);
   wait_vm_and_barrier<NDMA>();
 
   if constexpr (PIPE && ABITS == 8) {
@@ -380,7 +477,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
       for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = 0.0f;
-    for (int kt = 0; kt < nkt; ++kt) {
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
       issue_stage(kt + 2);
       const uint8_t* st = smem + (kt % STAGES) * LY::STAGE;
       read_wscale(st, kt, wsv);
@@ -433,7 +530,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
       for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = 0.0f;
-    for (int kt = 0; kt < nkt; ++kt) {
+    for (int kt = kt_begin; kt < kt_end; ++kt) {
       issue_stage(kt + 2);
       const uint8_t* st = smem + (kt % STAGES) * LY::STAGE;
       const uint8_t* st_prev = smem + ((kt + STAGES - 1) % STAGES) * LY::STAGE;
@@ -454,7 +551,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
           const v4i af1 = unpack_frag(pa.z, pa.w);
           // previous block: second half of the previous stage, or first half of this one
           if (hb == 0) {
-            fold4(st_prev, 1, acc[tm], tm, wsv_prev, kt > 0);
+            fold4(st_prev, 1, acc[tm], tm, wsv_prev, kt > kt_begin);
           } else {
             fold4(st, 0, acc[tm], tm, wsv, true);
           }
@@ -470,7 +567,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
       wait_vm_and_barrier<NDMA>();
     }
     {
-      const uint8_t* st_last = smem + ((nkt - 1) % STAGES) * LY::STAGE;
+      const uint8_t* st_last = smem + ((kt_end - 1) % STAGES) * LY::STAGE;
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) fold4(st_last, 1, acc[tm], tm, wsv_prev, true);
     }
@@ -532,110 +629,167 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
   // reused (or the workgroup ends)
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   if constexpr (!NEED_SCALE) return;
-
-  // Epilogue: row factor, bias, cast, then store through LDS so that every
-  // lane writes 16 contiguous bytes (whole 128-byte lines).  Each wave stages
-  // 64 rows x 128 bytes (both 32-column tiles for 16-bit outputs, one for
-  // fp32) in its own LDS region; the ring is idle once every wave is past the
-  // barrier below.  Loads of bias and row factors come before the stores (as
-  // far as the compiler knows the output may alias them).
-  __syncthreads();
-  constexpr int EP_PITCH = 144;  // bytes per staged row (16-byte aligned, spreads banks)
-  uint8_t* ep = smem + wave * 64 * EP_PITCH;
-  const bool cols_ok = n0 + wn * 64 < N;  // N % 64 == 0: a wave's 64 columns are all in or all out
-  float bcol[TN];
+  if constexpr (PIPE) {
+    if (unit >= 0) {
+      // split tail: this K range's fp32 sums of the tile, row-major [BM][BN]
+      float* P = a.partial + static_cast<size_t>(unit) * BM * BN;
 #pragma unroll
-  for (int tn = 0; tn < TN; ++tn) {
-    const int n = min(n0 + wn * 64 + tn * 32 + (lane & 31), N - 1);
-    bcol[tn] = (EPI == kEpiOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
-  }
-  const int esz = (EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32) ? 4 : 2;
-  const int npass = esz == 4 ? 2 : 1;  // fp32: one 32-column tile per pass
+      for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm) {
-    float rowf[16];
+        for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = min(m0 + wm * 64 + tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3), M - 1);
-      rowf[r] = 1.0f;
-      if constexpr (EPI == kEpiOut) {
-        if constexpr (ABITS == 8) {
-          rowf[r] = static_cast<const float*>(a.act_scale)[m];
-        } else {
-          rowf[r] = 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
-        }
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < 16; ++r)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const float v = EPI == kEpiPartial ? y[tm][tn][r] : __builtin_fmaf(y[tm][tn][r], rowf[r], bcol[tn]);
-        y[tm][tn][r] = v;
-      }
-  }
-  for (int pass = 0; pass < npass; ++pass) {
-    // stage: row (within the wave's 64) = tm*32 + (r>>2)*8 + (lane>>5)*4 + (r&3)
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        uint8_t* rp = ep + row * EP_PITCH;
-        if (esz == 4) {
-          reinterpret_cast<float*>(rp)[lane & 31] = y[tm][pass][r];
-        } else {
-#pragma unroll
-          for (int tn = 0; tn < TN; ++tn) {
-            const float v = y[tm][tn][r];
-            const uint32_t b = a.out_dtype == SQ_OUT_BF16 ? f32_to_bf16(v) : f32_to_f16(v);
-            reinterpret_cast<uint16_t*>(rp)[tn * 32 + (lane & 31)] = static_cast<uint16_t>(b);
+          for (int r = 0; r < 16; ++r) {
+            const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+            P[row * BN + wn * 64 + tn * 32 + (lane & 31)] = y[tm][tn][r];
           }
-        }
-      }
-    // read back 16-byte chunks (8 rows of 128 bytes per instruction) and store
-    if (cols_ok) {
-      const size_t row_bytes = static_cast<size_t>(N) * esz;
-      uint8_t* gbase = static_cast<uint8_t*>(a.out) + static_cast<size_t>(n0 + wn * 64 + pass * 32) * esz;
-#pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int row = i * 8 + (lane >> 3);
-        const int m = m0 + wm * 64 + row;
-        const uint4 v = *reinterpret_cast<const uint4*>(ep + row * EP_PITCH + (lane & 7) * 16);
-        if (m < M) *reinterpret_cast<uint4*>(gbase + static_cast<size_t>(m) * row_bytes + (lane & 7) * 16) = v;
-      }
+      return;
     }
   }
+
+  __syncthreads();
+  store_tile<ABITS, EPI>(a, y, m0, n0, wm, wn, wave, lane, smem);
+}
+
+// Second kernel of a split tail: adds the `split` partial sums of every
+// output of the split tiles in range order (so the result does not depend on
+// which range finished first) and finishes it exactly as store_tile does
+// (one fma with the row factor and the bias, then the cast).  Four adjacent
+// outputs per thread, 16-byte loads.
+template <int ABITS, int EPI>
+__global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
+  constexpr int BM = Cfg<ABITS>::BM, BN = Cfg<ABITS>::BN;
+  constexpr int PER_TILE = BM * BN / 4;  // threads per tile
+  const int g = blockIdx.x * 256 + threadIdx.x;
+  const int ti = g / PER_TILE;
+  const int e = (g % PER_TILE) * 4;
+  const int row = e / BN, col = e % BN;
+  const int ntm = (a.M + BM - 1) / BM;
+  const int ntn = (a.N + BN - 1) / BN;
+  int tile_m, tile_n;
+  supertile(a.ndp + ti, ntm, ntn, tile_m, tile_n);
+  const int m = tile_m * BM + row;
+  const int n = tile_n * BN + col;
+  if (m >= a.M || n >= a.N) return;  // N % 64 == 0: the 4 columns are all in or all out
+  const float* P = a.partial + static_cast<size_t>(ti) * a.split * BM * BN + row * BN + col;
+  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll 8
+  for (int sl = 0; sl < a.split; ++sl) {
+    const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * BM * BN);
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  float y[4] = {acc.x, acc.y, acc.z, acc.w};
+  if constexpr (EPI == kEpiOut) {
+    const float rowf = ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
+                                  : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float b = a.bias != nullptr ? bf16_to_f32(a.bias[n + j]) : 0.0f;
+      y[j] = __builtin_fmaf(y[j], rowf, b);
+    }
+  }
+  if (EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32) {
+    *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * a.N + n) =
+        make_float4(y[0], y[1], y[2], y[3]);
+  } else {
+    uint32_t h[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) h[j] = a.out_dtype == SQ_OUT_BF16 ? f32_to_bf16(y[j]) : f32_to_f16(y[j]);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + static_cast<size_t>(m) * a.N + n) =
+        make_uint2(h[0] | (h[1] << 16), h[2] | (h[3] << 16));
+  }
+}
+
+// Workgroups that fit on the device at once (two per CU), capped at 512.
+int device_slots() {
+  static std::atomic<int> cache[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 512;
+  int v = cache[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
+    int cus = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 512;
+    v = std::min(2 * cus, 512);
+    cache[dev].store(v, std::memory_order_relaxed);
+  }
+  return v;
+}
+
+constexpr size_t kUnitBytes = 128 * 128 * sizeof(float);  // partial sums of one tile range
+
+// Split plan: the tiles that fill whole rounds of `slots` run whole; each of
+// the R left over is split into S >= 2 K ranges of >= 2 stages (S * R <=
+// slots / 2 when whole rounds run, <= slots otherwise), if `partial_bytes`
+// holds R * S units.  Only the pipelined paths split (their blocks never
+// straddle a range boundary).
+struct Plan {
+  int ntiles, ndp, split;
+};
+Plan plan_split(int act_bits, int epi, int32_t M, int32_t N, int32_t K, int32_t w_group, int slots,
+                size_t partial_bytes) {
+  const int ntiles = ((M + 127) / 128) * ((N + 127) / 128);
+  Plan p{ntiles, ntiles, 1};
+  const bool pipe = (epi == kEpiOut || epi == kEpiPartial) && (act_bits == 4 || w_group == KT);
+  const int nkt = K / KT;
+  const int rest = ntiles % slots;
+  if (!pipe || rest == 0 || nkt < 4) return p;
+  int split = std::min(nkt / 2, ntiles >= slots ? slots / rest / 2 : slots / rest);
+  while (split >= 2 && static_cast<size_t>(rest) * split * kUnitBytes > partial_bytes) --split;
+  if (split < 2) return p;
+  p.ndp = ntiles - rest;
+  p.split = split;
+  return p;
 }
 
 template <int ABITS, int EPI, bool W128>
-hipError_t launch_t(const GemmArgs& a, hipStream_t s) {
-  using CF = Cfg<ABITS>;
-  const unsigned grid = static_cast<unsigned>(((a.M + CF::BM - 1) / CF::BM) * ((a.N + CF::BN - 1) / CF::BN));
-  hipLaunchKernelGGL((gemm_w4_kernel<ABITS, EPI, W128>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
-  return hipGetLastError();
+hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
+  GemmArgs a = a0;
+  const Plan p = plan_split(ABITS, EPI, a.M, a.N, a.K, a.w_group, device_slots(), partial ? partial_bytes : 0);
+  a.ndp = p.ndp;
+  a.split = p.split;
+  a.partial = p.split > 1 ? partial : nullptr;
+  const int rest = p.ntiles - p.ndp;
+  const unsigned grid = static_cast<unsigned>(p.ndp + rest * p.split);
+  hipLaunchKernelGGL((gemm_w4_kernel<ABITS, EPI, W128>), dim3(grid), dim3(Cfg<ABITS>::NTHREADS), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || rest == 0 || p.split == 1) return e;
+  if constexpr (EPI == kEpiOut || EPI == kEpiPartial) {
+    constexpr int per_tile_blocks = Cfg<ABITS>::BM * Cfg<ABITS>::BN / 4 / 256;
+    hipLaunchKernelGGL((gemm_tail_kernel<ABITS, EPI>), dim3(rest * per_tile_blocks), dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+  return hipErrorInvalidValue;
 }
 
 template <int EPI>
-hipError_t launch_a8(const GemmArgs& a, hipStream_t s) {
-  return a.w_group == KT ? launch_t<8, EPI, true>(a, s) : launch_t<8, EPI, false>(a, s);
+hipError_t launch_a8(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
+  return a.w_group == KT ? launch_t<8, EPI, true>(a, s, partial, partial_bytes)
+                         : launch_t<8, EPI, false>(a, s, partial, partial_bytes);
 }
 
 }  // namespace
 
-hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s) {
+size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t w_group) {
+  const Plan p = plan_split(act_bits, kEpiOut, M, N, K, w_group, device_slots(), ~static_cast<size_t>(0));
+  return static_cast<size_t>(p.ntiles - p.ndp) * (p.split > 1 ? p.split : 0) * kUnitBytes;
+}
+
+hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
+                       size_t partial_bytes) {
   if (act_bits == 8) {
     switch (epi) {
-      case kEpiOut: return launch_a8<kEpiOut>(a, s);
-      case kEpiPartial: return launch_a8<kEpiPartial>(a, s);
-      case kEpiInt32: return launch_t<8, kEpiInt32, false>(a, s);
-      case kEpiDump: return launch_t<8, kEpiDump, false>(a, s);
+      case kEpiOut: return launch_a8<kEpiOut>(a, s, partial, partial_bytes);
+      case kEpiPartial: return launch_a8<kEpiPartial>(a, s, partial, partial_bytes);
+      case kEpiInt32: return launch_t<8, kEpiInt32, false>(a, s, nullptr, 0);
+      case kEpiDump: return launch_t<8, kEpiDump, false>(a, s, nullptr, 0);
     }
   } else {
     switch (epi) {
-      case kEpiOut: return launch_t<4, kEpiOut, false>(a, s);
-      case kEpiPartial: return launch_t<4, kEpiPartial, false>(a, s);
-      case kEpiDump: return launch_t<4, kEpiDump, false>(a, s);
+      case kEpiOut: return launch_t<4, kEpiOut, false>(a, s, partial, partial_bytes);
+      case kEpiPartial: return launch_t<4, kEpiPartial, false>(a, s, partial, partial_bytes);
+      case kEpiDump: return launch_t<4, kEpiDump, false>(a, s, nullptr, 0);
     }
   }
   return hipErrorInvalidValue;

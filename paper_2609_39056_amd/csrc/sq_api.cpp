@@ -2,6 +2,8 @@
 // layout and kernel dispatch.  Nothing here allocates, frees or synchronizes.
 #include <stdint.h>
 
+#include <algorithm>
+
 #include "sq_internal.h"
 
 using namespace sq;
@@ -54,20 +56,32 @@ size_t act_scale_bytes(int32_t M, int32_t K, int32_t bits) {
   return bits == 8 ? static_cast<size_t>(M) * 4 : static_cast<size_t>(M) * (K / kA4Group) * 2;
 }
 
+// Split-K partial sums of the GEMM: sized for the plan with 128-wide weight
+// groups (the only 8-bit case that splits), an upper bound for every w_group.
+size_t gemm_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
+  return std::max<size_t>(kAlign, round_up(gemm_partial_bytes(bits, M, N, K, kKTile)));
+}
+
+// fused workspace: Q_X | scales | GEMM partial sums (each 256-byte aligned)
 struct FusedWs {
   void* qx;
   void* scale;
+  float* partial;
+  size_t partial_bytes;
 };
-FusedWs fused_ws(void* ws, int32_t M, int32_t K, int32_t bits) {
+FusedWs fused_ws(void* ws, size_t ws_bytes, int32_t M, int32_t K, int32_t bits) {
   uint8_t* p = static_cast<uint8_t*>(ws);
   FusedWs f;
   f.qx = p;
   f.scale = p + round_up(qx_bytes(M, K, bits));
+  const size_t off = round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits));
+  f.partial = reinterpret_cast<float*>(p + off);
+  f.partial_bytes = ws_bytes - off;
   return f;
 }
 
-size_t fused_ws_bytes(int32_t M, int32_t K, int32_t bits) {
-  return round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits));
+size_t fused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
+  return round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits)) + gemm_ws_bytes(M, K, N, bits);
 }
 
 size_t unfused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
@@ -131,11 +145,12 @@ sq_status linear_fused(int32_t bits, const uint16_t* x, int32_t M, const sq_act_
   if (!valid_m(M)) return SQ_ERR_SHAPE;
   if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
   if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 16)) return SQ_ERR_ALIGN;
-  if (ws_bytes < fused_ws_bytes(M, w->K, bits)) return SQ_ERR_WORKSPACE;
-  FusedWs f = fused_ws(ws, M, w->K, bits);
+  if (ws_bytes < fused_ws_bytes(M, w->K, w->N, bits)) return SQ_ERR_WORKSPACE;
+  FusedWs f = fused_ws(ws, ws_bytes, M, w->K, bits);
   st = quantize(x, M, w->K, act, f.qx, f.scale, stream);
   if (st != SQ_OK) return st;
-  return hip_status(launch_gemm(bits, kEpiOut, gemm_args(f.qx, f.scale, M, act, w, y, out_dtype), stream));
+  return hip_status(launch_gemm(bits, kEpiOut, gemm_args(f.qx, f.scale, M, act, w, y, out_dtype), stream,
+                                f.partial, f.partial_bytes));
 }
 
 }  // namespace
@@ -157,8 +172,9 @@ const char* sq_status_string(int32_t status) {
 
 size_t sq_workspace_bytes(int32_t variant, int32_t M, int32_t K, int32_t N, int32_t act_bits) {
   if (!valid_m(M) || !valid_k(K) || !valid_n(N) || (act_bits != 8 && act_bits != 4)) return 0;
-  if (variant == SQ_VARIANT_FUSED) return fused_ws_bytes(M, K, act_bits);
+  if (variant == SQ_VARIANT_FUSED) return fused_ws_bytes(M, K, N, act_bits);
   if (variant == SQ_VARIANT_UNFUSED) return unfused_ws_bytes(M, K, N, act_bits);
+  if (variant == SQ_VARIANT_GEMM) return gemm_ws_bytes(M, K, N, act_bits);
   return 0;
 }
 
@@ -185,19 +201,21 @@ sq_status sq_quantize_act(const uint16_t* x, int32_t M, int32_t K, const sq_act_
 }
 
 sq_status sq_gemm_w4a8(const int8_t* qx, const float* row_scale, int32_t M, const sq_weight* w,
-                       void* y, int32_t out_dtype, hipStream_t stream) {
+                       void* y, int32_t out_dtype, void* workspace, size_t ws_bytes, hipStream_t stream) {
   if (qx == nullptr || row_scale == nullptr || y == nullptr) return SQ_ERR_NULL;
   sq_status st = check_weight(w);
   if (st != SQ_OK) return st;
   if (!valid_m(M)) return SQ_ERR_SHAPE;
   if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
   if (!aligned(qx, 16) || !aligned(y, 16) || !aligned(row_scale, 4)) return SQ_ERR_ALIGN;
-  return hip_status(launch_gemm(8, kEpiOut, gemm_args(qx, row_scale, M, nullptr, w, y, out_dtype), stream));
+  if (workspace != nullptr && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  return hip_status(launch_gemm(8, kEpiOut, gemm_args(qx, row_scale, M, nullptr, w, y, out_dtype), stream,
+                                static_cast<float*>(workspace), workspace ? ws_bytes : 0));
 }
 
 sq_status sq_gemm_w4a4(const uint8_t* qx, const uint16_t* group_scale, int32_t M,
                        const sq_act_params* act, const sq_weight* w, void* y, int32_t out_dtype,
-                       hipStream_t stream) {
+                       void* workspace, size_t ws_bytes, hipStream_t stream) {
   if (qx == nullptr || group_scale == nullptr || y == nullptr) return SQ_ERR_NULL;
   sq_status st = check_weight(w);
   if (st != SQ_OK) return st;
@@ -207,7 +225,9 @@ sq_status sq_gemm_w4a4(const uint8_t* qx, const uint16_t* group_scale, int32_t M
   if (!valid_m(M)) return SQ_ERR_SHAPE;
   if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
   if (!aligned(qx, 16) || !aligned(y, 16) || !aligned(group_scale, 4)) return SQ_ERR_ALIGN;
-  return hip_status(launch_gemm(4, kEpiOut, gemm_args(qx, group_scale, M, act, w, y, out_dtype), stream));
+  if (workspace != nullptr && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  return hip_status(launch_gemm(4, kEpiOut, gemm_args(qx, group_scale, M, act, w, y, out_dtype), stream,
+                                static_cast<float*>(workspace), workspace ? ws_bytes : 0));
 }
 
 sq_status sq_linear_w4a8(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,

@@ -75,7 +75,18 @@ struct GemmArgs {
   void* out;                // y, partial sums, int32 C or block dump
   int32_t M, N, K, w_group;
   int32_t out_dtype;
+  // Split-K tail (set by launch_gemm): output tiles [0, ndp) of the logical
+  // order are computed whole; each of the remaining ones is computed by
+  // `split` workgroups over consecutive K ranges, which leave fp32 partial
+  // sums in `partial`, and one more kernel adds them up and finishes the tile.
+  int32_t ndp, split;
+  float* partial;
 };
+
+// Bytes of the partial-sum buffer the split-K tail may use for a GEMM of this
+// shape (0 when it never splits); any buffer at least this large lets
+// launch_gemm choose its plan freely, a smaller one restricts it.
+size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t w_group);
 
 struct PackArgs {
   const float* w;
@@ -88,7 +99,10 @@ struct PackArgs {
 // ---------------------------------------------------------------- launchers (return hipError_t)
 hipError_t launch_quantize_act(int act_bits, const QuantArgs& a, hipStream_t s);
 hipError_t launch_pack_weights(const PackArgs& a, hipStream_t s);
-hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s);
+// `partial` / `partial_bytes`: scratch for the split-K tail (may be NULL / 0:
+// every tile is then computed whole).
+hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial = nullptr,
+                       size_t partial_bytes = 0);
 
 // unfused stages
 struct UnfusedArgs {

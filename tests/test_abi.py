@@ -59,6 +59,13 @@ def test_workspace_bytes(L):
     assert B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, K, 100, 8) == 0
     assert B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, K, N, 5) == 0
     assert B.sq_workspace_bytes(7, M, K, N, 8) == 0
+    # GEMM scratch (split-K partial sums): at least 256 bytes, 256-aligned, and
+    # included in the fused workspace
+    g8 = B.sq_workspace_bytes(B.SQ_VARIANT_GEMM, M, K, N, 8)
+    assert g8 >= 256 and g8 % 256 == 0
+    assert fused8 >= M * K + 4 * M + g8
+    assert B.sq_workspace_bytes(B.SQ_VARIANT_GEMM, 88, 256, 256, 8) == 256  # 2 stages: never split
+    assert B.sq_workspace_bytes(B.SQ_VARIANT_GEMM, M, K, 100, 8) == 0
 
 
 def act(**kw):
@@ -126,11 +133,13 @@ def test_linear_bits_mismatch(L):
 
 def test_gemm_and_pack_reject(L):
     w = wt()
-    assert L.sq_gemm_w4a8(None, A, 88, ctypes.byref(w), A, 0, None) == NULL
-    assert L.sq_gemm_w4a8(A, A, 0, ctypes.byref(w), A, 0, None) == SHAPE
+    assert L.sq_gemm_w4a8(None, A, 88, ctypes.byref(w), A, 0, None, 0, None) == NULL
+    assert L.sq_gemm_w4a8(A, A, 0, ctypes.byref(w), A, 0, None, 0, None) == SHAPE
+    assert L.sq_gemm_w4a8(A, A, 88, ctypes.byref(w), A, 0, A + 8, 1 << 20, None) == ALIGN
     a4 = act(act_bits=4)
-    assert L.sq_gemm_w4a4(A, A, 88, ctypes.byref(act()), ctypes.byref(w), A, 0, None) == UNSUP
-    assert L.sq_gemm_w4a4(A, A + 2, 88, ctypes.byref(a4), ctypes.byref(w), A, 0, None) == ALIGN
+    assert L.sq_gemm_w4a4(A, A, 88, ctypes.byref(act()), ctypes.byref(w), A, 0, None, 0, None) == UNSUP
+    assert L.sq_gemm_w4a4(A, A + 2, 88, ctypes.byref(a4), ctypes.byref(w), A, 0, None, 0, None) == ALIGN
+    assert L.sq_gemm_w4a4(A, A, 88, ctypes.byref(a4), ctypes.byref(w), A, 0, A + 4, 1 << 20, None) == ALIGN
     assert L.sq_pack_weights(A, None, 256, 256, 96, A, A, None) == UNSUP
     assert L.sq_pack_weights(A, None, 100, 256, 128, A, A, None) == SHAPE
     assert L.sq_pack_weights(None, None, 256, 256, 128, A, A, None) == NULL

@@ -174,10 +174,12 @@ def test_linear_cfg1(bits, mode, out, G):
 @pytest.mark.parametrize("bits", [8, 4])
 @pytest.mark.parametrize("M,K,N,G,bias", [(1, 256, 64, 128, True), (63, 384, 192, 384, True),
                                           (130, 2048, 320, 128, False), (200, 1024, 128, 1024, True),
-                                          (97, 13824, 64, 128, True)])
+                                          (97, 13824, 64, 128, True), (70, 1664, 192, 128, True)])
 def test_linear_shapes(bits, M, K, N, G, bias):
     """Ragged M and N tiles, a weight step per output channel (G = K, the
-    paper's granularity), no bias, the largest K."""
+    paper's granularity), no bias, the largest K.  With fewer output tiles
+    than workgroup slots the tiles are split along K: 1664 = 13 stages gives
+    uneven ranges."""
     L = layer(M, K, N, seed=[4, M, K, N])
     pw, W = oracle_weight(L, G, with_bias=bias)
     act = act_params(L, 1, bits, 0)
@@ -188,17 +190,21 @@ def test_linear_shapes(bits, M, K, N, G, bias):
 
 
 @pytest.mark.parametrize("bits", [8, 4])
-def test_gemm_entry_points(bits):
-    """The second kernel alone, fed the oracle's codes and scales."""
+@pytest.mark.parametrize("with_ws", [False, True])
+def test_gemm_entry_points(bits, with_ws):
+    """The second kernel alone, fed the oracle's codes and scales; without a
+    workspace every tile is computed whole, with one the tiles are split along
+    K (partial sums added by the second kernel)."""
     L = layer(150, 512, 192, seed=5)
     pw, W = oracle_weight(L, 128)
     res = oracle_linear(L, 2, bits, 0, pw, 128)
     y = torch.empty((L.M, L.N), dtype=torch.float32, device="cuda")
+    ws = B.alloc_workspace(B.SQ_VARIANT_GEMM, L.M, L.K, L.N, bits) if with_ws else None
     if bits == 8:
-        B.sq_gemm_w4a8(torch.from_numpy(res["qx"]).cuda(), f32_to_dev(res["scale"]), W, y, F32)
+        B.sq_gemm_w4a8(torch.from_numpy(res["qx"]).cuda(), f32_to_dev(res["scale"]), W, y, F32, workspace=ws)
     else:
         B.sq_gemm_w4a4(u8_to_dev(res["qx"]), u16_to_dev(res["scale"], torch.float16), act_params(L, 2, 4, 0), W,
-                       y, F32)
+                       y, F32, workspace=ws)
     check_output(y, res, F32)
 
 
