@@ -286,7 +286,8 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  // wave-uniform (an SGPR): keeps every per-wave LDS and global address scalar
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / CF::NWN, wn = wave % CF::NWN;
   const int h = lane >> 5;
   const int M = a.M, N = a.N, K = a.K;
@@ -373,28 +374,28 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
   };
 
   // ---- per-lane LDS read offsets (within a stage); the swizzle terms depend
-  // on the lane only, since every wave's first row and column are multiples of 16.
+  // on the lane only, since every wave's first row and column are multiples
+  // of 16, and a 32-row (32-column) step leaves them unchanged: the offsets of
+  // the second row (column) tile are the first's plus a constant, which the
+  // LDS reads take as an immediate.
   const int arow0 = wm * 64 + (lane & 31);
   const int bcol0 = wn * 64 + (lane & 31);
-  int offA[TM][4];
+  constexpr int A_TILE_STEP = ABITS == 8 ? 32 * KT : 32 * (KT / 2);
+  constexpr int B_TILE_STEP = 32 * (KT / 2);
+  int offA0[4];
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm)
+  for (int ks = 0; ks < 4; ++ks) {
+    if constexpr (ABITS == 8)
+      offA0[ks] = arow0 * KT + 16 * ((4 * (ks >> 1) + 2 * h + (ks & 1)) ^ ((arow0 >> 1) & 7));
+    else
+      offA0[ks] = arow0 * (KT / 2) + 16 * ((2 * (ks >> 1) + h) ^ ((arow0 >> 2) & 3));
+  }
+  int offB0[2];
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int row = arow0 + tm * 32;
-      if constexpr (ABITS == 8)
-        offA[tm][ks] = row * KT + 16 * ((4 * (ks >> 1) + 2 * h + (ks & 1)) ^ ((row >> 1) & 7));
-      else
-        offA[tm][ks] = row * (KT / 2) + 16 * ((2 * (ks >> 1) + h) ^ ((row >> 2) & 3));
-    }
-  int offB[TN][2];
-#pragma unroll
-  for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      const int col = bcol0 + tn * 32;
-      offB[tn][k2] = LY::A_BYTES + col * (KT / 2) + 16 * ((2 * k2 + h) ^ ((col >> 2) & 3));
-    }
+  for (int k2 = 0; k2 < 2; ++k2)
+    offB0[k2] = LY::A_BYTES + bcol0 * (KT / 2) + 16 * ((2 * k2 + h) ^ ((bcol0 >> 2) & 3));
+  auto offA = [&](int tm, int ks) { return offA0[ks] + tm * A_TILE_STEP; };
+  auto offB = [&](int tn, int k2) { return offB0[k2] + tn * B_TILE_STEP; };
 
   float y[TM][TN][16];
 #pragma unroll
@@ -420,15 +421,15 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
       if constexpr (ABITS == 8) {
-        af[tm] = *reinterpret_cast<const v4i*>(st + offA[tm][ks]);
+        af[tm] = *reinterpret_cast<const v4i*>(st + offA(tm, ks));
       } else {
-        if ((ks & 1) == 0) pa[tm] = *reinterpret_cast<const uint4*>(st + offA[tm][ks]);
+        if ((ks & 1) == 0) pa[tm] = *reinterpret_cast<const uint4*>(st + offA(tm, ks));
         af[tm] = (ks & 1) ? unpack_frag(pa[tm].z, pa[tm].w) : unpack_frag(pa[tm].x, pa[tm].y);
       }
     }
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
-      if ((ks & 1) == 0) pb[tn] = *reinterpret_cast<const uint4*>(st + offB[tn][ks >> 1]);
+      if ((ks & 1) == 0) pb[tn] = *reinterpret_cast<const uint4*>(st + offB(tn, ks >> 1));
       bf[tn] = (ks & 1) ? unpack_frag(pb[tn].z, pb[tn].w) : unpack_frag(pb[tn].x, pb[tn].y);
     }
   };
@@ -486,7 +487,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
       for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
         for (int k2 = 0; k2 < 2; ++k2) {
-          const uint4 pb = *reinterpret_cast<const uint4*>(st + offB[tn][k2]);
+          const uint4 pb = *reinterpret_cast<const uint4*>(st + offB(tn, k2));
           bfull[tn][2 * k2] = unpack_frag(pb.x, pb.y);
           bfull[tn][2 * k2 + 1] = unpack_frag(pb.z, pb.w);
         }
@@ -494,7 +495,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
       for (int tm = 0; tm < TM; ++tm) {
         v4i af[4];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) af[ks] = *reinterpret_cast<const v4i*>(st + offA[tm][ks]);
+        for (int ks = 0; ks < 4; ++ks) af[ks] = *reinterpret_cast<const v4i*>(st + offA(tm, ks));
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
           fold8(acc[tm][tn], wsv_prev[tn], y[tm][tn]);
@@ -540,13 +541,13 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmAr
         v4i bf[TN][2];
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
-          const uint4 pb = *reinterpret_cast<const uint4*>(st + offB[tn][hb]);
+          const uint4 pb = *reinterpret_cast<const uint4*>(st + offB(tn, hb));
           bf[tn][0] = unpack_frag(pb.x, pb.y);
           bf[tn][1] = unpack_frag(pb.z, pb.w);
         }
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm) {
-          const uint4 pa = *reinterpret_cast<const uint4*>(st + offA[tm][2 * hb]);
+          const uint4 pa = *reinterpret_cast<const uint4*>(st + offA(tm, 2 * hb));
           const v4i af0 = unpack_frag(pa.x, pa.y);
           const v4i af1 = unpack_frag(pa.z, pa.w);
           // previous block: second half of the previous stage, or first half of this one
