@@ -38,6 +38,8 @@ namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
 typedef int v16i __attribute__((ext_vector_type(16)));
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));  // converted with round to nearest even
 typedef __attribute__((address_space(3))) uint8_t lds_u8_t;
 
 constexpr int KT = kKTile;   // 128 channels per stage
@@ -124,13 +126,15 @@ __device__ __forceinline__ void dma(const void* base, uint32_t voff, uint32_t ld
 }
 #pragma clang diagnostic pop
 
-// Wait until at most N of this wave's vector-memory operations are in flight,
-// then synchronize the workgroup.  One asm block with a memory clobber: no LDS
-// access moves across it (a fenced __syncthreads would instead drain every
-// outstanding load, including the stages still in flight).
+// Wait until at most N of this wave's vector-memory operations are in flight
+// and all of its LDS reads are done, then synchronize the workgroup: after it
+// the stage about to be read has landed and no wave still reads the slot the
+// next loads (or the epilogue) will overwrite.  One asm block with a memory
+// clobber: no LDS access moves across it (a fenced __syncthreads would instead
+// drain every outstanding load, including the stages still in flight).
 template <int N>
 __device__ __forceinline__ void wait_vm_and_barrier() {
-  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
 // LDS layout of one pipeline stage (no padding; 16-byte chunks XOR-swizzled
@@ -185,470 +189,605 @@ __device__ __forceinline__ void dump_block(const GemmArgs& a, const v16i (&acc)[
     }
 }
 
-// Epilogue of one 128 x 128 output tile: row factor, bias, cast, then store
-// through LDS so that every lane writes 16 contiguous bytes (whole 128-byte
-// lines).  Each wave stages 64 rows x 128 bytes (both 32-column tiles for
-// 16-bit outputs, one for fp32) in its own region of `smem` (>= 4 x 9 KB, not
-// in use by any wave of the workgroup).  Loads of bias and row factors come
-// before the stores (as far as the compiler knows the output may alias them).
+// 4 x 4 transpose across the lanes of a quad (lane i = lane & 3): in, lane i
+// holds v[q] = element (row q, column i); out, it holds v[j] = element
+// (row i, column j).  Two exchanges through DPP quad permutations (VALU only):
+// with lane ^ 1 the rows whose low bit differs from the lane's, then with
+// lane ^ 2 the column pairs of the row the partner keeps.
+__device__ __forceinline__ float dpp_xor1(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
+}
+__device__ __forceinline__ float dpp_xor2(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
+}
+__device__ __forceinline__ void quad_transpose(float (&v)[4], int lane) {
+  const bool o1 = lane & 1, o2 = lane & 2;
+  // after stage 1 lane i holds rows p, p + 2 (p = i & 1) at columns (i & ~1) + {0, 1}
+  const float r0 = dpp_xor1(o1 ? v[0] : v[1]);
+  const float r1 = dpp_xor1(o1 ? v[2] : v[3]);
+  const float a00 = o1 ? r0 : v[0], a01 = o1 ? v[1] : r0;
+  const float a10 = o1 ? r1 : v[2], a11 = o1 ? v[3] : r1;
+  // stage 2: lanes with bit 1 clear keep row p, the others row p + 2
+  const float u0 = dpp_xor2(o2 ? a00 : a10);
+  const float u1 = dpp_xor2(o2 ? a01 : a11);
+  v[0] = o2 ? u0 : a00;
+  v[1] = o2 ? u1 : a01;
+  v[2] = o2 ? a10 : u0;
+  v[3] = o2 ? a11 : u1;
+}
+
+// Row factor of output row m0 + wm * 64 + lane (8-bit: r_i; 4-bit: the
+// inverse gain kappa_i; 1 for partial sums) and the bias of the lane's two
+// columns, loaded when a tile starts so that their latency hides under its
+// main loop.
+template <int ABITS, int EPI>
+struct EpiInputs {
+  float rowf;
+  float bias[TN];
+  __device__ __forceinline__ void load(const GemmArgs& a, int m0, int n0, int wm, int wn, int lane) {
+    const int m = min(m0 + wm * 64 + lane, a.M - 1);
+    rowf = 1.0f;
+    if constexpr (EPI == kEpiOut) {
+      if constexpr (ABITS == 8) {
+        rowf = static_cast<const float*>(a.act_scale)[m];
+      } else {
+        rowf = 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
+      }
+    }
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int n = min(n0 + wn * 64 + tn * 32 + (lane & 31), a.N - 1);
+      bias[tn] = (EPI == kEpiOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
+    }
+  }
+};
+
+// Epilogue of one 128 x 128 output tile, from registers: row factor, bias,
+// cast, store.  In the MFMA layout a lane holds one column and, for each group
+// g of four registers, four consecutive rows; a quad transpose turns that into
+// one row and four consecutive columns, so each lane writes 16 bytes (fp32) or
+// 8 bytes (16-bit outputs) and eight lanes cover a row's 32 columns.  The row
+// factors are fetched from the lane that loaded them (ds_bpermute).
 template <int ABITS, int EPI>
 __device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN][16], int m0, int n0, int wm,
-                                           int wn, int wave, int lane, uint8_t* smem) {
+                                           int wn, int lane_in, const EpiInputs<ABITS, EPI>& in) {
+  // An opaque copy of the lane index: the per-lane values below are then
+  // computed here, not hoisted out of a surrounding tile loop (where they
+  // would hold registers through the whole main loop).
+  int lane = lane_in;
+  asm volatile("" : "+v"(lane));
   const int M = a.M, N = a.N;
-  constexpr int EP_PITCH = 144;  // bytes per staged row (16-byte aligned, spreads banks)
-  uint8_t* ep = smem + wave * 64 * EP_PITCH;
-  const bool cols_ok = n0 + wn * 64 < N;  // N % 64 == 0: a wave's 64 columns are all in or all out
-  float bcol[TN];
-#pragma unroll
-  for (int tn = 0; tn < TN; ++tn) {
-    const int n = min(n0 + wn * 64 + tn * 32 + (lane & 31), N - 1);
-    bcol[tn] = (EPI == kEpiOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
-  }
-  const int esz = (EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32) ? 4 : 2;
-  const int npass = esz == 4 ? 2 : 1;  // fp32: one 32-column tile per pass
+  if (n0 + wn * 64 >= N) return;  // N % 64 == 0: a wave's 64 columns are all in or all out
+  const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
+  const int rf_bits = __float_as_int(in.rowf);
+  const int half = (lane >> 5) * 16;  // lanes 32..63 hold rows 4 further down
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
     float rowf[16];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = min(m0 + wm * 64 + tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3), M - 1);
-      rowf[r] = 1.0f;
-      if constexpr (EPI == kEpiOut) {
-        if constexpr (ABITS == 8) {
-          rowf[r] = static_cast<const float*>(a.act_scale)[m];
-        } else {
-          rowf[r] = 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
-        }
-      }
-    }
-#pragma unroll
     for (int r = 0; r < 16; ++r)
+      rowf[r] = __int_as_float(__builtin_amdgcn_ds_bpermute(half + (tm * 32 + (r >> 2) * 8 + (r & 3)) * 4, rf_bits));
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) {
-        const float v = EPI == kEpiPartial ? y[tm][tn][r] : __builtin_fmaf(y[tm][tn][r], rowf[r], bcol[tn]);
-        y[tm][tn][r] = v;
-      }
-  }
-  // constant trip count: `pass` indexes y, which must stay in registers
+    for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-  for (int pass = 0; pass < 2; ++pass) {
-    if (pass >= npass) break;
-    // stage: row (within the wave's 64) = tm*32 + (r>>2)*8 + (lane>>5)*4 + (r&3)
+      for (int g = 0; g < 4; ++g) {
+        float v[4];
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-        uint8_t* rp = ep + row * EP_PITCH;
-        if (esz == 4) {
-          reinterpret_cast<float*>(rp)[lane & 31] = y[tm][pass][r];
-        } else {
-#pragma unroll
-          for (int tn = 0; tn < TN; ++tn) {
-            const float v = y[tm][tn][r];
-            const uint32_t b = a.out_dtype == SQ_OUT_BF16 ? f32_to_bf16(v) : f32_to_f16(v);
-            reinterpret_cast<uint16_t*>(rp)[tn * 32 + (lane & 31)] = static_cast<uint16_t>(b);
+        for (int q = 0; q < 4; ++q) {
+          const int r = g * 4 + q;
+          v[q] = EPI == kEpiPartial ? y[tm][tn][r] : __builtin_fmaf(y[tm][tn][r], rowf[r], in.bias[tn]);
+        }
+        quad_transpose(v, lane);
+        const int m = m0 + wm * 64 + tm * 32 + g * 8 + (lane >> 5) * 4 + (lane & 3);
+        const int n = n0 + wn * 64 + tn * 32 + (lane & 28);
+        if (m < M) {
+          if (f32out) {
+            *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * N + n) =
+                make_float4(v[0], v[1], v[2], v[3]);
+          } else {
+            uint2 w;
+            if (a.out_dtype == SQ_OUT_BF16) {
+              const bf16x2 lo = __builtin_convertvector((float2v){v[0], v[1]}, bf16x2);
+              const bf16x2 hi = __builtin_convertvector((float2v){v[2], v[3]}, bf16x2);
+              w = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+            } else {
+              w = make_uint2(f32_to_f16(v[0]) | (f32_to_f16(v[1]) << 16), f32_to_f16(v[2]) | (f32_to_f16(v[3]) << 16));
+            }
+            *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + static_cast<size_t>(m) * N + n) = w;
           }
         }
       }
-    // read back 16-byte chunks (8 rows of 128 bytes per instruction) and store
-    if (cols_ok) {
-      const size_t row_bytes = static_cast<size_t>(N) * esz;
-      uint8_t* gbase = static_cast<uint8_t*>(a.out) + static_cast<size_t>(n0 + wn * 64 + pass * 32) * esz;
+  }
+}
+
+// Per-lane LDS read offsets of the MFMA fragments within a stage.  The swizzle
+// terms depend on the lane only, since every wave's first row and column are
+// multiples of 16, and a 32-row (32-column) step leaves them unchanged: the
+// offsets of the second row (column) tile are the first's plus a constant,
+// which the LDS reads take as an immediate.
+template <int ABITS>
+struct FragOffsets {
+  static constexpr int A_TILE_STEP = ABITS == 8 ? 32 * KT : 32 * (KT / 2);
+  static constexpr int B_TILE_STEP = 32 * (KT / 2);
+  int a0[4];
+  int b0[2];
+  __device__ __forceinline__ FragOffsets(int wm, int wn, int lane) {
+    const int h = lane >> 5;
+    const int arow0 = wm * 64 + (lane & 31);
+    const int bcol0 = wn * 64 + (lane & 31);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) {
-        const int row = i * 8 + (lane >> 3);
-        const int m = m0 + wm * 64 + row;
-        const uint4 v = *reinterpret_cast<const uint4*>(ep + row * EP_PITCH + (lane & 7) * 16);
-        if (m < M) *reinterpret_cast<uint4*>(gbase + static_cast<size_t>(m) * row_bytes + (lane & 7) * 16) = v;
+    for (int ks = 0; ks < 4; ++ks) {
+      if constexpr (ABITS == 8)
+        a0[ks] = arow0 * KT + 16 * ((4 * (ks >> 1) + 2 * h + (ks & 1)) ^ ((arow0 >> 1) & 7));
+      else
+        a0[ks] = arow0 * (KT / 2) + 16 * ((2 * (ks >> 1) + h) ^ ((arow0 >> 2) & 3));
+    }
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2)
+      b0[k2] = Layout<ABITS>::A_BYTES + bcol0 * (KT / 2) + 16 * ((2 * k2 + h) ^ ((bcol0 >> 2) & 3));
+  }
+  __device__ __forceinline__ int a(int tm, int ks) const { return a0[ks] + tm * A_TILE_STEP; }
+  __device__ __forceinline__ int b(int tn, int k2) const { return b0[k2] + tn * B_TILE_STEP; }
+};
+
+// This wave's direct loads of one stage: per-lane 32-bit offsets within the
+// tile (rows and columns past the matrix are clamped to the last one) and the
+// wave's LDS destinations.
+template <int ABITS>
+struct StageLoads {
+  using LY = Layout<ABITS>;
+  uint32_t voffA[LY::A_DMA];
+  uint32_t voffB[LY::B_DMA];
+  uint32_t voffS;
+  uint32_t wcol2;  // first of the two output channels whose fp16 steps this lane's dword holds
+
+  __device__ __forceinline__ void set(int m0, int n0, int M, int N, int K, int wave, int wn, int lane) {
+    const uint32_t a_row_bytes = ABITS == 8 ? K : K / 2;
+#pragma unroll
+    for (int i = 0; i < LY::A_DMA; ++i) {
+      if constexpr (ABITS == 8) {
+        const int row = 8 * (LY::A_DMA * wave + i) + (lane >> 3);
+        const int c = (lane & 7) ^ ((row >> 1) & 7);
+        voffA[i] = static_cast<uint32_t>(min(m0 + row, M - 1) - m0) * a_row_bytes + c * 16;
+      } else {
+        const int row = 16 * (LY::A_DMA * wave + i) + (lane >> 2);
+        const int c = (lane & 3) ^ ((row >> 2) & 3);
+        voffA[i] = static_cast<uint32_t>(min(m0 + row, M - 1) - m0) * a_row_bytes + c * 16;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < LY::B_DMA; ++i) {
+      const int col = 16 * (LY::B_DMA * wave + i) + (lane >> 2);
+      const int c = (lane & 3) ^ ((col >> 2) & 3);
+      voffB[i] = static_cast<uint32_t>(min(n0 + col, N - 1) - n0) * static_cast<uint32_t>(K / 2) + c * 16;
+    }
+    voffS = 0;
+    if constexpr (ABITS == 4) {
+      const int row = LY::S_ROWS * wave + (lane % LY::S_ROWS);
+      voffS = static_cast<uint32_t>(min(m0 + row, M - 1) - m0) * static_cast<uint32_t>((K / kA4Group) * 2);
+    }
+    // N is even, so the pair is clamped inside the row
+    wcol2 = static_cast<uint32_t>(min(n0 + wn * 64 + 2 * (lane & 31), N - 2));
+  }
+
+  // stage kt of the tile at (m0, n0) into the ring slot at LDS address st
+  template <bool SIGMA, bool STEPS>
+  __device__ __forceinline__ void issue(const GemmArgs& a, int m0, int n0, int kt, uint32_t st, int wave) const {
+    const int K = a.K;
+    const uint8_t* bA = static_cast<const uint8_t*>(a.qx) +
+                        static_cast<size_t>(m0) * (ABITS == 8 ? K : K / 2) + kt * (ABITS == 8 ? KT : KT / 2);
+    const uint8_t* bB = a.qw + static_cast<size_t>(n0) * (K / 2) + kt * (KT / 2);
+#pragma unroll
+    for (int i = 0; i < LY::A_DMA; ++i) dma<16>(bA, voffA[i], st + (LY::A_DMA * wave + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < LY::B_DMA; ++i) dma<16>(bB, voffB[i], st + LY::A_BYTES + (LY::B_DMA * wave + i) * 1024);
+    if constexpr (SIGMA) {
+      const uint8_t* bS = static_cast<const uint8_t*>(a.act_scale) + static_cast<size_t>(m0) * (K / kA4Group) * 2 + kt * 4;
+      dma<4>(bS, voffS, st + LY::A_BYTES + LY::B_BYTES + wave * 256);
+    }
+    if constexpr (STEPS) {
+      const uint32_t e = static_cast<uint32_t>((kt * KT) / a.w_group) * static_cast<uint32_t>(a.N) + wcol2;
+      dma<4>(a.w_scale, e * 2, st + LY::A_BYTES + LY::B_BYTES + LY::S_BYTES + wave * 256);
+    }
+  }
+};
+
+// Weight steps of a stage for the wave's columns, widened-code factor folded in.
+template <int ABITS>
+__device__ __forceinline__ void read_wscale(const uint8_t* st, int wave, int lane, float (&w)[TN]) {
+  using LY = Layout<ABITS>;
+  constexpr float WFOLD = ABITS == 8 ? 0.0625f : 0.00390625f;  // 1/16 or 1/256
+  const uint32_t* Wst = reinterpret_cast<const uint32_t*>(st + LY::A_BYTES + LY::B_BYTES + LY::S_BYTES + wave * 256);
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    const int c = tn * 32 + (lane & 31);  // column within the wave's 64
+    const uint32_t pair = Wst[c >> 1];
+    w[tn] = f16_to_f32((c & 1) ? (pair >> 16) : (pair & 0xFFFFu)) * WFOLD;
+  }
+}
+
+// y += fp32(C) * Delta_W for one 32 x 32 tile (8-bit activations)
+__device__ __forceinline__ void fold8(const v16i& c, float w, float (&yt)[16]) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) yt[r] = __builtin_fmaf(static_cast<float>(c[r]), w, yt[r]);
+}
+
+// y += (fp32(C) * sigma_row) * Delta_W for row tile tm and both column tiles
+// (4-bit activations); sigma of block half hb from the stage at st
+template <int ABITS>
+__device__ __forceinline__ void fold4(float (&y)[TM][TN][16], const uint8_t* st, int hb, const v16i (&c)[TN], int wm,
+                                      int tm, int lane, const float (&w)[TN], bool valid) {
+  using LY = Layout<ABITS>;
+  const uint8_t* S = st + LY::A_BYTES + LY::B_BYTES;
+#pragma unroll
+  for (int r4 = 0; r4 < 4; ++r4) {
+    const int ml = wm * 64 + tm * 32 + r4 * 8 + (lane >> 5) * 4;
+    const uint4 sp = *reinterpret_cast<const uint4*>(S + (ml / LY::S_ROWS) * 256 + (ml % LY::S_ROWS) * 4);
+    const uint32_t w4[4] = {sp.x, sp.y, sp.z, sp.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float sg = valid ? f16_to_f32(hb ? (w4[i] >> 16) : (w4[i] & 0xFFFFu)) : 0.0f;
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int r = r4 * 4 + i;
+        y[tm][tn][r] = __builtin_fmaf(static_cast<float>(c[tn][r]) * sg, w[tn], y[tm][tn][r]);
       }
     }
   }
 }
 
-
-// ABITS: 8 or 4.  EPI: EpiMode.  W128: 8-bit activations with one weight step
-// per 128 input channels (one K-block per pipeline stage).
-// PIPE (full or partial epilogue, and either 4-bit activations or W128): the
-// overlapped path.  Otherwise blocks are folded (or dumped) when they end.
-template <int ABITS, int EPI, bool W128>
-__global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_w4_kernel(GemmArgs a) {
+// The pipelined GEMM (8-bit activations with one weight step per 128 input
+// channels, and 4-bit activations): persistent workgroups.  Work items are the
+// output tiles computed whole (the first ndp of the logical order) followed by
+// the K ranges of the split tail tiles; workgroup g takes items g, g + G,
+// g + 2G, ...  The loads run two stages ahead along the workgroup's whole item
+// sequence, so the next tile's first stages are in flight during the current
+// tile's epilogue, and the epilogue's stores drain while the next tile
+// computes.  Workgroups never wait for one another.
+//
+// 8-bit activations, one block per stage, tile-major: for each 32 x 32 tile,
+// fold the previous block's accumulator into y, then run the tile's four MFMAs
+// of this block; the fold of the next tile (VALU) overlaps these MFMAs.
+// 4-bit activations: blocks are the two halves of a stage, row-tile-major:
+// fold the previous block's accumulators of a row tile (they share its group
+// steps), then run its MFMAs of this block; four stages, since the previous
+// stage's group steps are still read while the stage two ahead loads.
+template <int ABITS, int EPI>
+__global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(GemmArgs a) {
   using LY = Layout<ABITS>;
   using CF = Cfg<ABITS>;
   constexpr int BM = CF::BM, BN = CF::BN, STAGES = CF::STAGES;
-  constexpr bool NEED_SCALE = (EPI == kEpiOut || EPI == kEpiPartial);
-  constexpr bool LOAD_SIGMA = ABITS == 4 && NEED_SCALE;
-  constexpr bool PIPE = NEED_SCALE && (ABITS == 4 || W128);
-  constexpr int NDMA = LY::A_DMA + LY::B_DMA + (LOAD_SIGMA ? 1 : 0) + (NEED_SCALE ? 1 : 0);
-  constexpr float WFOLD = ABITS == 8 ? 0.0625f : 0.00390625f;  // 1/16 or 1/256
+  constexpr bool A4 = ABITS == 4;
+  constexpr int NDMA = LY::A_DMA + LY::B_DMA + (A4 ? 1 : 0) + 1;
+  constexpr uint32_t RING = STAGES * LY::STAGE;
+  static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
 
-  __shared__ __align__(1024) uint8_t smem[STAGES * LY::STAGE];
+  __shared__ __align__(1024) uint8_t smem[RING];
 
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
+  const int lane = threadIdx.x & 63;
   // wave-uniform (an SGPR): keeps every per-wave LDS and global address scalar
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm = wave / CF::NWN, wn = wave % CF::NWN;
-  const int h = lane >> 5;
   const int M = a.M, N = a.N, K = a.K;
-
-  const int ntm = (M + BM - 1) / BM;
-  const int ntn = (N + BN - 1) / BN;
-  const int nkt = K / KT;
-  // whole tile, or one K range [kt_begin, kt_end) of a split tail tile
-  int lid, kt_begin = 0, kt_end = nkt, unit = -1;
-  if (static_cast<int>(blockIdx.x) < a.ndp) {
-    lid = xcd_order(blockIdx.x, a.ndp);
-  } else {
-    unit = blockIdx.x - a.ndp;
-    lid = a.ndp + unit / a.split;
-    const int sl = unit % a.split;
-    kt_begin = sl * nkt / a.split;
-    kt_end = (sl + 1) * nkt / a.split;
-  }
-  int tile_m, tile_n;
-  supertile(lid, ntm, ntn, tile_m, tile_n);
-  const int m0 = tile_m * BM;
-  const int n0 = tile_n * BN;
-  const uint8_t* qx = static_cast<const uint8_t*>(a.qx);
+  const int ntm = (M + BM - 1) / BM, ntn = (N + BN - 1) / BN, nkt = K / KT;
+  const int nitems = a.ndp + (ntm * ntn - a.ndp) * a.split;
+  const int G = gridDim.x;
+  if (static_cast<int>(blockIdx.x) >= nitems) return;
   const uint32_t smem_lds = lds_offset(smem);
 
-  // ---- this wave's direct loads: uniform bases (the tile's first row /
-  // column, advanced per stage) and 32-bit per-lane offsets within the tile
-  const size_t a_row_bytes = ABITS == 8 ? static_cast<size_t>(K) : static_cast<size_t>(K / 2);
-  const uint8_t* baseA = qx + static_cast<size_t>(m0) * a_row_bytes;
-  const uint8_t* baseB = a.qw + static_cast<size_t>(n0) * (K / 2);
-  const uint8_t* baseS = LOAD_SIGMA ? static_cast<const uint8_t*>(a.act_scale) + static_cast<size_t>(m0) * (K / kA4Group) * 2
-                                    : nullptr;
-  uint32_t voffA[LY::A_DMA];
-  uint32_t voffB[LY::B_DMA];
-  uint32_t voffS = 0;
-  if constexpr (ABITS == 8) {
-#pragma unroll
-    for (int i = 0; i < LY::A_DMA; ++i) {
-      const int row = 8 * (LY::A_DMA * wave + i) + (lane >> 3);
-      const int c = (lane & 7) ^ ((row >> 1) & 7);
-      voffA[i] = static_cast<uint32_t>((min(m0 + row, M - 1) - m0) * a_row_bytes) + c * 16;
+  // item -> tile origin and K range [kt0, kt1); unit >= 0 marks a split range
+  struct Item {
+    int m0, n0, kt0, kt1, unit;
+  };
+  auto item_of = [&](int it) {
+    Item r;
+    int lid;
+    if (it < a.ndp) {
+      lid = xcd_order(it, a.ndp);
+      r.kt0 = 0;
+      r.kt1 = nkt;
+      r.unit = -1;
+    } else {
+      r.unit = it - a.ndp;
+      lid = a.ndp + r.unit / a.split;
+      const int sl = r.unit % a.split;
+      r.kt0 = sl * nkt / a.split;
+      r.kt1 = (sl + 1) * nkt / a.split;
     }
-  } else {
-#pragma unroll
-    for (int i = 0; i < LY::A_DMA; ++i) {
-      const int row = 16 * (LY::A_DMA * wave + i) + (lane >> 2);
-      const int c = (lane & 3) ^ ((row >> 2) & 3);
-      voffA[i] = static_cast<uint32_t>((min(m0 + row, M - 1) - m0) * a_row_bytes) + c * 16;
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < LY::B_DMA; ++i) {
-    const int col = 16 * (LY::B_DMA * wave + i) + (lane >> 2);
-    const int c = (lane & 3) ^ ((col >> 2) & 3);
-    voffB[i] = static_cast<uint32_t>((min(n0 + col, N - 1) - n0) * (K / 2)) + c * 16;
-  }
-  if constexpr (LOAD_SIGMA) {
-    const int row = LY::S_ROWS * wave + (lane % LY::S_ROWS);
-    voffS = static_cast<uint32_t>((min(m0 + row, M - 1) - m0) * (K / kA4Group) * 2);
-  }
-  // weight steps: the dword of output channels c, c + 1 of this wave's 64
-  // (c even; N is even, so the pair is clamped inside the row)
-  const uint32_t wcol2 = static_cast<uint32_t>(min(n0 + wn * 64 + 2 * (lane & 31), N - 2));
+    int tm, tn;
+    supertile(lid, ntm, ntn, tm, tn);
+    r.m0 = tm * BM;
+    r.n0 = tn * BN;
+    return r;
+  };
 
-  // Loads stage kt into ring slot kt % STAGES.  Past the last stage of the
-  // range the source is clamped to that stage: the slot written is free (its
-  // stage was consumed before the previous barrier) and is never read again,
-  // and the loop body stays free of branches, so its MFMAs and VALU work can
-  // be interleaved.
-  auto issue_stage = [&](int kt_slot) {
-    const uint32_t st = smem_lds + (kt_slot % STAGES) * LY::STAGE;
-    const int kt = min(kt_slot, kt_end - 1);
-    const uint8_t* bA = baseA + kt * (ABITS == 8 ? KT : KT / 2);
-    const uint8_t* bB = baseB + kt * (KT / 2);
-#pragma unroll
-    for (int i = 0; i < LY::A_DMA; ++i) dma<16>(bA, voffA[i], st + (LY::A_DMA * wave + i) * 1024);
-#pragma unroll
-    for (int i = 0; i < LY::B_DMA; ++i) dma<16>(bB, voffB[i], st + LY::A_BYTES + (LY::B_DMA * wave + i) * 1024);
-    if constexpr (LOAD_SIGMA) dma<4>(baseS + kt * 4, voffS, st + LY::A_BYTES + LY::B_BYTES + wave * 256);
-    if constexpr (NEED_SCALE) {
-      const uint32_t e = static_cast<uint32_t>((kt * KT) / a.w_group) * static_cast<uint32_t>(N) + wcol2;
-      dma<4>(a.w_scale, e * 2, st + LY::A_BYTES + LY::B_BYTES + LY::S_BYTES + wave * 256);
+  // ---- the load cursor: (item, stage) two stages ahead of the computation
+  int d_it = blockIdx.x;
+  Item d = item_of(d_it);
+  int d_kt = d.kt0;
+  uint32_t d_slot = 0;  // byte offset of the ring slot the next stage goes to
+  StageLoads<ABITS> ld;
+  ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
+  auto issue = [&]() {
+    ld.template issue<A4, true>(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
+    d_slot = d_slot + LY::STAGE == RING ? 0 : d_slot + LY::STAGE;
+  };
+  // Past the last stage of the last item the same stage is loaded again (in
+  // bounds, into a free slot), so every iteration issues the same loads.
+  auto advance = [&]() {
+    if (d_kt + 1 < d.kt1) {
+      ++d_kt;
+    } else if (d_it + G < nitems) {
+      d_it += G;
+      d = item_of(d_it);
+      d_kt = d.kt0;
+      ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
     }
   };
 
-  // ---- per-lane LDS read offsets (within a stage); the swizzle terms depend
-  // on the lane only, since every wave's first row and column are multiples
-  // of 16, and a 32-row (32-column) step leaves them unchanged: the offsets of
-  // the second row (column) tile are the first's plus a constant, which the
-  // LDS reads take as an immediate.
-  const int arow0 = wm * 64 + (lane & 31);
-  const int bcol0 = wn * 64 + (lane & 31);
-  constexpr int A_TILE_STEP = ABITS == 8 ? 32 * KT : 32 * (KT / 2);
-  constexpr int B_TILE_STEP = 32 * (KT / 2);
-  int offA0[4];
-#pragma unroll
-  for (int ks = 0; ks < 4; ++ks) {
-    if constexpr (ABITS == 8)
-      offA0[ks] = arow0 * KT + 16 * ((4 * (ks >> 1) + 2 * h + (ks & 1)) ^ ((arow0 >> 1) & 7));
-    else
-      offA0[ks] = arow0 * (KT / 2) + 16 * ((2 * (ks >> 1) + h) ^ ((arow0 >> 2) & 3));
-  }
-  int offB0[2];
-#pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2)
-    offB0[k2] = LY::A_BYTES + bcol0 * (KT / 2) + 16 * ((2 * k2 + h) ^ ((bcol0 >> 2) & 3));
-  auto offA = [&](int tm, int ks) { return offA0[ks] + tm * A_TILE_STEP; };
-  auto offB = [&](int tn, int k2) { return offB0[k2] + tn * B_TILE_STEP; };
+  const FragOffsets<ABITS> off(wm, wn, lane);
 
-  float y[TM][TN][16];
+  issue();
+  advance();
+  issue();
+  advance();
+  wait_vm_and_barrier<NDMA>();
+
+  uint32_t c_slot = 0;  // byte offset of the ring slot of the stage being computed
+  auto next_slot = [&](uint32_t s) { return s + LY::STAGE == RING ? 0u : s + LY::STAGE; };
+  auto prev_slot = [&](uint32_t s) { return s == 0 ? RING - LY::STAGE : s - LY::STAGE; };
+
+  // The accumulators are set once: each tile's first fold scales whatever they
+  // hold (finite integers) by a zero step.
+  v16i acc[TM][TN];
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) y[tm][tn][r] = 0.0f;
-
-  // weight steps of stage kt for the owned columns, widened-code factor folded in
-  auto read_wscale = [&](const uint8_t* st, int kt, float (&w)[TN]) {
-    const uint32_t* Wst = reinterpret_cast<const uint32_t*>(st + LY::A_BYTES + LY::B_BYTES + LY::S_BYTES + wave * 256);
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      const int c = tn * 32 + (lane & 31);  // column within the wave's 64
-      const uint32_t pair = Wst[c >> 1];
-      w[tn] = f16_to_f32((c & 1) ? (pair >> 16) : (pair & 0xFFFFu)) * WFOLD;
-    }
-  };
-
-  // MFMA fragments of k-step ks of a stage.
-  auto frags = [&](const uint8_t* st, int ks, v4i (&af)[TM], v4i (&bf)[TN], uint4 (&pa)[TM], uint4 (&pb)[TN]) {
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      if constexpr (ABITS == 8) {
-        af[tm] = *reinterpret_cast<const v4i*>(st + offA(tm, ks));
-      } else {
-        if ((ks & 1) == 0) pa[tm] = *reinterpret_cast<const uint4*>(st + offA(tm, ks));
-        af[tm] = (ks & 1) ? unpack_frag(pa[tm].z, pa[tm].w) : unpack_frag(pa[tm].x, pa[tm].y);
-      }
-    }
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      if ((ks & 1) == 0) pb[tn] = *reinterpret_cast<const uint4*>(st + offB(tn, ks >> 1));
-      bf[tn] = (ks & 1) ? unpack_frag(pb[tn].z, pb[tn].w) : unpack_frag(pb[tn].x, pb[tn].y);
-    }
-  };
-
-  // y += fp32(C) * Delta_W for one 32 x 32 tile (8-bit activations)
-  auto fold8 = [&](const v16i& c, float w, float (&yt)[16]) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) yt[r] = __builtin_fmaf(static_cast<float>(c[r]), w, yt[r]);
-  };
-  // y += (fp32(C) * sigma_row) * Delta_W for row-tile tm and both column
-  // tiles (4-bit activations); sigma from stage `st`, block half hb
-  auto fold4 = [&](const uint8_t* st, int hb, const v16i (&c)[TN], int tm, const float (&w)[TN], bool valid) {
-    const uint8_t* S = st + LY::A_BYTES + LY::B_BYTES;
-#pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int ml = wm * 64 + tm * 32 + r4 * 8 + (lane >> 5) * 4;
-      const uint4 sp = *reinterpret_cast<const uint4*>(S + (ml / LY::S_ROWS) * 256 + (ml % LY::S_ROWS) * 4);
-      const uint32_t w4[4] = {sp.x, sp.y, sp.z, sp.w};
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float sg = valid ? f16_to_f32(hb ? (w4[i] >> 16) : (w4[i] & 0xFFFFu)) : 0.0f;
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
-          const int r = r4 * 4 + i;
-          y[tm][tn][r] = __builtin_fmaf(static_cast<float>(c[tn][r]) * sg, w[tn], y[tm][tn][r]);
-        }
-      }
-    }
-  };
-
-  issue_stage(kt_begin);
-  issue_stage(kt_begin + 1);
-  wait_vm_and_barrier<NDMA>();
-
-  if constexpr (PIPE && ABITS == 8) {
-    // ---------------- 8-bit activations, one block per stage.  Tile-major:
-    // for each 32 x 32 tile, fold the previous block's accumulator into y,
-    // then run the tile's four MFMAs of this block; the fold of the next tile
-    // (VALU) overlaps these MFMAs.
-    // zero accumulators and steps: the fold before the first block adds 0
-    v16i acc[TM][TN];
+    for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
+  for (int it = blockIdx.x;;) {
+    const Item c = item_of(it);
+    EpiInputs<ABITS, EPI> ein;
+    ein.load(a, c.m0, c.n0, wm, wn, lane);
+    float y[TM][TN][16];
     float wsv_prev[TN], wsv[TN];
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = 0.0f;
-    for (int kt = kt_begin; kt < kt_end; ++kt) {
-      issue_stage(kt + 2);
-      const uint8_t* st = smem + (kt % STAGES) * LY::STAGE;
-      read_wscale(st, kt, wsv);
-      v4i bfull[TN][4];
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-        for (int k2 = 0; k2 < 2; ++k2) {
-          const uint4 pb = *reinterpret_cast<const uint4*>(st + offB(tn, k2));
-          bfull[tn][2 * k2] = unpack_frag(pb.x, pb.y);
-          bfull[tn][2 * k2 + 1] = unpack_frag(pb.z, pb.w);
-        }
+        for (int r = 0; r < 16; ++r) y[tm][tn][r] = 0.0f;
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        v4i af[4];
+    for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = 0.0f;  // the fold before the first block adds 0
+
+    if constexpr (!A4) {
+      for (int kt = c.kt0; kt < c.kt1; ++kt) {
+        issue();
+        advance();
+        const uint8_t* st = smem + c_slot;
+        read_wscale<ABITS>(st, wave, lane, wsv);
+        v4i bfull[TN][4];
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks) af[ks] = *reinterpret_cast<const v4i*>(st + offA(tm, ks));
+        for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
-          fold8(acc[tm][tn], wsv_prev[tn], y[tm][tn]);
-          acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[0], bfull[tn][0], (v16i)(0), 0, 0, 0);
-#pragma unroll
-          for (int ks = 1; ks < 4; ++ks)
-            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks], bfull[tn][ks], acc[tm][tn], 0, 0, 0);
-        }
-      }
-      // issue order: each MFMA followed by a share of the VALU work (folds,
-      // unpacking), so the VALU runs under the matrix cores
-#pragma unroll
-      for (int i = 0; i < TM * TN * 4; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);  // up to ten VALU
-      }
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
-      wait_vm_and_barrier<NDMA>();
-    }
-#pragma unroll
-    for (int t = 0; t < TM * TN; ++t) fold8(acc[t >> 1][t & 1], wsv_prev[t & 1], y[t >> 1][t & 1]);
-  } else if constexpr (PIPE && ABITS == 4) {
-    // ---------------- 4-bit activations: blocks are the two halves of a
-    // stage.  Row-tile-major: fold the previous block's accumulators of a
-    // row tile (they share its group steps), then run its MFMAs of this block.
-    // zero accumulators and steps: the fold before the first block adds 0
-    v16i acc[TM][TN];
-    float wsv_prev[TN], wsv[TN];
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = 0.0f;
-    for (int kt = kt_begin; kt < kt_end; ++kt) {
-      issue_stage(kt + 2);
-      const uint8_t* st = smem + (kt % STAGES) * LY::STAGE;
-      const uint8_t* st_prev = smem + ((kt + STAGES - 1) % STAGES) * LY::STAGE;
-      read_wscale(st, kt, wsv);
-#pragma unroll
-      for (int hb = 0; hb < 2; ++hb) {
-        v4i bf[TN][2];
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
-          const uint4 pb = *reinterpret_cast<const uint4*>(st + offB(tn, hb));
-          bf[tn][0] = unpack_frag(pb.x, pb.y);
-          bf[tn][1] = unpack_frag(pb.z, pb.w);
-        }
+          for (int k2 = 0; k2 < 2; ++k2) {
+            const uint4 pb = *reinterpret_cast<const uint4*>(st + off.b(tn, k2));
+            bfull[tn][2 * k2] = unpack_frag(pb.x, pb.y);
+            bfull[tn][2 * k2 + 1] = unpack_frag(pb.z, pb.w);
+          }
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm) {
-          const uint4 pa = *reinterpret_cast<const uint4*>(st + offA(tm, 2 * hb));
-          const v4i af0 = unpack_frag(pa.x, pa.y);
-          const v4i af1 = unpack_frag(pa.z, pa.w);
-          // previous block: second half of the previous stage, or first half of this one
-          if (hb == 0) {
-            fold4(st_prev, 1, acc[tm], tm, wsv_prev, kt > kt_begin);
-          } else {
-            fold4(st, 0, acc[tm], tm, wsv, true);
-          }
+          v4i af[4];
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) af[ks] = *reinterpret_cast<const v4i*>(st + off.a(tm, ks));
 #pragma unroll
           for (int tn = 0; tn < TN; ++tn) {
-            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af0, bf[tn][0], (v16i)(0), 0, 0, 0);
-            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af1, bf[tn][1], acc[tm][tn], 0, 0, 0);
+            fold8(acc[tm][tn], wsv_prev[tn], y[tm][tn]);
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[0], bfull[tn][0], (v16i)(0), 0, 0, 0);
+#pragma unroll
+            for (int ks = 1; ks < 4; ++ks)
+              acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks], bfull[tn][ks], acc[tm][tn], 0, 0, 0);
           }
         }
-      }
+        // issue order: each MFMA followed by a share of the VALU work (folds,
+        // unpacking), so the VALU runs under the matrix cores
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
-      wait_vm_and_barrier<NDMA>();
-    }
-    {
-      const uint8_t* st_last = smem + ((kt_end - 1) % STAGES) * LY::STAGE;
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm) fold4(st_last, 1, acc[tm], tm, wsv_prev, true);
-    }
-  } else {
-    // ---------------- blocks folded or dumped when they end
-    v16i acc[TM][TN];
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
-    for (int kt = 0; kt < nkt; ++kt) {
-      issue_stage(kt + 2);
-      const uint8_t* st = smem + (kt % STAGES) * LY::STAGE;
-      float wsv[TN];
-      if constexpr (NEED_SCALE) read_wscale(st, kt, wsv);
-      if constexpr (ABITS == 8) {
-        if ((kt * KT) % a.w_group == 0) {
-#pragma unroll
-          for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-            for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
+        for (int i = 0; i < TM * TN * 4; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);  // up to ten VALU
         }
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
+        wait_vm_and_barrier<NDMA>();
+        c_slot = next_slot(c_slot);
       }
-      uint4 pa[TM], pb[TN];
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) {
-        v4i af[TM], bf[TN];
-        frags(st, ks, af, bf, pa, pb);
-        const bool zero_c = ABITS == 4 && (ks & 1) == 0;
+      for (int t = 0; t < TM * TN; ++t) fold8(acc[t / TN][t % TN], wsv_prev[t % TN], y[t / TN][t % TN]);
+    } else {
+      for (int kt = c.kt0; kt < c.kt1; ++kt) {
+        issue();
+        advance();
+        const uint8_t* st = smem + c_slot;
+        const uint8_t* st_prev = smem + prev_slot(c_slot);
+        read_wscale<ABITS>(st, wave, lane, wsv);
 #pragma unroll
-        for (int tm = 0; tm < TM; ++tm)
+        for (int hb = 0; hb < 2; ++hb) {
+          v4i bf[TN][2];
 #pragma unroll
           for (int tn = 0; tn < TN; ++tn) {
-            if (zero_c)
-              acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm], bf[tn], (v16i)(0), 0, 0, 0);
-            else
-              acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm], bf[tn], acc[tm][tn], 0, 0, 0);
+            const uint4 pb = *reinterpret_cast<const uint4*>(st + off.b(tn, hb));
+            bf[tn][0] = unpack_frag(pb.x, pb.y);
+            bf[tn][1] = unpack_frag(pb.z, pb.w);
           }
-        if constexpr (ABITS == 4) {
-          if ((ks & 1) == 1) dump_block<ABITS>(a, acc, kt * 2 + (ks >> 1), m0, n0, wm, wn, lane);
-        }
-      }
-      if constexpr (ABITS == 8) {
-        if (((kt + 1) * KT) % a.w_group == 0) {  // end of a weight group
-          if constexpr (EPI == kEpiDump) {
-            dump_block<ABITS>(a, acc, ((kt + 1) * KT) / a.w_group - 1, m0, n0, wm, wn, lane);
-          } else if constexpr (NEED_SCALE) {
 #pragma unroll
-            for (int t = 0; t < TM * TN; ++t) fold8(acc[t >> 1][t & 1], wsv[t & 1], y[t >> 1][t & 1]);
+          for (int tm = 0; tm < TM; ++tm) {
+            const uint4 pa = *reinterpret_cast<const uint4*>(st + off.a(tm, 2 * hb));
+            const v4i af0 = unpack_frag(pa.x, pa.y);
+            const v4i af1 = unpack_frag(pa.z, pa.w);
+            // previous block: second half of the previous stage, or first half of this one
+            if (hb == 0) {
+              fold4<ABITS>(y, st_prev, 1, acc[tm], wm, tm, lane, wsv_prev, kt > c.kt0);
+            } else {
+              fold4<ABITS>(y, st, 0, acc[tm], wm, tm, lane, wsv, true);
+            }
+#pragma unroll
+            for (int tn = 0; tn < TN; ++tn) {
+              acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af0, bf[tn][0], (v16i)(0), 0, 0, 0);
+              acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af1, bf[tn][1], acc[tm][tn], 0, 0, 0);
+            }
           }
         }
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
+        wait_vm_and_barrier<NDMA>();
+        c_slot = next_slot(c_slot);
       }
-      wait_vm_and_barrier<NDMA>();
+      const uint8_t* st_last = smem + prev_slot(c_slot);
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) fold4<ABITS>(y, st_last, 1, acc[tm], wm, tm, lane, wsv_prev, true);
     }
-    if constexpr (EPI == kEpiInt32) dump_block<ABITS>(a, acc, 0, m0, n0, wm, wn, lane);
-  }
 
-  // drain the clamped loads issued by the last iterations before the LDS is
-  // reused (or the workgroup ends)
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  if constexpr (!NEED_SCALE) return;
-  if constexpr (PIPE) {
-    if (unit >= 0) {
+    if (c.unit >= 0) {
       // split tail: this K range's fp32 sums of the tile, row-major [BM][BN]
-      float* P = a.partial + static_cast<size_t>(unit) * BM * BN;
+      int ln = lane;  // opaque copy: keep the addresses out of the tile loop's live registers
+      asm volatile("" : "+v"(ln));
+      float* P = a.partial + static_cast<size_t>(c.unit) * BM * BN;
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
-            const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
-            P[row * BN + wn * 64 + tn * 32 + (lane & 31)] = y[tm][tn][r];
+            const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
+            P[row * BN + wn * 64 + tn * 32 + (ln & 31)] = y[tm][tn][r];
           }
-      return;
+    } else {
+      store_tile<ABITS, EPI>(a, y, c.m0, c.n0, wm, wn, lane, ein);
     }
+    it += G;
+    if (it >= nitems) break;
   }
+  // drain the loads still in flight (the re-issued last stages) before the
+  // workgroup ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
 
-  __syncthreads();
-  store_tile<ABITS, EPI>(a, y, m0, n0, wm, wn, wave, lane, smem);
+// The non-pipelined GEMM: one output tile per workgroup, all of K.  Blocks are
+// folded (or written out) when they end.  Used for 8-bit activations whose
+// weight blocks span several stages (w_group > 128), and for the int32
+// outputs (the unfused path's C and the test hook's block dump).
+template <int ABITS, int EPI>
+__global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_simple_kernel(GemmArgs a) {
+  using LY = Layout<ABITS>;
+  using CF = Cfg<ABITS>;
+  constexpr int BM = CF::BM, BN = CF::BN, STAGES = CF::STAGES;
+  constexpr bool NEED_SCALE = (EPI == kEpiOut || EPI == kEpiPartial);
+  static_assert(!(NEED_SCALE && ABITS == 4), "4-bit activations with weight steps take the pipelined kernel");
+  constexpr int NDMA = LY::A_DMA + LY::B_DMA + (NEED_SCALE ? 1 : 0);
+
+  __shared__ __align__(1024) uint8_t smem[STAGES * LY::STAGE];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / CF::NWN, wn = wave % CF::NWN;
+  const int M = a.M, N = a.N, K = a.K;
+  const int ntm = (M + BM - 1) / BM, ntn = (N + BN - 1) / BN, nkt = K / KT;
+  int tile_m, tile_n;
+  supertile(xcd_order(blockIdx.x, gridDim.x), ntm, ntn, tile_m, tile_n);
+  const int m0 = tile_m * BM;
+  const int n0 = tile_n * BN;
+  const uint32_t smem_lds = lds_offset(smem);
+
+  StageLoads<ABITS> ld;
+  ld.set(m0, n0, M, N, K, wave, wn, lane);
+  // stage kt into slot kt % STAGES; past the last stage the source is clamped
+  // to it (the slot written is free and never read again)
+  auto issue_stage = [&](int kt_slot) {
+    ld.template issue<false, NEED_SCALE>(a, m0, n0, min(kt_slot, nkt - 1), smem_lds + (kt_slot % STAGES) * LY::STAGE,
+                                         wave);
+  };
+  const FragOffsets<ABITS> off(wm, wn, lane);
+
+  float y[TM][TN][16];
+  v16i acc[TM][TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      acc[tm][tn] = (v16i)(0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) y[tm][tn][r] = 0.0f;
+    }
+
+  issue_stage(0);
+  issue_stage(1);
+  wait_vm_and_barrier<NDMA>();
+  for (int kt = 0; kt < nkt; ++kt) {
+    issue_stage(kt + 2);
+    const uint8_t* st = smem + (kt % STAGES) * LY::STAGE;
+    float wsv[TN];
+    if constexpr (NEED_SCALE) read_wscale<ABITS>(st, wave, lane, wsv);
+    if constexpr (ABITS == 8) {
+      if ((kt * KT) % a.w_group == 0) {
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
+      }
+    }
+    uint4 pa[TM], pb[TN];
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) {
+      v4i af[TM], bf[TN];
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        if constexpr (ABITS == 8) {
+          af[tm] = *reinterpret_cast<const v4i*>(st + off.a(tm, ks));
+        } else {
+          if ((ks & 1) == 0) pa[tm] = *reinterpret_cast<const uint4*>(st + off.a(tm, ks));
+          af[tm] = (ks & 1) ? unpack_frag(pa[tm].z, pa[tm].w) : unpack_frag(pa[tm].x, pa[tm].y);
+        }
+      }
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        if ((ks & 1) == 0) pb[tn] = *reinterpret_cast<const uint4*>(st + off.b(tn, ks >> 1));
+        bf[tn] = (ks & 1) ? unpack_frag(pb[tn].z, pb[tn].w) : unpack_frag(pb[tn].x, pb[tn].y);
+      }
+      const bool zero_c = ABITS == 4 && (ks & 1) == 0;
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          if (zero_c)
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm], bf[tn], (v16i)(0), 0, 0, 0);
+          else
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm], bf[tn], acc[tm][tn], 0, 0, 0);
+        }
+      if constexpr (ABITS == 4) {
+        if ((ks & 1) == 1) dump_block<ABITS>(a, acc, kt * 2 + (ks >> 1), m0, n0, wm, wn, lane);
+      }
+    }
+    if constexpr (ABITS == 8) {
+      if (((kt + 1) * KT) % a.w_group == 0) {  // end of a weight group
+        if constexpr (EPI == kEpiDump) {
+          dump_block<ABITS>(a, acc, ((kt + 1) * KT) / a.w_group - 1, m0, n0, wm, wn, lane);
+        } else if constexpr (NEED_SCALE) {
+#pragma unroll
+          for (int t = 0; t < TM * TN; ++t) fold8(acc[t / TN][t % TN], wsv[t % TN], y[t / TN][t % TN]);
+        }
+      }
+    }
+    wait_vm_and_barrier<NDMA>();
+  }
+  if constexpr (EPI == kEpiInt32) dump_block<ABITS>(a, acc, 0, m0, n0, wm, wn, lane);
+
+  // drain the clamped loads issued by the last iterations before the LDS is
+  // reused (or the workgroup ends)
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if constexpr (NEED_SCALE) {
+    EpiInputs<ABITS, EPI> ein;
+    ein.load(a, m0, n0, wm, wn, lane);
+    store_tile<ABITS, EPI>(a, y, m0, n0, wm, wn, lane, ein);
+  }
 }
 
 // Second kernel of a split tail: adds the `split` partial sums of every
@@ -744,24 +883,28 @@ Plan plan_split(int act_bits, int epi, int32_t M, int32_t N, int32_t K, int32_t 
   return p;
 }
 
-template <int ABITS, int EPI, bool W128>
+template <int ABITS, int EPI, bool PIPE>
 hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
   GemmArgs a = a0;
-  const Plan p = plan_split(ABITS, EPI, a.M, a.N, a.K, a.w_group, device_slots(), partial ? partial_bytes : 0);
+  const int slots = device_slots();
+  const Plan p = plan_split(ABITS, EPI, a.M, a.N, a.K, a.w_group, slots, partial ? partial_bytes : 0);
   a.ndp = p.ndp;
   a.split = p.split;
   a.partial = p.split > 1 ? partial : nullptr;
   const int rest = p.ntiles - p.ndp;
-  const unsigned grid = static_cast<unsigned>(p.ndp + rest * p.split);
-  hipLaunchKernelGGL((gemm_w4_kernel<ABITS, EPI, W128>), dim3(grid), dim3(Cfg<ABITS>::NTHREADS), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || rest == 0 || p.split == 1) return e;
-  if constexpr (EPI == kEpiOut || EPI == kEpiPartial) {
+  if constexpr (PIPE) {
+    const int nitems = p.ndp + rest * p.split;
+    const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
+    hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI>), dim3(grid), dim3(Cfg<ABITS>::NTHREADS), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || rest == 0 || p.split == 1) return e;
     constexpr int per_tile_blocks = Cfg<ABITS>::BM * Cfg<ABITS>::BN / 4 / 256;
     hipLaunchKernelGGL((gemm_tail_kernel<ABITS, EPI>), dim3(rest * per_tile_blocks), dim3(256), 0, s, a);
     return hipGetLastError();
+  } else {
+    hipLaunchKernelGGL((gemm_simple_kernel<ABITS, EPI>), dim3(p.ntiles), dim3(Cfg<ABITS>::NTHREADS), 0, s, a);
+    return hipGetLastError();
   }
-  return hipErrorInvalidValue;
 }
 
 template <int EPI>
@@ -788,8 +931,8 @@ hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, 
     }
   } else {
     switch (epi) {
-      case kEpiOut: return launch_t<4, kEpiOut, false>(a, s, partial, partial_bytes);
-      case kEpiPartial: return launch_t<4, kEpiPartial, false>(a, s, partial, partial_bytes);
+      case kEpiOut: return launch_t<4, kEpiOut, true>(a, s, partial, partial_bytes);
+      case kEpiPartial: return launch_t<4, kEpiPartial, true>(a, s, partial, partial_bytes);
       case kEpiDump: return launch_t<4, kEpiDump, false>(a, s, nullptr, 0);
     }
   }
