@@ -46,7 +46,13 @@ def parse():
     p.add_argument("--gpus", type=int, default=1)
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
+    p.add_argument("--sample-every", type=int, default=4,
+                   help="record per-kernel HIP events on every n-th timed step (events cost host time)")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    p.add_argument("--suite", metavar="PATH", default=None,
+                   help="instead of the one-line benchmark, measure every layer configuration (per-layer "
+                        "kernels, the unfused path, and the 28-layer x 10-step sweep as one HIP graph) and "
+                        "write one JSON record per line to PATH")
     p.add_argument("--cpu-rows", type=int, default=0,
                    help="rows of each layer the oracle times (0 = all: one whole step)")
     return p.parse_args()
@@ -122,8 +128,160 @@ def cpu_baseline(layers, rows_per_layer):
                        f"accumulation, fp32 epilogue); weights packed beforehand; TOPS = 2*rows*K*N / time")
 
 
+def run_suite(args):
+    """Every layer configuration, one JSON record per measurement."""
+    import torch
+
+    from paper_2609_39056_amd import binding as B
+    from paper_2609_39056_amd import synth
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    B.lib()
+    BF16 = B.SQ_OUT_BF16
+    fout = open(args.suite, "w")
+
+    def emit(rec):
+        line = json.dumps(rec)
+        print(line, flush=True)
+        fout.write(line + "\n")
+        fout.flush()
+
+    def timed(fn, reps, warm=3):
+        for _ in range(warm):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps  # us per call
+
+    def alg_bytes(M, K, N):  # bf16 X, int4 W, fp16 steps, bf16 Y, bias, stream map
+        return M * K * 2 + N * K // 2 + (K // W_GROUP) * N * 2 + M * N * 2 + 2 * N + 4 * M
+
+    def layer_record(group, name, L, W, bits, reps):
+        M, K = L["x"].shape
+        N = W.N
+        act = B.ActParams(tok2stream=L["tok2stream"], gamma=L["gamma"], step=min(3, L["gamma"].shape[0] - 1),
+                          act_bits=bits, dinv=L["dinv"])
+        qx, sc = B.act_buffers(M, K, bits, dev)
+        wsg = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, K, N, bits, dev)
+        wsf = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, K, N, bits, dev)
+        wsu = B.alloc_workspace(B.SQ_VARIANT_UNFUSED, M, K, N, bits, dev)
+        y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+        us_k1 = timed(lambda: B.sq_quantize_act(L["x"], act, qx, sc), reps)
+        if bits == 8:
+            us_k2 = timed(lambda: B.sq_gemm_w4a8(qx, sc, W, y, BF16, workspace=wsg), reps)
+        else:
+            us_k2 = timed(lambda: B.sq_gemm_w4a4(qx, sc, act, W, y, BF16, workspace=wsg), reps)
+        fused = B.sq_linear_w4a8 if bits == 8 else B.sq_linear_w4a4
+        us_api = timed(lambda: fused(L["x"], act, W, y, BF16, wsf), reps)
+        us_unf = timed(lambda: B.sq_linear_unfused(L["x"], act, W, y, BF16, wsu), max(3, reps // 4))
+        ops = 2.0 * M * K * N
+        ab = alg_bytes(M, K, N)
+        k1b = M * K * 2 + (M * K if bits == 8 else M * K // 2) + (4 * M if bits == 8 else 2 * M * (K // 64)) + 4 * M
+        emit(dict(group=group, linear=name, act_bits=bits, M=M, K=K, N=N,
+                  bound="mfma" if ops / ab >= PEAK_INT8_TOPS / PEAK_HBM_GBS * 1e3 else "hbm",
+                  us_quant=round(us_k1, 2), us_gemm=round(us_k2, 2), us_layer=round(us_api, 2),
+                  tops_layer=round(ops / us_api / 1e6, 1), tops_gemm=round(ops / us_k2 / 1e6, 1),
+                  frac_int8_layer=round(ops / us_api / 1e6 / PEAK_INT8_TOPS, 4),
+                  frac_int8_gemm=round(ops / us_k2 / 1e6 / PEAK_INT8_TOPS, 4),
+                  gbs_layer=round(ab / us_api / 1e3, 1), frac_hbm_layer=round(ab / us_api / 1e3 / PEAK_HBM_GBS, 4),
+                  quant_gbs=round(k1b / us_k1 / 1e3, 1), us_unfused=round(us_unf, 2),
+                  fused_speedup=round(us_unf / us_api, 3)))
+        del qx, sc, wsg, wsf, wsu, y
+
+    def layer_group(group, linears, tokens, bits_list, outl, reps, T=10, batch=1):
+        for li, (name, (K, N)) in enumerate(linears.items()):
+            L = synth.device_layer(K, N, tokens, T=T, seed=1000 + li, outlier_frac=outl, batch=batch, device=dev)
+            W = B.prepare_weight(L.pop("w"), L["d"], W_GROUP, bias=L["bias"])
+            for bits in bits_list:
+                layer_record(group, name, L, W, bits, reps)
+            del L, W
+            torch.cuda.empty_cache()
+
+    layer_group("single 256x256 linear, 88 tokens (64+8+16), 2 steps", {"small": (256, 256)}, (64, 8, 16),
+                (8, 4), 0.02, 400, T=2)
+    layer_group("2B-class linears, W4A8, 4192 tokens (4096+32+64)", synth.LINEARS_2B, synth.TOKENS_2B, (8,), 0.02, 60)
+    layer_group("2B-class linears, W4A4, 4192 tokens, stream outliers 1%/2%/5%", synth.LINEARS_2B, synth.TOKENS_2B,
+                (4,), (0.01, 0.02, 0.05), 60)
+    layer_group("14B-class linears, 8384 tokens (8192+64+128)", synth.LINEARS_14B, synth.TOKENS_14B, (8, 4), 0.02, 12)
+
+    # ---- denoising-loop sweep: 28 layers x 10 steps x {qkv, out, up, down} of
+    # the 2B class, every layer with its own weights (0.7 GB packed: more than
+    # the 256 MB last-level cache), captured as one HIP graph
+    NL, T = 28, T_STEPS
+    lin = synth.LINEARS_2B
+    ref = {name: synth.device_layer(K, N, synth.TOKENS_2B, T=T, seed=2000 + i, device=dev, with_weight=False)
+           for i, (name, (K, N)) in enumerate(lin.items())}
+    g = torch.Generator(device=dev)
+    g.manual_seed(7)
+    weights = []
+    for layer in range(NL):
+        ws = {}
+        for name, (K, N) in lin.items():
+            w = torch.randn((N, K), generator=g, device=dev) * 0.02
+            ws[name] = B.prepare_weight(w, ref[name]["d"], W_GROUP, bias=ref[name]["bias"])
+            del w
+        weights.append(ws)
+    torch.cuda.synchronize()
+    variants = [("batch 1, 4192 tokens", synth.TOKENS_2B, 1), ("batch 4, 16768 tokens", synth.TOKENS_2B, 4),
+                ("action only, 64 tokens", (0, 0, 64), 1), ("action only, 128 tokens", (0, 0, 128), 1)]
+    for label, tokens, batch in variants:
+        inputs = {name: synth.device_layer(K, N, tokens, T=T, seed=3000 + i, batch=batch, device=dev,
+                                           with_weight=False)
+                  for i, (name, (K, N)) in enumerate(lin.items())}
+        for bits in (8, 4):
+            fused = B.sq_linear_w4a8 if bits == 8 else B.sq_linear_w4a4
+            bufs = {}
+            for name, (K, N) in lin.items():
+                M = inputs[name]["x"].shape[0]
+                bufs[name] = dict(y=torch.empty((M, N), dtype=torch.bfloat16, device=dev),
+                                  ws=B.alloc_workspace(B.SQ_VARIANT_FUSED, M, K, N, bits, dev),
+                                  acts=[B.ActParams(tok2stream=inputs[name]["tok2stream"], gamma=inputs[name]["gamma"],
+                                                    step=t, act_bits=bits, dinv=inputs[name]["dinv"])
+                                        for t in range(T)])
+
+            def sweep_once():
+                for t in range(T):
+                    for layer in range(NL):
+                        for name in lin:
+                            b = bufs[name]
+                            fused(inputs[name]["x"], b["acts"][t], weights[layer][name], b["y"], BF16, b["ws"])
+
+            sweep_once()  # eager warm-up
+            torch.cuda.synchronize()
+            us_eager = timed(sweep_once, 2, warm=0)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                sweep_once()
+            us_graph = timed(graph.replay, 5, warm=2)
+            calls = T * NL * len(lin)
+            ops = T * NL * sum(2.0 * inputs[n]["x"].shape[0] * K * N for n, (K, N) in lin.items())
+            ab = T * NL * sum(alg_bytes(inputs[n]["x"].shape[0], K, N) for n, (K, N) in lin.items())
+            emit(dict(group="denoising sweep: 28 layers x 10 steps x {qkv, out, up, down}, 2B class, one HIP graph",
+                      variant=label, act_bits=bits, calls=calls, tokens=int(inputs["up"]["x"].shape[0]),
+                      ms_graph=round(us_graph / 1e3, 3), ms_eager=round(us_eager / 1e3, 3),
+                      us_per_call=round(us_graph / calls, 2), tops=round(ops / us_graph / 1e6, 1),
+                      frac_int8=round(ops / us_graph / 1e6 / PEAK_INT8_TOPS, 4),
+                      gbs=round(ab / us_graph / 1e3, 1), frac_hbm=round(ab / us_graph / 1e3 / PEAK_HBM_GBS, 4)))
+            del graph, bufs
+        del inputs
+        torch.cuda.empty_cache()
+    fout.close()
+
+
 def main():
     args = parse()
+    if args.suite:
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        run_suite(args)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
               f"(the layer is row-parallel: each GPU would take its own slice of the tokens)", file=sys.stderr)
@@ -172,27 +330,30 @@ def main():
             act.step = tau
             fn(ly["x"], act, ly["W"], ly["y"], B.SQ_OUT_BF16, ly[ws_key][bits], stream)
 
-    # ---- main timed region: fused W4A8, events around every kernel
+    # ---- main timed region: fused W4A8; HIP events around every kernel of
+    # every n-th step (on the stream the kernels run on)
     for s in range(args.warmup):
         fused_step(s % T_STEPS)
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    every = max(1, args.sample_every)
+    sampled = list(range(0, args.steps, every))
+    evs = {s: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for s in sampled}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for s in range(args.steps):
-        fused_step(s % T_STEPS, evs[s])
+        fused_step(s % T_STEPS, evs.get(s))
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ms_per_step = wall * 1e3 / args.steps
 
     k1 = np.zeros(2)
     k2 = np.zeros(2)
-    for e in evs:
+    for e in evs.values():
         for i in range(2):
             k1[i] += e[2 * i].elapsed_time(e[2 * i + 1])
             k2[i] += e[2 * i + 1].elapsed_time(e[2 * i + 2])
-    k1 /= args.steps
-    k2 /= args.steps  # ms per launch, per layer
+    k1 /= len(evs)
+    k2 /= len(evs)  # ms per launch, per layer
 
     ops = [2.0 * M * ly["K"] * ly["N"] for ly in layers]
     ops_step = sum(ops)
@@ -268,7 +429,8 @@ def main():
             "act_bits": 8, "w_group": W_GROUP,
         },
         "roofline": {
-            "bound": "mfma", "kernel": "gemm_w4_kernel<8,0> (sq_gemm_w4a8)",
+            "bound": "mfma", "kernel": "gemm_pipe_kernel<8,0> + gemm_tail_kernel<8,0> (sq_gemm_w4a8)",
+            "launches": 2 * len(evs),
             "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",
             "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": measured_traffic(),
         },

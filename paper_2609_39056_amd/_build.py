@@ -38,12 +38,13 @@ FLAGS = [
 SOURCES = ["sq_api.cpp", "quant_act.hip", "pack_weights.hip", "gemm_w4.hip", "unfused.hip"]
 
 
-_REMARK = re.compile(r"remark: Function Name: (\S+)|remark:\s+(ScratchSize \[bytes/lane\]|VGPRs Spill|SGPRs Spill): (\d+)")
+_REMARK = re.compile(r"remark: Function Name: (\S+)|remark:\s+(ScratchSize \[bytes/lane\]|VGPRs Spill): (\d+)")
 
 
 def _check_resources(src: str, stderr: str) -> None:
     """Every kernel must keep its working set in registers and LDS: any
-    scratch (private memory) use or register spill fails the build."""
+    scratch (private memory) use or vector-register spill fails the build.
+    (Scalar registers spill into vector-register lanes, not memory.)"""
     kernel, bad = None, []
     for m in _REMARK.finditer(stderr):
         if m.group(1):

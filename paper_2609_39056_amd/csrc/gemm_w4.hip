@@ -29,6 +29,7 @@
 // casts.
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <type_traits>
 
 #include "sq_internal.h"
@@ -658,7 +659,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
-            P[row * BN + wn * 64 + tn * 32 + (ln & 31)] = y[tm][tn][r];
+            if (c.m0 + row < M) P[row * BN + wn * 64 + tn * 32 + (ln & 31)] = y[tm][tn][r];  // rows past M unused
           }
     } else {
       store_tile<ABITS, EPI>(a, y, c.m0, c.n0, wm, wn, lane, ein);
@@ -859,25 +860,37 @@ int device_slots() {
 
 constexpr size_t kUnitBytes = 128 * 128 * sizeof(float);  // partial sums of one tile range
 
-// Split plan: the tiles that fill whole rounds of `slots` run whole; each of
-// the R left over is split into S >= 2 K ranges of >= 2 stages (S * R <=
-// slots / 2 when whole rounds run, <= slots otherwise), if `partial_bytes`
-// holds R * S units.  Only the pipelined paths split (their blocks never
-// straddle a range boundary).
+// Split plan: the tiles that fill whole rounds of `slots` run whole; the R
+// left over (all of them when there are fewer tiles than slots) are each split
+// into S K ranges when that is faster.  In units of one stage of one tile on
+// one workgroup, the split tail takes about nkt / S stages plus the partial
+// sums' traffic, c * R * S with c = (rows * 128 * 8 bytes written and read
+// back) / (about 4.4 MB moved per stage time), plus about two for the extra
+// launch; S ~ sqrt(nkt / (c R)), with ranges of >= 2 stages, R * S <= slots
+// and R * S units fitting in `partial_bytes`.  Only the pipelined paths split
+// (their blocks never straddle a range boundary).
 struct Plan {
   int ntiles, ndp, split;
 };
 Plan plan_split(int act_bits, int epi, int32_t M, int32_t N, int32_t K, int32_t w_group, int slots,
                 size_t partial_bytes) {
-  const int ntiles = ((M + 127) / 128) * ((N + 127) / 128);
+  const int ntm = (M + 127) / 128, ntn = (N + 127) / 128;
+  const int ntiles = ntm * ntn;
   Plan p{ntiles, ntiles, 1};
   const bool pipe = (epi == kEpiOut || epi == kEpiPartial) && (act_bits == 4 || w_group == KT);
   const int nkt = K / KT;
   const int rest = ntiles % slots;
   if (!pipe || rest == 0 || nkt < 4) return p;
-  int split = std::min(nkt / 2, ntiles >= slots ? slots / rest / 2 : slots / rest);
+  // rows of a left-over tile: the left-over tiles are the last ones of the
+  // logical order, which lie in the last row of tiles when there are few
+  const int rows = (ntm == 1 || rest <= ntn) ? M - 128 * (ntm - 1) : 128;
+  const double c = rows * 128.0 * 8.0 / 4.4e6;
+  int split = static_cast<int>(std::lround(std::sqrt(nkt / (c * rest))));
+  split = std::min(std::min(split, nkt / 2), slots / rest);
   while (split >= 2 && static_cast<size_t>(rest) * split * kUnitBytes > partial_bytes) --split;
   if (split < 2) return p;
+  const double t_split = static_cast<double>(nkt) / split + c * rest * split + 2.0;
+  if (t_split >= nkt) return p;
   p.ndp = ntiles - rest;
   p.split = split;
   return p;

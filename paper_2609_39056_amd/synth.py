@@ -162,6 +162,50 @@ def make_layer(
     )
 
 
+def device_layer(K: int, N: int, stream_counts=(4096, 32, 64), T: int = 10, seed: int = 0,
+                 outlier_frac=0.02, batch: int = 1, device="cuda", with_weight: bool = True) -> dict:
+    """The same recipe as make_layer, drawn on the GPU with torch's seeded
+    generator, for throughput runs at sizes where drawing on the host is slow.
+    Returns device tensors: x (bf16 [M, K]), tok2stream (int32 [M]),
+    w (fp32 [N, K], when with_weight), d and dinv (fp32 [K]), bias (bf16 [N]),
+    gamma (fp32 [T, S]).  Not bit-identical to make_layer (different
+    generator); the parity tests use make_layer."""
+    import torch
+
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    S = len(stream_counts)
+    per_stream = isinstance(outlier_frac, (tuple, list))
+    fr = list(outlier_frac) if per_stream else [outlier_frac] * S
+    shared = torch.randperm(K, generator=g, device=device)
+    sets = [torch.randperm(K, generator=g, device=device)[: int(round(f * K))] if per_stream
+            else shared[: int(round(f * K))] for f in fr]
+    blocks, ids = [], []
+    for _ in range(batch):
+        for s, n in enumerate(stream_counts):
+            if n == 0:
+                continue
+            xs = torch.randn((n, K), generator=g, device=device) * STREAM_MAGNITUDE[s % len(STREAM_MAGNITUDE)]
+            xs[:, sets[s]] *= OUTLIER_GAIN
+            blocks.append(xs)
+            ids.append(torch.full((n,), s, dtype=torch.int32, device=device))
+    x = torch.cat(blocks).to(torch.bfloat16)
+    tok2stream = torch.cat(ids)
+    w = torch.randn((N, K), generator=g, device=device) * 0.02
+    bias = (torch.randn((N,), generator=g, device=device) * 0.02).to(torch.bfloat16)
+    gamma = torch.exp(torch.randn((T, S), generator=g, device=device) * 0.3)
+    amax_x = x.float().abs().amax(dim=0).double()
+    amax_w = w.abs().amax(dim=0).double()
+    ratio = torch.where(amax_w > 0, amax_x / torch.where(amax_w > 0, amax_w, torch.ones_like(amax_w)),
+                        torch.ones_like(amax_w))
+    d = torch.clamp(torch.sqrt(torch.where(ratio > 0, ratio, torch.ones_like(ratio))), 2.0**-6, 2.0**6).float()
+    out = dict(x=x.contiguous(), tok2stream=tok2stream.contiguous(), d=d.contiguous(),
+               dinv=(1.0 / d).contiguous(), bias=bias.contiguous(), gamma=gamma.contiguous())
+    if with_weight:
+        out["w"] = w.contiguous()
+    return out
+
+
 def stratified_rows(tok2stream: np.ndarray, n_video: int = 256, seed: int = 0) -> np.ndarray:
     """Row sample for oracle checks at full size: every row of the small
     streams (id != 0) plus ``n_video`` random rows of stream 0, sorted."""
@@ -173,7 +217,7 @@ def stratified_rows(tok2stream: np.ndarray, n_video: int = 256, seed: int = 0) -
 
 
 # The workload configurations (token counts per stream; linears as (K, N)).
-CFG1 = dict(name="cfg1 single 256x256 linear, 88 tokens, A8", K=256, N=256,
+SMALL_LAYER = dict(name="single 256x256 linear, 88 tokens", K=256, N=256,
             stream_counts=(64, 8, 16), T=2)
 LINEARS_2B = {"qkv": (2048, 6144), "out": (2048, 2048), "up": (2048, 8192), "down": (8192, 2048)}
 LINEARS_14B = {"qkv": (5120, 15360), "out": (5120, 5120), "up": (5120, 13824), "down": (13824, 5120)}

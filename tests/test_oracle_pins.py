@@ -300,7 +300,7 @@ def test_weight_quantizer(w_group):
 def test_quantized_layer_is_close_to_full_precision():
     """Sanity of the whole chain on the 88-token 256x256 layer: W4A8 output
     stays close to the full-precision X W (normalized error of Eq. (3))."""
-    L = synth.make_layer(**{k: v for k, v in synth.CFG1.items() if k != "name"}, seed=0)
+    L = synth.make_layer(**{k: v for k, v in synth.SMALL_LAYER.items() if k != "name"}, seed=0)
     pw = O.pack_weights(L.w, L.d, 128)
     r = O.linear(L.x_bits, L.tok2stream, L.gamma, 0, pw["codes"], pw["w_scale"], 128,
                  dinv=L.dinv, bias_bits=L.bias_bits)

@@ -155,7 +155,7 @@ FUSED = {8: B.sq_linear_w4a8, 4: B.sq_linear_w4a4}
 @pytest.mark.parametrize("mode", [0, 1])
 @pytest.mark.parametrize("out", [F32, BF16, F16])
 @pytest.mark.parametrize("G", [128, 256])
-def test_linear_cfg1(bits, mode, out, G):
+def test_linear_small_layer(bits, mode, out, G):
     """The 88-token 256 x 256 layer (64 video, 8 proprio, 16 action tokens,
     2 denoising steps), fused and unfused."""
     L = synth.make_layer(K=256, N=256, stream_counts=(64, 8, 16), T=2, seed=0)
@@ -195,7 +195,7 @@ def test_gemm_entry_points(bits, with_ws):
     """The second kernel alone, fed the oracle's codes and scales; without a
     workspace every tile is computed whole, with one the tiles are split along
     K (partial sums added by the second kernel)."""
-    L = layer(150, 512, 192, seed=5)
+    L = layer(150, 1024, 192, seed=5)
     pw, W = oracle_weight(L, 128)
     res = oracle_linear(L, 2, bits, 0, pw, 128)
     y = torch.empty((L.M, L.N), dtype=torch.float32, device="cuda")
