@@ -203,6 +203,18 @@ def run_suite(args):
             del L, W
             torch.cuda.empty_cache()
 
+    # dispatch cost of one HIP graph node: a graph of 150 one-element kernels
+    one = torch.zeros(1, device=dev)
+    one.add_(1)
+    torch.cuda.synchronize()
+    gph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(gph):
+        for _ in range(150):
+            one.add_(1)
+    emit(dict(group="dispatch cost", what="one-element kernel per HIP graph node",
+              us_per_node=round(timed(gph.replay, 10, warm=2) / 150, 2)))
+    del gph
+
     layer_group("single 256x256 linear, 88 tokens (64+8+16), 2 steps", {"small": (256, 256)}, (64, 8, 16),
                 (8, 4), 0.02, 400, T=2)
     layer_group("2B-class linears, W4A8, 4192 tokens (4096+32+64)", synth.LINEARS_2B, synth.TOKENS_2B, (8,), 0.02, 60)
