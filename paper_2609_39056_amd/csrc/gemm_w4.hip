@@ -47,20 +47,29 @@ constexpr int KT = kKTile;   // 128 channels per stage
 constexpr int TM = 2;        // 32-row MFMA tiles per wave
 constexpr int TN = 2;        // 32-col MFMA tiles per wave
 constexpr int GROUP_M = 8;   // m-tiles per supertile (L2 reuse)
+constexpr bool kPipeWide = false;  // tile shape of the pipelined kernel (see Cfg)
 
-// Workgroup shape: NWM x NWN waves of 64 x 64 outputs; a STAGES-deep LDS ring.
-// Two workgroups share a CU (LDS <= 80 KB each), so while one waits at its
-// barrier the other's waves keep the SIMDs busy.  The 4-bit path folds a
-// block from the previous stage during the current one, which must therefore
-// outlive the loads two stages ahead: four stages.
-template <int ABITS>
+// Workgroup shape: NWM x NWN waves of 64 x 64 outputs (the most a wave's
+// registers hold: an int32 accumulator and an fp32 sum per output); a
+// STAGES-deep LDS ring loaded DIST stages ahead.  The 4-bit path folds a block
+// from the previous stage during the current one, which must therefore
+// outlive the loads DIST stages ahead: one more stage.
+//   WIDE: 128 x 256 tiles, 8 waves, one workgroup per CU, loads three stages
+//   ahead.  A third fewer operand bytes per MFMA, but both waves on a SIMD
+//   then belong to one workgroup and stall at its barriers together; measured
+//   slower than two independent 128 x 128 workgroups per CU (kPipeWide).
+//   otherwise: 128 x 128 tiles, 4 waves, two workgroups per CU, loads two
+//   stages ahead.
+template <int ABITS, bool WIDE = false>
 struct Cfg {
-  static constexpr int NWM = 2, NWN = 2;
+  static constexpr int NWM = 2, NWN = WIDE ? 4 : 2;
   static constexpr int NWAVE = NWM * NWN;
   static constexpr int NTHREADS = NWAVE * 64;
   static constexpr int BM = 64 * NWM;
   static constexpr int BN = 64 * NWN;
-  static constexpr int STAGES = ABITS == 8 ? 3 : 4;
+  static constexpr int DIST = WIDE ? 3 : 2;
+  static constexpr int STAGES = DIST + (ABITS == 8 ? 1 : 2);
+  static constexpr int WGS_PER_CU = WIDE ? 1 : 2;
 };
 
 __device__ __forceinline__ v4i unpack_frag(uint32_t p0, uint32_t p1) {
@@ -156,9 +165,9 @@ __device__ __forceinline__ void wait_vm_and_barrier() {
 // k-steps.  Activations and weights use the same assignment, so every product
 // pairs equal channels, and k-steps {0, 1} cover channels [0, 64), {2, 3}
 // cover [64, 128): a 64-wide block never straddles an MFMA.
-template <int ABITS>
+template <int ABITS, bool WIDE>
 struct Layout {
-  using CF = Cfg<ABITS>;
+  using CF = Cfg<ABITS, WIDE>;
   static constexpr int A_BYTES = ABITS == 8 ? CF::BM * KT : CF::BM * KT / 2;
   static constexpr int B_BYTES = CF::BN * KT / 2;
   static constexpr int S_BYTES = ABITS == 4 ? CF::NWAVE * 256 : 0;
@@ -306,7 +315,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN]
 // multiples of 16, and a 32-row (32-column) step leaves them unchanged: the
 // offsets of the second row (column) tile are the first's plus a constant,
 // which the LDS reads take as an immediate.
-template <int ABITS>
+template <int ABITS, bool WIDE>
 struct FragOffsets {
   static constexpr int A_TILE_STEP = ABITS == 8 ? 32 * KT : 32 * (KT / 2);
   static constexpr int B_TILE_STEP = 32 * (KT / 2);
@@ -325,7 +334,7 @@ struct FragOffsets {
     }
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2)
-      b0[k2] = Layout<ABITS>::A_BYTES + bcol0 * (KT / 2) + 16 * ((2 * k2 + h) ^ ((bcol0 >> 2) & 3));
+      b0[k2] = Layout<ABITS, WIDE>::A_BYTES + bcol0 * (KT / 2) + 16 * ((2 * k2 + h) ^ ((bcol0 >> 2) & 3));
   }
   __device__ __forceinline__ int a(int tm, int ks) const { return a0[ks] + tm * A_TILE_STEP; }
   __device__ __forceinline__ int b(int tn, int k2) const { return b0[k2] + tn * B_TILE_STEP; }
@@ -334,9 +343,9 @@ struct FragOffsets {
 // This wave's direct loads of one stage: per-lane 32-bit offsets within the
 // tile (rows and columns past the matrix are clamped to the last one) and the
 // wave's LDS destinations.
-template <int ABITS>
+template <int ABITS, bool WIDE>
 struct StageLoads {
-  using LY = Layout<ABITS>;
+  using LY = Layout<ABITS, WIDE>;
   uint32_t voffA[LY::A_DMA];
   uint32_t voffB[LY::B_DMA];
   uint32_t voffS;
@@ -394,9 +403,9 @@ struct StageLoads {
 };
 
 // Weight steps of a stage for the wave's columns, widened-code factor folded in.
-template <int ABITS>
+template <int ABITS, bool WIDE>
 __device__ __forceinline__ void read_wscale(const uint8_t* st, int wave, int lane, float (&w)[TN]) {
-  using LY = Layout<ABITS>;
+  using LY = Layout<ABITS, WIDE>;
   constexpr float WFOLD = ABITS == 8 ? 0.0625f : 0.00390625f;  // 1/16 or 1/256
   const uint32_t* Wst = reinterpret_cast<const uint32_t*>(st + LY::A_BYTES + LY::B_BYTES + LY::S_BYTES + wave * 256);
 #pragma unroll
@@ -415,10 +424,10 @@ __device__ __forceinline__ void fold8(const v16i& c, float w, float (&yt)[16]) {
 
 // y += (fp32(C) * sigma_row) * Delta_W for row tile tm and both column tiles
 // (4-bit activations); sigma of block half hb from the stage at st
-template <int ABITS>
+template <int ABITS, bool WIDE>
 __device__ __forceinline__ void fold4(float (&y)[TM][TN][16], const uint8_t* st, int hb, const v16i (&c)[TN], int wm,
                                       int tm, int lane, const float (&w)[TN], bool valid) {
-  using LY = Layout<ABITS>;
+  using LY = Layout<ABITS, WIDE>;
   const uint8_t* S = st + LY::A_BYTES + LY::B_BYTES;
 #pragma unroll
   for (int r4 = 0; r4 < 4; ++r4) {
@@ -454,12 +463,14 @@ __device__ __forceinline__ void fold4(float (&y)[TM][TN][16], const uint8_t* st,
 // steps), then run its MFMAs of this block; four stages, since the previous
 // stage's group steps are still read while the stage two ahead loads.
 template <int ABITS, int EPI>
-__global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(GemmArgs a) {
-  using LY = Layout<ABITS>;
-  using CF = Cfg<ABITS>;
+__global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm_pipe_kernel(GemmArgs a) {
+  using LY = Layout<ABITS, kPipeWide>;
+  using CF = Cfg<ABITS, kPipeWide>;
+  static_assert(CF::NTHREADS == (kPipeWide ? 512 : 256) && CF::WGS_PER_CU == (kPipeWide ? 1 : 2), "launch bounds");
   constexpr int BM = CF::BM, BN = CF::BN, STAGES = CF::STAGES;
   constexpr bool A4 = ABITS == 4;
   constexpr int NDMA = LY::A_DMA + LY::B_DMA + (A4 ? 1 : 0) + 1;
+  constexpr int AHEAD = (CF::DIST - 1) * NDMA;  // loads issued after the stage waited for
   constexpr uint32_t RING = STAGES * LY::STAGE;
   static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
 
@@ -507,7 +518,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
   Item d = item_of(d_it);
   int d_kt = d.kt0;
   uint32_t d_slot = 0;  // byte offset of the ring slot the next stage goes to
-  StageLoads<ABITS> ld;
+  StageLoads<ABITS, kPipeWide> ld;
   ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
   auto issue = [&]() {
     ld.template issue<A4, true>(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
@@ -526,13 +537,14 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
     }
   };
 
-  const FragOffsets<ABITS> off(wm, wn, lane);
+  const FragOffsets<ABITS, kPipeWide> off(wm, wn, lane);
 
-  issue();
-  advance();
-  issue();
-  advance();
-  wait_vm_and_barrier<NDMA>();
+#pragma unroll
+  for (int i = 0; i < CF::DIST; ++i) {
+    issue();
+    advance();
+  }
+  wait_vm_and_barrier<AHEAD>();
 
   uint32_t c_slot = 0;  // byte offset of the ring slot of the stage being computed
   auto next_slot = [&](uint32_t s) { return s + LY::STAGE == RING ? 0u : s + LY::STAGE; };
@@ -565,7 +577,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
         issue();
         advance();
         const uint8_t* st = smem + c_slot;
-        read_wscale<ABITS>(st, wave, lane, wsv);
+        read_wscale<ABITS, kPipeWide>(st, wave, lane, wsv);
         v4i bfull[TN][4];
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
@@ -598,7 +610,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
         }
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
-        wait_vm_and_barrier<NDMA>();
+        wait_vm_and_barrier<AHEAD>();
         c_slot = next_slot(c_slot);
       }
 #pragma unroll
@@ -609,7 +621,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
         advance();
         const uint8_t* st = smem + c_slot;
         const uint8_t* st_prev = smem + prev_slot(c_slot);
-        read_wscale<ABITS>(st, wave, lane, wsv);
+        read_wscale<ABITS, kPipeWide>(st, wave, lane, wsv);
 #pragma unroll
         for (int hb = 0; hb < 2; ++hb) {
           v4i bf[TN][2];
@@ -626,9 +638,9 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
             const v4i af1 = unpack_frag(pa.z, pa.w);
             // previous block: second half of the previous stage, or first half of this one
             if (hb == 0) {
-              fold4<ABITS>(y, st_prev, 1, acc[tm], wm, tm, lane, wsv_prev, kt > c.kt0);
+              fold4<ABITS, kPipeWide>(y, st_prev, 1, acc[tm], wm, tm, lane, wsv_prev, kt > c.kt0);
             } else {
-              fold4<ABITS>(y, st, 0, acc[tm], wm, tm, lane, wsv, true);
+              fold4<ABITS, kPipeWide>(y, st, 0, acc[tm], wm, tm, lane, wsv, true);
             }
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) {
@@ -639,12 +651,12 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
         }
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
-        wait_vm_and_barrier<NDMA>();
+        wait_vm_and_barrier<AHEAD>();
         c_slot = next_slot(c_slot);
       }
       const uint8_t* st_last = smem + prev_slot(c_slot);
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) fold4<ABITS>(y, st_last, 1, acc[tm], wm, tm, lane, wsv_prev, true);
+      for (int tm = 0; tm < TM; ++tm) fold4<ABITS, kPipeWide>(y, st_last, 1, acc[tm], wm, tm, lane, wsv_prev, true);
     }
 
     if (c.unit >= 0) {
@@ -678,8 +690,9 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_pipe_kernel(Gemm
 // outputs (the unfused path's C and the test hook's block dump).
 template <int ABITS, int EPI>
 __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_simple_kernel(GemmArgs a) {
-  using LY = Layout<ABITS>;
-  using CF = Cfg<ABITS>;
+  using LY = Layout<ABITS, false>;
+  using CF = Cfg<ABITS, false>;
+  static_assert(CF::DIST == 2, "the loop below loads two stages ahead");
   constexpr int BM = CF::BM, BN = CF::BN, STAGES = CF::STAGES;
   constexpr bool NEED_SCALE = (EPI == kEpiOut || EPI == kEpiPartial);
   static_assert(!(NEED_SCALE && ABITS == 4), "4-bit activations with weight steps take the pipelined kernel");
@@ -698,7 +711,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_simple_kernel(Ge
   const int n0 = tile_n * BN;
   const uint32_t smem_lds = lds_offset(smem);
 
-  StageLoads<ABITS> ld;
+  StageLoads<ABITS, false> ld;
   ld.set(m0, n0, M, N, K, wave, wn, lane);
   // stage kt into slot kt % STAGES; past the last stage the source is clamped
   // to it (the slot written is free and never read again)
@@ -706,7 +719,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_simple_kernel(Ge
     ld.template issue<false, NEED_SCALE>(a, m0, n0, min(kt_slot, nkt - 1), smem_lds + (kt_slot % STAGES) * LY::STAGE,
                                          wave);
   };
-  const FragOffsets<ABITS> off(wm, wn, lane);
+  const FragOffsets<ABITS, false> off(wm, wn, lane);
 
   float y[TM][TN][16];
   v16i acc[TM][TN];
@@ -726,7 +739,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_simple_kernel(Ge
     issue_stage(kt + 2);
     const uint8_t* st = smem + (kt % STAGES) * LY::STAGE;
     float wsv[TN];
-    if constexpr (NEED_SCALE) read_wscale<ABITS>(st, wave, lane, wsv);
+    if constexpr (NEED_SCALE) read_wscale<ABITS, false>(st, wave, lane, wsv);
     if constexpr (ABITS == 8) {
       if ((kt * KT) % a.w_group == 0) {
 #pragma unroll
@@ -798,7 +811,7 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_simple_kernel(Ge
 // outputs per thread, 16-byte loads.
 template <int ABITS, int EPI>
 __global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
-  constexpr int BM = Cfg<ABITS>::BM, BN = Cfg<ABITS>::BN;
+  constexpr int BM = Cfg<ABITS, kPipeWide>::BM, BN = Cfg<ABITS, kPipeWide>::BN;
   constexpr int PER_TILE = BM * BN / 4;  // threads per tile
   const int g = blockIdx.x * 256 + threadIdx.x;
   const int ti = g / PER_TILE;
@@ -843,51 +856,51 @@ __global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
   }
 }
 
-// Workgroups that fit on the device at once (two per CU), capped at 512.
-int device_slots() {
+// Compute units of the current device (256 on MI355X; also the fallback when
+// there is no device, e.g. for host-only workspace queries), capped at 256.
+int device_cus() {
   static std::atomic<int> cache[64];
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 512;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
   int v = cache[dev].load(std::memory_order_relaxed);
   if (v == 0) {
     int cus = 0;
-    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 512;
-    v = std::min(2 * cus, 512);
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0) return 256;
+    v = std::min(cus, 256);
     cache[dev].store(v, std::memory_order_relaxed);
   }
   return v;
 }
 
-constexpr size_t kUnitBytes = 128 * 128 * sizeof(float);  // partial sums of one tile range
-
-// Split plan: the tiles that fill whole rounds of `slots` run whole; the R
-// left over (all of them when there are fewer tiles than slots) are each split
-// into S K ranges when that is faster.  In units of one stage of one tile on
-// one workgroup, the split tail takes about nkt / S stages plus the partial
-// sums' traffic, c * R * S with c = (rows * 128 * 8 bytes written and read
-// back) / (about 4.4 MB moved per stage time), plus about two for the extra
-// launch; S ~ sqrt(nkt / (c R)), with ranges of >= 2 stages, R * S <= slots
-// and R * S units fitting in `partial_bytes`.  Only the pipelined paths split
-// (their blocks never straddle a range boundary).
+// Split plan of the pipelined kernel (tiles of BM x BN, `slots` workgroups at
+// once): the tiles that fill whole rounds run whole; the R left over (all of
+// them when there are fewer tiles than slots) are each split into S K ranges
+// when that is faster.  In units of one stage of one tile on one workgroup,
+// the split tail takes about nkt / S stages plus the partial sums' traffic,
+// c * R * S with c = (rows * BN * 8 bytes written and read back) / (about
+// 4.4 MB moved per stage time), plus about two for the extra launch;
+// S ~ sqrt(nkt / (c R)), with ranges of >= 2 stages, R * S <= slots and R * S
+// units of BM * BN floats fitting in `partial_bytes`.  Only the pipelined
+// paths split (their blocks never straddle a range boundary).
 struct Plan {
   int ntiles, ndp, split;
 };
-Plan plan_split(int act_bits, int epi, int32_t M, int32_t N, int32_t K, int32_t w_group, int slots,
-                size_t partial_bytes) {
-  const int ntm = (M + 127) / 128, ntn = (N + 127) / 128;
+template <int BM, int BN>
+Plan plan_split(bool pipe, int32_t M, int32_t N, int32_t K, int slots, size_t partial_bytes) {
+  const int ntm = (M + BM - 1) / BM, ntn = (N + BN - 1) / BN;
   const int ntiles = ntm * ntn;
   Plan p{ntiles, ntiles, 1};
-  const bool pipe = (epi == kEpiOut || epi == kEpiPartial) && (act_bits == 4 || w_group == KT);
   const int nkt = K / KT;
   const int rest = ntiles % slots;
   if (!pipe || rest == 0 || nkt < 4) return p;
   // rows of a left-over tile: the left-over tiles are the last ones of the
   // logical order, which lie in the last row of tiles when there are few
-  const int rows = (ntm == 1 || rest <= ntn) ? M - 128 * (ntm - 1) : 128;
-  const double c = rows * 128.0 * 8.0 / 4.4e6;
+  const int rows = (ntm == 1 || rest <= ntn) ? M - BM * (ntm - 1) : BM;
+  const double c = rows * static_cast<double>(BN) * 8.0 / 4.4e6;
   int split = static_cast<int>(std::lround(std::sqrt(nkt / (c * rest))));
   split = std::min(std::min(split, nkt / 2), slots / rest);
-  while (split >= 2 && static_cast<size_t>(rest) * split * kUnitBytes > partial_bytes) --split;
+  constexpr size_t unit = static_cast<size_t>(BM) * BN * sizeof(float);
+  while (split >= 2 && static_cast<size_t>(rest) * split * unit > partial_bytes) --split;
   if (split < 2) return p;
   const double t_split = static_cast<double>(nkt) / split + c * rest * split + 2.0;
   if (t_split >= nkt) return p;
@@ -896,26 +909,38 @@ Plan plan_split(int act_bits, int epi, int32_t M, int32_t N, int32_t K, int32_t 
   return p;
 }
 
+template <int ABITS>
+Plan pipe_plan(int32_t M, int32_t N, int32_t K, size_t partial_bytes) {
+  using CF = Cfg<ABITS, kPipeWide>;
+  return plan_split<CF::BM, CF::BN>(true, M, N, K, device_cus() * CF::WGS_PER_CU, partial_bytes);
+}
+
 template <int ABITS, int EPI, bool PIPE>
 hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
   GemmArgs a = a0;
-  const int slots = device_slots();
-  const Plan p = plan_split(ABITS, EPI, a.M, a.N, a.K, a.w_group, slots, partial ? partial_bytes : 0);
-  a.ndp = p.ndp;
-  a.split = p.split;
-  a.partial = p.split > 1 ? partial : nullptr;
-  const int rest = p.ntiles - p.ndp;
   if constexpr (PIPE) {
+    using CF = Cfg<ABITS, kPipeWide>;
+    const int slots = device_cus() * CF::WGS_PER_CU;
+    const Plan p = pipe_plan<ABITS>(a.M, a.N, a.K, partial ? partial_bytes : 0);
+    a.ndp = p.ndp;
+    a.split = p.split;
+    a.partial = p.split > 1 ? partial : nullptr;
+    const int rest = p.ntiles - p.ndp;
     const int nitems = p.ndp + rest * p.split;
     const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
-    hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI>), dim3(grid), dim3(Cfg<ABITS>::NTHREADS), 0, s, a);
+    hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || rest == 0 || p.split == 1) return e;
-    constexpr int per_tile_blocks = Cfg<ABITS>::BM * Cfg<ABITS>::BN / 4 / 256;
+    constexpr int per_tile_blocks = CF::BM * CF::BN / 4 / 256;
     hipLaunchKernelGGL((gemm_tail_kernel<ABITS, EPI>), dim3(rest * per_tile_blocks), dim3(256), 0, s, a);
     return hipGetLastError();
   } else {
-    hipLaunchKernelGGL((gemm_simple_kernel<ABITS, EPI>), dim3(p.ntiles), dim3(Cfg<ABITS>::NTHREADS), 0, s, a);
+    using CF = Cfg<ABITS, false>;
+    const int ntiles = ((a.M + CF::BM - 1) / CF::BM) * ((a.N + CF::BN - 1) / CF::BN);
+    a.ndp = ntiles;
+    a.split = 1;
+    a.partial = nullptr;
+    hipLaunchKernelGGL((gemm_simple_kernel<ABITS, EPI>), dim3(ntiles), dim3(CF::NTHREADS), 0, s, a);
     return hipGetLastError();
   }
 }
@@ -929,8 +954,11 @@ hipError_t launch_a8(const GemmArgs& a, hipStream_t s, float* partial, size_t pa
 }  // namespace
 
 size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t w_group) {
-  const Plan p = plan_split(act_bits, kEpiOut, M, N, K, w_group, device_slots(), ~static_cast<size_t>(0));
-  return static_cast<size_t>(p.ntiles - p.ndp) * (p.split > 1 ? p.split : 0) * kUnitBytes;
+  if (act_bits == 8 && w_group != KT) return 0;  // the non-pipelined kernel never splits
+  const Plan p = act_bits == 8 ? pipe_plan<8>(M, N, K, ~static_cast<size_t>(0))
+                               : pipe_plan<4>(M, N, K, ~static_cast<size_t>(0));
+  const size_t unit = static_cast<size_t>(Cfg<8, kPipeWide>::BM) * Cfg<8, kPipeWide>::BN * sizeof(float);
+  return static_cast<size_t>(p.ntiles - p.ndp) * (p.split > 1 ? p.split : 0) * unit;
 }
 
 hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
