@@ -34,7 +34,8 @@ PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
 COPY_MIB = 512               # plain device copy run after the timed region (counter calibration)
 TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_w4a8_2B_mlp_M4192_hbm_traffic.md")
-GEMM_SOURCES = ("paper_2609_39056_amd/csrc/gemm_w4.hip", "paper_2609_39056_amd/csrc/sq_internal.h")
+GEMM_SOURCES = ("paper_2609_39056_amd/csrc/gemm_w4.hip", "paper_2609_39056_amd/csrc/gemm_frag.h",
+                "paper_2609_39056_amd/csrc/sq_internal.h")
 TOKENS = (4096, 32, 64)
 LINEARS = (("up", 2048, 8192), ("down", 8192, 2048))
 T_STEPS = 10
@@ -148,15 +149,24 @@ def run_suite(args):
         fout.flush()
 
     def timed(fn, reps, warm=3):
+        """Device time per call: `reps` calls captured as one HIP graph, so the
+        host's launch rate does not bound small layers; one warm replay, then
+        one timed replay."""
         for _ in range(warm):
             fn()
         torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                fn()
+        g.replay()
+        torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        for _ in range(reps):
-            fn()
+        g.replay()
         e1.record()
         torch.cuda.synchronize()
+        del g
         return e0.elapsed_time(e1) * 1e3 / reps  # us per call
 
     def alg_bytes(M, K, N):  # bf16 X, int4 W, fp16 steps, bf16 Y, bias, stream map

@@ -1,0 +1,75 @@
+// Register-level pieces shared by the GEMM kernels: operand types, the int4
+// widening of packed fragments, the 8-bit block fold, the quad transpose of
+// the register epilogue and raw buffer resources.
+#pragma once
+
+#include "sq_internal.h"
+
+namespace sq {
+namespace {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+typedef float float2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));  // converted with round to nearest even
+typedef __attribute__((address_space(3))) uint8_t lds_u8_t;
+
+constexpr int KT = kKTile;   // 128 channels per stage
+
+__device__ __forceinline__ v4i unpack_frag(uint32_t p0, uint32_t p1) {
+  uint32_t l0, h0, l1, h1;
+  unpack_int4x8_times16(p0, l0, h0);
+  unpack_int4x8_times16(p1, l1, h1);
+  v4i r;
+  r[0] = static_cast<int>(l0);
+  r[1] = static_cast<int>(h0);
+  r[2] = static_cast<int>(l1);
+  r[3] = static_cast<int>(h1);
+  return r;
+}
+
+// 4 x 4 transpose across the lanes of a quad (lane i = lane & 3): in, lane i
+// holds v[q] = element (row q, column i); out, it holds v[j] = element
+// (row i, column j).  Two exchanges through DPP quad permutations (VALU only):
+// with lane ^ 1 the rows whose low bit differs from the lane's, then with
+// lane ^ 2 the column pairs of the row the partner keeps.
+__device__ __forceinline__ float dpp_xor1(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0xB1, 0xF, 0xF, false));  // quad_perm [1,0,3,2]
+}
+__device__ __forceinline__ float dpp_xor2(float x) {
+  return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(x), 0x4E, 0xF, 0xF, false));  // quad_perm [2,3,0,1]
+}
+__device__ __forceinline__ void quad_transpose(float (&v)[4], int lane) {
+  const bool o1 = lane & 1, o2 = lane & 2;
+  // after stage 1 lane i holds rows p, p + 2 (p = i & 1) at columns (i & ~1) + {0, 1}
+  const float r0 = dpp_xor1(o1 ? v[0] : v[1]);
+  const float r1 = dpp_xor1(o1 ? v[2] : v[3]);
+  const float a00 = o1 ? r0 : v[0], a01 = o1 ? v[1] : r0;
+  const float a10 = o1 ? r1 : v[2], a11 = o1 ? v[3] : r1;
+  // stage 2: lanes with bit 1 clear keep row p, the others row p + 2
+  const float u0 = dpp_xor2(o2 ? a00 : a10);
+  const float u1 = dpp_xor2(o2 ? a01 : a11);
+  v[0] = o2 ? u0 : a00;
+  v[1] = o2 ? u1 : a01;
+  v[2] = o2 ? a10 : u0;
+  v[3] = o2 ? a11 : u1;
+}
+
+// y += fp32(C) * Delta_W for one 32 x 32 tile (8-bit activations)
+__device__ __forceinline__ void fold8(const v16i& c, float w, float (&yt)[16]) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) yt[r] = __builtin_fmaf(static_cast<float>(c[r]), w, yt[r]);
+}
+
+// Word 3 of a raw buffer resource (32-bit data format, no swizzle).
+constexpr int kBufWord3 = 0x00020000;
+
+// Raw buffer resource over [base, base + bytes): loads past the end return 0.
+template <typename T>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const T* base, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<T*>(base), 0, bytes, kBufWord3);
+}
+
+}  // namespace
+}  // namespace sq
