@@ -1,6 +1,6 @@
 // Weight-streaming GEMM for few tokens (the second fused kernel of Sec. 4.4
-// when the layer runs the action and proprioception streams alone): same
-// operands, block accumulation and epilogue as the tiled kernel.
+// when a layer runs the action and proprioception streams alone, at most 128
+// tokens): the operands, block accumulation and epilogue of the tiled kernel.
 #include <algorithm>
 
 #include "gemm_frag.h"
@@ -11,36 +11,42 @@ namespace {
 
 constexpr int TM = 2;  // 32-row MFMA tiles per wave
 
-// Skinny GEMM for few tokens (M <= kSkinnyMaxM; 8-bit activations, one weight
-// step per 128 input channels).  The work is streaming the weights.  A
-// workgroup owns 64 rows x 32 output channels over a range of K; its four waves
-// take alternate stages of that range and keep their own fp32 sums, which are
-// added through LDS in wave order at the end.  Operands go straight from
-// global memory into registers (the codes of <= 128 tokens stay in L2), one
-// stage ahead, so the main loop has no LDS traffic and no barriers.  When the
-// output channels alone give too few workgroups, K is also split across
-// workgroups: each leaves fp32 sums of its 64 x 32 outputs, which a second
-// kernel adds in range order.
+// The work is streaming the weights.  A workgroup owns 64 rows x 32 output
+// channels over a range of K; its four waves take alternate stages of that
+// range and keep their own fp32 sums, added through LDS in wave order at the
+// end, each wave then finishing a quarter of the outputs.  Every byte of a
+// stage (activation codes, packed weights, weight steps) is copied by direct
+// global -> LDS loads into the wave's own ring of LDS slots, loaded two stages
+// ahead: 1 KB per instruction, so the activation rows that all workgroups
+// read go through the vector memory path in whole cache lines.  Each wave
+// reads only what it loaded itself, so the main loop waits on its own load
+// counter and has no barriers.  When the output channels alone give too few
+// workgroups, K is also split across workgroups: each leaves fp32 sums of its
+// 64 x 32 outputs, which a second kernel adds in range order.
 constexpr int SK_BM = 64;  // rows per workgroup
 constexpr int SK_BN = 32;  // output channels per workgroup
+constexpr int SK_DIST = 2;                  // stages loaded ahead
+constexpr int SK_SLOTS = SK_DIST + 1;       // ring slots per wave
+constexpr int SK_A = SK_BM * KT;            // activation codes of a stage (8 KB)
+constexpr int SK_B = SK_BN * (KT / 2);      // packed weights of a stage (2 KB)
+constexpr int SK_SLOT = SK_A + SK_B + 256;  // + the 32 fp16 weight steps (one 256 B load)
+constexpr int SK_NDMA = SK_A / 1024 + SK_B / 1024 + 1;  // direct loads per stage and wave
+static_assert(4 * SK_BM * SK_BN * 4 <= 4 * SK_SLOTS * SK_SLOT, "the wave sums fit in the ring");
 
-// The operands of one stage for one lane: activation fragments of the two
-// 32-row tiles (16 bytes per k-step), the packed weight chunks of the two
-// k-step pairs, and the column's fp16 weight step.
-struct SkinnyFrag {
-  v4i a[TM][4];
-  v4u b[2];
-  uint32_t w;
-};
-
+// LDS layout of a slot (16-byte chunks XOR-swizzled, as in the tiled kernel,
+// so that fragment reads are free of bank conflicts):
+//   activation row r (128 B) at r * 128, chunk c at position c ^ ((r >> 1) & 7)
+//   weight column n (64 B) at SK_A + n * 64, chunk c at position c ^ ((n >> 2) & 3)
+//   weight steps at SK_A + SK_B: dword i holds columns 2i, 2i + 1
+// Lane (column n = lane & 31, h = lane >> 5) feeds k-step s of a stage with the
+// channels [64 (s >> 1) + 32 h + 16 (s & 1), +16) of both operands.
 template <int EPI>
-__global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GemmArgs a) {
-  __shared__ float red[3][TM * 16][64];  // sums of waves 1..3
+__global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
+  __shared__ __attribute__((aligned(16))) uint8_t ring[4][SK_SLOTS][SK_SLOT];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int M = a.M, N = a.N, K = a.K;
   const int nkt = K / KT;
-  const int strips = N / SK_BN;
   const int S = a.split;
   const int strip = blockIdx.x / S, range = blockIdx.x % S;
   const int m0 = blockIdx.y * SK_BM, n0 = strip * SK_BN;
@@ -48,30 +54,44 @@ __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GemmArgs a) {
   const int h = lane >> 5, col = lane & 31;
   const int rows = min(M - m0, SK_BM);
 
-  // Sources as buffer loads (an optimiser cannot merge those across the
-  // loop's two register sets, which would undo the prefetch).  Activation
-  // rows past the matrix read the last row; the stage offset goes in the
-  // scalar offset.
-  const __amdgpu_buffer_rsrc_t rA = buffer_rsrc(static_cast<const int8_t*>(a.qx) + static_cast<size_t>(m0) * K, rows * K);
-  const __amdgpu_buffer_rsrc_t rB = buffer_rsrc(a.qw + static_cast<size_t>(n0) * (K / 2), SK_BN * (K / 2));
-  const __amdgpu_buffer_rsrc_t rW = buffer_rsrc(a.w_scale + n0, ((nkt - 1) * N + SK_BN) * 2);
-  int aoff[TM];
+  // direct-load sources: rows past the matrix read its last row
+  uint32_t voffA[SK_A / 1024];
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm) aoff[tm] = min(tm * 32 + col, rows - 1) * K + 32 * h;
-  const int boff = col * (K / 2) + 16 * h;
-
-  auto load = [&](int kt, SkinnyFrag& f) {
+  for (int i = 0; i < SK_A / 1024; ++i) {
+    const int r = 8 * i + (lane >> 3);
+    voffA[i] = static_cast<uint32_t>(min(r, rows - 1) * K + 16 * ((lane & 7) ^ ((r >> 1) & 7)));
+  }
+  uint32_t voffB[SK_B / 1024];
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+  for (int i = 0; i < SK_B / 1024; ++i) {
+    const int n = 16 * i + (lane >> 2);
+    voffB[i] = static_cast<uint32_t>(n * (K / 2) + 16 * ((lane & 3) ^ ((n >> 2) & 3)));
+  }
+  const uint32_t voffW = 4 * (lane & 15);  // lanes 16..63 repeat the 16 dwords
+  const uint32_t ring0 = lds_offset(&ring[wave][0][0]);
+  const int8_t* qx = static_cast<const int8_t*>(a.qx) + static_cast<size_t>(m0) * K;
+  const uint8_t* qw = a.qw + static_cast<size_t>(n0) * (K / 2);
+  auto issue = [&](int kt, int slot) {
+    const uint32_t st = ring0 + slot * SK_SLOT;
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks)
-        f.a[tm][ks] = __builtin_bit_cast(
-            v4i, __builtin_amdgcn_raw_buffer_load_b128(rA, aoff[tm] + 64 * (ks >> 1) + 16 * (ks & 1), kt * KT, 0));
+    for (int i = 0; i < SK_A / 1024; ++i) dma<16>(qx + kt * KT, voffA[i], st + i * 1024);
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) f.b[k2] = __builtin_amdgcn_raw_buffer_load_b128(rB, boff + 32 * k2, kt * (KT / 2), 0);
-    f.w = __builtin_amdgcn_raw_buffer_load_b16(rW, col * 2, kt * N * 2, 0);  // group-major steps, one group per stage
-    __builtin_amdgcn_sched_barrier(0);  // keep the stage's loads ahead of the work after them
+    for (int i = 0; i < SK_B / 1024; ++i) dma<16>(qw + kt * (KT / 2), voffB[i], st + SK_A + i * 1024);
+    dma<4>(a.w_scale + static_cast<size_t>(kt) * N + n0, voffW, st + SK_A + SK_B);  // group-major steps
   };
+
+  // fragment offsets within a slot
+  int aoff[TM][4];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+    const int r = tm * 32 + col;
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks) aoff[tm][ks] = r * 128 + 16 * ((4 * (ks >> 1) + 2 * h + (ks & 1)) ^ ((r >> 1) & 7));
+  }
+  int boff[2];
+#pragma unroll
+  for (int k2 = 0; k2 < 2; ++k2) boff[k2] = SK_A + col * 64 + 16 * ((2 * k2 + h) ^ ((col >> 2) & 3));
+  const int woff = SK_A + SK_B + 4 * (col >> 1);
 
   float y[TM][16];
   v16i acc[TM];
@@ -83,69 +103,85 @@ __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GemmArgs a) {
   }
   float wprev = 0.0f;  // the fold before the first block adds 0
 
-  // y += fp32(C) * Delta_W of the previous block, then this block's MFMAs; a
-  // stage that is not this wave's folds with step 0 (adds exactly 0)
-  auto compute = [&](const SkinnyFrag& f, bool valid) {
+  // y += fp32(C) * Delta_W of the previous block, then this block's MFMAs
+  auto compute = [&](int slot) {
+    const uint8_t* st = &ring[wave][slot][0];
+    // every LDS read of the stage first: one latency per stage
+    uint4 pb[2];
+    v4i af[TM][4];
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) pb[k2] = *reinterpret_cast<const uint4*>(st + boff[k2]);
+    const uint32_t wpair = *reinterpret_cast<const uint32_t*>(st + woff);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int ks = 0; ks < 4; ++ks) af[tm][ks] = *reinterpret_cast<const v4i*>(st + aoff[tm][ks]);
+    __builtin_amdgcn_sched_barrier(0);
     v4i bf[4];
-    bf[0] = unpack_frag(f.b[0][0], f.b[0][1]);
-    bf[1] = unpack_frag(f.b[0][2], f.b[0][3]);
-    bf[2] = unpack_frag(f.b[1][0], f.b[1][1]);
-    bf[3] = unpack_frag(f.b[1][2], f.b[1][3]);
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      bf[2 * k2] = unpack_frag(pb[k2].x, pb[k2].y);
+      bf[2 * k2 + 1] = unpack_frag(pb[k2].z, pb[k2].w);
+    }
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
       fold8(acc[tm], wprev, y[tm]);
-      acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.a[tm][0], bf[0], (v16i)(0), 0, 0, 0);
+      acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][0], bf[0], (v16i)(0), 0, 0, 0);
 #pragma unroll
-      for (int ks = 1; ks < 4; ++ks) acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(f.a[tm][ks], bf[ks], acc[tm], 0, 0, 0);
+      for (int ks = 1; ks < 4; ++ks) acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[ks], acc[tm], 0, 0, 0);
     }
-    wprev = valid ? f16_to_f32(f.w) * 0.0625f : 0.0f;  // widened weight codes carry a factor 16
+    // widened weight codes carry a factor 16
+    wprev = f16_to_f32((col & 1) ? (wpair >> 16) : (wpair & 0xFFFFu)) * 0.0625f;
   };
 
-  // this wave's stages kt0 + wave + 4j, j < nst, a pair per iteration in two
-  // register sets.  The body has no branch, so every load stays ahead of its
-  // use: the next stage is always loaded (past the end, the last one again)
-  // and each wait leaves one stage of loads in flight.  With nst odd the
-  // pair's second stage is a repeat that folds with step 0.
+  // this wave's stages kt0 + wave + 4j, j < nst; past the end the last stage
+  // is loaded again, so every wait leaves the same number of loads in flight
   const int nst = kt1 - kt0 > wave ? (kt1 - kt0 - wave + 3) / 4 : 0;
   auto stage = [&](int j) { return kt0 + wave + 4 * min(j, nst - 1); };
-  SkinnyFrag f0, f1;
   if (nst > 0) {
-    load(stage(0), f0);
-    for (int j = 0; j < nst; j += 2) {
-      load(stage(j + 1), f1);
-      compute(f0, true);
-      load(stage(j + 2), f0);
-      compute(f1, j + 1 < nst);
+#pragma unroll
+    for (int p = 0; p < SK_DIST; ++p) issue(stage(p), p);
+    for (int j = 0; j < nst; ++j) {
+      wait_vm<SK_NDMA * (SK_DIST - 1)>();             // stage j has landed
+      issue(stage(j + SK_DIST), (j + SK_DIST) % SK_SLOTS);  // into the slot read last iteration
+      compute(j % SK_SLOTS);
     }
   }
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) fold8(acc[tm], wprev, y[tm]);
 
-  // add the four waves' sums in wave order
-  if (wave > 0) {
+  // the four waves' sums, added in wave order; wave g then finishes register
+  // group g of both tiles: rows tm * 32 + 8 g + 4 h + q, q < 4
+  wait_vm<0>();     // no direct load still writes the ring
+  __syncthreads();  // and no wave still reads it
+  float* red = reinterpret_cast<float*>(&ring[0][0][0]);  // [wave][tm * 16 + r][lane]
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+  for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) red[wave - 1][tm * 16 + r][lane] = y[tm][r];
-  }
+    for (int r = 0; r < 16; ++r) red[(wave * 32 + tm * 16 + r) * 64 + lane] = y[tm][r];
   __syncthreads();
-  if (wave != 0) return;
+  const int g = wave;
+  float v[TM][4];
 #pragma unroll
-  for (int w = 0; w < 3; ++w)
+  for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+    for (int q = 0; q < 4; ++q) {
+      const int r = 4 * g + q;
+      float t = red[(tm * 16 + r) * 64 + lane];
 #pragma unroll
-      for (int r = 0; r < 16; ++r) y[tm][r] += red[w][tm * 16 + r][lane];
+      for (int w = 1; w < 4; ++w) t += red[(w * 32 + tm * 16 + r) * 64 + lane];
+      v[tm][q] = t;
+    }
 
   if (S > 1) {
     // this K range's sums, [row][col] of the 64 x 32 block (rows < M)
-    float* P = a.partial + (static_cast<size_t>(blockIdx.y * strips + strip) * S + range) * (SK_BM * SK_BN);
+    float* P = a.partial + (static_cast<size_t>(blockIdx.y * (N / SK_BN) + strip) * S + range) * (SK_BM * SK_BN);
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int row = tm * 32 + (r >> 2) * 8 + h * 4 + (r & 3);
-        if (m0 + row < M) P[row * SK_BN + col] = y[tm][r];
+      for (int q = 0; q < 4; ++q) {
+        const int row = tm * 32 + 8 * g + 4 * h + q;
+        if (row < rows) P[row * SK_BN + col] = v[tm][q];
       }
     return;
   }
@@ -153,42 +189,39 @@ __global__ __launch_bounds__(256, 2) void gemm_skinny_kernel(GemmArgs a) {
   // a quad transpose gives each lane four consecutive channels of one row
   float rowf = 1.0f, bias = 0.0f;
   if constexpr (EPI == kEpiOut) {
-    rowf = static_cast<const float*>(a.act_scale)[min(m0 + lane, M - 1)];
+    rowf = static_cast<const float*>(a.act_scale)[m0 + min(lane, rows - 1)];
     if (a.bias != nullptr) bias = bf16_to_f32(a.bias[n0 + col]);
   }
   const int rf_bits = __float_as_int(rowf);
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm)
+  for (int tm = 0; tm < TM; ++tm) {
+    float o[4];
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      float v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r = g * 4 + q;
-        const float rf = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 32 + g * 8 + h * 4 + q) * 4, rf_bits));
-        v[q] = EPI == kEpiPartial ? y[tm][r] : __builtin_fmaf(y[tm][r], rf, bias);
-      }
-      quad_transpose(v, lane);
-      const int m = m0 + tm * 32 + g * 8 + h * 4 + (lane & 3);
-      const int n = n0 + (lane & 28);
-      if (m < M) {
-        if (f32out) {
-          *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * N + n) =
-              make_float4(v[0], v[1], v[2], v[3]);
+    for (int q = 0; q < 4; ++q) {
+      const float rf = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 32 + 8 * g + 4 * h + q) * 4, rf_bits));
+      o[q] = EPI == kEpiPartial ? v[tm][q] : __builtin_fmaf(v[tm][q], rf, bias);
+    }
+    quad_transpose(o, lane);
+    const int row = tm * 32 + 8 * g + 4 * h + (lane & 3);
+    const int n = n0 + (lane & 28);
+    if (row < rows) {
+      const size_t m = static_cast<size_t>(m0 + row);
+      if (f32out) {
+        *reinterpret_cast<float4*>(static_cast<float*>(a.out) + m * N + n) = make_float4(o[0], o[1], o[2], o[3]);
+      } else {
+        uint2 w;
+        if (a.out_dtype == SQ_OUT_BF16) {
+          const bf16x2 lo = __builtin_convertvector((float2v){o[0], o[1]}, bf16x2);
+          const bf16x2 hi = __builtin_convertvector((float2v){o[2], o[3]}, bf16x2);
+          w = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
         } else {
-          uint2 w;
-          if (a.out_dtype == SQ_OUT_BF16) {
-            const bf16x2 lo = __builtin_convertvector((float2v){v[0], v[1]}, bf16x2);
-            const bf16x2 hi = __builtin_convertvector((float2v){v[2], v[3]}, bf16x2);
-            w = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
-          } else {
-            w = make_uint2(f32_to_f16(v[0]) | (f32_to_f16(v[1]) << 16), f32_to_f16(v[2]) | (f32_to_f16(v[3]) << 16));
-          }
-          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + static_cast<size_t>(m) * N + n) = w;
+          w = make_uint2(f32_to_f16(o[0]) | (f32_to_f16(o[1]) << 16), f32_to_f16(o[2]) | (f32_to_f16(o[3]) << 16));
         }
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + m * N + n) = w;
       }
     }
+  }
 }
 
 // Second kernel of a split skinny GEMM: adds the `split` partial sums of every
@@ -240,12 +273,22 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
 
 }  // namespace
 
-// K ranges per strip of the skinny GEMM: about one workgroup per CU, with at
-// least four stages (one per wave) in every range.
+// K ranges per strip: S workgroups share a strip when that shortens its
+// waves' stage chains by more than the second kernel costs.  Measured on
+// MI355X: a stage costs a wave about 0.65 us, the second kernel and its
+// launch about 5 us, i.e. about 8 stages.  At most one workgroup per CU (one
+// fits, by LDS), and at least four stages (one per wave) in every range.
 static int skinny_split(int32_t M, int32_t N, int32_t K) {
   const int blocks = (N / SK_BN) * ((M + SK_BM - 1) / SK_BM);
   const int nkt = K / KT;
-  return std::max(1, std::min(device_cus() / blocks, nkt / 4));
+  const int smax = std::max(1, std::min(device_cus() / blocks, nkt / 4));
+  int best = 1;
+  double best_cost = (nkt + 3) / 4;
+  for (int S = 2; S <= smax; ++S) {
+    const double cost = (nkt / S + 3) / 4 + 8.0;
+    if (cost < best_cost) best = S, best_cost = cost;
+  }
+  return best;
 }
 size_t skinny_partial_bytes(int32_t M, int32_t N, int32_t K) {
   const int S = skinny_split(M, N, K);

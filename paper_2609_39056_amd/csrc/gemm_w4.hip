@@ -87,37 +87,6 @@ __device__ __forceinline__ void supertile(int lid, int ntm, int ntn, int& tm, in
   tn = in_group / gm;
 }
 
-// LDS byte offset of a __shared__ object.
-__device__ __forceinline__ uint32_t lds_offset(const void* p) {
-  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_u8_t*)p));
-}
-
-// One direct global -> LDS load per lane (16 or 4 bytes) from base + voff:
-// lane i's data lands at LDS offset `lds` + i * SIZE.  `base` and `lds` must
-// be wave-uniform (an SGPR pair and M0); the per-lane part is a 32-bit offset.
-// Issued from inline asm so that the compiler, which cannot see which LDS
-// bytes such a load writes, does not wait for all of them before every LDS
-// read; the kernel waits for them explicitly (wait_vm_and_barrier).  Nothing
-// else in these kernels uses M0.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"
-template <int SIZE>
-__device__ __forceinline__ void dma(const void* base, uint32_t voff, uint32_t lds) {
-  // readfirstlane returns a signed int: widen through uint32_t (no sign extension)
-  const uint64_t b = reinterpret_cast<uint64_t>(base);
-  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(b))));
-  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(static_cast<uint32_t>(b >> 32))));
-  const uint64_t sb = (static_cast<uint64_t>(hi) << 32) | static_cast<uint64_t>(lo);
-  const uint32_t m0v = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(lds)));
-  if constexpr (SIZE == 16) {
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(m0v), "v"(voff), "s"(sb) : "memory", "m0");
-  } else {
-    static_assert(SIZE == 4, "unsupported size");
-    asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dword %1, %2" ::"s"(m0v), "v"(voff), "s"(sb) : "memory", "m0");
-  }
-}
-#pragma clang diagnostic pop
-
 // Wait until at most N of this wave's vector-memory operations are in flight
 // and all of its LDS reads are done, then synchronize the workgroup: after it
 // the stage about to be read has landed and no wave still reads the slot the
