@@ -15,34 +15,45 @@ constexpr int TM = 2;  // 32-row MFMA tiles per wave
 // channels over a range of K; its four waves take alternate stages of that
 // range and keep their own fp32 sums, added through LDS in wave order at the
 // end, each wave then finishing a quarter of the outputs.  Every byte of a
-// stage (activation codes, packed weights, weight steps) is copied by direct
-// global -> LDS loads into the wave's own ring of LDS slots, loaded two stages
-// ahead: 1 KB per instruction, so the activation rows that all workgroups
-// read go through the vector memory path in whole cache lines.  Each wave
-// reads only what it loaded itself, so the main loop waits on its own load
-// counter and has no barriers.  When the output channels alone give too few
-// workgroups, K is also split across workgroups: each leaves fp32 sums of its
-// 64 x 32 outputs, which a second kernel adds in range order.
+// stage (activation codes, 4-bit group steps, packed weights, weight steps)
+// is copied by direct global -> LDS loads into the wave's own ring of LDS
+// slots, loaded two stages ahead: whole cache lines per instruction, so the
+// activation rows that every workgroup reads cost little on the vector memory
+// path.  Each wave reads only what it loaded itself, so the main loop waits on
+// its own load counter and has no barriers.  When the output channels alone
+// give too few workgroups, K is also split across workgroups: each leaves
+// fp32 sums of its 64 x 32 outputs, which a second kernel adds in range order.
 constexpr int SK_BM = 64;  // rows per workgroup
 constexpr int SK_BN = 32;  // output channels per workgroup
-constexpr int SK_DIST = 2;                  // stages loaded ahead
-constexpr int SK_SLOTS = SK_DIST + 1;       // ring slots per wave
-constexpr int SK_A = SK_BM * KT;            // activation codes of a stage (8 KB)
-constexpr int SK_B = SK_BN * (KT / 2);      // packed weights of a stage (2 KB)
-constexpr int SK_SLOT = SK_A + SK_B + 256;  // + the 32 fp16 weight steps (one 256 B load)
-constexpr int SK_NDMA = SK_A / 1024 + SK_B / 1024 + 1;  // direct loads per stage and wave
-static_assert(4 * SK_BM * SK_BN * 4 <= 4 * SK_SLOTS * SK_SLOT, "the wave sums fit in the ring");
+constexpr int SK_DIST = 2;             // stages loaded ahead
+constexpr int SK_SLOTS = SK_DIST + 1;  // ring slots per wave
 
 // LDS layout of a slot (16-byte chunks XOR-swizzled, as in the tiled kernel,
 // so that fragment reads are free of bank conflicts):
-//   activation row r (128 B) at r * 128, chunk c at position c ^ ((r >> 1) & 7)
-//   weight column n (64 B) at SK_A + n * 64, chunk c at position c ^ ((n >> 2) & 3)
-//   weight steps at SK_A + SK_B: dword i holds columns 2i, 2i + 1
+//   8-bit activation row r (128 B) at r * 128, chunk c at position c ^ ((r >> 1) & 7)
+//   4-bit activation row r (64 B) at r * 64, chunk c at position c ^ ((r >> 2) & 3)
+//   weight column n (64 B) at B_OFF + n * 64, chunk c at position c ^ ((n >> 2) & 3)
+//   4-bit group steps at S_OFF: row r's dword (the stage's two fp16 steps) at r * 4
+//   weight steps at W_OFF: dword i holds columns 2i, 2i + 1
 // Lane (column n = lane & 31, h = lane >> 5) feeds k-step s of a stage with the
-// channels [64 (s >> 1) + 32 h + 16 (s & 1), +16) of both operands.
-template <int EPI>
-__global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
-  __shared__ __attribute__((aligned(16))) uint8_t ring[4][SK_SLOTS][SK_SLOT];
+// channels [64 (s >> 1) + 32 h + 16 (s & 1), +16) of both operands; 64-wide
+// blocks are k-steps {0, 1} and {2, 3}.
+template <int ABITS>
+struct Sk {
+  static constexpr int A = SK_BM * (ABITS == 8 ? KT : KT / 2);  // activation codes (8 / 4 KB)
+  static constexpr int B = SK_BN * (KT / 2);                    // packed weights (2 KB)
+  static constexpr int SIG = ABITS == 4 ? 256 : 0;              // 4-bit group steps
+  static constexpr int B_OFF = A, S_OFF = A + B, W_OFF = A + B + SIG;
+  static constexpr int SLOT = W_OFF + 256;                      // + one 256 B load of weight steps
+  static constexpr int NDMA = A / 1024 + B / 1024 + (ABITS == 4 ? 1 : 0) + 1;  // loads per stage and wave
+  static constexpr int WGS_PER_CU = 4 * SK_SLOTS * SLOT * 2 <= 160 * 1024 ? 2 : 1;
+  static_assert(4 * SK_BM * SK_BN * 4 <= 4 * SK_SLOTS * SLOT, "the wave sums fit in the ring");
+};
+
+template <int ABITS, int EPI>
+__global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel(GemmArgs a) {
+  using L = Sk<ABITS>;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[4][SK_SLOTS][L::SLOT];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int M = a.M, N = a.N, K = a.K;
@@ -53,45 +64,60 @@ __global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
   const int kt0 = range * nkt / S, kt1 = (range + 1) * nkt / S;
   const int h = lane >> 5, col = lane & 31;
   const int rows = min(M - m0, SK_BM);
+  const int arow = ABITS == 8 ? K : K / 2;  // bytes of an activation row
 
   // direct-load sources: rows past the matrix read its last row
-  uint32_t voffA[SK_A / 1024];
+  uint32_t voffA[L::A / 1024];
 #pragma unroll
-  for (int i = 0; i < SK_A / 1024; ++i) {
-    const int r = 8 * i + (lane >> 3);
-    voffA[i] = static_cast<uint32_t>(min(r, rows - 1) * K + 16 * ((lane & 7) ^ ((r >> 1) & 7)));
+  for (int i = 0; i < L::A / 1024; ++i) {
+    if constexpr (ABITS == 8) {
+      const int r = 8 * i + (lane >> 3);
+      voffA[i] = static_cast<uint32_t>(min(r, rows - 1) * arow + 16 * ((lane & 7) ^ ((r >> 1) & 7)));
+    } else {
+      const int r = 16 * i + (lane >> 2);
+      voffA[i] = static_cast<uint32_t>(min(r, rows - 1) * arow + 16 * ((lane & 3) ^ ((r >> 2) & 3)));
+    }
   }
-  uint32_t voffB[SK_B / 1024];
+  uint32_t voffB[L::B / 1024];
 #pragma unroll
-  for (int i = 0; i < SK_B / 1024; ++i) {
+  for (int i = 0; i < L::B / 1024; ++i) {
     const int n = 16 * i + (lane >> 2);
     voffB[i] = static_cast<uint32_t>(n * (K / 2) + 16 * ((lane & 3) ^ ((n >> 2) & 3)));
   }
+  const uint32_t voffS = static_cast<uint32_t>(min(lane, rows - 1) * (K / kA4Group) * 2);  // row lane
   const uint32_t voffW = 4 * (lane & 15);  // lanes 16..63 repeat the 16 dwords
   const uint32_t ring0 = lds_offset(&ring[wave][0][0]);
-  const int8_t* qx = static_cast<const int8_t*>(a.qx) + static_cast<size_t>(m0) * K;
+  const uint8_t* qx = static_cast<const uint8_t*>(a.qx) + static_cast<size_t>(m0) * arow;
   const uint8_t* qw = a.qw + static_cast<size_t>(n0) * (K / 2);
+  const uint16_t* sig = static_cast<const uint16_t*>(a.act_scale) + static_cast<size_t>(m0) * (K / kA4Group);
   auto issue = [&](int kt, int slot) {
-    const uint32_t st = ring0 + slot * SK_SLOT;
+    const uint32_t st = ring0 + slot * L::SLOT;
 #pragma unroll
-    for (int i = 0; i < SK_A / 1024; ++i) dma<16>(qx + kt * KT, voffA[i], st + i * 1024);
+    for (int i = 0; i < L::A / 1024; ++i) dma<16>(qx + kt * (arow / nkt), voffA[i], st + i * 1024);
 #pragma unroll
-    for (int i = 0; i < SK_B / 1024; ++i) dma<16>(qw + kt * (KT / 2), voffB[i], st + SK_A + i * 1024);
-    dma<4>(a.w_scale + static_cast<size_t>(kt) * N + n0, voffW, st + SK_A + SK_B);  // group-major steps
+    for (int i = 0; i < L::B / 1024; ++i) dma<16>(qw + kt * (KT / 2), voffB[i], st + L::B_OFF + i * 1024);
+    if constexpr (ABITS == 4) dma<4>(sig + 2 * kt, voffS, st + L::S_OFF);  // the stage's two groups
+    dma<4>(a.w_scale + static_cast<size_t>(kt) * N + n0, voffW, st + L::W_OFF);  // group-major steps
   };
 
-  // fragment offsets within a slot
+  // fragment offsets within a slot: activations per (row tile, k-step) for
+  // 8-bit, per (row tile, k-step pair) for packed 4-bit rows
   int aoff[TM][4];
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
     const int r = tm * 32 + col;
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) aoff[tm][ks] = r * 128 + 16 * ((4 * (ks >> 1) + 2 * h + (ks & 1)) ^ ((r >> 1) & 7));
+    for (int ks = 0; ks < 4; ++ks) {
+      if constexpr (ABITS == 8)
+        aoff[tm][ks] = r * 128 + 16 * ((4 * (ks >> 1) + 2 * h + (ks & 1)) ^ ((r >> 1) & 7));
+      else
+        aoff[tm][ks] = r * 64 + 16 * ((2 * (ks >> 1) + h) ^ ((r >> 2) & 3));
+    }
   }
   int boff[2];
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) boff[k2] = SK_A + col * 64 + 16 * ((2 * k2 + h) ^ ((col >> 2) & 3));
-  const int woff = SK_A + SK_B + 4 * (col >> 1);
+  for (int k2 = 0; k2 < 2; ++k2) boff[k2] = L::B_OFF + col * 64 + 16 * ((2 * k2 + h) ^ ((col >> 2) & 3));
+  const int woff = L::W_OFF + 4 * (col >> 1);
 
   float y[TM][16];
   v16i acc[TM];
@@ -101,9 +127,11 @@ __global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) y[tm][r] = 0.0f;
   }
-  float wprev = 0.0f;  // the fold before the first block adds 0
+  float wprev = 0.0f;  // 8-bit: the fold before the first block adds 0
 
-  // y += fp32(C) * Delta_W of the previous block, then this block's MFMAs
+  // 8-bit: y += fp32(C) * Delta_W of the previous block, then this block's
+  // MFMAs.  4-bit: both 64-blocks of the stage, then
+  // y += (fp32(C) * sigma_row) * Delta_W for each.
   auto compute = [&](int slot) {
     const uint8_t* st = &ring[wave][slot][0];
     // every LDS read of the stage first: one latency per stage
@@ -115,7 +143,22 @@ __global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int ks = 0; ks < 4; ++ks) af[tm][ks] = *reinterpret_cast<const v4i*>(st + aoff[tm][ks]);
+      for (int ks = 0; ks < 4; ++ks) {
+        if constexpr (ABITS == 8) {
+          af[tm][ks] = *reinterpret_cast<const v4i*>(st + aoff[tm][ks]);
+        } else if ((ks & 1) == 0) {
+          const uint4 pa = *reinterpret_cast<const uint4*>(st + aoff[tm][ks]);
+          af[tm][ks] = __builtin_bit_cast(v4i, pa);  // packed: widened below
+        }
+      }
+    uint4 sp[TM][4];  // 4-bit: group steps of the lane's 16 rows per tile
+    if constexpr (ABITS == 4) {
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int g = 0; g < 4; ++g)
+          sp[tm][g] = *reinterpret_cast<const uint4*>(st + L::S_OFF + (tm * 32 + 8 * g + 4 * h) * 4);
+    }
     __builtin_amdgcn_sched_barrier(0);
     v4i bf[4];
 #pragma unroll
@@ -123,15 +166,43 @@ __global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
       bf[2 * k2] = unpack_frag(pb[k2].x, pb[k2].y);
       bf[2 * k2 + 1] = unpack_frag(pb[k2].z, pb[k2].w);
     }
+    const float wstep = f16_to_f32((col & 1) ? (wpair >> 16) : (wpair & 0xFFFFu));
+    if constexpr (ABITS == 8) {
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      fold8(acc[tm], wprev, y[tm]);
-      acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][0], bf[0], (v16i)(0), 0, 0, 0);
+      for (int tm = 0; tm < TM; ++tm) {
+        fold8(acc[tm], wprev, y[tm]);
+        acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][0], bf[0], (v16i)(0), 0, 0, 0);
 #pragma unroll
-      for (int ks = 1; ks < 4; ++ks) acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[ks], acc[tm], 0, 0, 0);
+        for (int ks = 1; ks < 4; ++ks)
+          acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[ks], acc[tm], 0, 0, 0);
+      }
+      wprev = wstep * 0.0625f;  // widened weight codes carry a factor 16
+    } else {
+      const float w = wstep * 0.00390625f;  // widened codes of both operands carry 16 * 16
+      v16i c[2][TM];
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          const uint4 pa = __builtin_bit_cast(uint4, af[tm][2 * hb]);
+          c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.x, pa.y), bf[2 * hb], (v16i)(0), 0, 0, 0);
+          c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.z, pa.w), bf[2 * hb + 1], c[hb][tm], 0, 0, 0);
+        }
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+          for (int g = 0; g < 4; ++g) {
+            const uint32_t s4[4] = {sp[tm][g].x, sp[tm][g].y, sp[tm][g].z, sp[tm][g].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float sg = f16_to_f32(hb ? (s4[q] >> 16) : (s4[q] & 0xFFFFu));
+              const int r = 4 * g + q;
+              y[tm][r] = __builtin_fmaf(static_cast<float>(c[hb][tm][r]) * sg, w, y[tm][r]);
+            }
+          }
     }
-    // widened weight codes carry a factor 16
-    wprev = f16_to_f32((col & 1) ? (wpair >> 16) : (wpair & 0xFFFFu)) * 0.0625f;
   };
 
   // this wave's stages kt0 + wave + 4j, j < nst; past the end the last stage
@@ -142,13 +213,15 @@ __global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
 #pragma unroll
     for (int p = 0; p < SK_DIST; ++p) issue(stage(p), p);
     for (int j = 0; j < nst; ++j) {
-      wait_vm<SK_NDMA * (SK_DIST - 1)>();             // stage j has landed
+      wait_vm<L::NDMA * (SK_DIST - 1)>();                  // stage j has landed
       issue(stage(j + SK_DIST), (j + SK_DIST) % SK_SLOTS);  // into the slot read last iteration
       compute(j % SK_SLOTS);
     }
   }
+  if constexpr (ABITS == 8) {
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm) fold8(acc[tm], wprev, y[tm]);
+    for (int tm = 0; tm < TM; ++tm) fold8(acc[tm], wprev, y[tm]);
+  }
 
   // the four waves' sums, added in wave order; wave g then finishes register
   // group g of both tiles: rows tm * 32 + 8 g + 4 h + q, q < 4
@@ -185,11 +258,16 @@ __global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
       }
     return;
   }
-  // epilogue: row factor (fetched from the lane that loaded it), bias, cast;
-  // a quad transpose gives each lane four consecutive channels of one row
+  // epilogue: row factor (8-bit: r_i; 4-bit: kappa_i = 1 / gamma_s(i), the
+  // compensation of Eq. 8), fetched from the lane that loaded it; bias; cast.
+  // A quad transpose gives each lane four consecutive channels of one row.
   float rowf = 1.0f, bias = 0.0f;
   if constexpr (EPI == kEpiOut) {
-    rowf = static_cast<const float*>(a.act_scale)[m0 + min(lane, rows - 1)];
+    const int m = m0 + min(lane, rows - 1);
+    if constexpr (ABITS == 8)
+      rowf = static_cast<const float*>(a.act_scale)[m];
+    else
+      rowf = 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
     if (a.bias != nullptr) bias = bf16_to_f32(a.bias[n0 + col]);
   }
   const int rf_bits = __float_as_int(rowf);
@@ -227,7 +305,7 @@ __global__ __launch_bounds__(256, 1) void gemm_skinny_kernel(GemmArgs a) {
 // Second kernel of a split skinny GEMM: adds the `split` partial sums of every
 // output in range order and finishes it as the skinny epilogue does.  Four
 // adjacent outputs per thread.
-template <int EPI>
+template <int ABITS, int EPI>
 __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   const int strips = a.N / SK_BN;
   const int g = blockIdx.x * 256 + threadIdx.x;  // one thread per 4 outputs of a 64 x 32 block
@@ -248,7 +326,8 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   }
   float y[4] = {acc.x, acc.y, acc.z, acc.w};
   if constexpr (EPI == kEpiOut) {
-    const float rowf = static_cast<const float*>(a.act_scale)[m];
+    const float rowf = ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
+                                  : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float b = a.bias != nullptr ? bf16_to_f32(a.bias[n + j]) : 0.0f;
@@ -271,17 +350,16 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   }
 }
 
-}  // namespace
-
 // K ranges per strip: S workgroups share a strip when that shortens its
 // waves' stage chains by more than the second kernel costs.  Measured on
 // MI355X: a stage costs a wave about 0.65 us, the second kernel and its
-// launch about 5 us, i.e. about 8 stages.  At most one workgroup per CU (one
-// fits, by LDS), and at least four stages (one per wave) in every range.
-static int skinny_split(int32_t M, int32_t N, int32_t K) {
+// launch about 5 us, i.e. about 8 stages.  At most the workgroups that fit at
+// once (by LDS), and at least four stages (one per wave) in every range.
+template <int ABITS>
+int split_t(int32_t M, int32_t N, int32_t K) {
   const int blocks = (N / SK_BN) * ((M + SK_BM - 1) / SK_BM);
   const int nkt = K / KT;
-  const int smax = std::max(1, std::min(device_cus() / blocks, nkt / 4));
+  const int smax = std::max(1, std::min(device_cus() * Sk<ABITS>::WGS_PER_CU / blocks, nkt / 4));
   int best = 1;
   double best_cost = (nkt + 3) / 4;
   for (int S = 2; S <= smax; ++S) {
@@ -290,32 +368,47 @@ static int skinny_split(int32_t M, int32_t N, int32_t K) {
   }
   return best;
 }
-size_t skinny_partial_bytes(int32_t M, int32_t N, int32_t K) {
-  const int S = skinny_split(M, N, K);
+
+int skinny_split(int act_bits, int32_t M, int32_t N, int32_t K) {
+  return act_bits == 8 ? split_t<8>(M, N, K) : split_t<4>(M, N, K);
+}
+
+template <int ABITS, int EPI>
+hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
+  GemmArgs a = a0;
+  int S = skinny_split(ABITS, a.M, a.N, a.K);
+  if (S > 1 && (partial == nullptr || partial_bytes < skinny_partial_bytes(ABITS, a.M, a.N, a.K))) S = 1;
+  a.split = S;
+  a.partial = S > 1 ? partial : nullptr;
+  const int strips = a.N / SK_BN, mblocks = (a.M + SK_BM - 1) / SK_BM;
+  hipLaunchKernelGGL((gemm_skinny_kernel<ABITS, EPI>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || S == 1) return e;
+  const int threads = strips * mblocks * (SK_BM * SK_BN / 4);
+  hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI>), dim3((threads + 255) / 256), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+size_t skinny_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K) {
+  const int S = skinny_split(act_bits, M, N, K);
   if (S <= 1) return 0;
   return static_cast<size_t>(N / SK_BN) * ((M + SK_BM - 1) / SK_BM) * S * (SK_BM * SK_BN) * sizeof(float);
 }
 
-template <int EPI>
-hipError_t launch_skinny_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
-  GemmArgs a = a0;
-  int S = skinny_split(a.M, a.N, a.K);
-  if (S > 1 && (partial == nullptr || partial_bytes < skinny_partial_bytes(a.M, a.N, a.K))) S = 1;
-  a.split = S;
-  a.partial = S > 1 ? partial : nullptr;
-  const int strips = a.N / SK_BN, mblocks = (a.M + SK_BM - 1) / SK_BM;
-  hipLaunchKernelGGL((gemm_skinny_kernel<EPI>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || S == 1) return e;
-  const int threads = strips * mblocks * (SK_BM * SK_BN / 4);
-  hipLaunchKernelGGL((gemm_skinny_tail_kernel<EPI>), dim3((threads + 255) / 256), dim3(256), 0, s, a);
-  return hipGetLastError();
-}
-
-hipError_t launch_skinny(int epi, const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
-  switch (epi) {
-    case kEpiOut: return launch_skinny_t<kEpiOut>(a, s, partial, partial_bytes);
-    case kEpiPartial: return launch_skinny_t<kEpiPartial>(a, s, partial, partial_bytes);
+hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
+                         size_t partial_bytes) {
+  if (act_bits == 8) {
+    switch (epi) {
+      case kEpiOut: return launch_t<8, kEpiOut>(a, s, partial, partial_bytes);
+      case kEpiPartial: return launch_t<8, kEpiPartial>(a, s, partial, partial_bytes);
+    }
+  } else {
+    switch (epi) {
+      case kEpiOut: return launch_t<4, kEpiOut>(a, s, partial, partial_bytes);
+      case kEpiPartial: return launch_t<4, kEpiPartial>(a, s, partial, partial_bytes);
+    }
   }
   return hipErrorInvalidValue;
 }

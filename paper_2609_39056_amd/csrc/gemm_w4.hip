@@ -849,7 +849,7 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
 
 template <int EPI>
 hipError_t launch_a8(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
-  if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(EPI, a, s, partial, partial_bytes);
+  if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(8, EPI, a, s, partial, partial_bytes);
   return a.w_group == KT ? launch_t<8, EPI, true>(a, s, partial, partial_bytes)
                          : launch_t<8, EPI, false>(a, s, partial, partial_bytes);
 }
@@ -874,7 +874,7 @@ int device_cus() {
 
 size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t w_group) {
   if (act_bits == 8 && w_group != KT) return 0;  // the non-pipelined kernel never splits
-  if (act_bits == 8 && M <= kSkinnyMaxM) return skinny_partial_bytes(M, N, K);
+  if (w_group == KT && M <= kSkinnyMaxM) return skinny_partial_bytes(act_bits, M, N, K);
   const Plan p = act_bits == 8 ? pipe_plan<8>(M, N, K, ~static_cast<size_t>(0))
                                : pipe_plan<4>(M, N, K, ~static_cast<size_t>(0));
   const size_t unit = static_cast<size_t>(Cfg<8, kPipeWide>::BM) * Cfg<8, kPipeWide>::BN * sizeof(float);
@@ -892,8 +892,11 @@ hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, 
     }
   } else {
     switch (epi) {
-      case kEpiOut: return launch_t<4, kEpiOut, true>(a, s, partial, partial_bytes);
-      case kEpiPartial: return launch_t<4, kEpiPartial, true>(a, s, partial, partial_bytes);
+      case kEpiOut:
+      case kEpiPartial:
+        if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(4, epi, a, s, partial, partial_bytes);
+        return epi == kEpiOut ? launch_t<4, kEpiOut, true>(a, s, partial, partial_bytes)
+                              : launch_t<4, kEpiPartial, true>(a, s, partial, partial_bytes);
       case kEpiDump: return launch_t<4, kEpiDump, false>(a, s, nullptr, 0);
     }
   }

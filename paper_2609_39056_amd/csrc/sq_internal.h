@@ -91,12 +91,13 @@ size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t
 // Compute units of the current device (256 when there is none), capped at 256.
 int device_cus();
 
-// Weight-streaming GEMM for M <= kSkinnyMaxM (8-bit activations, 128-wide
-// weight groups; epi kEpiOut or kEpiPartial).  Splits K across workgroups
-// when `partial` holds skinny_partial_bytes(M, N, K) bytes.
+// Weight-streaming GEMM for M <= kSkinnyMaxM (8- or 4-bit activations,
+// 128-wide weight groups; epi kEpiOut or kEpiPartial).  Splits K across
+// workgroups when `partial` holds skinny_partial_bytes(...) bytes.
 constexpr int kSkinnyMaxM = 128;
-size_t skinny_partial_bytes(int32_t M, int32_t N, int32_t K);
-hipError_t launch_skinny(int epi, const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes);
+size_t skinny_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K);
+hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
+                         size_t partial_bytes);
 
 struct PackArgs {
   const float* w;

@@ -208,24 +208,29 @@ def test_gemm_entry_points(bits, with_ws):
     check_output(y, res, F32)
 
 
+@pytest.mark.parametrize("bits", [8, 4])
 @pytest.mark.parametrize("M,K,N", [(1, 2048, 2048), (2, 128, 64), (33, 8192, 2048), (64, 2048, 6144),
                                    (65, 5120, 320), (128, 1024, 1024), (100, 13824, 128)])
 @pytest.mark.parametrize("out", [F32, BF16])
-def test_few_tokens_w4a8(M, K, N, out):
-    """Layers of at most 128 tokens (the action and proprio streams alone):
-    8-bit activations take the weight-streaming kernel.  Fused linear, and the
-    second kernel alone without a workspace (K never split) and with one (K
-    split across workgroups when the output channels give too few)."""
+def test_few_tokens(bits, M, K, N, out):
+    """Layers of at most 128 tokens (the action and proprio streams alone)
+    take the weight-streaming kernel.  Fused linear, and the second kernel
+    alone without a workspace (K never split) and with one (K split across
+    workgroups when that is faster: 8192 and 13824 channels here)."""
     L = layer(M, K, N, seed=[9, M, K, N])
     pw, W = oracle_weight(L, 128)
-    act = act_params(L, 1, 8, 0)
-    res = oracle_linear(L, 1, 8, 0, pw, 128)
-    y, _ = run_linear(B.sq_linear_w4a8, L, act, W, out)
+    act = act_params(L, 1, bits, 0)
+    res = oracle_linear(L, 1, bits, 0, pw, 128)
+    y, _ = run_linear(FUSED[bits], L, act, W, out)
     check_output(y, res, out)
     for with_ws in (False, True):
-        ws = B.alloc_workspace(B.SQ_VARIANT_GEMM, L.M, L.K, L.N, 8) if with_ws else None
+        ws = B.alloc_workspace(B.SQ_VARIANT_GEMM, L.M, L.K, L.N, bits) if with_ws else None
         y = torch.full((L.M, L.N), float("nan"), dtype=TORCH_OUT[out], device="cuda")
-        B.sq_gemm_w4a8(torch.from_numpy(res["qx"]).cuda(), f32_to_dev(res["scale"]), W, y, out, workspace=ws)
+        if bits == 8:
+            B.sq_gemm_w4a8(torch.from_numpy(res["qx"]).cuda(), f32_to_dev(res["scale"]), W, y, out, workspace=ws)
+        else:
+            B.sq_gemm_w4a4(u8_to_dev(res["qx"]), u16_to_dev(res["scale"], torch.float16), act, W, y, out,
+                           workspace=ws)
         check_output(y, res, out)
 
 
