@@ -148,13 +148,22 @@ def run_suite(args):
         fout.write(line + "\n")
         fout.flush()
 
-    def timed(fn, reps, warm=3):
+    def timed(fn, reps, warm=3, graph=True):
         """Device time per call: `reps` calls captured as one HIP graph, so the
         host's launch rate does not bound small layers; one warm replay, then
-        one timed replay."""
+        one timed replay.  graph=False times `reps` eager calls (for fn that
+        replays a graph itself)."""
         for _ in range(warm):
             fn()
         torch.cuda.synchronize()
+        if not graph:
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(reps):
+                fn()
+            e1.record()
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) * 1e3 / reps
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             for _ in range(reps):
@@ -222,7 +231,7 @@ def run_suite(args):
         for _ in range(150):
             one.add_(1)
     emit(dict(group="dispatch cost", what="one-element kernel per HIP graph node",
-              us_per_node=round(timed(gph.replay, 10, warm=2) / 150, 2)))
+              us_per_node=round(timed(gph.replay, 10, warm=2, graph=False) / 150, 2)))
     del gph
 
     layer_group("single 256x256 linear, 88 tokens (64+8+16), 2 steps", {"small": (256, 256)}, (64, 8, 16),
@@ -276,11 +285,11 @@ def run_suite(args):
 
             sweep_once()  # eager warm-up
             torch.cuda.synchronize()
-            us_eager = timed(sweep_once, 2, warm=0)
+            us_eager = timed(sweep_once, 2, warm=0, graph=False)
             graph = torch.cuda.CUDAGraph()
             with torch.cuda.graph(graph):
                 sweep_once()
-            us_graph = timed(graph.replay, 5, warm=2)
+            us_graph = timed(graph.replay, 5, warm=2, graph=False)
             calls = T * NL * len(lin)
             ops = T * NL * sum(2.0 * inputs[n]["x"].shape[0] * K * N for n, (K, N) in lin.items())
             ab = T * NL * sum(alg_bytes(inputs[n]["x"].shape[0], K, N) for n, (K, N) in lin.items())
