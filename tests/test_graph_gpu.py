@@ -1,0 +1,76 @@
+"""The library's calls inside a captured HIP graph: every replay equals the
+eager call bit for bit.  Between replays the same buffers are overwritten by
+eager calls on other inputs, so a replay that reused stale workspace contents,
+or a captured node that only worked the first time, would show."""
+import pytest
+import torch
+
+from gpu_util import act_params, oracle_weight, u16_to_dev
+from paper_2609_39056_amd import binding as B
+from paper_2609_39056_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+def split(M):
+    a = max(M // 6, 0)
+    p = max(M // 10, 0)
+    return (M - a - p, p, a)
+
+
+FUSED = {8: B.sq_linear_w4a8, 4: B.sq_linear_w4a4}
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("M,K,N", [(64, 8192, 2048), (300, 2048, 512), (600, 1024, 384)])
+def test_graph_replays_match_eager(bits, M, K, N):
+    """64 tokens x 8192 channels: weight-streaming kernel with a K split and
+    its second kernel; 300 and 600 tokens: the tiled kernel with its split
+    tail.  Fused linear and the GEMM entry point with a workspace."""
+    L1 = synth.make_layer(K=K, N=N, stream_counts=split(M), T=3, seed=[11, M, K, N])
+    L2 = synth.make_layer(K=K, N=N, stream_counts=split(M), T=3, seed=[12, M, K, N])
+    _, W = oracle_weight(L1, 128)
+    x1 = u16_to_dev(L1.x_bits, torch.bfloat16)
+    x2 = u16_to_dev(L2.x_bits, torch.bfloat16)
+    act1, act2 = act_params(L1, 1, bits, 0), act_params(L2, 2, bits, 0)
+    ws = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, K, N, bits)
+    wsg = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, K, N, bits)
+    qx, sc = B.act_buffers(M, K, bits)
+    y = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    y_gemm = torch.empty((M, N), dtype=torch.float32, device="cuda")
+
+    def call(x, act):
+        FUSED[bits](x, act, W, y, B.SQ_OUT_BF16, ws)
+        B.sq_quantize_act(x, act, qx, sc)
+        if bits == 8:
+            B.sq_gemm_w4a8(qx, sc, W, y_gemm, B.SQ_OUT_F32, workspace=wsg)
+        else:
+            B.sq_gemm_w4a4(qx, sc, act, W, y_gemm, B.SQ_OUT_F32, workspace=wsg)
+
+    call(x1, act1)
+    torch.cuda.synchronize()
+    ref, ref_gemm = y.clone(), y_gemm.clone()
+    call(x2, act2)
+    torch.cuda.synchronize()
+    other = y.clone()
+    assert not torch.equal(other.view(torch.int16), ref.view(torch.int16))
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(x1, act1)
+    for rep in range(3):
+        call(x2, act2)  # eager work on the same buffers between replays
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), other.view(torch.int16))
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), f"replay {rep}"
+        assert torch.equal(y_gemm.view(torch.int32), ref_gemm.view(torch.int32)), f"replay {rep}"
+    del g
