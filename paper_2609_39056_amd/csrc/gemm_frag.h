@@ -100,6 +100,16 @@ __device__ __forceinline__ void wait_vm() {
   asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
+// fp32(C) * sigma for the fp16 step in half HI of `pair` (4-bit activation
+// group steps, two per dword): one v_fma_mix_f32 converts the half and
+// multiplies with one rounding, the same value as the conversion followed by
+// an fp32 multiply.
+typedef _Float16 half2v __attribute__((ext_vector_type(2)));
+template <int HI>
+__device__ __forceinline__ float mul_step16(float cf, uint32_t pair) {
+  return __builtin_fmaf(cf, static_cast<float>(__builtin_bit_cast(half2v, pair)[HI]), 0.0f);
+}
+
 // Word 3 of a raw buffer resource (32-bit data format, no swizzle).
 constexpr int kBufWord3 = 0x00020000;
 

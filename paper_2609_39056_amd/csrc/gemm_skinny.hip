@@ -130,8 +130,8 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
   float wprev = 0.0f;  // 8-bit: the fold before the first block adds 0
 
   // 8-bit: y += fp32(C) * Delta_W of the previous block, then this block's
-  // MFMAs.  4-bit: both 64-blocks of the stage, then
-  // y += (fp32(C) * sigma_row) * Delta_W for each.
+  // MFMAs.  4-bit: the MFMAs of both 64-blocks of the stage, then their fold
+  // with the row group steps and the stage's weight step.
   auto compute = [&](int slot) {
     const uint8_t* st = &ring[wave][slot][0];
     // every LDS read of the stage first: one latency per stage
@@ -188,20 +188,22 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
           c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.x, pa.y), bf[2 * hb], (v16i)(0), 0, 0, 0);
           c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.z, pa.w), bf[2 * hb + 1], c[hb][tm], 0, 0, 0);
         }
+      // both blocks share the stage's weight step:
+      // y += (fp32(C_0) sigma_0 + fp32(C_1) sigma_1) * Delta_W
 #pragma unroll
-      for (int hb = 0; hb < 2; ++hb)
+      for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-        for (int tm = 0; tm < TM; ++tm)
+        for (int g = 0; g < 4; ++g) {
+          const uint32_t s4[4] = {sp[tm][g].x, sp[tm][g].y, sp[tm][g].z, sp[tm][g].w};
 #pragma unroll
-          for (int g = 0; g < 4; ++g) {
-            const uint32_t s4[4] = {sp[tm][g].x, sp[tm][g].y, sp[tm][g].z, sp[tm][g].w};
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float sg = f16_to_f32(hb ? (s4[q] >> 16) : (s4[q] & 0xFFFFu));
-              const int r = 4 * g + q;
-              y[tm][r] = __builtin_fmaf(static_cast<float>(c[hb][tm][r]) * sg, w, y[tm][r]);
-            }
+          for (int q = 0; q < 4; ++q) {
+            const int r = 4 * g + q;
+            const float t = mul_step16<0>(static_cast<float>(c[0][tm][r]), s4[q]);
+            const float u = __builtin_fmaf(static_cast<float>(c[1][tm][r]),
+                                           static_cast<float>(__builtin_bit_cast(half2v, s4[q])[1]), t);
+            y[tm][r] = __builtin_fmaf(u, w, y[tm][r]);
           }
+        }
     }
   };
 

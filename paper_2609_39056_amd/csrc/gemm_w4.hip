@@ -344,7 +344,7 @@ __device__ __forceinline__ void read_wscale(const uint8_t* st, int wave, int lan
 // (4-bit activations); sigma of block half hb from the stage at st
 template <int ABITS, bool WIDE>
 __device__ __forceinline__ void fold4(float (&y)[TM][TN][16], const uint8_t* st, int hb, const v16i (&c)[TN], int wm,
-                                      int tm, int lane, const float (&w)[TN], bool valid) {
+                                      int tm, int lane, const float (&w)[TN]) {
   using LY = Layout<ABITS, WIDE>;
   const uint8_t* S = st + LY::A_BYTES + LY::B_BYTES;
 #pragma unroll
@@ -354,11 +354,12 @@ __device__ __forceinline__ void fold4(float (&y)[TM][TN][16], const uint8_t* st,
     const uint32_t w4[4] = {sp.x, sp.y, sp.z, sp.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float sg = valid ? f16_to_f32(hb ? (w4[i] >> 16) : (w4[i] & 0xFFFFu)) : 0.0f;
+      const uint32_t pair = w4[i];
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int r = r4 * 4 + i;
-        y[tm][tn][r] = __builtin_fmaf(static_cast<float>(c[tn][r]) * sg, w[tn], y[tm][tn][r]);
+        const float cf = static_cast<float>(c[tn][r]);
+        y[tm][tn][r] = __builtin_fmaf(hb ? mul_step16<1>(cf, pair) : mul_step16<0>(cf, pair), w[tn], y[tm][tn][r]);
       }
     }
   }
@@ -404,6 +405,16 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
   const int G = gridDim.x;
   if (static_cast<int>(blockIdx.x) >= nitems) return;
   const uint32_t smem_lds = lds_offset(smem);
+  if constexpr (A4) {
+    // An item's first fold scales the previous slot's group steps by a zero
+    // weight step; the steps there are another item's (finite) or, before
+    // the ring's first use, these zeros: never a NaN or infinity.
+    for (int i = threadIdx.x; i < STAGES * (LY::S_BYTES / 4); i += CF::NTHREADS) {
+      const int s = i / (LY::S_BYTES / 4), e = i % (LY::S_BYTES / 4);
+      reinterpret_cast<uint32_t*>(smem + s * LY::STAGE + LY::A_BYTES + LY::B_BYTES)[e] = 0u;
+    }
+    __syncthreads();
+  }
 
   // item -> tile origin and K range [kt0, kt1); unit >= 0 marks a split range
   struct Item {
@@ -556,9 +567,9 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
             const v4i af1 = unpack_frag(pa.z, pa.w);
             // previous block: second half of the previous stage, or first half of this one
             if (hb == 0) {
-              fold4<ABITS, kPipeWide>(y, st_prev, 1, acc[tm], wm, tm, lane, wsv_prev, kt > c.kt0);
+              fold4<ABITS, kPipeWide>(y, st_prev, 1, acc[tm], wm, tm, lane, wsv_prev);
             } else {
-              fold4<ABITS, kPipeWide>(y, st, 0, acc[tm], wm, tm, lane, wsv, true);
+              fold4<ABITS, kPipeWide>(y, st, 0, acc[tm], wm, tm, lane, wsv);
             }
 #pragma unroll
             for (int tn = 0; tn < TN; ++tn) {
@@ -574,7 +585,7 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
       }
       const uint8_t* st_last = smem + prev_slot(c_slot);
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) fold4<ABITS, kPipeWide>(y, st_last, 1, acc[tm], wm, tm, lane, wsv_prev, true);
+      for (int tm = 0; tm < TM; ++tm) fold4<ABITS, kPipeWide>(y, st_last, 1, acc[tm], wm, tm, lane, wsv_prev);
     }
 
     if (c.unit >= 0) {
