@@ -51,7 +51,7 @@ def parse():
     p.add_argument("--steps", type=int, default=200)
     p.add_argument("--warmup", type=int, default=20)
     p.add_argument("--sample-every", type=int, default=4,
-                   help="record per-kernel HIP events on every n-th timed step (events cost host time)")
+                   help="per-kernel HIP events on steps/n steps of the per-kernel pass (events cost host time)")
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--suite", metavar="PATH", default=None,
                    help="instead of the one-line benchmark, measure every layer configuration (per-layer "
@@ -366,12 +366,14 @@ def main():
 
     # ---- per-kernel breakdown: the same step as its two C-ABI calls per
     # layer (sq_quantize_act, sq_gemm_w4a8), HIP events around every kernel of
-    # every n-th step, on the stream the kernels run on
+    # the sampled steps, on the stream the kernels run on.  The samples are
+    # taken in the pass's second half (clocks settle over the first), as many
+    # as steps / sample_every.
     for s in range(args.warmup):
         fused_step(s % T_STEPS)
     torch.cuda.synchronize()
     every = max(1, args.sample_every)
-    sampled = list(range(0, args.steps, every))
+    sampled = list(range(args.steps // 2, args.steps, max(1, every // 2)))[: max(1, args.steps // every)]
     evs = {s: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for s in sampled}
     torch.cuda.synchronize()
     t1 = time.perf_counter()
