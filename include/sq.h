@@ -28,8 +28,9 @@
  *   transposed, [N, K] (K contiguous), as packed int4.  Y is [M, N].
  * - Shapes: 1 <= M <= 2^24; K % 128 == 0 and 128 <= K <= 32768; N % 64 == 0
  *   and 64 <= N <= 2^20.
- * - Alignment: x, qx, qw, y and workspace 16 bytes; every other pointer 4
- *   bytes (2 for bf16/fp16 arrays).
+ * - Alignment: x, qx, qw, y and workspace 16 bytes; the bf16 bias 2 bytes;
+ *   every other pointer 4 bytes (the kernels read the fp16 weight and group
+ *   steps in pairs).
  * - Inputs must be finite; X D^-1 gamma must stay finite in fp32.
  *
  * Packed int4 layout (weights and A4 activations)

@@ -42,7 +42,7 @@ sq_status check_weight(const sq_weight* w) {
   if (w == nullptr || w->qw == nullptr || w->w_scale == nullptr) return SQ_ERR_NULL;
   if (!valid_k(w->K) || !valid_n(w->N)) return SQ_ERR_SHAPE;
   if (w->w_group < kKTile || w->w_group % kKTile != 0 || w->K % w->w_group != 0) return SQ_ERR_UNSUPPORTED;
-  if (!aligned(w->qw, 16) || !aligned(w->w_scale, 2)) return SQ_ERR_ALIGN;
+  if (!aligned(w->qw, 16) || !aligned(w->w_scale, 4)) return SQ_ERR_ALIGN;
   if (w->bias != nullptr && !aligned(w->bias, 2)) return SQ_ERR_ALIGN;
   return SQ_OK;
 }
@@ -183,7 +183,7 @@ sq_status sq_pack_weights(const float* w, const float* d, int32_t N, int32_t K, 
   if (w == nullptr || qw == nullptr || w_scale == nullptr) return SQ_ERR_NULL;
   if (!valid_k(K) || !valid_n(N)) return SQ_ERR_SHAPE;
   if (w_group < kKTile || w_group % kKTile != 0 || K % w_group != 0) return SQ_ERR_UNSUPPORTED;
-  if (!aligned(w, 16) || !aligned(qw, 16) || !aligned(w_scale, 2)) return SQ_ERR_ALIGN;
+  if (!aligned(w, 16) || !aligned(qw, 16) || !aligned(w_scale, 4)) return SQ_ERR_ALIGN;
   if (d != nullptr && !aligned(d, 16)) return SQ_ERR_ALIGN;
   PackArgs p{w, d, qw, w_scale, N, K, w_group};
   return hip_status(launch_pack_weights(p, stream));
@@ -196,7 +196,7 @@ sq_status sq_quantize_act(const uint16_t* x, int32_t M, int32_t K, const sq_act_
   if (st != SQ_OK) return st;
   if (!valid_m(M)) return SQ_ERR_SHAPE;
   if (!aligned(x, 16) || !aligned(qx, 16)) return SQ_ERR_ALIGN;
-  if (!aligned(act_scale, act->act_bits == 8 ? 4 : 2)) return SQ_ERR_ALIGN;
+  if (!aligned(act_scale, 4)) return SQ_ERR_ALIGN;
   return quantize(x, M, K, act, qx, act_scale, stream);
 }
 

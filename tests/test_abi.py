@@ -117,7 +117,7 @@ def lin(L, fn="sq_linear_w4a8", x=A, M=88, a=None, w=None, y=A, out=0, ws=A, nby
     (dict(out=3), UNSUP), (dict(y=A + 4), ALIGN), (dict(ws=A + 8), ALIGN), (dict(nbytes=16), WS),
     (dict(w=wt(N=100)), SHAPE), (dict(w=wt(K=200)), SHAPE), (dict(w=wt(w_group=64)), UNSUP),
     (dict(w=wt(K=384, w_group=256)), UNSUP), (dict(w=wt(qw=None)), NULL), (dict(w=wt(w_scale=None)), NULL),
-    (dict(w=wt(qw=A + 4)), ALIGN),
+    (dict(w=wt(qw=A + 4)), ALIGN), (dict(w=wt(w_scale=A + 2)), ALIGN),
 ])
 def test_linear_rejects(L, fn, kw, code):
     if fn == "sq_linear_w4a4":
