@@ -13,7 +13,7 @@ namespace {
 __global__ __launch_bounds__(256) void pack_weights_kernel(PackArgs a) {
   const int lane = threadIdx.x & 63;
   const int ng = a.K / a.w_group;
-  const long wave = static_cast<long>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  const long wave = static_cast<long>(flat_wg()) * 4 + (threadIdx.x >> 6);
   if (wave >= static_cast<long>(a.N) * ng) return;
   const int j = static_cast<int>(wave / ng);
   const int b = static_cast<int>(wave % ng);
@@ -72,8 +72,7 @@ __global__ __launch_bounds__(256) void pack_weights_kernel(PackArgs a) {
 
 hipError_t launch_pack_weights(const PackArgs& a, hipStream_t s) {
   const long waves = static_cast<long>(a.N) * (a.K / a.w_group);
-  const unsigned grid = static_cast<unsigned>((waves + 3) / 4);
-  hipLaunchKernelGGL(pack_weights_kernel, dim3(grid), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(pack_weights_kernel, wg_grid(static_cast<size_t>((waves + 3) / 4)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

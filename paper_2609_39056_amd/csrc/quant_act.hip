@@ -37,7 +37,7 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(QuantArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int lr = (wave % WPR) * 64 + lane;
   const int M = a.M, nch = a.K >> 3;
-  const int row = blockIdx.x * RPW + wave / WPR;
+  const int row = static_cast<int>(flat_wg()) * RPW + wave / WPR;  // past M in the grid's last row: no stores
   const int rowc = min(row, M - 1);
   const bool dynamic = a.range_mode == SQ_RANGE_DYNAMIC;
   const bool has_d = a.dinv != nullptr;
@@ -159,8 +159,8 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(QuantArgs a) {
 template <int BITS, int WPR, int NCH>
 hipError_t launch_one(const QuantArgs& a, hipStream_t s) {
   constexpr int RPW = 4 / WPR;
-  const unsigned grid = static_cast<unsigned>((a.M + RPW - 1) / RPW);
-  hipLaunchKernelGGL((quantize_act_kernel<BITS, WPR, NCH>), dim3(grid), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((quantize_act_kernel<BITS, WPR, NCH>), wg_grid((static_cast<size_t>(a.M) + RPW - 1) / RPW),
+                     dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

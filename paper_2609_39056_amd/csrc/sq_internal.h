@@ -44,6 +44,18 @@ __device__ __forceinline__ void unpack_int4x8_times16(uint32_t p, uint32_t& lo, 
   hi = p & 0xF0F0F0F0u;
 }
 
+// ---------------------------------------------------------------- launch grids
+// A launch of n workgroups as an x * y grid with x <= 65536: a dispatch
+// counts work-items per grid dimension in 32 bits, which one dimension of 256-
+// thread workgroups would overflow from 2^24 workgroups on.  Kernels take
+// flat_wg() as their index and leave when it is past n (the last grid row
+// may be partly beyond).
+inline dim3 wg_grid(size_t n) {
+  const size_t x = n < 65536 ? (n == 0 ? 1 : n) : 65536;
+  return dim3(static_cast<unsigned>(x), static_cast<unsigned>((n + x - 1) / x));
+}
+__device__ __forceinline__ size_t flat_wg() { return static_cast<size_t>(blockIdx.y) * gridDim.x + blockIdx.x; }
+
 // ---------------------------------------------------------------- launch arguments
 struct QuantArgs {
   const uint16_t* x;

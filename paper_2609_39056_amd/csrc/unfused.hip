@@ -24,7 +24,9 @@ namespace {
 
 // U1: one workgroup per row.
 __global__ __launch_bounds__(256) void u1_scale_kernel(UnfusedArgs a) {
-  const int row = blockIdx.x;
+  const size_t wg = flat_wg();
+  if (wg >= static_cast<size_t>(a.M)) return;  // the whole workgroup: before any barrier
+  const int row = static_cast<int>(wg);
   const int tid = threadIdx.x;
   const int nch = a.K / 8;
   const uint16_t* xr = a.x + static_cast<size_t>(row) * a.K;
@@ -188,7 +190,7 @@ unsigned grid_for(size_t n) {
 
 hipError_t launch_unfused(const UnfusedArgs& a, hipStream_t s) {
   hipError_t e;
-  hipLaunchKernelGGL(u1_scale_kernel, dim3(a.M), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(u1_scale_kernel, wg_grid(static_cast<size_t>(a.M)), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   hipLaunchKernelGGL(u2_gain_kernel, dim3(grid_for(static_cast<size_t>(a.M) * a.K / 4)), dim3(256), 0, s, a);
   if ((e = hipGetLastError()) != hipSuccess) return e;
