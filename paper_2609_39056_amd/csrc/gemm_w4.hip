@@ -26,7 +26,9 @@
 // the row scale r_i factors out and is applied once in the epilogue) or
 // y += (fp32(C) * sigma_i) * Delta_W (4-bit).  The epilogue multiplies by r_i (8-bit) or by
 // kappa_i = 1/gamma_s(i) (4-bit, the compensation of Eq. 8), adds the bias and
-// casts.
+// casts.  With one weight step per output channel (w_group = K, the weight
+// format of the paper's experiments) and 8-bit activations there is a single
+// block: the int32 sums run over all of K and are converted once per tile.
 #include <algorithm>
 #include <atomic>
 #include <cmath>
@@ -381,14 +383,15 @@ __device__ __forceinline__ void fold4(float (&y)[TM][TN][16], const uint8_t* st,
 // fold the previous block's accumulators of a row tile (they share its group
 // steps), then run its MFMAs of this block; four stages, since the previous
 // stage's group steps are still read while the stage two ahead loads.
-template <int ABITS, int EPI>
+template <int ABITS, int EPI, bool PC>
 __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm_pipe_kernel(GemmArgs a) {
   using LY = Layout<ABITS, kPipeWide>;
   using CF = Cfg<ABITS, kPipeWide>;
   static_assert(CF::NTHREADS == (kPipeWide ? 512 : 256) && CF::WGS_PER_CU == (kPipeWide ? 1 : 2), "launch bounds");
+  static_assert(!PC || ABITS == 8, "one weight step per channel: 8-bit activations (4-bit ones have 64-wide steps)");
   constexpr int BM = CF::BM, BN = CF::BN, STAGES = CF::STAGES;
   constexpr bool A4 = ABITS == 4;
-  constexpr int NDMA = LY::A_DMA + LY::B_DMA + (A4 ? 1 : 0) + 1;
+  constexpr int NDMA = LY::A_DMA + LY::B_DMA + (A4 ? 1 : 0) + (PC ? 0 : 1);
   constexpr int AHEAD = (CF::DIST - 1) * NDMA;  // loads issued after the stage waited for
   constexpr uint32_t RING = STAGES * LY::STAGE;
   static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
@@ -450,7 +453,7 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
   StageLoads<ABITS, kPipeWide> ld;
   ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
   auto issue = [&]() {
-    ld.template issue<A4, true>(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
+    ld.template issue<A4, !PC>(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
     d_slot = d_slot + LY::STAGE == RING ? 0 : d_slot + LY::STAGE;
   };
   // Past the last stage of the last item the same stage is loaded again (in
@@ -492,16 +495,68 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
     ein.load(a, c.m0, c.n0, wm, wn, lane);
     float y[TM][TN][16];
     float wsv_prev[TN], wsv[TN];
+    if constexpr (!PC) {
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+      for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
+        for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) y[tm][tn][r] = 0.0f;
+          for (int r = 0; r < 16; ++r) y[tm][tn][r] = 0.0f;
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = 0.0f;  // the fold before the first block adds 0
+      for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = 0.0f;  // the fold before the first block adds 0
+    }
 
-    if constexpr (!A4) {
+    if constexpr (PC) {
+      // One weight step per output channel (w_group = K): the int32 sums of
+      // the item's whole K range stay in the accumulators and are converted
+      // once, after its last stage; the loop is MFMAs, the weight widening
+      // and the loads only.  A split range hands its exact int32 sums to the
+      // second kernel (as raw bits in y), which adds them in integers.
+      float wpc[TN];
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int n = min(c.n0 + wn * 64 + tn * 32 + (lane & 31), N - 1);
+        wpc[tn] = f16_to_f32(a.w_scale[n]) * 0.0625f;  // the widened codes' factor 16 folded in
+      }
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
+      for (int kt = c.kt0; kt < c.kt1; ++kt) {
+        issue();
+        advance();
+        const uint8_t* st = smem + c_slot;
+        v4i bfull[TN][4];
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int k2 = 0; k2 < 2; ++k2) {
+            const uint4 pb = *reinterpret_cast<const uint4*>(st + off.b(tn, k2));
+            bfull[tn][2 * k2] = unpack_frag(pb.x, pb.y);
+            bfull[tn][2 * k2 + 1] = unpack_frag(pb.z, pb.w);
+          }
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          v4i af[4];
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks) af[ks] = *reinterpret_cast<const v4i*>(st + off.a(tm, ks));
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks)
+              acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks], bfull[tn][ks], acc[tm][tn], 0, 0, 0);
+        }
+        wait_vm_and_barrier<AHEAD>();
+        c_slot = next_slot(c_slot);
+      }
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            y[tm][tn][r] = c.unit >= 0 ? __int_as_float(acc[tm][tn][r]) : static_cast<float>(acc[tm][tn][r]) * wpc[tn];
+    } else if constexpr (!A4) {
       for (int kt = c.kt0; kt < c.kt1; ++kt) {
         issue();
         advance();
@@ -589,7 +644,8 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
     }
 
     if (c.unit >= 0) {
-      // split tail: this K range's fp32 sums of the tile, row-major [BM][BN]
+      // split tail: this K range's fp32 sums of the tile (int32 with one step
+      // per channel), row-major [BM][BN]
       int ln = lane;  // opaque copy: keep the addresses out of the tile loop's live registers
       asm volatile("" : "+v"(ln));
       float* P = a.partial + static_cast<size_t>(c.unit) * BM * BN;
@@ -736,9 +792,11 @@ __global__ __launch_bounds__(Cfg<ABITS>::NTHREADS, 2) void gemm_simple_kernel(Ge
 // Second kernel of a split tail: adds the `split` partial sums of every
 // output of the split tiles in range order (so the result does not depend on
 // which range finished first) and finishes it exactly as store_tile does
-// (one fma with the row factor and the bias, then the cast).  Four adjacent
-// outputs per thread, 16-byte loads.
-template <int ABITS, int EPI>
+// (one fma with the row factor and the bias, then the cast).  With one weight
+// step per channel (PC) the partials are int32 sums, added exactly and then
+// converted and scaled as the unsplit tile is.  Four adjacent outputs per
+// thread, 16-byte loads.
+template <int ABITS, int EPI, bool PC>
 __global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
   constexpr int BM = Cfg<ABITS, kPipeWide>::BM, BN = Cfg<ABITS, kPipeWide>::BN;
   constexpr int PER_TILE = BM * BN / 4;  // threads per tile
@@ -754,16 +812,35 @@ __global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
   const int n = tile_n * BN + col;
   if (m >= a.M || n >= a.N) return;  // N % 64 == 0: the 4 columns are all in or all out
   const float* P = a.partial + static_cast<size_t>(ti) * a.split * BM * BN + row * BN + col;
-  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  float y[4];
+  if constexpr (PC) {
+    int4 acc = make_int4(0, 0, 0, 0);
 #pragma unroll 8
-  for (int sl = 0; sl < a.split; ++sl) {
-    const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * BM * BN);
-    acc.x += v.x;
-    acc.y += v.y;
-    acc.z += v.z;
-    acc.w += v.w;
+    for (int sl = 0; sl < a.split; ++sl) {
+      const int4 v = *reinterpret_cast<const int4*>(P + static_cast<size_t>(sl) * BM * BN);
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    const int ci[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = static_cast<float>(ci[j]) * (f16_to_f32(a.w_scale[n + j]) * 0.0625f);
+  } else {
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+#pragma unroll 8
+    for (int sl = 0; sl < a.split; ++sl) {
+      const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * BM * BN);
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    y[0] = acc.x;
+    y[1] = acc.y;
+    y[2] = acc.z;
+    y[3] = acc.w;
   }
-  float y[4] = {acc.x, acc.y, acc.z, acc.w};
   if constexpr (EPI == kEpiOut) {
     const float rowf = ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
                                   : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
@@ -828,7 +905,7 @@ Plan pipe_plan(int32_t M, int32_t N, int32_t K, size_t partial_bytes) {
   return plan_split<CF::BM, CF::BN>(true, M, N, K, device_cus() * CF::WGS_PER_CU, partial_bytes);
 }
 
-template <int ABITS, int EPI, bool PIPE>
+template <int ABITS, int EPI, bool PIPE, bool PC = false>
 hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
   GemmArgs a = a0;
   if constexpr (PIPE) {
@@ -841,11 +918,11 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
     const int rest = p.ntiles - p.ndp;
     const int nitems = p.ndp + rest * p.split;
     const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
-    hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
+    hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI, PC>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || rest == 0 || p.split == 1) return e;
     constexpr int per_tile_blocks = CF::BM * CF::BN / 4 / 256;
-    hipLaunchKernelGGL((gemm_tail_kernel<ABITS, EPI>), dim3(rest * per_tile_blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gemm_tail_kernel<ABITS, EPI, PC>), dim3(rest * per_tile_blocks), dim3(256), 0, s, a);
     return hipGetLastError();
   } else {
     using CF = Cfg<ABITS, false>;
@@ -858,11 +935,16 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
   }
 }
 
+// 8-bit activations: 128-wide weight groups take the weight-streaming kernel
+// (few tokens) or the pipelined one; one step per output channel (w_group =
+// K) the pipelined one with int32 sums over K; other group widths the
+// non-pipelined kernel.
 template <int EPI>
 hipError_t launch_a8(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
   if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(8, EPI, a, s, partial, partial_bytes);
-  return a.w_group == KT ? launch_t<8, EPI, true>(a, s, partial, partial_bytes)
-                         : launch_t<8, EPI, false>(a, s, partial, partial_bytes);
+  if (a.w_group == KT) return launch_t<8, EPI, true>(a, s, partial, partial_bytes);
+  if (a.w_group == a.K) return launch_t<8, EPI, true, true>(a, s, partial, partial_bytes);
+  return launch_t<8, EPI, false>(a, s, partial, partial_bytes);
 }
 
 }  // namespace
@@ -884,7 +966,7 @@ int device_cus() {
 }
 
 size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t w_group) {
-  if (act_bits == 8 && w_group != KT) return 0;  // the non-pipelined kernel never splits
+  if (act_bits == 8 && w_group != KT && w_group != K) return 0;  // the non-pipelined kernel never splits
   if (w_group == KT && M <= kSkinnyMaxM) return skinny_partial_bytes(act_bits, M, N, K);
   const Plan p = act_bits == 8 ? pipe_plan<8>(M, N, K, ~static_cast<size_t>(0))
                                : pipe_plan<4>(M, N, K, ~static_cast<size_t>(0));

@@ -56,10 +56,12 @@ size_t act_scale_bytes(int32_t M, int32_t K, int32_t bits) {
   return bits == 8 ? static_cast<size_t>(M) * 4 : static_cast<size_t>(M) * (K / kA4Group) * 2;
 }
 
-// Split-K partial sums of the GEMM: sized for the plan with 128-wide weight
-// groups (the only 8-bit case that splits), an upper bound for every w_group.
+// Split-K partial sums of the GEMM: the larger of the plans for 128-wide
+// weight groups and for one step per output channel (the cases that split),
+// an upper bound for every w_group.
 size_t gemm_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
-  return std::max<size_t>(kAlign, round_up(gemm_partial_bytes(bits, M, N, K, kKTile)));
+  const size_t p = std::max(gemm_partial_bytes(bits, M, N, K, kKTile), gemm_partial_bytes(bits, M, N, K, K));
+  return std::max<size_t>(kAlign, round_up(p));
 }
 
 // fused workspace: Q_X | scales | GEMM partial sums (each 256-byte aligned)

@@ -29,14 +29,16 @@ FUSED = {8: B.sq_linear_w4a8, 4: B.sq_linear_w4a4}
 
 
 @pytest.mark.parametrize("bits", [8, 4])
-@pytest.mark.parametrize("M,K,N", [(64, 8192, 2048), (300, 2048, 512), (600, 1024, 384)])
-def test_graph_replays_match_eager(bits, M, K, N):
+@pytest.mark.parametrize("M,K,N,per_channel", [(64, 8192, 2048, False), (300, 2048, 512, False),
+                                               (600, 1024, 384, False), (300, 2048, 512, True)])
+def test_graph_replays_match_eager(bits, M, K, N, per_channel):
     """64 tokens x 8192 channels: weight-streaming kernel with a K split and
     its second kernel; 300 and 600 tokens: the tiled kernel with its split
-    tail.  Fused linear and the GEMM entry point with a workspace."""
+    tail, with 128-wide weight groups or one step per output channel.  Fused
+    linear and the GEMM entry point with a workspace."""
     L1 = synth.make_layer(K=K, N=N, stream_counts=split(M), T=3, seed=[11, M, K, N])
     L2 = synth.make_layer(K=K, N=N, stream_counts=split(M), T=3, seed=[12, M, K, N])
-    _, W = oracle_weight(L1, 128)
+    _, W = oracle_weight(L1, K if per_channel else 128)
     x1 = u16_to_dev(L1.x_bits, torch.bfloat16)
     x2 = u16_to_dev(L2.x_bits, torch.bfloat16)
     act1, act2 = act_params(L1, 1, bits, 0), act_params(L2, 2, bits, 0)

@@ -52,17 +52,18 @@ def run_fused(bits, x, act, W, M, out):
     return y, ws
 
 
-@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("bits,G", [(8, 128), (4, 128), (8, 32768)])
 @pytest.mark.parametrize("M", [37, 200])
-def test_max_k(bits, M):
+def test_max_k(bits, G, M):
     """K = 32768: 37 tokens (weight-streaming kernel, K split across
-    workgroups) and 200 (tiled kernel); every output against the oracle."""
+    workgroups) and 200 (tiled kernel); with one weight step per channel the
+    int32 sums span all 32768 channels.  Every output against the oracle."""
     K, N = 32768, 64
     L = synth.make_layer(K=K, N=N, stream_counts=split(M), T=3, seed=[20, M, K], permute=True)
-    pw, W = dev_weight(L.w, L.d, L.bias_bits)
+    pw, W = dev_weight(L.w, L.d, L.bias_bits, G)
     act = act_params(L, 1, bits, 0)
     y, ws = run_fused(bits, u16_to_dev(L.x_bits, torch.bfloat16), act, W, M, F32)
-    res = oracle_rows(L.x_bits, L.tok2stream, L.gamma, 1, pw, L.dinv, L.clip, L.bias_bits, bits)
+    res = oracle_rows(L.x_bits, L.tok2stream, L.gamma, 1, pw, L.dinv, L.clip, L.bias_bits, bits, G)
     check_output(y, res, F32)
     rb = K if bits == 8 else K // 2
     assert np.array_equal(ws[: M * rb].view(M, rb).cpu().numpy(), res["qx"].view(np.uint8).reshape(M, rb))

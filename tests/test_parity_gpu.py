@@ -234,6 +234,29 @@ def test_few_tokens(bits, M, K, N, out):
         check_output(y, res, out)
 
 
+@pytest.mark.parametrize("M,K,N", [(4192, 1024, 2048), (300, 2048, 384), (1000, 8192, 256), (64, 2048, 512),
+                                   (129, 256, 128)])
+@pytest.mark.parametrize("out", [F32, BF16])
+def test_per_channel_weights(M, K, N, out):
+    """One weight step per output channel (G = K, the paper's weight format)
+    with 8-bit activations: int32 sums over all of K in the pipelined kernel.
+    4192 x 2048 outputs are 528 tiles, 512 computed whole and 16 split along
+    K (int32 partial sums added by the second kernel); the smaller layers are
+    split entirely, 256 channels (two stages) not at all.  Fused linear, and
+    the second kernel alone without and with a workspace."""
+    L = layer(M, K, N, seed=[13, M, K, N])
+    pw, W = oracle_weight(L, K)
+    act = act_params(L, 1, 8, 0)
+    res = oracle_linear(L, 1, 8, 0, pw, K)
+    y, _ = run_linear(B.sq_linear_w4a8, L, act, W, out)
+    check_output(y, res, out)
+    for with_ws in (False, True):
+        ws = B.alloc_workspace(B.SQ_VARIANT_GEMM, L.M, L.K, L.N, 8) if with_ws else None
+        y = torch.full((L.M, L.N), float("nan"), dtype=TORCH_OUT[out], device="cuda")
+        B.sq_gemm_w4a8(torch.from_numpy(res["qx"]).cuda(), f32_to_dev(res["scale"]), W, y, out, workspace=ws)
+        check_output(y, res, out)
+
+
 @pytest.mark.parametrize("bits", [8, 4])
 def test_gpu_prepared_weights_chain(bits):
     """Weights folded and packed on the GPU (sq_pack_weights), then the fused
