@@ -67,14 +67,17 @@ def make_layers(torch, B, synth, dev):
     for li, (name, K, N) in enumerate(LINEARS):
         L = synth.make_layer(K=K, N=N, stream_counts=TOKENS, T=T_STEPS, seed=[0, 2, li])
         x = torch.from_numpy(L.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
-        W = B.prepare_weight(torch.from_numpy(L.w).to(dev), torch.from_numpy(L.d).to(dev), W_GROUP,
-                             bias=torch.from_numpy(L.bias_bits.view(np.int16)).view(torch.bfloat16).to(dev))
+        w, d = torch.from_numpy(L.w).to(dev), torch.from_numpy(L.d).to(dev)
+        bias = torch.from_numpy(L.bias_bits.view(np.int16)).view(torch.bfloat16).to(dev)
+        W = B.prepare_weight(w, d, W_GROUP, bias=bias)
+        W_pc = B.prepare_weight(w, d, K, bias=bias)  # one step per output channel (context line)
+        del w
         acts = {}
         for bits in (8, 4):
             acts[bits] = B.ActParams(tok2stream=torch.from_numpy(L.tok2stream).to(dev),
                                      gamma=torch.from_numpy(L.gamma).to(dev), step=0, act_bits=bits,
                                      dinv=torch.from_numpy(L.dinv).to(dev))
-        layers.append(dict(name=name, K=K, N=N, L=L, x=x, W=W, acts=acts))
+        layers.append(dict(name=name, K=K, N=N, L=L, x=x, W=W, W_pc=W_pc, acts=acts))
     return layers
 
 
@@ -181,8 +184,8 @@ def run_suite(args):
         del g
         return e0.elapsed_time(e1) * 1e3 / reps  # us per call
 
-    def alg_bytes(M, K, N):  # bf16 X, int4 W, fp16 steps, bf16 Y, bias, stream map
-        return M * K * 2 + N * K // 2 + (K // W_GROUP) * N * 2 + M * N * 2 + 2 * N + 4 * M
+    def alg_bytes(M, K, N, wg=W_GROUP):  # bf16 X, int4 W, fp16 steps, bf16 Y, bias, stream map
+        return M * K * 2 + N * K // 2 + (K // wg) * N * 2 + M * N * 2 + 2 * N + 4 * M
 
     def layer_record(group, name, L, W, bits, reps):
         M, K = L["x"].shape
@@ -203,9 +206,9 @@ def run_suite(args):
         us_api = timed(lambda: fused(L["x"], act, W, y, BF16, wsf), reps)
         us_unf = timed(lambda: B.sq_linear_unfused(L["x"], act, W, y, BF16, wsu), max(3, reps // 4))
         ops = 2.0 * M * K * N
-        ab = alg_bytes(M, K, N)
+        ab = alg_bytes(M, K, N, W.w_group)
         k1b = M * K * 2 + (M * K if bits == 8 else M * K // 2) + (4 * M if bits == 8 else 2 * M * (K // 64)) + 4 * M
-        emit(dict(group=group, linear=name, act_bits=bits, M=M, K=K, N=N,
+        emit(dict(group=group, linear=name, act_bits=bits, M=M, K=K, N=N, w_group=W.w_group,
                   bound="mfma" if ops / ab >= PEAK_INT8_TOPS / PEAK_HBM_GBS * 1e3 else "hbm",
                   us_quant=round(us_k1, 2), us_gemm=round(us_k2, 2), us_layer=round(us_api, 2),
                   tops_layer=round(ops / us_api / 1e6, 1), tops_gemm=round(ops / us_k2 / 1e6, 1),
@@ -216,10 +219,10 @@ def run_suite(args):
                   fused_speedup=round(us_unf / us_api, 3)))
         del qx, sc, wsg, wsf, wsu, y
 
-    def layer_group(group, linears, tokens, bits_list, outl, reps, T=10, batch=1):
+    def layer_group(group, linears, tokens, bits_list, outl, reps, T=10, batch=1, per_channel=False):
         for li, (name, (K, N)) in enumerate(linears.items()):
             L = synth.device_layer(K, N, tokens, T=T, seed=1000 + li, outlier_frac=outl, batch=batch, device=dev)
-            W = B.prepare_weight(L.pop("w"), L["d"], W_GROUP, bias=L["bias"])
+            W = B.prepare_weight(L.pop("w"), L["d"], K if per_channel else W_GROUP, bias=L["bias"])
             for bits in bits_list:
                 layer_record(group, name, L, W, bits, reps)
             del L, W
@@ -243,6 +246,10 @@ def run_suite(args):
     layer_group("2B-class linears, W4A4, 4192 tokens, stream outliers 1%/2%/5%", synth.LINEARS_2B, synth.TOKENS_2B,
                 (4,), (0.01, 0.02, 0.05), 60)
     layer_group("14B-class linears, 8384 tokens (8192+64+128)", synth.LINEARS_14B, synth.TOKENS_14B, (8, 4), 0.02, 12)
+    layer_group("2B-class linears, W4A8, one weight step per output channel (the paper's weight format)",
+                synth.LINEARS_2B, synth.TOKENS_2B, (8,), 0.02, 60, per_channel=True)
+    layer_group("14B-class linears, W4A8, one weight step per output channel", synth.LINEARS_14B, synth.TOKENS_14B,
+                (8,), 0.02, 12, per_channel=True)
 
     # ---- denoising-loop sweep: 28 layers x 10 steps x {qkv, out, up, down} of
     # the 2B class, every layer with its own weights (0.7 GB packed: more than
@@ -344,11 +351,11 @@ def main():
         ly["ws_fused"] = {b: B.alloc_workspace(B.SQ_VARIANT_FUSED, M, ly["K"], ly["N"], b, dev) for b in (8, 4)}
         ly["ws_gemm"] = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, ly["K"], ly["N"], 8, dev)
 
-    def variant_step(tau, fn, bits, ws_key):
+    def variant_step(tau, fn, bits, ws_key, w_key="W"):
         for ly in layers:
             act = ly["acts"][bits]
             act.step = tau
-            fn(ly["x"], act, ly["W"], ly["y"], B.SQ_OUT_BF16, ly[ws_key][bits], stream)
+            fn(ly["x"], act, ly[w_key], ly["y"], B.SQ_OUT_BF16, ly[ws_key][bits], stream)
 
     def fused_step(tau, events=None):
         for i, ly in enumerate(layers):
@@ -430,19 +437,20 @@ def main():
         for i, ly in enumerate(layers)}
 
     # ---- unfused W4A8 and fused W4A4 on the same layers (context)
-    def time_variant(fn, bits, ws_key, steps):
+    def time_variant(fn, bits, ws_key, steps, w_key="W"):
         for s in range(max(3, args.warmup // 4)):
-            variant_step(s % T_STEPS, fn, bits, ws_key)
+            variant_step(s % T_STEPS, fn, bits, ws_key, w_key)
         torch.cuda.synchronize()
         t = time.perf_counter()
         for s in range(steps):
-            variant_step(s % T_STEPS, fn, bits, ws_key)
+            variant_step(s % T_STEPS, fn, bits, ws_key, w_key)
         torch.cuda.synchronize()
         return (time.perf_counter() - t) * 1e3 / steps
 
     vsteps = max(10, args.steps // 4)
     ms_unfused = time_variant(B.sq_linear_unfused, 8, "ws_unf", vsteps)
     ms_w4a4 = time_variant(B.sq_linear_w4a4, 4, "ws_fused", vsteps)
+    ms_pc = time_variant(B.sq_linear_w4a8, 8, "ws_fused", vsteps, "W_pc")
 
     # ---- a plain device copy of known size: the reference for the HBM byte
     # counters (FETCH_SIZE / WRITE_SIZE) of the profiled GEMM launches
@@ -478,7 +486,7 @@ def main():
             "act_bits": 8, "w_group": W_GROUP,
         },
         "roofline": {
-            "bound": "mfma", "kernel": "gemm_pipe_kernel<8,0> + gemm_tail_kernel<8,0> (sq_gemm_w4a8)",
+            "bound": "mfma", "kernel": "gemm_pipe_kernel<8,0,false> + gemm_tail_kernel<8,0,false> (sq_gemm_w4a8)",
             "launches": 2 * len(evs),
             "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",
             "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": measured_traffic(),
@@ -491,6 +499,8 @@ def main():
         "w4a8_as_k1_k2_calls": {"ms_per_step": round(ms_split, 5)},
         "fused_w4a4": {"ms_per_step": round(ms_w4a4, 5),
                        "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2)},
+        "fused_w4a8_per_channel_steps": {"ms_per_step": round(ms_pc, 5),
+                                         "tops": round(ops_step / (ms_pc * 1e-3) / 1e12, 2)},
         "hbm_copy": {"bytes": 2 * (COPY_MIB << 20), "us": round(copy_us, 1),
                      "gbs": round(2 * (COPY_MIB << 20) / (copy_us * 1e-6) / 1e9, 1)},
     }
