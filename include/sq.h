@@ -175,7 +175,18 @@ sq_status sq_linear_w4a8(const uint16_t* x, int32_t M, const sq_act_params* act,
                          void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
                          hipStream_t stream);
 
-/* The fused linear with 4-bit activations (act->act_bits == 4). */
+/* The fused linear with 4-bit activations (act->act_bits == 4).
+ * With more than 128 tokens, or weight groups wider than 128, the codes go
+ * to gfx950's fp8 matrix cores (v_mfma_f32_32x32x64_f8f6f4): the first kernel
+ * writes each code as the fp8 e4m3 byte of code * 2^-9 (sign and magnitude;
+ * |code| <= 7 is an exact subnormal), and the weight nibbles are read as
+ * code + 8.  Products and block sums are exact in fp32, so the outputs equal
+ * those of sq_quantize_act followed by sq_gemm_w4a4 bit for bit.
+ * Workspace layout (each part 256-byte aligned, in this order): the codes
+ * (fp8 bytes [M][K], else packed int4 [M][K/2]); sigma fp16 [M][K/64];
+ * with fp8 codes kc fp32 [M][K/64] = -8 S sigma 2^-18, S the code sum of the
+ * row's 64-group; then the GEMM's partial sums.  With 8-bit activations:
+ * Q_X int8 [M][K], r fp32 [M], partial sums. */
 sq_status sq_linear_w4a4(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                          void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
                          hipStream_t stream);

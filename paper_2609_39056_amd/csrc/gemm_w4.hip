@@ -89,6 +89,35 @@ __device__ __forceinline__ void supertile(int lid, int ntm, int ntn, int& tm, in
   tn = in_group / gm;
 }
 
+// Work item `it` of a persistent pipelined GEMM: the output tiles computed
+// whole (the first ndp of the logical order, XCD-ordered) followed by the K
+// ranges of the split tail tiles.  Tile origin and K range [kt0, kt1); unit
+// >= 0 numbers a split range.
+struct PipeItem {
+  int m0, n0, kt0, kt1, unit;
+};
+__device__ __forceinline__ PipeItem pipe_item(const GemmArgs& a, int it, int ntm, int ntn, int nkt, int BM, int BN) {
+  PipeItem r;
+  int lid;
+  if (it < a.ndp) {
+    lid = xcd_order(it, a.ndp);
+    r.kt0 = 0;
+    r.kt1 = nkt;
+    r.unit = -1;
+  } else {
+    r.unit = it - a.ndp;
+    lid = a.ndp + r.unit / a.split;
+    const int sl = r.unit % a.split;
+    r.kt0 = sl * nkt / a.split;
+    r.kt1 = (sl + 1) * nkt / a.split;
+  }
+  int tm, tn;
+  supertile(lid, ntm, ntn, tm, tn);
+  r.m0 = tm * BM;
+  r.n0 = tn * BN;
+  return r;
+}
+
 // Wait until at most N of this wave's vector-memory operations are in flight
 // and all of its LDS reads are done, then synchronize the workgroup: after it
 // the stage about to be read has landed and no wave still reads the slot the
@@ -419,35 +448,11 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
     __syncthreads();
   }
 
-  // item -> tile origin and K range [kt0, kt1); unit >= 0 marks a split range
-  struct Item {
-    int m0, n0, kt0, kt1, unit;
-  };
-  auto item_of = [&](int it) {
-    Item r;
-    int lid;
-    if (it < a.ndp) {
-      lid = xcd_order(it, a.ndp);
-      r.kt0 = 0;
-      r.kt1 = nkt;
-      r.unit = -1;
-    } else {
-      r.unit = it - a.ndp;
-      lid = a.ndp + r.unit / a.split;
-      const int sl = r.unit % a.split;
-      r.kt0 = sl * nkt / a.split;
-      r.kt1 = (sl + 1) * nkt / a.split;
-    }
-    int tm, tn;
-    supertile(lid, ntm, ntn, tm, tn);
-    r.m0 = tm * BM;
-    r.n0 = tn * BN;
-    return r;
-  };
+  auto item_of = [&](int it) { return pipe_item(a, it, ntm, ntn, nkt, BM, BN); };
 
   // ---- the load cursor: (item, stage) two stages ahead of the computation
   int d_it = blockIdx.x;
-  Item d = item_of(d_it);
+  PipeItem d = item_of(d_it);
   int d_kt = d.kt0;
   uint32_t d_slot = 0;  // byte offset of the ring slot the next stage goes to
   StageLoads<ABITS, kPipeWide> ld;
@@ -490,7 +495,7 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
   for (int it = blockIdx.x;;) {
-    const Item c = item_of(it);
+    const PipeItem c = item_of(it);
     EpiInputs<ABITS, EPI> ein;
     ein.load(a, c.m0, c.n0, wm, wn, lane);
     float y[TM][TN][16];
@@ -666,6 +671,280 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
   }
   // drain the loads still in flight (the re-issued last stages) before the
   // workgroup ends
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// ---------------------------------------------------------------- 4-bit activations on the fp8 matrix cores
+// The fused linear's 4-bit path for the tiled kernel.  The first kernel wrote
+// each activation code as the fp8 e4m3 byte of code * 2^-9 (sign and
+// magnitude; |code| <= 7 is an exact subnormal).  A packed weight nibble n
+// (two's complement) XOR 8 is code + 8 in 0..15, and the fp8 byte with that
+// value is (code + 8) * 2^-9 (subnormal below 8, normal above, one straight
+// line).  v_mfma_f32_32x32x64_f8f6f4 multiplies and sums one 64-wide block
+// exactly in fp32 (integers below 2^24 times 2^-18), giving
+// C' = (C + 8 S) 2^-18 with S the block's activation code sum; the first
+// kernel stored kc = -8 S sigma 2^-18 per (row, block), so one v_fma_mix
+// fma(C', sigma, kc) is round(C sigma) 2^-18, the same value as the int8
+// path's fp32(C) * sigma, and y += that * (Delta_W 2^18).  Per output and
+// block: two VALU ops instead of three, and no activation widening.
+struct F8Layout {
+  static constexpr int BM = 128, BN = 128, NWAVE = 4;
+  static constexpr int A_BYTES = BM * KT;      // fp8 code rows of 128 B, chunk c at c ^ ((r >> 1) & 7)
+  static constexpr int B_BYTES = BN * KT / 2;  // packed weight rows of 64 B, chunk c at c ^ ((r >> 2) & 3)
+  static constexpr int B_OFF = A_BYTES;
+  static constexpr int SG_OFF = B_OFF + B_BYTES;  // fp16 step pairs: wave w, row 32 w + i at w * 256 + i * 4
+  static constexpr int KC_OFF = SG_OFF + NWAVE * 256;  // kc: row 32 w + i, block half b at w * 256 + b * 128 + i * 4
+  static constexpr int W_OFF = KC_OFF + NWAVE * 256;   // weight-step pairs: columns 2 i, 2 i + 1 at i * 4
+  static constexpr int STAGE = W_OFF + 256;
+  // loads run one stage ahead; the previous stage's steps are still read
+  // while the current one is computed
+  static constexpr int STAGES = 3;
+  static constexpr int A_DMA = A_BYTES / 1024 / NWAVE, B_DMA = B_BYTES / 1024 / NWAVE;
+};
+
+struct F8Loads {
+  using LY = F8Layout;
+  uint32_t voffA[LY::A_DMA];
+  uint32_t voffB[LY::B_DMA];
+  uint32_t voffS, voffK, voffW;
+
+  __device__ __forceinline__ void set(const GemmArgs& a, int m0, int n0, int wave, int lane) {
+    const int M = a.M, N = a.N, K = a.K;
+#pragma unroll
+    for (int i = 0; i < LY::A_DMA; ++i) {
+      const int row = 8 * (LY::A_DMA * wave + i) + (lane >> 3);
+      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      voffA[i] = static_cast<uint32_t>(min(m0 + row, M - 1) - m0) * static_cast<uint32_t>(K) + c * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < LY::B_DMA; ++i) {
+      const int col = 16 * (LY::B_DMA * wave + i) + (lane >> 2);
+      const int c = (lane & 3) ^ ((col >> 2) & 3);
+      voffB[i] = static_cast<uint32_t>(min(n0 + col, N - 1) - n0) * static_cast<uint32_t>(K / 2) + c * 16;
+    }
+    const uint32_t groups = static_cast<uint32_t>(K / kA4Group);
+    voffS = static_cast<uint32_t>(min(m0 + 32 * wave + (lane & 31), M - 1) - m0) * groups * 2;
+    voffK = static_cast<uint32_t>(min(m0 + 32 * wave + (lane & 31), M - 1) - m0) * groups * 4 + (lane >> 5) * 4;
+    voffW = static_cast<uint32_t>(min(n0 + 2 * lane, N - 2));  // N is even: the pair stays in the row
+  }
+
+  // stage kt of the tile at (m0, n0) into the ring slot at LDS address st
+  __device__ __forceinline__ void issue(const GemmArgs& a, int m0, int n0, int kt, uint32_t st, int wave) const {
+    const int K = a.K;
+    const size_t groups = static_cast<size_t>(K / kA4Group);
+    const uint8_t* bA = static_cast<const uint8_t*>(a.qx) + static_cast<size_t>(m0) * K + kt * KT;
+    const uint8_t* bB = a.qw + static_cast<size_t>(n0) * (K / 2) + kt * (KT / 2);
+#pragma unroll
+    for (int i = 0; i < LY::A_DMA; ++i) dma<16>(bA, voffA[i], st + (LY::A_DMA * wave + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < LY::B_DMA; ++i) dma<16>(bB, voffB[i], st + LY::B_OFF + (LY::B_DMA * wave + i) * 1024);
+    const uint8_t* bS = static_cast<const uint8_t*>(a.act_scale) + static_cast<size_t>(m0) * groups * 2 + kt * 4;
+    dma<4>(bS, voffS, st + LY::SG_OFF + wave * 256);
+    const uint8_t* bK = reinterpret_cast<const uint8_t*>(a.kc) + static_cast<size_t>(m0) * groups * 4 + kt * 8;
+    dma<4>(bK, voffK, st + LY::KC_OFF + wave * 256);
+    if (wave == 0) {
+      const uint32_t e = static_cast<uint32_t>((kt * KT) / a.w_group) * static_cast<uint32_t>(a.N) + voffW;
+      dma<4>(a.w_scale, e * 2, st + LY::W_OFF);
+    }
+  }
+};
+
+// fp8 operand of 32 weight codes: one packed 16-byte chunk -> code + 8 per byte
+__device__ __forceinline__ v8i unpack_offset_frag(const uint4& p) {
+  const uint32_t w[4] = {p.x, p.y, p.z, p.w};
+  v8i r;
+#pragma unroll
+  for (int d = 0; d < 4; ++d) {
+    const uint32_t q = w[d] ^ 0x88888888u;  // each nibble: code + 8 (mod 16)
+    r[2 * d] = static_cast<int>(q & 0x0F0F0F0Fu);
+    r[2 * d + 1] = static_cast<int>((q >> 4) & 0x0F0F0F0Fu);
+  }
+  return r;
+}
+
+// y += round(C sigma) * Delta_W for row tile tm and both column tiles, block
+// half hb of the stage at st (w: Delta_W * 2^18 of the lane's two columns).
+// The lane's rows are 64 wm + 32 tm + 8 r4 + 4 h + i: wave block 2 wm + tm,
+// row 8 r4 + 4 h + i within it; `rowb` = wm * 512 + h * 16 (bytes of one
+// step pair or kc per row: 4), the rest are immediate offsets.
+__device__ __forceinline__ void fold_f8(float (&y)[TM][TN][16], const uint8_t* st, int hb, const v16f (&c)[TN],
+                                        int rowb, int tm, const float (&w)[TN]) {
+  using LY = F8Layout;
+#pragma unroll
+  for (int r4 = 0; r4 < 4; ++r4) {
+    const int o = rowb + tm * 256 + r4 * 32;
+    const uint4 sp = *reinterpret_cast<const uint4*>(st + LY::SG_OFF + o);
+    const uint4 kq = *reinterpret_cast<const uint4*>(st + LY::KC_OFF + o + hb * 128);
+    const uint32_t s4[4] = {sp.x, sp.y, sp.z, sp.w};
+    const uint32_t kb[4] = {kq.x, kq.y, kq.z, kq.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float sg = static_cast<float>(__builtin_bit_cast(half2v, s4[i])[hb]);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int r = r4 * 4 + i;
+        const float t = __builtin_fmaf(c[tn][r], sg, __uint_as_float(kb[i]));
+        y[tm][tn][r] = __builtin_fmaf(t, w[tn], y[tm][tn][r]);
+      }
+    }
+  }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256, 2) void gemm_a4f8_kernel(GemmArgs a) {
+  using LY = F8Layout;
+  constexpr int BM = LY::BM, BN = LY::BN;
+  constexpr uint32_t RING = LY::STAGES * LY::STAGE;
+  static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
+  static_assert(2 * RING <= 160 * 1024, "two workgroups per CU");
+
+  __shared__ __align__(1024) uint8_t smem[RING];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / 2, wn = wave % 2;
+  const int M = a.M, N = a.N, K = a.K;
+  const int ntm = (M + BM - 1) / BM, ntn = (N + BN - 1) / BN, nkt = K / KT;
+  const int nitems = a.ndp + (ntm * ntn - a.ndp) * a.split;
+  const int G = gridDim.x;
+  if (static_cast<int>(blockIdx.x) >= nitems) return;
+  const uint32_t smem_lds = lds_offset(smem);
+  // An item's first fold scales the previous slot's steps by a zero weight
+  // step: those are another item's (finite) or, before the ring's first use,
+  // these zeros.
+  for (int i = threadIdx.x; i < LY::STAGES * (2 * LY::NWAVE * 256 / 4); i += 256) {
+    const int s = i / (2 * LY::NWAVE * 256 / 4), e = i % (2 * LY::NWAVE * 256 / 4);
+    reinterpret_cast<uint32_t*>(smem + s * LY::STAGE + LY::SG_OFF)[e] = 0u;
+  }
+  __syncthreads();
+
+  int d_it = blockIdx.x;
+  PipeItem d = pipe_item(a, d_it, ntm, ntn, nkt, BM, BN);
+  int d_kt = d.kt0;
+  uint32_t d_slot = 0;
+  F8Loads ld;
+  ld.set(a, d.m0, d.n0, wave, lane);
+  auto issue = [&]() {
+    ld.issue(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
+    d_slot = d_slot + LY::STAGE == RING ? 0 : d_slot + LY::STAGE;
+  };
+  // past the last stage of the last item the same stage is loaded again
+  auto advance = [&]() {
+    if (d_kt + 1 < d.kt1) {
+      ++d_kt;
+    } else if (d_it + G < nitems) {
+      d_it += G;
+      d = pipe_item(a, d_it, ntm, ntn, nkt, BM, BN);
+      d_kt = d.kt0;
+      ld.set(a, d.m0, d.n0, wave, lane);
+    }
+  };
+  issue();
+  advance();
+  wait_vm_and_barrier<0>();
+
+  // per-lane LDS offsets of the fragments (row tile 1 / column tile 1: + 32 rows)
+  const int arow = wm * 64 + (lane & 31), bcol = wn * 64 + (lane & 31), h = lane >> 5;
+  int aoff[2][2], boff[2];
+#pragma unroll
+  for (int hb = 0; hb < 2; ++hb) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) aoff[hb][q] = arow * KT + 16 * ((4 * hb + 2 * h + q) ^ ((arow >> 1) & 7));
+    boff[hb] = LY::B_OFF + bcol * (KT / 2) + 16 * ((2 * hb + h) ^ ((bcol >> 2) & 3));
+  }
+  const int wc = wn * 64 + (lane & 31);  // the lane's first column within the tile
+  int rowb = wm * 512 + h * 16;           // step / kc offset of the lane's first row (see fold_f8)
+  asm volatile("" : "+v"(rowb));          // a per-lane base: keep the tile offsets as immediates
+
+  uint32_t c_slot = 0;
+  auto next_slot = [&](uint32_t s) { return s + LY::STAGE == RING ? 0u : s + LY::STAGE; };
+  auto prev_slot = [&](uint32_t s) { return s == 0 ? RING - LY::STAGE : s - LY::STAGE; };
+  auto read_w = [&](const uint8_t* st, float (&w)[TN]) {
+    const uint32_t* W = reinterpret_cast<const uint32_t*>(st + LY::W_OFF);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int col = wc + tn * 32;
+      const uint32_t pair = W[col >> 1];
+      w[tn] = f16_to_f32((col & 1) ? (pair >> 16) : (pair & 0xFFFFu)) * 262144.0f;  // * 2^18
+    }
+  };
+
+  v16f acc[TM][TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16f)(0.0f);
+  for (int it = blockIdx.x;;) {
+    const PipeItem c = pipe_item(a, it, ntm, ntn, nkt, BM, BN);
+    EpiInputs<4, EPI> ein;
+    ein.load(a, c.m0, c.n0, wm, wn, lane);
+    float y[TM][TN][16];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) y[tm][tn][r] = 0.0f;
+    float wsv_prev[TN] = {0.0f, 0.0f}, wsv[TN];
+    for (int kt = c.kt0; kt < c.kt1; ++kt) {
+      issue();
+      advance();
+      const uint8_t* st = smem + c_slot;
+      const uint8_t* st_prev = smem + prev_slot(c_slot);
+      read_w(st, wsv);
+#pragma unroll
+      for (int hb = 0; hb < 2; ++hb) {
+        v8i bf[TN];
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+          bf[tn] = unpack_offset_frag(*reinterpret_cast<const uint4*>(st + boff[hb] + tn * 32 * (KT / 2)));
+#pragma unroll
+        for (int tm = 0; tm < TM; ++tm) {
+          const uint4 a0 = *reinterpret_cast<const uint4*>(st + aoff[hb][0] + tm * 32 * KT);
+          const uint4 a1 = *reinterpret_cast<const uint4*>(st + aoff[hb][1] + tm * 32 * KT);
+          const v8i af = {static_cast<int>(a0.x), static_cast<int>(a0.y), static_cast<int>(a0.z),
+                          static_cast<int>(a0.w), static_cast<int>(a1.x), static_cast<int>(a1.y),
+                          static_cast<int>(a1.z), static_cast<int>(a1.w)};
+          // previous block: second half of the previous stage, or first half of this one
+          if (hb == 0) {
+            fold_f8(y, st_prev, 1, acc[tm], rowb, tm, wsv_prev);
+          } else {
+            fold_f8(y, st, 0, acc[tm], rowb, tm, wsv);
+          }
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+            acc[tm][tn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bf[tn], (v16f)(0.0f), 0, 0, 0, 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
+      wait_vm_and_barrier<0>();
+      c_slot = next_slot(c_slot);
+    }
+    const uint8_t* st_last = smem + prev_slot(c_slot);
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) fold_f8(y, st_last, 1, acc[tm], rowb, tm, wsv_prev);
+
+    if (c.unit >= 0) {
+      // split tail: this K range's fp32 sums of the tile, row-major [BM][BN]
+      int ln = lane;
+      asm volatile("" : "+v"(ln));
+      float* P = a.partial + static_cast<size_t>(c.unit) * BM * BN;
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
+            if (c.m0 + row < M) P[row * BN + wn * 64 + tn * 32 + (ln & 31)] = y[tm][tn][r];
+          }
+    } else {
+      store_tile<4, EPI>(a, y, c.m0, c.n0, wm, wn, lane, ein);
+    }
+    it += G;
+    if (it >= nitems) break;
+  }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
@@ -939,6 +1218,27 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
 // (few tokens) or the pipelined one; one step per output channel (w_group =
 // K) the pipelined one with int32 sums over K; other group widths the
 // non-pipelined kernel.
+// The fp8 4-bit kernel: the same tiles, work list and split tail as the
+// 4-bit pipelined kernel.
+template <int EPI>
+hipError_t launch_a4f8(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
+  GemmArgs a = a0;
+  const int slots = device_cus() * 2;
+  const Plan p = pipe_plan<4>(a.M, a.N, a.K, partial ? partial_bytes : 0);
+  a.ndp = p.ndp;
+  a.split = p.split;
+  a.partial = p.split > 1 ? partial : nullptr;
+  const int rest = p.ntiles - p.ndp;
+  const int nitems = p.ndp + rest * p.split;
+  hipLaunchKernelGGL((gemm_a4f8_kernel<EPI>), dim3(static_cast<unsigned>(std::min(nitems, slots))), dim3(256), 0, s,
+                     a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || rest == 0 || p.split == 1) return e;
+  constexpr int per_tile_blocks = F8Layout::BM * F8Layout::BN / 4 / 256;
+  hipLaunchKernelGGL((gemm_tail_kernel<4, EPI, false>), dim3(rest * per_tile_blocks), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int EPI>
 hipError_t launch_a8(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
   if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(8, EPI, a, s, partial, partial_bytes);
@@ -987,6 +1287,9 @@ hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, 
     switch (epi) {
       case kEpiOut:
       case kEpiPartial:
+        if (a.kc != nullptr)
+          return epi == kEpiOut ? launch_a4f8<kEpiOut>(a, s, partial, partial_bytes)
+                                : launch_a4f8<kEpiPartial>(a, s, partial, partial_bytes);
         if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(4, epi, a, s, partial, partial_bytes);
         return epi == kEpiOut ? launch_t<4, kEpiOut, true>(a, s, partial, partial_bytes)
                               : launch_t<4, kEpiPartial, true>(a, s, partial, partial_bytes);

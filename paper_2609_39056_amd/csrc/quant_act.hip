@@ -27,8 +27,9 @@ __device__ __forceinline__ uint32_t pack_low_bytes(uint32_t w0, uint32_t w1, uin
   return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
 }
 
-template <int BITS, int WPR, int NCH>
+template <int BITS, int WPR, int NCH, bool F8>
 __global__ __launch_bounds__(256) void quantize_act_kernel(QuantArgs a) {
+  static_assert(!F8 || BITS == 4, "fp8 code bytes are a 4-bit format");
   static_assert(WPR == 1 || WPR == 4, "a row spans one wave or the whole workgroup");
   constexpr int RPW = 4 / WPR;   // rows per workgroup
   constexpr int LPR = 64 * WPR;  // lanes per row
@@ -119,8 +120,9 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(QuantArgs a) {
     if (lr == 0) static_cast<float*>(a.scale)[row] = delta / g;
   } else {
     if (row >= M) return;  // a row's lanes leave together
-    uint8_t* qr = static_cast<uint8_t*>(a.qx) + static_cast<size_t>(row) * (a.K / 2);
+    uint8_t* qr = static_cast<uint8_t*>(a.qx) + static_cast<size_t>(row) * (F8 ? a.K : a.K / 2);
     uint16_t* sr = static_cast<uint16_t*>(a.scale) + static_cast<size_t>(row) * (a.K / kA4Group);
+    float* kr = F8 ? a.kc + static_cast<size_t>(row) * (a.K / kA4Group) : nullptr;
 #pragma unroll
     for (int j = 0; j < NCH; ++j) {
       // range of the 64-group: the 8 adjacent lanes holding its chunks
@@ -137,20 +139,46 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(QuantArgs a) {
       float inv = 1.0f / delta;
       if (__builtin_isinf(inv)) inv = 0.0f;
       uint32_t b[8];
+      int csum = 0;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         float t = (v[j][e] * g) * inv;
         t = fminf(fmaxf(t, -QA), QA);
-        b[e] = rne_code_bits(t);
+        if constexpr (F8) {
+          // |code| = rne(|t|) (rounding is symmetric); the sign bit of t
+          // becomes the fp8 sign (a code 0 of negative t is -0: value 0)
+          const uint32_t m = rne_code_bits(fabsf(t)) & 0xFFu;
+          const uint32_t neg = __float_as_uint(t) >> 31;
+          b[e] = m | (neg << 7);
+          csum += neg ? -static_cast<int>(m) : static_cast<int>(m);
+        } else {
+          b[e] = rne_code_bits(t);
+        }
       }
-      // code e < 4 -> low nibble of byte e; code e >= 4 -> high nibble of byte e-4
-      const uint32_t lo = pack_low_bytes(b[0], b[1], b[2], b[3]);
-      const uint32_t hi = pack_low_bytes(b[4], b[5], b[6], b[7]);
-      const uint32_t word = (lo & 0x0F0F0F0Fu) | ((hi << 4) & 0xF0F0F0F0u);
       const int c = lr + j * LPR;
-      if (c < nch) {
-        *reinterpret_cast<uint32_t*>(qr + c * 4) = word;
-        if ((c & 7) == 0) sr[c >> 3] = static_cast<uint16_t>(dbits);
+      if constexpr (F8) {
+        // the 64-group's code sum: the 8 adjacent lanes holding its chunks
+        csum += __shfl_xor(csum, 1, 64);
+        csum += __shfl_xor(csum, 2, 64);
+        csum += __shfl_xor(csum, 4, 64);
+        if (c < nch) {
+          *reinterpret_cast<uint2*>(qr + c * 8) =
+              make_uint2(pack_low_bytes(b[0], b[1], b[2], b[3]), pack_low_bytes(b[4], b[5], b[6], b[7]));
+          if ((c & 7) == 0) {
+            sr[c >> 3] = static_cast<uint16_t>(dbits);
+            // exact: |8 S| < 2^12 and delta has an 11-bit significand
+            kr[c >> 3] = (static_cast<float>(-8 * csum) * delta) * 3.814697265625e-06f;  // * 2^-18
+          }
+        }
+      } else {
+        // code e < 4 -> low nibble of byte e; code e >= 4 -> high nibble of byte e-4
+        const uint32_t lo = pack_low_bytes(b[0], b[1], b[2], b[3]);
+        const uint32_t hi = pack_low_bytes(b[4], b[5], b[6], b[7]);
+        const uint32_t word = (lo & 0x0F0F0F0Fu) | ((hi << 4) & 0xF0F0F0F0u);
+        if (c < nch) {
+          *reinterpret_cast<uint32_t*>(qr + c * 4) = word;
+          if ((c & 7) == 0) sr[c >> 3] = static_cast<uint16_t>(dbits);
+        }
       }
     }
   }
@@ -159,8 +187,14 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(QuantArgs a) {
 template <int BITS, int WPR, int NCH>
 hipError_t launch_one(const QuantArgs& a, hipStream_t s) {
   constexpr int RPW = 4 / WPR;
-  hipLaunchKernelGGL((quantize_act_kernel<BITS, WPR, NCH>), wg_grid((static_cast<size_t>(a.M) + RPW - 1) / RPW),
-                     dim3(256), 0, s, a);
+  const dim3 grid = wg_grid((static_cast<size_t>(a.M) + RPW - 1) / RPW);
+  if constexpr (BITS == 4) {
+    if (a.kc != nullptr) {
+      hipLaunchKernelGGL((quantize_act_kernel<BITS, WPR, NCH, true>), grid, dim3(256), 0, s, a);
+      return hipGetLastError();
+    }
+  }
+  hipLaunchKernelGGL((quantize_act_kernel<BITS, WPR, NCH, false>), grid, dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -64,25 +64,40 @@ size_t gemm_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
   return std::max<size_t>(kAlign, round_up(p));
 }
 
-// fused workspace: Q_X | scales | GEMM partial sums (each 256-byte aligned)
+// fused workspace: Q_X | scales | (fp8 4-bit codes: kc) | GEMM partial sums,
+// each 256-byte aligned.  With 4-bit activations on the pipelined path
+// (a4_fp8_path) Q_X holds one fp8 byte per code and kc follows the scales.
 struct FusedWs {
   void* qx;
   void* scale;
+  float* kc;
   float* partial;
   size_t partial_bytes;
 };
-FusedWs fused_ws(void* ws, size_t ws_bytes, int32_t M, int32_t K, int32_t bits) {
+size_t kc_bytes(int32_t M, int32_t K) { return static_cast<size_t>(M) * (K / kA4Group) * 4; }
+FusedWs fused_ws(void* ws, size_t ws_bytes, int32_t M, int32_t K, int32_t bits, bool f8) {
   uint8_t* p = static_cast<uint8_t*>(ws);
   FusedWs f;
+  const size_t q = round_up(f8 ? static_cast<size_t>(M) * K : qx_bytes(M, K, bits));
   f.qx = p;
-  f.scale = p + round_up(qx_bytes(M, K, bits));
-  const size_t off = round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits));
+  f.scale = p + q;
+  size_t off = q + round_up(act_scale_bytes(M, K, bits));
+  f.kc = nullptr;
+  if (f8) {
+    f.kc = reinterpret_cast<float*>(p + off);
+    off += round_up(kc_bytes(M, K));
+  }
   f.partial = reinterpret_cast<float*>(p + off);
   f.partial_bytes = ws_bytes - off;
   return f;
 }
 
+// Sized for the larger layout (fp8 codes and kc for 4-bit activations): the
+// weight's group width, which picks the path, is not an argument here.
 size_t fused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
+  if (bits == 4)
+    return round_up(static_cast<size_t>(M) * K) + round_up(act_scale_bytes(M, K, bits)) + round_up(kc_bytes(M, K)) +
+           gemm_ws_bytes(M, K, N, bits);
   return round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits)) + gemm_ws_bytes(M, K, N, bits);
 }
 
@@ -95,8 +110,9 @@ size_t unfused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
 }
 
 sq_status quantize(const uint16_t* x, int32_t M, int32_t K, const sq_act_params* act, void* qx,
-                   void* scale, hipStream_t stream) {
+                   void* scale, hipStream_t stream, float* kc = nullptr) {
   QuantArgs q;
+  q.kc = kc;
   q.x = x;
   q.tok2stream = act->tok2stream;
   q.gamma = act->gamma;
@@ -148,11 +164,13 @@ sq_status linear_fused(int32_t bits, const uint16_t* x, int32_t M, const sq_act_
   if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
   if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 16)) return SQ_ERR_ALIGN;
   if (ws_bytes < fused_ws_bytes(M, w->K, w->N, bits)) return SQ_ERR_WORKSPACE;
-  FusedWs f = fused_ws(ws, ws_bytes, M, w->K, bits);
-  st = quantize(x, M, w->K, act, f.qx, f.scale, stream);
+  const bool f8 = bits == 4 && a4_fp8_path(M, w->w_group);
+  FusedWs f = fused_ws(ws, ws_bytes, M, w->K, bits, f8);
+  st = quantize(x, M, w->K, act, f.qx, f.scale, stream, f.kc);
   if (st != SQ_OK) return st;
-  return hip_status(launch_gemm(bits, kEpiOut, gemm_args(f.qx, f.scale, M, act, w, y, out_dtype), stream,
-                                f.partial, f.partial_bytes));
+  GemmArgs g = gemm_args(f.qx, f.scale, M, act, w, y, out_dtype);
+  g.kc = f.kc;
+  return hip_status(launch_gemm(bits, kEpiOut, g, stream, f.partial, f.partial_bytes));
 }
 
 }  // namespace

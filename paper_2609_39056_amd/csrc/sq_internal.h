@@ -65,6 +65,11 @@ struct QuantArgs {
   const float* dinv;
   void* qx;
   void* scale;
+  // 4-bit codes for the fp8 matrix cores (the fused linear's pipelined path):
+  // when kc is set, qx holds one byte per code, the fp8 e4m3 value code * 2^-9
+  // (sign and magnitude; |code| <= 7 is an exact subnormal), and kc holds the
+  // fp32 -8 * S * sigma * 2^-18 per (row, 64-group), S = the group's code sum.
+  float* kc;
   int32_t M, K, S, step, range_mode;
 };
 
@@ -81,6 +86,7 @@ struct GemmArgs {
   const int32_t* tok2stream;  // 4-bit kappa: s(i)
   const float* gamma;       // 4-bit kappa: gamma table
   int32_t S, step;
+  const float* kc;          // 4-bit codes as fp8 bytes (see QuantArgs::kc); NULL: packed int4
   const uint8_t* qw;
   const uint16_t* w_scale;
   const uint16_t* bias;
@@ -107,6 +113,9 @@ int device_cus();
 // 128-wide weight groups; epi kEpiOut or kEpiPartial).  Splits K across
 // workgroups when `partial` holds skinny_partial_bytes(...) bytes.
 constexpr int kSkinnyMaxM = 128;
+// 4-bit activations take the fp8 pipelined GEMM in the fused linear whenever
+// the weight-streaming kernel does not apply.
+inline bool a4_fp8_path(int32_t M, int32_t w_group) { return !(w_group == kKTile && M <= kSkinnyMaxM); }
 size_t skinny_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K);
 hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
                          size_t partial_bytes);

@@ -88,3 +88,60 @@ def check_output(y_dev, res, out_dtype, rows=None):
     err = np.abs(gv - y_or.astype(np.float64))
     assert np.all(err <= 1e-5 * A + ulp), "cast output outside 1e-5*A + 1 ulp"
     return int(d[nc].max(initial=0))
+
+
+def _align(n):
+    return (n + 255) // 256 * 256
+
+
+def fused_first_kernel_output(ws, M, K, bits, w_group, rows=None):
+    """What the fused linear's first kernel left in its workspace (the layout
+    include/sq.h documents), for `rows` (default all): the codes as int
+    [rows, K], the scales as raw bits (uint32 r, or uint16 sigma [rows, K/64])
+    and, for 4-bit codes on the fp8 path, kc as fp32 [rows, K/64] (else None).
+    Rows are selected on the device."""
+    ri = None if rows is None else torch.as_tensor(np.asarray(rows, dtype=np.int64), device=ws.device)
+    pick = (lambda t: t) if ri is None else (lambda t: t[ri])
+    if bits == 8:
+        codes = pick(ws[: M * K].view(M, K)).cpu().numpy().view(np.int8).astype(np.int64)
+        off = _align(M * K)
+        r = pick(ws[off: off + 4 * M].view(torch.int32)).cpu().numpy().view(np.uint32)
+        return codes, r, None
+    f8 = not (w_group == 128 and M <= 128)
+    g = K // 64
+    if f8:
+        b = pick(ws[: M * K].view(M, K)).cpu().numpy().astype(np.int64)
+        codes = np.where(b & 0x80, -(b & 0x7F), b & 0x7F)
+        off = _align(M * K)
+    else:
+        packed = pick(ws[: M * K // 2].view(M, K // 2)).cpu().numpy()
+        codes = O.unpack_int4(packed).astype(np.int64)
+        off = _align(M * K // 2)
+    sigma = pick(ws[off: off + 2 * M * g].view(torch.int16).view(M, g)).cpu().numpy().view(np.uint16)
+    kc = None
+    if f8:
+        off += _align(2 * M * g)
+        kc = pick(ws[off: off + 4 * M * g].view(torch.float32).view(M, g)).cpu().numpy()
+    return codes, sigma, kc
+
+
+def check_first_kernel_output(ws, M, K, bits, w_group, res, rows=None):
+    """Codes and stored scales bit-exact against the oracle's quantize step
+    (res: O.linear's result for the same rows); fp8 4-bit path: kc too."""
+    codes, sc, kc = fused_first_kernel_output(ws, M, K, bits, w_group, rows)
+    assert np.array_equal(codes, res["codes"].astype(np.int64))
+    if bits == 8:
+        assert np.array_equal(sc, np.asarray(res["scale"], dtype=np.float32).view(np.uint32))
+    else:
+        assert np.array_equal(sc, np.asarray(res["scale"]).view(np.uint16))
+        if kc is not None:  # values exact (a zero sum may give either sign of zero)
+            assert np.array_equal(kc, expected_kc(codes, sc))
+
+
+def expected_kc(codes, sigma_bits):
+    """-8 * S * sigma * 2^-18 per (row, 64-group), S the group's code sum
+    (exact in fp32: |8 S| < 2^12 and sigma has an 11-bit significand)."""
+    M, K = codes.shape
+    S = codes.reshape(M, K // 64, 64).sum(axis=2)
+    sig = sigma_bits.view(np.float16).astype(np.float64)
+    return (-8.0 * S * sig * 2.0 ** -18).astype(np.float32)

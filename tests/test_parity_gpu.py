@@ -8,8 +8,8 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import (act_params, bits16, check_output, f32_to_dev, i32_to_dev, oracle_weight,
-                      u16_to_dev, u8_to_dev)
+from gpu_util import (act_params, bits16, check_first_kernel_output, check_output, f32_to_dev, i32_to_dev,
+                      oracle_weight, u16_to_dev, u8_to_dev)
 from oracle import sq_oracle as O
 from paper_2609_39056_amd import binding as B
 from paper_2609_39056_amd import synth
@@ -166,9 +166,8 @@ def test_linear_small_layer(bits, mode, out, G):
         for fn in (FUSED[bits], B.sq_linear_unfused):
             y, ws = run_linear(fn, L, act, W, out)
             check_output(y, res, out)
-            if fn is not B.sq_linear_unfused:  # the workspace holds Q_X first
-                n = L.M * L.K if bits == 8 else L.M * L.K // 2
-                assert np.array_equal(ws[:n].cpu().numpy(), res["qx"].reshape(-1).view(np.uint8))
+            if fn is not B.sq_linear_unfused:  # the first kernel's codes and scales, from the workspace
+                check_first_kernel_output(ws, L.M, L.K, bits, G, res)
 
 
 @pytest.mark.parametrize("bits", [8, 4])
@@ -257,6 +256,30 @@ def test_per_channel_weights(M, K, N, out):
         check_output(y, res, out)
 
 
+@pytest.mark.parametrize("M,K,N,G", [(4192, 1024, 2048, 128), (300, 2048, 384, 128), (200, 1024, 128, 1024),
+                                     (129, 256, 192, 128), (1000, 8192, 256, 8192)])
+def test_a4_fp8_path_equals_int8_path(M, K, N, G):
+    """4-bit activations on the fp8 matrix cores (the fused linear with more
+    than 128 tokens or wide weight groups) against the int8 path (the first
+    kernel's packed codes, then sq_gemm_w4a4): the first kernel's codes,
+    steps and kc against the oracle, and the outputs bit for bit equal,
+    with whole tiles, split tails, ragged M and N, and per-channel steps."""
+    L = layer(M, K, N, seed=[14, M, K, N], outlier_frac=(0.01, 0.02, 0.05))
+    pw, W = oracle_weight(L, G)
+    act = act_params(L, 2, 4, 0)
+    y, ws = run_linear(B.sq_linear_w4a4, L, act, W, F32)
+    rows = synth.stratified_rows(L.tok2stream, 64, seed=1) if M > 1000 else None
+    res = oracle_linear(L, 2, 4, 0, pw, G, rows=rows)
+    check_first_kernel_output(ws, M, K, 4, G, res, rows=rows)
+    check_output(y, res, F32, rows=rows)
+    qx, sc = B.act_buffers(M, K, 4)
+    B.sq_quantize_act(xdev(L), act, qx, sc)
+    y_int = torch.full_like(y, float("nan"))
+    B.sq_gemm_w4a4(qx, sc, act, W, y_int, F32, workspace=B.alloc_workspace(B.SQ_VARIANT_GEMM, M, K, N, 4))
+    torch.cuda.synchronize()
+    assert torch.equal(y.view(torch.int32), y_int.view(torch.int32))
+
+
 @pytest.mark.parametrize("bits", [8, 4])
 def test_gpu_prepared_weights_chain(bits):
     """Weights folded and packed on the GPU (sq_pack_weights), then the fused
@@ -301,7 +324,5 @@ def test_full_size_sampled_rows(name, bits, tokens, K, N, outl):
     rows = synth.stratified_rows(L.tok2stream, 256, seed=0)
     res = oracle_linear(L, step, bits, 0, pw, 128, rows=rows)
     check_output(y, res, BF16, rows=rows)
-    # codes of the sampled rows, read back from the workspace
-    rb = L.K if bits == 8 else L.K // 2
-    q = ws[: L.M * rb].view(L.M, rb)[torch.as_tensor(rows, device="cuda")]
-    assert np.array_equal(q.cpu().numpy(), res["qx"].view(np.uint8).reshape(len(rows), rb))
+    # codes and scales of the sampled rows, read back from the workspace
+    check_first_kernel_output(ws, L.M, L.K, bits, 128, res, rows=rows)
