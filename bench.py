@@ -452,6 +452,26 @@ def main():
     ms_w4a4 = time_variant(B.sq_linear_w4a4, 4, "ws_fused", vsteps)
     ms_pc = time_variant(B.sq_linear_w4a8, 8, "ws_fused", vsteps, "W_pc")
 
+    # ---- the int8 matrix-core rate this GPU sustains (sq_probe_mfma_i8: back
+    # to back MFMAs on register operands at the GEMM's occupancy), as a
+    # measured ceiling beside the published peak: zero operands, random
+    # operands, and random operands with the 128-group fold's VALU work
+    sink = B.probe_sink(dev)
+    n_wg = sink.numel() // 256
+    probe_iters = 20000
+    ceiling = {}
+    for label, rnd, fold in (("zero_operands", 0, 0), ("random_operands", 1, 0),
+                             ("random_operands_with_128_group_fold", 1, 1)):
+        B.sq_probe_mfma_i8(200, rnd, fold, sink, stream)
+        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        p0.record(stream)
+        B.sq_probe_mfma_i8(probe_iters, rnd, fold, sink, stream)
+        p1.record(stream)
+        torch.cuda.synchronize()
+        probe_ops = n_wg * 4 * probe_iters * 16 * 2.0 * 32 ** 3
+        ceiling[label] = round(probe_ops / (p0.elapsed_time(p1) * 1e-3) / 1e12, 1)
+    del sink
+
     # ---- a plain device copy of known size: the reference for the HBM byte
     # counters (FETCH_SIZE / WRITE_SIZE) of the profiled GEMM launches
     src = torch.empty(COPY_MIB << 20, dtype=torch.uint8, device=dev).fill_(1)
@@ -490,7 +510,10 @@ def main():
             "launches": 2 * len(evs),
             "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",
             "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": measured_traffic(),
+            "measured_ceiling": ceiling["random_operands_with_128_group_fold"],
+            "frac_of_measured_ceiling": round(gemm_tops / ceiling["random_operands_with_128_group_fold"], 4),
         },
+        "mfma_i8_ceiling_tops": ceiling,
         "per_layer": per_layer,
         "quant_kernel_gbs": round(k1_gbs, 1),
         "unfused_w4a8": {"ms_per_step": round(ms_unfused, 5),

@@ -202,6 +202,20 @@ sq_status sq_linear_unfused(const uint16_t* x, int32_t M, const sq_act_params* a
                             void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
                             hipStream_t stream);
 
+/* Measurement hook: the int8 matrix-core rate the GPU sustains, as a
+ * ceiling beside the published peak.  Launches sq_probe_mfma_i8_sink_bytes()
+ * / 1024 workgroups (two per CU) whose waves each issue iters * 16
+ * v_mfma_i32_32x32x32_i8 back to back on register operands (2 * 32^3 int8
+ * ops each), with no memory traffic: operands all zero (random_operands ==
+ * 0) or pseudo-random; with fold != 0 each 32x32 accumulator is also
+ * converted and fma'd into fp32 once per four MFMAs, as the dequantization of
+ * one 128-channel block.  The caller times the call (e.g. with HIP events);
+ * sink is int32 scratch of at least sq_probe_mfma_i8_sink_bytes() bytes that
+ * keeps the work live.  iters in [1, 2^24]. */
+size_t sq_probe_mfma_i8_sink_bytes(void);
+sq_status sq_probe_mfma_i8(int32_t iters, int32_t random_operands, int32_t fold, int32_t* sink, size_t sink_bytes,
+                           hipStream_t stream);
+
 /* Test hook: runs the fused GEMM main loop on already-quantized activations
  * and writes every int32 block accumulator instead of the epilogue:
  * acc_out[b][i][j] = sum over K-block b of q_ik * w_jk, with blocks of

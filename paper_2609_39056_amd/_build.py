@@ -35,7 +35,8 @@ FLAGS = [
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 
-SOURCES = ["sq_api.cpp", "quant_act.hip", "pack_weights.hip", "gemm_w4.hip", "gemm_skinny.hip", "unfused.hip"]
+SOURCES = ["sq_api.cpp", "quant_act.hip", "pack_weights.hip", "gemm_w4.hip", "gemm_skinny.hip", "unfused.hip",
+           "mfma_probe.hip"]
 
 
 _REMARK = re.compile(r"remark: Function Name: (\S+)|remark:\s+(ScratchSize \[bytes/lane\]|VGPRs Spill): (\d+)")

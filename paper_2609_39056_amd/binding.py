@@ -77,6 +77,8 @@ _SIGS = {
     "sq_linear_w4a4": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_unfused": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_debug_block_acc_i32": (_I, [_P, _I, _I, ctypes.POINTER(sq_weight), _P, _P]),
+    "sq_probe_mfma_i8_sink_bytes": (_S, []),
+    "sq_probe_mfma_i8": (_I, [_I, _I, _I, _P, _S, _P]),
 }
 
 _lib = None
@@ -258,3 +260,15 @@ def act_buffers(M: int, K: int, act_bits: int, device="cuda"):
                 torch.empty((M,), dtype=torch.float32, device=device))
     return (torch.empty((M, K // 2), dtype=torch.uint8, device=device),
             torch.empty((M, K // A4_GROUP), dtype=torch.float16, device=device))
+
+
+def sq_probe_mfma_i8(iters: int, random_operands: bool, fold: bool, sink: torch.Tensor, stream=None) -> None:
+    """Matrix-core rate probe (include/sq.h): iters * 16 int8 MFMAs per wave
+    of a full-occupancy grid, register operands only; sink is int32 scratch of
+    sq_probe_mfma_i8_sink_bytes() bytes."""
+    _check(lib().sq_probe_mfma_i8(iters, int(random_operands), int(fold), _ptr(sink), sink.numel() * 4,
+                                  _stream(stream)), "sq_probe_mfma_i8")
+
+
+def probe_sink(device="cuda") -> torch.Tensor:
+    return torch.empty(lib().sq_probe_mfma_i8_sink_bytes() // 4, dtype=torch.int32, device=device)

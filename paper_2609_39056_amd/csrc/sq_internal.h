@@ -160,4 +160,8 @@ struct UnfusedArgs {
 };
 hipError_t launch_unfused(const UnfusedArgs& a, hipStream_t s);
 
+// matrix-core rate probe (measurement hook)
+int mfma_probe_workgroups();
+hipError_t launch_mfma_probe(int32_t* sink, int32_t iters, int32_t random, int32_t fold, hipStream_t s);
+
 }  // namespace sq

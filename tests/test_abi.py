@@ -150,3 +150,15 @@ def test_gemm_and_pack_reject(L):
 
 def test_binding_loads_only_the_built_library():
     assert B.LIB_PATH.endswith(os.path.join("paper_2609_39056_amd", "lib", "libsq.so"))
+
+
+def test_mfma_probe_checks(L):
+    """The matrix-core probe validates before launching (no GPU needed)."""
+    n = L.sq_probe_mfma_i8_sink_bytes()
+    assert n > 0 and n % 1024 == 0
+    A = ctypes.c_void_p(1 << 20)  # never dereferenced: every call below fails validation
+    assert L.sq_probe_mfma_i8(10, 1, 0, None, n, None) == NULL
+    assert L.sq_probe_mfma_i8(0, 1, 0, A, n, None) == SHAPE
+    assert L.sq_probe_mfma_i8((1 << 24) + 1, 1, 0, A, n, None) == SHAPE
+    assert L.sq_probe_mfma_i8(10, 1, 0, A, n - 4, None) == WS
+    assert L.sq_probe_mfma_i8(10, 1, 0, ctypes.c_void_p((1 << 20) + 2), n, None) == ALIGN

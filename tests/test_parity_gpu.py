@@ -326,3 +326,16 @@ def test_full_size_sampled_rows(name, bits, tokens, K, N, outl):
     check_output(y, res, BF16, rows=rows)
     # codes and scales of the sampled rows, read back from the workspace
     check_first_kernel_output(ws, L.M, L.K, bits, 128, res, rows=rows)
+
+
+def test_mfma_probe_runs():
+    """The matrix-core probe (a measurement hook) runs on the GPU and writes
+    its sink; zero operands leave every accumulator zero."""
+    sink = B.probe_sink()
+    sink.fill_(7)
+    B.sq_probe_mfma_i8(3, False, False, sink)
+    torch.cuda.synchronize()
+    assert int(sink.abs().max()) == 0
+    B.sq_probe_mfma_i8(3, True, True, sink)
+    torch.cuda.synchronize()
+    assert int(sink.abs().max()) > 0
