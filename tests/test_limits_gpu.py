@@ -68,18 +68,18 @@ def test_max_k(bits, G, M):
     check_first_kernel_output(ws, M, K, bits, G, res)
 
 
-@pytest.mark.parametrize("M", [3, 200])
-def test_max_n(M):
+@pytest.mark.parametrize("bits,M", [(8, 3), (8, 200), (4, 200)])
+def test_max_n(bits, M):
     """N = 2^20 output channels at K = 128: 32768 strips of the weight-streaming
     kernel (3 tokens), 16384 tiles of the tiled kernel (200 tokens, 8 rows
-    checked)."""
+    checked; 4-bit codes on the fp8 matrix cores)."""
     K, N = 128, 1 << 20
     L = synth.make_layer(K=K, N=N, stream_counts=split(M), T=2, seed=[21, M], permute=True)
     pw, W = dev_weight(L.w, L.d, L.bias_bits)
-    act = act_params(L, 0, 8, 0)
-    y, _ = run_fused(8, u16_to_dev(L.x_bits, torch.bfloat16), act, W, M, BF16)
+    act = act_params(L, 0, bits, 0)
+    y, _ = run_fused(bits, u16_to_dev(L.x_bits, torch.bfloat16), act, W, M, BF16)
     rows = np.arange(M) if M <= 8 else np.array([0, 1, 63, 64, 127, 128, 198, 199])
-    res = oracle_rows(L.x_bits[rows], L.tok2stream[rows], L.gamma, 0, pw, L.dinv, L.clip, L.bias_bits, 8)
+    res = oracle_rows(L.x_bits[rows], L.tok2stream[rows], L.gamma, 0, pw, L.dinv, L.clip, L.bias_bits, bits)
     check_output(y, res, BF16, rows=rows)
 
 
