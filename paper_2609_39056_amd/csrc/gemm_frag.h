@@ -64,6 +64,16 @@ __device__ __forceinline__ void fold8(const v16i& c, float w, float (&yt)[16]) {
   for (int r = 0; r < 16; ++r) yt[r] = __builtin_fmaf(static_cast<float>(c[r]), w, yt[r]);
 }
 
+// The same fold for an accumulator that started from the integer 0x4B400000
+// (the bits of 1.5 * 2^23) instead of 0: for |C| < 2^22 those bits are the
+// float 1.5 * 2^23 + C, so one full-rate subtraction gives fp32(C) exactly,
+// where v_cvt_f32_i32 issues at about half rate.
+constexpr int kMagicAcc = 0x4B400000;
+__device__ __forceinline__ void fold8_biased(const v16i& c, float w, float (&yt)[16]) {
+#pragma unroll
+  for (int r = 0; r < 16; ++r) yt[r] = __builtin_fmaf(__int_as_float(c[r]) - 12582912.0f, w, yt[r]);
+}
+
 // LDS byte offset of a __shared__ object.
 __device__ __forceinline__ uint32_t lds_offset(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_u8_t*)p));

@@ -23,7 +23,9 @@
 // tile; just before a tile's first MFMA of block b + 1 its accumulator of
 // block b is folded into the fp32 sum, so the VALU folding one tile overlaps
 // the matrix cores working on the previous one: y += fp32(C) * Delta_W (8-bit;
-// the row scale r_i factors out and is applied once in the epilogue) or
+// the row scale r_i factors out and is applied once in the epilogue; the
+// block's int32 sum starts from a float bias, so that one full-rate
+// subtraction converts it) or
 // y += (fp32(C) * sigma_i) * Delta_W (4-bit).  The epilogue multiplies by r_i (8-bit) or by
 // kappa_i = 1/gamma_s(i) (4-bit, the compensation of Eq. 8), adds the bias and
 // casts.  With one weight step per output channel (w_group = K, the weight
@@ -494,6 +496,10 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = (v16i)(0);
+  // 8-bit activations, 128-wide groups: each block's sum starts from the bits
+  // of 1.5 * 2^23 (fold8_biased); |16 C| <= 128 * 128 * 128 = 2^21 for any
+  // int8 codes, inside the exact range
+  const v16i magic = (v16i)(kMagicAcc);
   for (int it = blockIdx.x;;) {
     const PipeItem c = item_of(it);
     EpiInputs<ABITS, EPI> ein;
@@ -583,8 +589,8 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
           for (int ks = 0; ks < 4; ++ks) af[ks] = *reinterpret_cast<const v4i*>(st + off.a(tm, ks));
 #pragma unroll
           for (int tn = 0; tn < TN; ++tn) {
-            fold8(acc[tm][tn], wsv_prev[tn], y[tm][tn]);
-            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[0], bfull[tn][0], (v16i)(0), 0, 0, 0);
+            fold8_biased(acc[tm][tn], wsv_prev[tn], y[tm][tn]);
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[0], bfull[tn][0], magic, 0, 0, 0);
 #pragma unroll
             for (int ks = 1; ks < 4; ++ks)
               acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks], bfull[tn][ks], acc[tm][tn], 0, 0, 0);
@@ -603,7 +609,7 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
         c_slot = next_slot(c_slot);
       }
 #pragma unroll
-      for (int t = 0; t < TM * TN; ++t) fold8(acc[t / TN][t % TN], wsv_prev[t % TN], y[t / TN][t % TN]);
+      for (int t = 0; t < TM * TN; ++t) fold8_biased(acc[t / TN][t % TN], wsv_prev[t % TN], y[t / TN][t % TN]);
     } else {
       for (int kt = c.kt0; kt < c.kt1; ++kt) {
         issue();
