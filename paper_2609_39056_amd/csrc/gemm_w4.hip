@@ -267,6 +267,25 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN]
   }
 }
 
+// A split range's sums of one BM x BN tile (unit `unit` of the partial
+// buffer, row-major, rows past M not written), in the MFMA layout.
+template <int BM, int BN>
+__device__ __forceinline__ void write_partial(const GemmArgs& a, const float (&y)[TM][TN][16], int unit, int m0, int wm,
+                                              int wn, int lane_in) {
+  int ln = lane_in;  // opaque copy: keep the addresses out of the tile loop's live registers
+  asm volatile("" : "+v"(ln));
+  float* P = a.partial + static_cast<size_t>(unit) * BM * BN;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
+        if (m0 + row < a.M) P[row * BN + wn * 64 + tn * 32 + (ln & 31)] = y[tm][tn][r];
+      }
+}
+
 // Per-lane LDS read offsets of the MFMA fragments within a stage.  The swizzle
 // terms depend on the lane only, since every wave's first row and column are
 // multiples of 16, and a 32-row (32-column) step leaves them unchanged: the
@@ -655,20 +674,8 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
     }
 
     if (c.unit >= 0) {
-      // split tail: this K range's fp32 sums of the tile (int32 with one step
-      // per channel), row-major [BM][BN]
-      int ln = lane;  // opaque copy: keep the addresses out of the tile loop's live registers
-      asm volatile("" : "+v"(ln));
-      float* P = a.partial + static_cast<size_t>(c.unit) * BM * BN;
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
-            if (c.m0 + row < M) P[row * BN + wn * 64 + tn * 32 + (ln & 31)] = y[tm][tn][r];  // rows past M unused
-          }
+      // split tail: this K range's fp32 sums (int32 with one step per channel)
+      write_partial<BM, BN>(a, y, c.unit, c.m0, wm, wn, lane);
     } else {
       store_tile<ABITS, EPI>(a, y, c.m0, c.n0, wm, wn, lane, ein);
     }
@@ -932,19 +939,7 @@ __global__ __launch_bounds__(256, 2) void gemm_a4f8_kernel(GemmArgs a) {
     for (int tm = 0; tm < TM; ++tm) fold_f8(y, st_last, 1, acc[tm], rowb, tm, wsv_prev);
 
     if (c.unit >= 0) {
-      // split tail: this K range's fp32 sums of the tile, row-major [BM][BN]
-      int ln = lane;
-      asm volatile("" : "+v"(ln));
-      float* P = a.partial + static_cast<size_t>(c.unit) * BM * BN;
-#pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int row = wm * 64 + tm * 32 + (r >> 2) * 8 + (ln >> 5) * 4 + (r & 3);
-            if (c.m0 + row < M) P[row * BN + wn * 64 + tn * 32 + (ln & 31)] = y[tm][tn][r];
-          }
+      write_partial<BM, BN>(a, y, c.unit, c.m0, wm, wn, lane);  // split tail: this K range's fp32 sums
     } else {
       store_tile<4, EPI>(a, y, c.m0, c.n0, wm, wn, lane, ein);
     }
