@@ -176,8 +176,8 @@ sq_status sq_linear_w4a8(const uint16_t* x, int32_t M, const sq_act_params* act,
                          hipStream_t stream);
 
 /* The fused linear with 4-bit activations (act->act_bits == 4).
- * With more than 128 tokens, or weight groups wider than 128, the codes go
- * to gfx950's fp8 matrix cores (v_mfma_f32_32x32x64_f8f6f4): the first kernel
+ * With more than 128 tokens the codes go to gfx950's fp8 matrix cores
+ * (v_mfma_f32_32x32x64_f8f6f4): the first kernel
  * writes each code as the fp8 e4m3 byte of code * 2^-9 (sign and magnitude;
  * |code| <= 7 is an exact subnormal), and the weight nibbles are read as
  * code + 8.  Products and block sums are exact in fp32, so the outputs equal

@@ -23,6 +23,10 @@ constexpr int TM = 2;  // 32-row MFMA tiles per wave
 // its own load counter and has no barriers.  When the output channels alone
 // give too few workgroups, K is also split across workgroups: each leaves
 // fp32 sums of its 64 x 32 outputs, which a second kernel adds in range order.
+// With one weight step per output channel (PC: w_group = K, 8-bit
+// activations) there is no fold in the loop: each wave keeps int32 sums over
+// its stages, the four are added in integers, and the total is converted and
+// scaled once (split ranges hand int32 sums to the second kernel).
 constexpr int SK_BM = 64;  // rows per workgroup
 constexpr int SK_BN = 32;  // output channels per workgroup
 constexpr int SK_DIST = 2;             // stages loaded ahead
@@ -50,9 +54,10 @@ struct Sk {
   static_assert(4 * SK_BM * SK_BN * 4 <= 4 * SK_SLOTS * SLOT, "the wave sums fit in the ring");
 };
 
-template <int ABITS, int EPI>
+template <int ABITS, int EPI, bool PC>
 __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel(GemmArgs a) {
   using L = Sk<ABITS>;
+  static_assert(!PC || ABITS == 8, "one weight step per channel: 8-bit activations");
   __shared__ __attribute__((aligned(16))) uint8_t ring[4][SK_SLOTS][L::SLOT];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -97,7 +102,8 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
 #pragma unroll
     for (int i = 0; i < L::B / 1024; ++i) dma<16>(qw + kt * (KT / 2), voffB[i], st + L::B_OFF + i * 1024);
     if constexpr (ABITS == 4) dma<4>(sig + 2 * kt, voffS, st + L::S_OFF);  // the stage's two groups
-    dma<4>(a.w_scale + static_cast<size_t>(kt) * N + n0, voffW, st + L::W_OFF);  // group-major steps
+    // group-major steps of the stage's weight group
+    dma<4>(a.w_scale + static_cast<size_t>((kt * KT) / a.w_group) * N + n0, voffW, st + L::W_OFF);
   };
 
   // fragment offsets within a slot: activations per (row tile, k-step) for
@@ -130,7 +136,7 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
   float wprev = 0.0f;  // 8-bit: the fold before the first block adds 0
 
   // 8-bit: y += fp32(C) * Delta_W of the previous block, then this block's
-  // MFMAs.  4-bit: the MFMAs of both 64-blocks of the stage, then their fold
+  // MFMAs.  4-bit: the MFMAs of both 64-blocks of the stage, then their folds
   // with the row group steps and the stage's weight step.
   auto compute = [&](int slot) {
     const uint8_t* st = &ring[wave][slot][0];
@@ -167,7 +173,14 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
       bf[2 * k2 + 1] = unpack_frag(pb[k2].z, pb[k2].w);
     }
     const float wstep = f16_to_f32((col & 1) ? (wpair >> 16) : (wpair & 0xFFFFu));
-    if constexpr (ABITS == 8) {
+    if constexpr (PC) {
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int ks = 0; ks < 4; ++ks)
+          acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[ks], acc[tm], 0, 0, 0);
+      (void)wstep;
+    } else if constexpr (ABITS == 8) {
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm) {
         fold8(acc[tm], wprev, y[tm]);
@@ -188,8 +201,7 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
           c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.x, pa.y), bf[2 * hb], (v16i)(0), 0, 0, 0);
           c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.z, pa.w), bf[2 * hb + 1], c[hb][tm], 0, 0, 0);
         }
-      // both blocks share the stage's weight step:
-      // y += (fp32(C_0) sigma_0 + fp32(C_1) sigma_1) * Delta_W
+      // block by block, as the tiled kernels: y += (fp32(C_b) sigma_b) * Delta_W
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
@@ -198,10 +210,8 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             const int r = 4 * g + q;
-            const float t = mul_step16<0>(static_cast<float>(c[0][tm][r]), s4[q]);
-            const float u = __builtin_fmaf(static_cast<float>(c[1][tm][r]),
-                                           static_cast<float>(__builtin_bit_cast(half2v, s4[q])[1]), t);
-            y[tm][r] = __builtin_fmaf(u, w, y[tm][r]);
+            y[tm][r] = __builtin_fmaf(mul_step16<0>(static_cast<float>(c[0][tm][r]), s4[q]), w, y[tm][r]);
+            y[tm][r] = __builtin_fmaf(mul_step16<1>(static_cast<float>(c[1][tm][r]), s4[q]), w, y[tm][r]);
           }
         }
     }
@@ -220,7 +230,7 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
       compute(j % SK_SLOTS);
     }
   }
-  if constexpr (ABITS == 8) {
+  if constexpr (ABITS == 8 && !PC) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) fold8(acc[tm], wprev, y[tm]);
   }
@@ -233,7 +243,8 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) red[(wave * 32 + tm * 16 + r) * 64 + lane] = y[tm][r];
+    for (int r = 0; r < 16; ++r)
+      red[(wave * 32 + tm * 16 + r) * 64 + lane] = PC ? __int_as_float(acc[tm][r]) : y[tm][r];
   __syncthreads();
   const int g = wave;
   float v[TM][4];
@@ -242,10 +253,17 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int r = 4 * g + q;
-      float t = red[(tm * 16 + r) * 64 + lane];
+      if constexpr (PC) {  // int32 sums: exact in any order; raw bits while split
+        int t = __float_as_int(red[(tm * 16 + r) * 64 + lane]);
 #pragma unroll
-      for (int w = 1; w < 4; ++w) t += red[(w * 32 + tm * 16 + r) * 64 + lane];
-      v[tm][q] = t;
+        for (int w = 1; w < 4; ++w) t += __float_as_int(red[(w * 32 + tm * 16 + r) * 64 + lane]);
+        v[tm][q] = __int_as_float(t);
+      } else {
+        float t = red[(tm * 16 + r) * 64 + lane];
+#pragma unroll
+        for (int w = 1; w < 4; ++w) t += red[(w * 32 + tm * 16 + r) * 64 + lane];
+        v[tm][q] = t;
+      }
     }
 
   if (S > 1) {
@@ -259,6 +277,13 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
         if (row < rows) P[row * SK_BN + col] = v[tm][q];
       }
     return;
+  }
+  if constexpr (PC) {  // the one conversion, with the column's step (widened codes: factor 16)
+    const float wpc = f16_to_f32(a.w_scale[n0 + col]) * 0.0625f;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[tm][q] = static_cast<float>(__float_as_int(v[tm][q])) * wpc;
   }
   // epilogue: row factor (8-bit: r_i; 4-bit: kappa_i = 1 / gamma_s(i), the
   // compensation of Eq. 8), fetched from the lane that loaded it; bias; cast.
@@ -305,9 +330,10 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
 }
 
 // Second kernel of a split skinny GEMM: adds the `split` partial sums of every
-// output in range order and finishes it as the skinny epilogue does.  Four
-// adjacent outputs per thread.
-template <int ABITS, int EPI>
+// output in range order (int32 sums with one step per channel, then the one
+// conversion) and finishes it as the skinny epilogue does.  Four adjacent
+// outputs per thread.
+template <int ABITS, int EPI, bool PC>
 __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   const int strips = a.N / SK_BN;
   const int g = blockIdx.x * 256 + threadIdx.x;  // one thread per 4 outputs of a 64 x 32 block
@@ -318,15 +344,33 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   const int m = mb * SK_BM + row, n = strip * SK_BN + c;
   if (mb * SK_BM >= a.M || m >= a.M) return;
   const float* P = a.partial + static_cast<size_t>(blk) * a.split * (SK_BM * SK_BN) + row * SK_BN + c;
-  float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-  for (int sl = 0; sl < a.split; ++sl) {
-    const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * (SK_BM * SK_BN));
-    acc.x += v.x;
-    acc.y += v.y;
-    acc.z += v.z;
-    acc.w += v.w;
+  float y[4];
+  if constexpr (PC) {
+    int4 acc = make_int4(0, 0, 0, 0);
+    for (int sl = 0; sl < a.split; ++sl) {
+      const int4 v = *reinterpret_cast<const int4*>(P + static_cast<size_t>(sl) * (SK_BM * SK_BN));
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    const int ci[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = static_cast<float>(ci[j]) * (f16_to_f32(a.w_scale[n + j]) * 0.0625f);
+  } else {
+    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+    for (int sl = 0; sl < a.split; ++sl) {
+      const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * (SK_BM * SK_BN));
+      acc.x += v.x;
+      acc.y += v.y;
+      acc.z += v.z;
+      acc.w += v.w;
+    }
+    y[0] = acc.x;
+    y[1] = acc.y;
+    y[2] = acc.z;
+    y[3] = acc.w;
   }
-  float y[4] = {acc.x, acc.y, acc.z, acc.w};
   if constexpr (EPI == kEpiOut) {
     const float rowf = ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
                                   : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
@@ -375,7 +419,7 @@ int skinny_split(int act_bits, int32_t M, int32_t N, int32_t K) {
   return act_bits == 8 ? split_t<8>(M, N, K) : split_t<4>(M, N, K);
 }
 
-template <int ABITS, int EPI>
+template <int ABITS, int EPI, bool PC>
 hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
   GemmArgs a = a0;
   int S = skinny_split(ABITS, a.M, a.N, a.K);
@@ -383,11 +427,11 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
   a.split = S;
   a.partial = S > 1 ? partial : nullptr;
   const int strips = a.N / SK_BN, mblocks = (a.M + SK_BM - 1) / SK_BM;
-  hipLaunchKernelGGL((gemm_skinny_kernel<ABITS, EPI>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((gemm_skinny_kernel<ABITS, EPI, PC>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || S == 1) return e;
   const int threads = strips * mblocks * (SK_BM * SK_BN / 4);
-  hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI>), dim3((threads + 255) / 256), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI, PC>), dim3((threads + 255) / 256), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -402,14 +446,19 @@ size_t skinny_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K) {
 hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
                          size_t partial_bytes) {
   if (act_bits == 8) {
+    const bool pc = a.w_group != KT;  // then w_group == K (skinny_applies)
     switch (epi) {
-      case kEpiOut: return launch_t<8, kEpiOut>(a, s, partial, partial_bytes);
-      case kEpiPartial: return launch_t<8, kEpiPartial>(a, s, partial, partial_bytes);
+      case kEpiOut:
+        return pc ? launch_t<8, kEpiOut, true>(a, s, partial, partial_bytes)
+                  : launch_t<8, kEpiOut, false>(a, s, partial, partial_bytes);
+      case kEpiPartial:
+        return pc ? launch_t<8, kEpiPartial, true>(a, s, partial, partial_bytes)
+                  : launch_t<8, kEpiPartial, false>(a, s, partial, partial_bytes);
     }
   } else {
     switch (epi) {
-      case kEpiOut: return launch_t<4, kEpiOut>(a, s, partial, partial_bytes);
-      case kEpiPartial: return launch_t<4, kEpiPartial>(a, s, partial, partial_bytes);
+      case kEpiOut: return launch_t<4, kEpiOut, false>(a, s, partial, partial_bytes);
+      case kEpiPartial: return launch_t<4, kEpiPartial, false>(a, s, partial, partial_bytes);
     }
   }
   return hipErrorInvalidValue;

@@ -1242,7 +1242,7 @@ hipError_t launch_a4f8(const GemmArgs& a0, hipStream_t s, float* partial, size_t
 
 template <int EPI>
 hipError_t launch_a8(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
-  if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(8, EPI, a, s, partial, partial_bytes);
+  if (skinny_applies(8, a.M, a.K, a.w_group)) return launch_skinny(8, EPI, a, s, partial, partial_bytes);
   if (a.w_group == KT) return launch_t<8, EPI, true>(a, s, partial, partial_bytes);
   if (a.w_group == a.K) return launch_t<8, EPI, true, true>(a, s, partial, partial_bytes);
   return launch_t<8, EPI, false>(a, s, partial, partial_bytes);
@@ -1268,7 +1268,7 @@ int device_cus() {
 
 size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t w_group) {
   if (act_bits == 8 && w_group != KT && w_group != K) return 0;  // the non-pipelined kernel never splits
-  if (w_group == KT && M <= kSkinnyMaxM) return skinny_partial_bytes(act_bits, M, N, K);
+  if (skinny_applies(act_bits, M, K, w_group)) return skinny_partial_bytes(act_bits, M, N, K);
   const Plan p = act_bits == 8 ? pipe_plan<8>(M, N, K, ~static_cast<size_t>(0))
                                : pipe_plan<4>(M, N, K, ~static_cast<size_t>(0));
   const size_t unit = static_cast<size_t>(Cfg<8, kPipeWide>::BM) * Cfg<8, kPipeWide>::BN * sizeof(float);
@@ -1291,7 +1291,7 @@ hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, 
         if (a.kc != nullptr)
           return epi == kEpiOut ? launch_a4f8<kEpiOut>(a, s, partial, partial_bytes)
                                 : launch_a4f8<kEpiPartial>(a, s, partial, partial_bytes);
-        if (a.w_group == KT && a.M <= kSkinnyMaxM) return launch_skinny(4, epi, a, s, partial, partial_bytes);
+        if (skinny_applies(4, a.M, a.K, a.w_group)) return launch_skinny(4, epi, a, s, partial, partial_bytes);
         return epi == kEpiOut ? launch_t<4, kEpiOut, true>(a, s, partial, partial_bytes)
                               : launch_t<4, kEpiPartial, true>(a, s, partial, partial_bytes);
       case kEpiDump: return launch_t<4, kEpiDump, false>(a, s, nullptr, 0);

@@ -164,7 +164,7 @@ sq_status linear_fused(int32_t bits, const uint16_t* x, int32_t M, const sq_act_
   if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
   if (!aligned(x, 16) || !aligned(y, 16) || !aligned(ws, 16)) return SQ_ERR_ALIGN;
   if (ws_bytes < fused_ws_bytes(M, w->K, w->N, bits)) return SQ_ERR_WORKSPACE;
-  const bool f8 = bits == 4 && a4_fp8_path(M, w->w_group);
+  const bool f8 = bits == 4 && a4_fp8_path(M, w->K, w->w_group);
   FusedWs f = fused_ws(ws, ws_bytes, M, w->K, bits, f8);
   st = quantize(x, M, w->K, act, f.qx, f.scale, stream, f.kc);
   if (st != SQ_OK) return st;

@@ -109,13 +109,17 @@ size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t
 // Compute units of the current device (256 when there is none), capped at 256.
 int device_cus();
 
-// Weight-streaming GEMM for M <= kSkinnyMaxM (8- or 4-bit activations,
-// 128-wide weight groups; epi kEpiOut or kEpiPartial).  Splits K across
-// workgroups when `partial` holds skinny_partial_bytes(...) bytes.
+// Weight-streaming GEMM for M <= kSkinnyMaxM (epi kEpiOut or kEpiPartial):
+// 4-bit activations with any weight groups, 8-bit ones with 128-wide groups
+// or one step per output channel.  Splits K across workgroups when `partial`
+// holds skinny_partial_bytes(...) bytes.
 constexpr int kSkinnyMaxM = 128;
+inline bool skinny_applies(int act_bits, int32_t M, int32_t K, int32_t w_group) {
+  return M <= kSkinnyMaxM && (act_bits == 4 || w_group == kKTile || w_group == K);
+}
 // 4-bit activations take the fp8 pipelined GEMM in the fused linear whenever
-// the weight-streaming kernel does not apply.
-inline bool a4_fp8_path(int32_t M, int32_t w_group) { return !(w_group == kKTile && M <= kSkinnyMaxM); }
+// the weight-streaming kernel does not apply (more than 128 tokens).
+inline bool a4_fp8_path(int32_t M, int32_t K, int32_t w_group) { return !skinny_applies(4, M, K, w_group); }
 size_t skinny_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K);
 hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
                          size_t partial_bytes);

@@ -65,7 +65,10 @@ def check_output(y_dev, res, out_dtype, rows=None):
         y = y_dev.cpu().numpy().astype(np.float64)
         err = np.abs(y - y_or.astype(np.float64))
         assert np.all(err <= 1e-5 * A), f"max err/A = {np.max(err / np.maximum(A, 1e-300))}"
-        nc = np.abs(y_or) >= 0.01 * A
+        # element-relative where the sum keeps a tenth of its magnitude: there
+        # 1e-5 |y| >= 1e-6 A, about 17 units of 2^-24 A, several times what a
+        # different summation order of the blocks costs
+        nc = np.abs(y_or) >= 0.1 * A
         if nc.any():
             rel = err[nc] / np.abs(y_or[nc].astype(np.float64))
             assert rel.max() <= 1e-5, f"max rel = {rel.max()}"
@@ -107,7 +110,7 @@ def fused_first_kernel_output(ws, M, K, bits, w_group, rows=None):
         off = _align(M * K)
         r = pick(ws[off: off + 4 * M].view(torch.int32)).cpu().numpy().view(np.uint32)
         return codes, r, None
-    f8 = not (w_group == 128 and M <= 128)
+    f8 = M > 128  # more than 128 tokens: the fp8 path (include/sq.h)
     g = K // 64
     if f8:
         b = pick(ws[: M * K].view(M, K)).cpu().numpy().astype(np.int64)

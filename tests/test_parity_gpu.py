@@ -211,15 +211,19 @@ def test_gemm_entry_points(bits, with_ws):
 @pytest.mark.parametrize("M,K,N", [(1, 2048, 2048), (2, 128, 64), (33, 8192, 2048), (64, 2048, 6144),
                                    (65, 5120, 320), (128, 1024, 1024), (100, 13824, 128)])
 @pytest.mark.parametrize("out", [F32, BF16])
-def test_few_tokens(bits, M, K, N, out):
+@pytest.mark.parametrize("per_channel", [False, True])
+def test_few_tokens(bits, M, K, N, out, per_channel):
     """Layers of at most 128 tokens (the action and proprio streams alone)
-    take the weight-streaming kernel.  Fused linear, and the second kernel
-    alone without a workspace (K never split) and with one (K split across
+    take the weight-streaming kernel, with 128-wide weight groups or one step
+    per output channel (8-bit: int32 sums over all of K, exact across the
+    waves and split ranges).  Fused linear, and the second kernel alone
+    without a workspace (K never split) and with one (K split across
     workgroups when that is faster: 8192 and 13824 channels here)."""
     L = layer(M, K, N, seed=[9, M, K, N])
-    pw, W = oracle_weight(L, 128)
+    G = K if per_channel else 128
+    pw, W = oracle_weight(L, G)
     act = act_params(L, 1, bits, 0)
-    res = oracle_linear(L, 1, bits, 0, pw, 128)
+    res = oracle_linear(L, 1, bits, 0, pw, G)
     y, _ = run_linear(FUSED[bits], L, act, W, out)
     check_output(y, res, out)
     for with_ws in (False, True):
