@@ -183,9 +183,10 @@ sq_status sq_linear_w4a8(const uint16_t* x, int32_t M, const sq_act_params* act,
  * code + 8.  Products and block sums are exact in fp32, so the outputs equal
  * those of sq_quantize_act followed by sq_gemm_w4a4 bit for bit.
  * Workspace layout (each part 256-byte aligned, in this order): the codes
- * (fp8 bytes [M][K], else packed int4 [M][K/2]); sigma fp16 [M][K/64];
- * with fp8 codes kc fp32 [M][K/64] = -8 S sigma 2^-18, S the code sum of the
- * row's 64-group; then the GEMM's partial sums.  With 8-bit activations:
+ * (fp8 bytes [M][K], else packed int4 [M][K/2]); sigma [M][K/64] (fp16, or
+ * with fp8 codes its value as fp32); with fp8 codes kc fp32 [M][K/64] =
+ * -8 S sigma 2^-18, S the code sum of the row's 64-group; then the GEMM's
+ * partial sums.  With 8-bit activations:
  * Q_X int8 [M][K], r fp32 [M], partial sums. */
 sq_status sq_linear_w4a4(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                          void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,

@@ -696,17 +696,19 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
 // line).  v_mfma_f32_32x32x64_f8f6f4 multiplies and sums one 64-wide block
 // exactly in fp32 (integers below 2^24 times 2^-18), giving
 // C' = (C + 8 S) 2^-18 with S the block's activation code sum; the first
-// kernel stored kc = -8 S sigma 2^-18 per (row, block), so one v_fma_mix
-// fma(C', sigma, kc) is round(C sigma) 2^-18, the same value as the int8
+// kernel stored kc = -8 S sigma 2^-18 and sigma (fp32) per (row, block), so
+// one fma(C', sigma, kc) is round(C sigma) 2^-18, the same value as the int8
 // path's fp32(C) * sigma, and y += that * (Delta_W 2^18).  Per output and
-// block: two VALU ops instead of three, and no activation widening.
+// block: two full-rate fmas instead of a conversion, a v_fma_mix_f32 (half
+// rate) and an fma, and no activation widening.
 struct F8Layout {
   static constexpr int BM = 128, BN = 128, NWAVE = 4;
   static constexpr int A_BYTES = BM * KT;      // fp8 code rows of 128 B, chunk c at c ^ ((r >> 1) & 7)
   static constexpr int B_BYTES = BN * KT / 2;  // packed weight rows of 64 B, chunk c at c ^ ((r >> 2) & 3)
   static constexpr int B_OFF = A_BYTES;
-  static constexpr int SG_OFF = B_OFF + B_BYTES;  // fp16 step pairs: wave w, row 32 w + i at w * 256 + i * 4
-  static constexpr int KC_OFF = SG_OFF + NWAVE * 256;  // kc: row 32 w + i, block half b at w * 256 + b * 128 + i * 4
+  // fp32 group steps sigma and kc: row 32 w + i, block half b at w * 256 + b * 128 + i * 4
+  static constexpr int SG_OFF = B_OFF + B_BYTES;
+  static constexpr int KC_OFF = SG_OFF + NWAVE * 256;
   static constexpr int W_OFF = KC_OFF + NWAVE * 256;   // weight-step pairs: columns 2 i, 2 i + 1 at i * 4
   static constexpr int STAGE = W_OFF + 256;
   // loads run one stage ahead; the previous stage's steps are still read
@@ -719,7 +721,7 @@ struct F8Loads {
   using LY = F8Layout;
   uint32_t voffA[LY::A_DMA];
   uint32_t voffB[LY::B_DMA];
-  uint32_t voffS, voffK, voffW;
+  uint32_t voffS, voffW;
 
   __device__ __forceinline__ void set(const GemmArgs& a, int m0, int n0, int wave, int lane) {
     const int M = a.M, N = a.N, K = a.K;
@@ -736,8 +738,8 @@ struct F8Loads {
       voffB[i] = static_cast<uint32_t>(min(n0 + col, N - 1) - n0) * static_cast<uint32_t>(K / 2) + c * 16;
     }
     const uint32_t groups = static_cast<uint32_t>(K / kA4Group);
-    voffS = static_cast<uint32_t>(min(m0 + 32 * wave + (lane & 31), M - 1) - m0) * groups * 2;
-    voffK = static_cast<uint32_t>(min(m0 + 32 * wave + (lane & 31), M - 1) - m0) * groups * 4 + (lane >> 5) * 4;
+    // sigma and kc: lane -> row 32 wave + (lane & 31), block half lane >> 5
+    voffS = static_cast<uint32_t>(min(m0 + 32 * wave + (lane & 31), M - 1) - m0) * groups * 4 + (lane >> 5) * 4;
     voffW = static_cast<uint32_t>(min(n0 + 2 * lane, N - 2));  // N is even: the pair stays in the row
   }
 
@@ -751,10 +753,10 @@ struct F8Loads {
     for (int i = 0; i < LY::A_DMA; ++i) dma<16>(bA, voffA[i], st + (LY::A_DMA * wave + i) * 1024);
 #pragma unroll
     for (int i = 0; i < LY::B_DMA; ++i) dma<16>(bB, voffB[i], st + LY::B_OFF + (LY::B_DMA * wave + i) * 1024);
-    const uint8_t* bS = static_cast<const uint8_t*>(a.act_scale) + static_cast<size_t>(m0) * groups * 2 + kt * 4;
+    const uint8_t* bS = static_cast<const uint8_t*>(a.act_scale) + static_cast<size_t>(m0) * groups * 4 + kt * 8;
     dma<4>(bS, voffS, st + LY::SG_OFF + wave * 256);
     const uint8_t* bK = reinterpret_cast<const uint8_t*>(a.kc) + static_cast<size_t>(m0) * groups * 4 + kt * 8;
-    dma<4>(bK, voffK, st + LY::KC_OFF + wave * 256);
+    dma<4>(bK, voffS, st + LY::KC_OFF + wave * 256);
     if (wave == 0) {
       const uint32_t e = static_cast<uint32_t>((kt * KT) / a.w_group) * static_cast<uint32_t>(a.N) + voffW;
       dma<4>(a.w_scale, e * 2, st + LY::W_OFF);
@@ -778,21 +780,21 @@ __device__ __forceinline__ v8i unpack_offset_frag(const uint4& p) {
 // y += round(C sigma) * Delta_W for row tile tm and both column tiles, block
 // half hb of the stage at st (w: Delta_W * 2^18 of the lane's two columns).
 // The lane's rows are 64 wm + 32 tm + 8 r4 + 4 h + i: wave block 2 wm + tm,
-// row 8 r4 + 4 h + i within it; `rowb` = wm * 512 + h * 16 (bytes of one
-// step pair or kc per row: 4), the rest are immediate offsets.
+// row 8 r4 + 4 h + i within it; `rowb` = wm * 512 + h * 16 (4 bytes of sigma
+// or kc per row and block), the rest are immediate offsets.
 __device__ __forceinline__ void fold_f8(float (&y)[TM][TN][16], const uint8_t* st, int hb, const v16f (&c)[TN],
                                         int rowb, int tm, const float (&w)[TN]) {
   using LY = F8Layout;
 #pragma unroll
   for (int r4 = 0; r4 < 4; ++r4) {
     const int o = rowb + tm * 256 + r4 * 32;
-    const uint4 sp = *reinterpret_cast<const uint4*>(st + LY::SG_OFF + o);
+    const uint4 sp = *reinterpret_cast<const uint4*>(st + LY::SG_OFF + o + hb * 128);
     const uint4 kq = *reinterpret_cast<const uint4*>(st + LY::KC_OFF + o + hb * 128);
     const uint32_t s4[4] = {sp.x, sp.y, sp.z, sp.w};
     const uint32_t kb[4] = {kq.x, kq.y, kq.z, kq.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float sg = static_cast<float>(__builtin_bit_cast(half2v, s4[i])[hb]);
+      const float sg = __uint_as_float(s4[i]);
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int r = r4 * 4 + i;

@@ -165,7 +165,8 @@ __global__ __launch_bounds__(256) void quantize_act_kernel(QuantArgs a) {
           *reinterpret_cast<uint2*>(qr + c * 8) =
               make_uint2(pack_low_bytes(b[0], b[1], b[2], b[3]), pack_low_bytes(b[4], b[5], b[6], b[7]));
           if ((c & 7) == 0) {
-            sr[c >> 3] = static_cast<uint16_t>(dbits);
+            // the fp16 step, widened exactly (an fp32 operand of the fold's fma)
+            reinterpret_cast<float*>(a.scale)[static_cast<size_t>(row) * (a.K / kA4Group) + (c >> 3)] = delta;
             // exact: |8 S| < 2^12 and delta has an 11-bit significand
             kr[c >> 3] = (static_cast<float>(-8 * csum) * delta) * 3.814697265625e-06f;  // * 2^-18
           }

@@ -66,7 +66,8 @@ size_t gemm_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
 
 // fused workspace: Q_X | scales | (fp8 4-bit codes: kc) | GEMM partial sums,
 // each 256-byte aligned.  With 4-bit activations on the pipelined path
-// (a4_fp8_path) Q_X holds one fp8 byte per code and kc follows the scales.
+// (a4_fp8_path) Q_X holds one fp8 byte per code, the steps are fp32 and kc
+// follows them.
 struct FusedWs {
   void* qx;
   void* scale;
@@ -81,7 +82,7 @@ FusedWs fused_ws(void* ws, size_t ws_bytes, int32_t M, int32_t K, int32_t bits, 
   const size_t q = round_up(f8 ? static_cast<size_t>(M) * K : qx_bytes(M, K, bits));
   f.qx = p;
   f.scale = p + q;
-  size_t off = q + round_up(act_scale_bytes(M, K, bits));
+  size_t off = q + round_up(f8 ? kc_bytes(M, K) : act_scale_bytes(M, K, bits));  // fp8 codes: fp32 steps
   f.kc = nullptr;
   if (f8) {
     f.kc = reinterpret_cast<float*>(p + off);
@@ -95,9 +96,8 @@ FusedWs fused_ws(void* ws, size_t ws_bytes, int32_t M, int32_t K, int32_t bits, 
 // Sized for the larger layout (fp8 codes and kc for 4-bit activations): the
 // weight's group width, which picks the path, is not an argument here.
 size_t fused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
-  if (bits == 4)
-    return round_up(static_cast<size_t>(M) * K) + round_up(act_scale_bytes(M, K, bits)) + round_up(kc_bytes(M, K)) +
-           gemm_ws_bytes(M, K, N, bits);
+  if (bits == 4)  // fp8 codes [M][K], fp32 steps and kc [M][K/64] each
+    return round_up(static_cast<size_t>(M) * K) + 2 * round_up(kc_bytes(M, K)) + gemm_ws_bytes(M, K, N, bits);
   return round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits)) + gemm_ws_bytes(M, K, N, bits);
 }
 

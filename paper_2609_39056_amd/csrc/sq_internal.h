@@ -67,8 +67,9 @@ struct QuantArgs {
   void* scale;
   // 4-bit codes for the fp8 matrix cores (the fused linear's pipelined path):
   // when kc is set, qx holds one byte per code, the fp8 e4m3 value code * 2^-9
-  // (sign and magnitude; |code| <= 7 is an exact subnormal), and kc holds the
-  // fp32 -8 * S * sigma * 2^-18 per (row, 64-group), S = the group's code sum.
+  // (sign and magnitude; |code| <= 7 is an exact subnormal), scale holds the
+  // group steps sigma as fp32 (the fp16 value, widened) and kc holds the fp32
+  // -8 * S * sigma * 2^-18 per (row, 64-group), S = the group's code sum.
   float* kc;
   int32_t M, K, S, step, range_mode;
 };

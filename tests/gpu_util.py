@@ -100,8 +100,9 @@ def _align(n):
 def fused_first_kernel_output(ws, M, K, bits, w_group, rows=None):
     """What the fused linear's first kernel left in its workspace (the layout
     include/sq.h documents), for `rows` (default all): the codes as int
-    [rows, K], the scales as raw bits (uint32 r, or uint16 sigma [rows, K/64])
-    and, for 4-bit codes on the fp8 path, kc as fp32 [rows, K/64] (else None).
+    [rows, K], the scales as raw bits (uint32 r, or uint16 sigma [rows, K/64];
+    the fp8 path stores sigma as fp32, returned as its fp16 bits) and, for
+    4-bit codes on the fp8 path, kc as fp32 [rows, K/64] (else None).
     Rows are selected on the device."""
     ri = None if rows is None else torch.as_tensor(np.asarray(rows, dtype=np.int64), device=ws.device)
     pick = (lambda t: t) if ri is None else (lambda t: t[ri])
@@ -120,11 +121,15 @@ def fused_first_kernel_output(ws, M, K, bits, w_group, rows=None):
         packed = pick(ws[: M * K // 2].view(M, K // 2)).cpu().numpy()
         codes = O.unpack_int4(packed).astype(np.int64)
         off = _align(M * K // 2)
-    sigma = pick(ws[off: off + 2 * M * g].view(torch.int16).view(M, g)).cpu().numpy().view(np.uint16)
     kc = None
-    if f8:
-        off += _align(2 * M * g)
+    if f8:  # fp32 steps (the fp16 values widened), then kc
+        s32 = pick(ws[off: off + 4 * M * g].view(torch.float32).view(M, g)).cpu().numpy()
+        sigma = s32.astype(np.float16).view(np.uint16)
+        assert np.array_equal(sigma.view(np.float16).astype(np.float32), s32), "steps not fp16 values"
+        off += _align(4 * M * g)
         kc = pick(ws[off: off + 4 * M * g].view(torch.float32).view(M, g)).cpu().numpy()
+    else:
+        sigma = pick(ws[off: off + 2 * M * g].view(torch.int16).view(M, g)).cpu().numpy().view(np.uint16)
     return codes, sigma, kc
 
 
