@@ -307,3 +307,50 @@ def full_precision_linear(x_bits, w, bias_bits=None):
     if bias_bits is not None:
         y = y + bf16_bits_to_f32(bias_bits).astype(np.float64)[None, :]
     return y
+
+
+# --------------------------------------------------------------------------
+# Activation calibration objective, Sec. 4.3 Eq. (9)
+# --------------------------------------------------------------------------
+def calib_reference(x_bits, qw_codes, w_scale_bits, w_group, dinv=None):
+    """The target of Eq. (9): X~ W^ with the activations unquantized,
+    X~ = X D^-1 (the fp32 product of the quantizer's first step), and the
+    fixed quantized weights W^ = code * Delta_W.  float64 [M, N]; every
+    product is exact in float64 and the sums carry float64 rounding only."""
+    x = bf16_bits_to_f32(np.asarray(x_bits, dtype=np.uint16))
+    if dinv is not None:
+        x = (x * np.asarray(dinv, dtype=F32)[None, :]).astype(F32)
+    codes = np.asarray(qw_codes, dtype=np.int64)
+    N, K = codes.shape
+    steps = f16_bits_to_f32(w_scale_bits).astype(np.float64)   # [N, K / w_group]
+    wq = codes.astype(np.float64) * np.repeat(steps, w_group, axis=1)[:, :K]
+    return x.astype(np.float64) @ wq.T
+
+
+def calib_objective(x_bits, tok2stream, num_streams, qw_codes, w_scale_bits, w_group, gammas, clips,
+                    omega, dinv=None, act_bits=8, ref=None):
+    """Eq. (9) for each candidate (gamma_s for every stream, shared threshold c):
+
+        L = sum_s omega_s / n_s * || gamma_s^-1 Q(gamma_s X~_s; c) W^ - X~_s W^ ||_F^2
+
+    The modulated output is the STATIC linear with the one-step gain table
+    [gamma] and clip [c], taken at its float64 value (y64: exact block sums
+    and the stored fp32 scales, no bias); n_s counts the tokens of stream s,
+    and a stream with none adds 0.  omega holds the map weights (uniform:
+    1 / S).  Returns float64 [n_candidates]."""
+    if ref is None:
+        ref = calib_reference(x_bits, qw_codes, w_scale_bits, w_group, dinv)
+    t2s = np.asarray(tok2stream)
+    out = []
+    for g, c in zip(np.asarray(gammas, dtype=F32), np.asarray(clips, dtype=F32)):
+        res = linear(x_bits, t2s, g[None, :], 0, qw_codes, w_scale_bits, w_group, dinv=dinv,
+                     clip=np.array([c], dtype=F32), bias_bits=None, range_mode=RANGE_STATIC, act_bits=act_bits)
+        d2 = ((res["y64"] - ref) ** 2).sum(axis=1)
+        L = 0.0
+        for s in range(num_streams):
+            rows = t2s == s
+            n = int(rows.sum())
+            if n:
+                L += float(omega[s]) / n * float(d2[rows].sum())
+        out.append(L)
+    return np.array(out, dtype=np.float64)

@@ -310,3 +310,63 @@ def test_quantized_layer_is_close_to_full_precision():
     ok = r["g"] <= 1.0
     eps = np.linalg.norm(r["y64"][ok] - y_fp[ok]) / np.linalg.norm(y_fp[ok])
     assert ok.any() and eps < 0.2
+
+
+# ---------------------------------------------------------------- calibration objective, Eq. (9)
+@pytest.mark.parametrize("act_bits", [8, 4])
+def test_calib_objective_zero_on_representable_input(act_bits):
+    """Sec. 4.3 Eq. (8)-(9): when every gamma_s x~ is a multiple of Delta =
+    c / q_max inside [-c, c], Q reproduces it exactly and gamma_s^-1 undoes
+    the gain, so the modulated output equals X~ W^ and the objective is 0
+    (up to float64 summation order).  Gains are powers of two, so every
+    scale involved is exact; a lost compensation, step or gain shows."""
+    qa = O.Q_MAX[act_bits]
+    rng = np.random.default_rng(11)
+    M, K, N, S = 12, 256, 64, 3
+    delta = 2.0 ** -4
+    c = np.float32(qa * delta)
+    gam = np.array([1.0, 2.0, 0.5], F32)
+    t2s = (np.arange(M) % S).astype(np.int32)
+    k = rng.integers(-qa, qa + 1, size=(M, K))
+    x = (k * delta / gam[t2s][:, None]).astype(F32)       # gamma_s x = k Delta, exact in bf16
+    x_bits = _bits(x)
+    assert np.array_equal(O.bf16_bits_to_f32(x_bits), x)
+    w = rng.standard_normal((N, K)).astype(F32) * 0.05
+    pw = O.pack_weights(w, None, 128)
+    ref = O.calib_reference(x_bits, pw["codes"], pw["w_scale"], 128)
+    L = O.calib_objective(x_bits, t2s, S, pw["codes"], pw["w_scale"], 128, gam[None, :], [c], np.ones(S) / S,
+                          act_bits=act_bits, ref=ref)
+    assert L[0] <= 1e-24 * float((ref ** 2).mean())
+    # the same input with the gains off: clipping and rounding errors appear
+    L1 = O.calib_objective(x_bits, t2s, S, pw["codes"], pw["w_scale"], 128, np.ones((1, S), F32), [c],
+                           np.ones(S) / S, act_bits=act_bits, ref=ref)
+    assert L1[0] > 1e-6 * float((ref ** 2).mean())
+
+
+def test_calib_objective_homogeneous():
+    """Eq. (1), (9): scaling X and c by 2 leaves the codes unchanged and
+    doubles both outputs exactly, so the objective grows by exactly 4."""
+    L_ = _layer(K=256, N=64, counts=(20, 4, 8), seed=12)
+    pw = O.pack_weights(L_.w, L_.d, 128)
+    x2 = O.f32_to_bf16_bits(2 * O.bf16_bits_to_f32(L_.x_bits))
+    g = np.array([[1.0, 1.5, 0.75], [0.9, 1.0, 1.25]], F32)
+    c = np.array([3.0, 5.0], F32)
+    om = np.array([0.5, 0.25, 0.25])
+    a = O.calib_objective(L_.x_bits, L_.tok2stream, 3, pw["codes"], pw["w_scale"], 128, g, c, om, dinv=L_.dinv)
+    b = O.calib_objective(x2, L_.tok2stream, 3, pw["codes"], pw["w_scale"], 128, g, 2 * c, om, dinv=L_.dinv)
+    assert np.array_equal(b, 4 * a)
+
+
+def test_calib_objective_streams_separate():
+    """Eq. (9): stream t's gain only moves stream t's term: with all weight
+    on stream 0, changing gamma_1 and gamma_2 leaves the objective unchanged,
+    and with all weight on stream 1 changing gamma_1 moves it."""
+    L_ = _layer(K=256, N=64, counts=(20, 6, 8), seed=13)
+    pw = O.pack_weights(L_.w, L_.d, 128)
+    g = np.array([[1.0, 1.0, 1.0], [1.0, 3.0, 0.3]], F32)
+    c = np.array([4.0, 4.0], F32)
+    on0 = O.calib_objective(L_.x_bits, L_.tok2stream, 3, pw["codes"], pw["w_scale"], 128, g, c, [1, 0, 0],
+                            dinv=L_.dinv)
+    on1 = O.calib_objective(L_.x_bits, L_.tok2stream, 3, pw["codes"], pw["w_scale"], 128, g, c, [0, 1, 0],
+                            dinv=L_.dinv)
+    assert on0[0] == on0[1] and on1[0] != on1[1]
