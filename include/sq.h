@@ -203,6 +203,50 @@ sq_status sq_linear_unfused(const uint16_t* x, int32_t M, const sq_act_params* a
                             void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
                             hipStream_t stream);
 
+/* Activation calibration (Sec. 4.3, Eq. 9).  For a linear with fixed
+ * quantized weights W^ = Q(D W), a candidate is one gain per stream
+ * gamma_s and one threshold c shared by the streams; its objective is
+ *
+ *     L = sum_s omega_s / n_s * || gamma_s^-1 Q(gamma_s X~_s; c) W^ - X~_s W^ ||_F^2
+ *
+ * over the calibration tokens X (rows of stream s: X_s, n_s of them), with
+ * X~ = X D^-1.  A stream with no token adds nothing.  The search over
+ * candidates is the caller's: evaluate a batch, keep the smallest.
+ *
+ * sq_calib_reference writes the target X~ W^ once per linear:
+ * y_ref[i][j] = sum_k x~_ik * code_jk * Delta_W, in fp64 (each product
+ * exact, x~ = fp32(x) * dinv rounded to fp32 as in the quantizer), fp64
+ * [M, N] row-major, 16-byte aligned.  dinv [K] as in sq_act_params (NULL:
+ * D = I).  w->bias is not used. */
+sq_status sq_calib_reference(const uint16_t* x, int32_t M, const float* dinv, const sq_weight* w, double* y_ref,
+                             hipStream_t stream);
+
+/* Bytes of device workspace for sq_calib_objective with this shape, bits
+ * and stream count (1 <= num_streams <= 4096); 0 for invalid arguments.
+ * Host-only. */
+size_t sq_calib_workspace_bytes(int32_t M, int32_t K, int32_t N, int32_t act_bits, int32_t num_streams);
+
+/* Evaluates L for num_candidates (1 .. 65536) candidates, in order:
+ *   cand_gamma  fp32 [num_candidates][num_streams]  gains, finite and > 0
+ *   cand_clip   fp32 [num_candidates]               thresholds c > 0
+ *   omega       fp64 [num_streams]                  stream weights (uniform: 1/S)
+ *   objective   fp64 [num_candidates]               out
+ * x, M, tok2stream, dinv and act_bits as for sq_linear_w4a8 / sq_linear_w4a4;
+ * y_ref from sq_calib_reference with the same x, dinv and w.  Each candidate
+ * runs the fused linear in STATIC range mode with the one-step tables
+ * (gamma, c), without the bias (it cancels), into fp32 Y_c, then
+ * L = sum_i omega_s(i) / n_s(i) * sum_j (Y_c,ij - y_ref,ij)^2, accumulated in
+ * fp64 in a fixed order (the result is reproducible).  Y_c differs from the
+ * exact modulated product by the fused linear's fp32 rounding.  Alignment:
+ * x, y_ref and workspace 16 bytes, omega and objective 8, the rest 4.
+ * Candidates are enqueued one after another on `stream`; a launch failure
+ * returns SQ_ERR_HIP after the earlier candidates were enqueued. */
+sq_status sq_calib_objective(const uint16_t* x, int32_t M, const int32_t* tok2stream, int32_t num_streams,
+                             const float* dinv, int32_t act_bits, const sq_weight* w, const double* y_ref,
+                             int32_t num_candidates, const float* cand_gamma, const float* cand_clip,
+                             const double* omega, double* objective, void* workspace, size_t workspace_bytes,
+                             hipStream_t stream);
+
 /* Measurement hook: the int8 matrix-core rate the GPU sustains, as a
  * ceiling beside the published peak.  Launches sq_probe_mfma_i8_sink_bytes()
  * / 1024 workgroups (two per CU) whose waves each issue iters * 16

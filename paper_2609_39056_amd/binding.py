@@ -77,6 +77,10 @@ _SIGS = {
     "sq_linear_w4a4": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_unfused": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_debug_block_acc_i32": (_I, [_P, _I, _I, ctypes.POINTER(sq_weight), _P, _P]),
+    "sq_calib_reference": (_I, [_P, _I, _P, ctypes.POINTER(sq_weight), _P, _P]),
+    "sq_calib_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
+    "sq_calib_objective": (_I, [_P, _I, _P, _I, _P, _I, ctypes.POINTER(sq_weight), _P, _I, _P, _P, _P, _P, _P, _S,
+                                _P]),
     "sq_probe_mfma_i8_sink_bytes": (_S, []),
     "sq_probe_mfma_i8": (_I, [_I, _I, _I, _P, _S, _P]),
 }
@@ -233,6 +237,34 @@ def sq_debug_block_acc_i32(qx: torch.Tensor, act_bits: int, w: Weight, acc_out: 
     ws = w.struct()
     _check(lib().sq_debug_block_acc_i32(_ptr(qx), M, act_bits, ctypes.byref(ws), _ptr(acc_out),
                                         _stream(stream)), "sq_debug_block_acc_i32")
+
+
+def sq_calib_reference(x: torch.Tensor, dinv: Optional[torch.Tensor], w: Weight, y_ref: torch.Tensor,
+                       stream=None) -> None:
+    """The Eq. (9) target X~ W^ into fp64 y_ref [M, N] (include/sq.h)."""
+    M = x.shape[0]
+    ws = w.struct()
+    _check(lib().sq_calib_reference(_ptr(x), M, _ptr(dinv), ctypes.byref(ws), _ptr(y_ref), _stream(stream)),
+           "sq_calib_reference")
+
+
+def sq_calib_workspace_bytes(M: int, K: int, N: int, act_bits: int, num_streams: int) -> int:
+    return int(lib().sq_calib_workspace_bytes(M, K, N, act_bits, num_streams))
+
+
+def sq_calib_objective(x: torch.Tensor, tok2stream: torch.Tensor, num_streams: int, dinv: Optional[torch.Tensor],
+                       act_bits: int, w: Weight, y_ref: torch.Tensor, cand_gamma: torch.Tensor,
+                       cand_clip: torch.Tensor, omega: torch.Tensor, objective: torch.Tensor,
+                       workspace: torch.Tensor, stream=None) -> None:
+    """Eq. (9) for every candidate row of cand_gamma [C, S] / cand_clip [C]
+    into fp64 objective [C] (include/sq.h)."""
+    M = x.shape[0]
+    C = cand_clip.shape[0]
+    ws = w.struct()
+    wp, wb = _ws(workspace)
+    _check(lib().sq_calib_objective(_ptr(x), M, _ptr(tok2stream), num_streams, _ptr(dinv), act_bits,
+                                    ctypes.byref(ws), _ptr(y_ref), C, _ptr(cand_gamma), _ptr(cand_clip),
+                                    _ptr(omega), _ptr(objective), wp, wb, _stream(stream)), "sq_calib_objective")
 
 
 # ------------------------------------------------------------------ helpers

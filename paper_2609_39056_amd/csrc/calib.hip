@@ -1,0 +1,212 @@
+// Activation calibration (Sec. 4.3, Eq. 9): the reconstruction error of one
+// linear under a candidate (gain per stream, shared threshold), weighted per
+// stream by omega_s / n_s.
+//
+//   - calib_reference_kernel: the target X~ W^ in fp64, X~ = fp32(x) * dinv
+//     (the quantizer's first step) and W^ = code * Delta_W.  Every product is
+//     exact in fp64 (24 x 15 significant bits), so the kernel differs from any
+//     other fp64 evaluation only in the order of its K sums.  128 x 128 output
+//     tiles, each thread 8 x 8 of them, K staged 16 at a time through LDS
+//     already widened to fp64.  Computed once per linear.
+//   - calib_count_kernel: n_s, the tokens of every stream (LDS histogram per
+//     workgroup, one global add per non-empty bin).
+//   - calib_row_error_kernel: e_i = omega_s(i) / n_s(i) * sum_j (y_ij - ref_ij)^2
+//     for the candidate's fp32 output y, one wave per row, fixed order.
+//   - calib_sum_kernel: L = sum_i e_i in one workgroup, fixed order.
+// The candidate's output itself comes from the fused linear (STATIC range,
+// one step, no bias), so the objective measures the arithmetic that runs.
+#include "sq_internal.h"
+
+namespace sq {
+namespace {
+
+constexpr int kRefTile = 128;  // output rows and columns per workgroup
+constexpr int kRefKc = 16;     // K per LDS stage
+
+__global__ __launch_bounds__(256) void calib_reference_kernel(const uint16_t* __restrict__ x,
+                                                              const float* __restrict__ dinv,
+                                                              const uint8_t* __restrict__ qw,
+                                                              const uint16_t* __restrict__ w_scale,
+                                                              double* __restrict__ y, int32_t M, int32_t N,
+                                                              int32_t K, int32_t w_group, int32_t tiles_n,
+                                                              size_t n_tiles) {
+  const size_t wg = flat_wg();
+  if (wg >= n_tiles) return;
+  const int64_t m0 = static_cast<int64_t>(wg / tiles_n) * kRefTile;
+  const int32_t n0 = static_cast<int32_t>(wg % tiles_n) * kRefTile;
+  __shared__ double xs[kRefKc][kRefTile];
+  __shared__ double ws[kRefKc][kRefTile];
+
+  const int t = threadIdx.x;
+  const int tx = t & 15, ty = t >> 4;
+  // staging: thread t fills row / column t/2 of the tile, channels 8*(t%2) .. +7 of the stage
+  const int sr = t >> 1, sh = t & 1;
+  const int64_t xm = m0 + sr;
+  const bool xin = xm < M;
+  const int32_t wn = n0 + sr;
+  const bool win = wn < N;
+  const uint16_t* xrow = x + (xin ? xm : 0) * static_cast<int64_t>(K);
+  const uint8_t* wrow = qw + static_cast<size_t>(win ? wn : 0) * (K / 2);
+
+  double acc[8][8];
+#pragma unroll
+  for (int r = 0; r < 8; ++r)
+#pragma unroll
+    for (int c = 0; c < 8; ++c) acc[r][c] = 0.0;
+
+  for (int32_t k0 = 0; k0 < K; k0 += kRefKc) {
+    const int32_t kb = k0 + sh * 8;
+    uint4 xv = make_uint4(0u, 0u, 0u, 0u);
+    if (xin) xv = *reinterpret_cast<const uint4*>(xrow + kb);
+    float d[8];
+    if (dinv != nullptr) {
+      const float4 d0 = *reinterpret_cast<const float4*>(dinv + kb);
+      const float4 d1 = *reinterpret_cast<const float4*>(dinv + kb + 4);
+      d[0] = d0.x; d[1] = d0.y; d[2] = d0.z; d[3] = d0.w;
+      d[4] = d1.x; d[5] = d1.y; d[6] = d1.z; d[7] = d1.w;
+    }
+    const uint32_t xw[4] = {xv.x, xv.y, xv.z, xv.w};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const float xf = bf16_to_f32((xw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
+      xs[sh * 8 + j][sr] = static_cast<double>(dinv != nullptr ? xf * d[j] : xf);
+    }
+    // 8 codes kb .. kb+7 sit in one dword: byte b holds code kb+b (low nibble)
+    // and code kb+b+4 (high nibble)
+    uint32_t p = 0u;
+    double step = 0.0;
+    if (win) {
+      p = *reinterpret_cast<const uint32_t*>(wrow + kb / 2);
+      step = static_cast<double>(f16_to_f32(w_scale[static_cast<size_t>(kb / w_group) * N + wn]));
+    }
+#pragma unroll
+    for (int b = 0; b < 4; ++b) {
+      const int lo = static_cast<int32_t>(p << (28 - 8 * b)) >> 28;
+      const int hi = static_cast<int32_t>(p << (24 - 8 * b)) >> 28;
+      ws[sh * 8 + b][sr] = static_cast<double>(lo) * step;
+      ws[sh * 8 + b + 4][sr] = static_cast<double>(hi) * step;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int kk = 0; kk < kRefKc; ++kk) {
+      double a[8], bv[8];
+#pragma unroll
+      for (int r = 0; r < 8; ++r) a[r] = xs[kk][ty + 16 * r];
+#pragma unroll
+      for (int c = 0; c < 8; ++c) bv[c] = ws[kk][tx + 16 * c];
+#pragma unroll
+      for (int r = 0; r < 8; ++r)
+#pragma unroll
+        for (int c = 0; c < 8; ++c) acc[r][c] = fma(a[r], bv[c], acc[r][c]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int r = 0; r < 8; ++r) {
+    const int64_t m = m0 + ty + 16 * r;
+    if (m >= M) continue;
+#pragma unroll
+    for (int c = 0; c < 8; ++c) {
+      const int32_t n = n0 + tx + 16 * c;
+      if (n < N) y[m * N + n] = acc[r][c];
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void calib_zero_kernel(int32_t* __restrict__ counts, int32_t S) {
+  for (int32_t s = blockIdx.x * 256 + threadIdx.x; s < S; s += gridDim.x * 256) counts[s] = 0;
+}
+
+__global__ __launch_bounds__(256) void calib_count_kernel(const int32_t* __restrict__ tok2stream, int32_t M,
+                                                          int32_t S, int32_t* __restrict__ counts) {
+  __shared__ int32_t bins[kCalibMaxStreams];
+  for (int32_t s = threadIdx.x; s < S; s += 256) bins[s] = 0;
+  __syncthreads();
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < M;
+       i += static_cast<int64_t>(gridDim.x) * 256) {
+    const int32_t s = tok2stream[i];
+    if (static_cast<uint32_t>(s) < static_cast<uint32_t>(S)) atomicAdd(&bins[s], 1);
+  }
+  __syncthreads();
+  for (int32_t s = threadIdx.x; s < S; s += 256)
+    if (bins[s] != 0) atomicAdd(&counts[s], bins[s]);
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+// One wave per row; four rows per workgroup.
+__global__ __launch_bounds__(256) void calib_row_error_kernel(const float* __restrict__ yq,
+                                                              const double* __restrict__ ref,
+                                                              const int32_t* __restrict__ tok2stream,
+                                                              const int32_t* __restrict__ counts,
+                                                              const double* __restrict__ omega, int32_t M,
+                                                              int32_t N, int32_t S, double* __restrict__ err) {
+  const int64_t i = static_cast<int64_t>(flat_wg()) * 4 + (threadIdx.x >> 6);
+  if (i >= M) return;
+  const int lane = threadIdx.x & 63;
+  const float4* yr = reinterpret_cast<const float4*>(yq + i * N);
+  const double2* rr = reinterpret_cast<const double2*>(ref + i * N);
+  double acc = 0.0;
+  for (int32_t j = lane; j < N / 4; j += 64) {
+    const float4 a = yr[j];
+    const double2 b0 = rr[2 * j], b1 = rr[2 * j + 1];
+    const double e0 = static_cast<double>(a.x) - b0.x, e1 = static_cast<double>(a.y) - b0.y;
+    const double e2 = static_cast<double>(a.z) - b1.x, e3 = static_cast<double>(a.w) - b1.y;
+    acc = fma(e0, e0, acc);
+    acc = fma(e1, e1, acc);
+    acc = fma(e2, e2, acc);
+    acc = fma(e3, e3, acc);
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    const int32_t s = tok2stream[i];
+    double w = 0.0;
+    if (static_cast<uint32_t>(s) < static_cast<uint32_t>(S)) w = omega[s] / static_cast<double>(counts[s]);
+    err[i] = w * acc;
+  }
+}
+
+__global__ __launch_bounds__(256) void calib_sum_kernel(const double* __restrict__ err, int32_t M,
+                                                        double* __restrict__ out) {
+  __shared__ double part[4];
+  double acc = 0.0;
+  for (int64_t i = threadIdx.x; i < M; i += 256) acc += err[i];
+  acc = wave_sum(acc);
+  if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
+  __syncthreads();
+  if (threadIdx.x == 0) *out = (part[0] + part[1]) + (part[2] + part[3]);
+}
+
+}  // namespace
+
+hipError_t launch_calib_reference(const CalibRefArgs& a, hipStream_t s) {
+  const int32_t tiles_n = (a.N + kRefTile - 1) / kRefTile;
+  const size_t n_tiles = static_cast<size_t>((a.M + kRefTile - 1) / kRefTile) * tiles_n;
+  hipLaunchKernelGGL(calib_reference_kernel, wg_grid(n_tiles), dim3(256), 0, s, a.x, a.dinv, a.qw, a.w_scale,
+                     a.y, a.M, a.N, a.K, a.w_group, tiles_n, n_tiles);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_counts(const int32_t* tok2stream, int32_t M, int32_t S, int32_t* counts, hipStream_t s) {
+  hipLaunchKernelGGL(calib_zero_kernel, dim3((S + 255) / 256), dim3(256), 0, s, counts, S);
+  const int64_t want = (static_cast<int64_t>(M) + 4095) / 4096;  // about 16 rows per thread
+  const int grid = static_cast<int>(want < 1024 ? want : 1024);
+  hipLaunchKernelGGL(calib_count_kernel, dim3(grid), dim3(256), 0, s, tok2stream, M, S, counts);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_error(const float* yq, const double* ref, const int32_t* tok2stream,
+                              const int32_t* counts, const double* omega, int32_t M, int32_t N, int32_t S,
+                              double* err, double* out, hipStream_t s) {
+  const size_t wgs = (static_cast<size_t>(M) + 3) / 4;
+  hipLaunchKernelGGL(calib_row_error_kernel, wg_grid(wgs), dim3(256), 0, s, yq, ref, tok2stream, counts, omega,
+                     M, N, S, err);
+  hipLaunchKernelGGL(calib_sum_kernel, dim3(1), dim3(256), 0, s, err, M, out);
+  return hipGetLastError();
+}
+
+}  // namespace sq

@@ -101,6 +101,14 @@ size_t fused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
   return round_up(qx_bytes(M, K, bits)) + round_up(act_scale_bytes(M, K, bits)) + gemm_ws_bytes(M, K, N, bits);
 }
 
+// calibration workspace: the fused linear's | y of one candidate fp32 [M][N] |
+// per-row errors fp64 [M] | stream counts int32 [S]
+constexpr int32_t kCalibMaxCandidates = 1 << 16;
+size_t calib_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits, int32_t S) {
+  return fused_ws_bytes(M, K, N, bits) + round_up(static_cast<size_t>(M) * N * 4) +
+         round_up(static_cast<size_t>(M) * 8) + round_up(static_cast<size_t>(S) * 4);
+}
+
 size_t unfused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
   const size_t mk4 = round_up(static_cast<size_t>(M) * K * 4);
   const size_t mn4 = round_up(static_cast<size_t>(M) * N * 4);
@@ -315,6 +323,73 @@ sq_status sq_linear_unfused(const uint16_t* x, int32_t M, const sq_act_params* a
   u.y2 = reinterpret_cast<float*>(p);
   u.y = y;
   return hip_status(launch_unfused(u, stream));
+}
+
+sq_status sq_calib_reference(const uint16_t* x, int32_t M, const float* dinv, const sq_weight* w, double* y_ref,
+                             hipStream_t stream) {
+  if (x == nullptr || y_ref == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(y_ref, 16)) return SQ_ERR_ALIGN;
+  if (dinv != nullptr && !aligned(dinv, 16)) return SQ_ERR_ALIGN;
+  CalibRefArgs a{x, dinv, w->qw, w->w_scale, y_ref, M, w->N, w->K, w->w_group};
+  return hip_status(launch_calib_reference(a, stream));
+}
+
+size_t sq_calib_workspace_bytes(int32_t M, int32_t K, int32_t N, int32_t act_bits, int32_t num_streams) {
+  if (!valid_m(M) || !valid_k(K) || !valid_n(N) || (act_bits != 8 && act_bits != 4)) return 0;
+  if (num_streams < 1 || num_streams > kCalibMaxStreams) return 0;
+  return calib_ws_bytes(M, K, N, act_bits, num_streams);
+}
+
+sq_status sq_calib_objective(const uint16_t* x, int32_t M, const int32_t* tok2stream, int32_t num_streams,
+                             const float* dinv, int32_t act_bits, const sq_weight* w, const double* y_ref,
+                             int32_t num_candidates, const float* cand_gamma, const float* cand_clip,
+                             const double* omega, double* objective, void* workspace, size_t ws_bytes,
+                             hipStream_t stream) {
+  if (x == nullptr || tok2stream == nullptr || y_ref == nullptr || cand_gamma == nullptr ||
+      cand_clip == nullptr || omega == nullptr || objective == nullptr || workspace == nullptr)
+    return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  if (act_bits != 8 && act_bits != 4) return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M) || num_streams < 1 || num_streams > kCalibMaxStreams || num_candidates < 1 ||
+      num_candidates > kCalibMaxCandidates)
+    return SQ_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(y_ref, 16) || !aligned(workspace, 16) || !aligned(tok2stream, 4) ||
+      !aligned(cand_gamma, 4) || !aligned(cand_clip, 4) || !aligned(omega, 8) || !aligned(objective, 8))
+    return SQ_ERR_ALIGN;
+  if (dinv != nullptr && !aligned(dinv, 16)) return SQ_ERR_ALIGN;
+  const int32_t K = w->K, N = w->N, S = num_streams;
+  if (ws_bytes < calib_ws_bytes(M, K, N, act_bits, S)) return SQ_ERR_WORKSPACE;
+
+  const size_t fused_bytes = fused_ws_bytes(M, K, N, act_bits);
+  uint8_t* p = static_cast<uint8_t*>(workspace);
+  float* yq = reinterpret_cast<float*>(p + fused_bytes);
+  double* err = reinterpret_cast<double*>(p + fused_bytes + round_up(static_cast<size_t>(M) * N * 4));
+  int32_t* counts = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(err) + round_up(static_cast<size_t>(M) * 8));
+  sq_weight wt = *w;
+  wt.bias = nullptr;  // the bias is on both sides of Eq. 9 and cancels
+  st = hip_status(launch_calib_counts(tok2stream, M, S, counts, stream));
+  if (st != SQ_OK) return st;
+  for (int32_t c = 0; c < num_candidates; ++c) {
+    sq_act_params a{};
+    a.tok2stream = tok2stream;
+    a.gamma = cand_gamma + static_cast<size_t>(c) * S;
+    a.clip = cand_clip + c;
+    a.dinv = dinv;
+    a.num_streams = S;
+    a.num_steps = 1;
+    a.step = 0;
+    a.range_mode = SQ_RANGE_STATIC;
+    a.act_bits = act_bits;
+    st = linear_fused(act_bits, x, M, &a, &wt, yq, SQ_OUT_F32, workspace, fused_bytes, stream);
+    if (st != SQ_OK) return st;
+    st = hip_status(launch_calib_error(yq, y_ref, tok2stream, counts, omega, M, N, S, err, objective + c, stream));
+    if (st != SQ_OK) return st;
+  }
+  return SQ_OK;
 }
 
 size_t sq_probe_mfma_i8_sink_bytes(void) { return static_cast<size_t>(mfma_probe_workgroups()) * 256 * 4; }

@@ -165,6 +165,24 @@ struct UnfusedArgs {
 };
 hipError_t launch_unfused(const UnfusedArgs& a, hipStream_t s);
 
+// calibration objective (Sec. 4.3, Eq. 9)
+constexpr int32_t kCalibMaxStreams = 4096;  // streams of one objective (an LDS histogram)
+struct CalibRefArgs {
+  const uint16_t* x;
+  const float* dinv;
+  const uint8_t* qw;
+  const uint16_t* w_scale;
+  double* y;  // [M][N] X~ W^
+  int32_t M, N, K, w_group;
+};
+hipError_t launch_calib_reference(const CalibRefArgs& a, hipStream_t s);
+// counts[s] = tokens of stream s (ids outside [0, S) are not counted)
+hipError_t launch_calib_counts(const int32_t* tok2stream, int32_t M, int32_t S, int32_t* counts, hipStream_t s);
+// err[i] = omega_s(i) / n_s(i) * ||y_i - ref_i||^2, then *out = sum_i err[i]
+hipError_t launch_calib_error(const float* yq, const double* ref, const int32_t* tok2stream,
+                              const int32_t* counts, const double* omega, int32_t M, int32_t N, int32_t S,
+                              double* err, double* out, hipStream_t s);
+
 // matrix-core rate probe (measurement hook)
 int mfma_probe_workgroups();
 hipError_t launch_mfma_probe(int32_t* sink, int32_t iters, int32_t random, int32_t fold, hipStream_t s);

@@ -162,3 +162,41 @@ def test_mfma_probe_checks(L):
     assert L.sq_probe_mfma_i8((1 << 24) + 1, 1, 0, A, n, None) == SHAPE
     assert L.sq_probe_mfma_i8(10, 1, 0, A, n - 4, None) == WS
     assert L.sq_probe_mfma_i8(10, 1, 0, ctypes.c_void_p((1 << 20) + 2), n, None) == ALIGN
+
+
+def calib(L, x=A, M=88, t2s=A, S=3, dinv=None, bits=8, w=None, ref=A, C=4, g=A, c=A, om=A, obj=A, ws=A,
+          nbytes=1 << 30):
+    w = wt() if w is None else w
+    return L.sq_calib_objective(x, M, t2s, S, dinv, bits, ctypes.byref(w), ref, C, g, c, om, obj, ws, nbytes, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(x=None), NULL), (dict(t2s=None), NULL), (dict(ref=None), NULL), (dict(g=None), NULL),
+    (dict(c=None), NULL), (dict(om=None), NULL), (dict(obj=None), NULL), (dict(ws=None), NULL),
+    (dict(bits=5), UNSUP), (dict(M=0), SHAPE), (dict(S=0), SHAPE), (dict(S=4097), SHAPE), (dict(C=0), SHAPE),
+    (dict(C=(1 << 16) + 1), SHAPE), (dict(x=A + 2), ALIGN), (dict(ref=A + 8), ALIGN), (dict(om=A + 4), ALIGN),
+    (dict(obj=A + 4), ALIGN), (dict(g=A + 2), ALIGN), (dict(dinv=A + 4), ALIGN), (dict(ws=A + 8), ALIGN),
+    (dict(nbytes=1024), WS), (dict(w=wt(N=100)), SHAPE), (dict(w=wt(qw=None)), NULL),
+])
+def test_calib_objective_rejects(L, kw, code):
+    assert calib(L, **kw) == code
+
+
+def test_calib_reference_rejects_and_sizes(L):
+    w = wt()
+    assert L.sq_calib_reference(None, 88, None, ctypes.byref(w), A, None) == NULL
+    assert L.sq_calib_reference(A, 88, None, ctypes.byref(w), None, None) == NULL
+    assert L.sq_calib_reference(A, 0, None, ctypes.byref(w), A, None) == SHAPE
+    assert L.sq_calib_reference(A, 88, None, ctypes.byref(wt(K=200)), A, None) == SHAPE
+    assert L.sq_calib_reference(A + 2, 88, None, ctypes.byref(w), A, None) == ALIGN
+    assert L.sq_calib_reference(A, 88, A + 4, ctypes.byref(w), A, None) == ALIGN
+    assert L.sq_calib_reference(A, 88, None, ctypes.byref(w), A + 8, None) == ALIGN
+    M, K, N = 1000, 2048, 4096
+    for bits in (8, 4):
+        n = B.sq_calib_workspace_bytes(M, K, N, bits, 3)
+        assert n % 256 == 0
+        assert n >= B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, M, K, N, bits) + 4 * M * N + 8 * M + 12
+    assert B.sq_calib_workspace_bytes(M, K, N, 8, 0) == 0
+    assert B.sq_calib_workspace_bytes(M, K, N, 8, 4097) == 0
+    assert B.sq_calib_workspace_bytes(M, K, 100, 8, 3) == 0
+    assert B.sq_calib_workspace_bytes(M, K, N, 6, 3) == 0

@@ -1,0 +1,187 @@
+"""GPU parity of the activation calibration objective (Sec. 4.3, Eq. 9)
+through the C ABI: the fp64 target X~ W^ against the oracle's, and the
+objective of every candidate against the oracle's, within a bound derived
+from the fused linear's fp32 contract; the candidate the GPU ranks first is
+the oracle's best within that bound; results are reproducible and do not
+depend on the batch a candidate is evaluated in."""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import f32_to_dev, i32_to_dev, u8_to_dev, u16_to_dev
+from oracle import sq_oracle as O
+from paper_2609_39056_amd import binding as B
+from paper_2609_39056_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+F32 = np.float32
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    B.lib()
+
+
+def weight(L, G):
+    pw = O.pack_weights(L.w, L.d, G)
+    W = B.Weight(qw=u8_to_dev(pw["qw"]), w_scale=u16_to_dev(pw["w_scale"].T, torch.float16), w_group=G,
+                 bias=u16_to_dev(L.bias_bits, torch.bfloat16))
+    return pw, W
+
+
+def abs_reference(L, pw, G, use_dinv=True):
+    """sum_k |x~_ik| |w^_jk| in fp64: the scale of the fp64 sums' rounding."""
+    xt = O.bf16_bits_to_f32(L.x_bits)
+    if use_dinv:
+        xt = (xt * L.dinv[None, :]).astype(F32)
+    wq = pw["codes"].astype(np.float64) * np.repeat(O.f16_bits_to_f32(pw["w_scale"]).astype(np.float64), G, axis=1)
+    return np.abs(xt.astype(np.float64)) @ np.abs(wq).T
+
+
+def gpu_reference(L, W, use_dinv=True):
+    M, N = L.x_bits.shape[0], W.N
+    ref = torch.full((M, N), float("nan"), dtype=torch.float64, device="cuda")
+    B.sq_calib_reference(u16_to_dev(L.x_bits, torch.bfloat16), f32_to_dev(L.dinv) if use_dinv else None, W, ref)
+    return ref
+
+
+def candidates(L, n_extra, seed):
+    """The layer's step tables plus perturbed ones: gains per stream and clips."""
+    rng = np.random.default_rng(seed)
+    g = [L.gamma[t] for t in range(L.gamma.shape[0])]
+    c = [L.clip[t] for t in range(L.clip.shape[0])]
+    for _ in range(n_extra):
+        g.append((L.gamma[0] * rng.lognormal(0.0, 0.4, L.gamma.shape[1])).astype(F32))
+        c.append(F32(L.clip[0] * rng.lognormal(0.0, 0.5)))
+    return np.stack(g).astype(F32), np.array(c, dtype=F32)
+
+
+def gpu_objective(L, W, bits, gammas, clips, omega, ref, S=None):
+    M, K, N = L.x_bits.shape[0], W.K, W.N
+    S = L.gamma.shape[1] if S is None else S
+    ws = torch.empty(B.sq_calib_workspace_bytes(M, K, N, bits, S), dtype=torch.uint8, device="cuda")
+    obj = torch.full((len(clips),), float("nan"), dtype=torch.float64, device="cuda")
+    B.sq_calib_objective(u16_to_dev(L.x_bits, torch.bfloat16), i32_to_dev(L.tok2stream), S, f32_to_dev(L.dinv),
+                         bits, W, ref, f32_to_dev(gammas), f32_to_dev(clips),
+                         torch.as_tensor(np.asarray(omega, dtype=np.float64), device="cuda"), obj, ws)
+    torch.cuda.synchronize()
+    return obj.cpu().numpy()
+
+
+def objective_bound(L, pw, G, bits, gammas, clips, omega, ref, ref_abs, S):
+    """Per candidate, how far the GPU objective may sit from the oracle's.
+    The GPU's output is y64 + d with |d| <= 1e-5 A (the fused linear's fp32
+    bound, A = sum of |terms|) plus fp32 rounding of y, and its target is
+    ref + r with |r| <= K 2^-52 sum|x~||w^|; with t = |d| + |r|, each squared
+    error moves by at most 2 |e| t + t^2, weighted as in the objective."""
+    K = L.x_bits.shape[1]
+    t2s = L.tok2stream
+    out = []
+    for g, c in zip(gammas, clips):
+        res = O.linear(L.x_bits, t2s, g[None, :], 0, pw["codes"], pw["w_scale"], G, dinv=L.dinv,
+                       clip=np.array([c], dtype=F32), bias_bits=None, range_mode=O.RANGE_STATIC, act_bits=bits)
+        e = np.abs(res["y64"] - ref)
+        t = 1e-5 * res["A"] + 2.0**-23 * np.abs(res["y64"]) + K * 2.0**-52 * ref_abs
+        row = (2 * e * t + t * t).sum(axis=1)
+        b = 0.0
+        for s in range(S):
+            n = int((t2s == s).sum())
+            if n:
+                b += float(omega[s]) / n * float(row[t2s == s].sum())
+        out.append(b)
+    return np.array(out)
+
+
+def check_objectives(got, want, bound):
+    err = np.abs(got - want)
+    assert np.all(np.isfinite(got))
+    assert np.all(err <= bound + 1e-12 * np.abs(want)), f"err {err} bound {bound} want {want}"
+    # the candidate ranked first on the GPU is the oracle's best within the bound
+    best = int(np.argmin(got))
+    assert want[best] <= want.min() + bound[best] + bound[int(np.argmin(want))] + 1e-12 * want.min()
+
+
+@pytest.mark.parametrize("use_dinv", [True, False])
+@pytest.mark.parametrize("G", [128, 256])
+@pytest.mark.parametrize("M,N", [(200, 192), (1, 64), (129, 128)])
+def test_calib_reference(M, N, G, use_dinv):
+    """X~ W^ in fp64 against the oracle: ragged rows (200 = 128 + 72), a
+    half tile of columns (192), a single row; one weight step per 128-channel
+    group or per output channel."""
+    K = 256
+    L = synth.make_layer(K=K, N=N, stream_counts=(max(M - 2, 1), 1, 1) if M > 2 else (M, 0, 0), seed=[40, M, N])
+    pw, W = weight(L, G)
+    got = gpu_reference(L, W, use_dinv).cpu().numpy()
+    want = O.calib_reference(L.x_bits, pw["codes"], pw["w_scale"], G, L.dinv if use_dinv else None)
+    ref_abs = abs_reference(L, pw, G, use_dinv)
+    assert np.all(np.abs(got - want) <= K * 2.0**-52 * ref_abs)
+
+
+@pytest.mark.parametrize("G", [128, 256])
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("M", [37, 200])
+def test_calib_objective(M, bits, G):
+    """Seven candidates on a three-stream layer (permuted rows), uniform and
+    uneven stream weights: 37 tokens (weight-streaming GEMM) and 200 (tiled;
+    4-bit codes on the fp8 matrix cores)."""
+    K, N = 256, 192
+    L = synth.make_layer(K=K, N=N, stream_counts=(M - M // 4 - M // 8, M // 8, M // 4), T=3, seed=[41, M, bits],
+                         permute=True)
+    pw, W = weight(L, G)
+    ref_dev = gpu_reference(L, W)
+    ref = O.calib_reference(L.x_bits, pw["codes"], pw["w_scale"], G, L.dinv)
+    ref_abs = abs_reference(L, pw, G)
+    gammas, clips = candidates(L, 4, seed=[42, M])
+    for omega in (np.full(3, 1 / 3), np.array([0.5, 0.2, 0.3])):
+        got = gpu_objective(L, W, bits, gammas, clips, omega, ref_dev)
+        want = O.calib_objective(L.x_bits, L.tok2stream, 3, pw["codes"], pw["w_scale"], G, gammas, clips, omega,
+                                 dinv=L.dinv, act_bits=bits, ref=ref)
+        bound = objective_bound(L, pw, G, bits, gammas, clips, omega, ref, ref_abs, 3)
+        check_objectives(got, want, bound)
+
+
+def test_calib_empty_stream_and_reuse():
+    """A stream with no token adds nothing (four streams, the second empty,
+    with weight 0.4); the same candidates evaluated again, one at a time and in
+    another order give bit-identical objectives."""
+    K, N, bits, G = 256, 128, 8, 128
+    L = synth.make_layer(K=K, N=N, stream_counts=(60, 0, 25, 15), T=2, seed=43, permute=True)
+    assert L.gamma.shape[1] == 4 and not np.any(L.tok2stream == 1)
+    pw, W = weight(L, G)
+    ref_dev = gpu_reference(L, W)
+    ref = O.calib_reference(L.x_bits, pw["codes"], pw["w_scale"], G, L.dinv)
+    gammas, clips = candidates(L, 3, seed=44)
+    omega = np.array([0.3, 0.4, 0.2, 0.1])
+    got = gpu_objective(L, W, bits, gammas, clips, omega, ref_dev)
+    want = O.calib_objective(L.x_bits, L.tok2stream, 4, pw["codes"], pw["w_scale"], G, gammas, clips, omega,
+                             dinv=L.dinv, act_bits=bits, ref=ref)
+    bound = objective_bound(L, pw, G, bits, gammas, clips, omega, ref, abs_reference(L, pw, G), 4)
+    check_objectives(got, want, bound)
+    again = gpu_objective(L, W, bits, gammas, clips, omega, ref_dev)
+    assert np.array_equal(got.view(np.uint64), again.view(np.uint64))
+    order = np.arange(len(clips))[::-1].copy()
+    rev = gpu_objective(L, W, bits, gammas[order], clips[order], omega, ref_dev)
+    assert np.array_equal(rev.view(np.uint64), got[order].view(np.uint64))
+    one = gpu_objective(L, W, bits, gammas[2:3], clips[2:3], omega, ref_dev)
+    assert one.view(np.uint64)[0] == got.view(np.uint64)[2]
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_calib_objective_larger(bits):
+    """512 calibration tokens of a K = 2048, N = 512 linear (16 K-blocks,
+    four tiles of rows), three candidates."""
+    K, N, G = 2048, 512, 128
+    L = synth.make_layer(K=K, N=N, stream_counts=(384, 48, 80), T=3, seed=[45, bits], permute=True)
+    pw, W = weight(L, G)
+    ref_dev = gpu_reference(L, W)
+    ref = O.calib_reference(L.x_bits, pw["codes"], pw["w_scale"], G, L.dinv)
+    gammas, clips = L.gamma.copy(), L.clip.copy()
+    omega = np.full(3, 1 / 3)
+    got = gpu_objective(L, W, bits, gammas, clips, omega, ref_dev)
+    want = O.calib_objective(L.x_bits, L.tok2stream, 3, pw["codes"], pw["w_scale"], G, gammas, clips, omega,
+                             dinv=L.dinv, act_bits=bits, ref=ref)
+    bound = objective_bound(L, pw, G, bits, gammas, clips, omega, ref, abs_reference(L, pw, G), 3)
+    check_objectives(got, want, bound)
