@@ -38,6 +38,11 @@ Readings where the paper leaves a choice:
   paper) or per 128-wide group of K.  The epilogue then sums, over K-blocks in
   ascending order, (FP32(C_block) * s) * Delta_W; with a single block this is
   Eq. (10) exactly.
+* Calibration, Sec. 4.3 Eq. (9): the paper gives the objective and its
+  constraints but no optimizer; the search here is a compass search in log
+  coordinates with every trial point projected onto the constraint set (the
+  token-weighted nearest point) and the step halved after a round without
+  progress.
 * int4 packing (both weights and A4 activations): for every 8 consecutive
   codes k = 8g..8g+7 the four bytes 4g..4g+3 hold code 8g+b in the low nibble
   and code 8g+b+4 in the high nibble of byte 4g+b.
@@ -354,3 +359,96 @@ def calib_objective(x_bits, tok2stream, num_streams, qw_codes, w_scale_bits, w_g
                 L += float(omega[s]) / n * float(d2[rows].sum())
         out.append(L)
     return np.array(out, dtype=np.float64)
+
+
+# ---------------------------------------------------------------- constrained search, Eq. (9)
+# The paper fixes the constraints of the joint (gamma, c) calibration (bounds
+# on c and on every gamma_s, and sum_s n_s log gamma_s = 0) but names no
+# search procedure.  The reading here: a compass (pattern) search in the log
+# coordinates (log gamma_1 .. log gamma_S, log c), each trial point projected
+# back onto the constraint set, with the step halved after a round that finds
+# no better point.
+
+def project_log_gains(v, counts, lo, hi, iters=64):
+    """The point u nearest to v in the token-weighted norm sum_s n_s (u_s - v_s)^2
+    with lo <= u_s <= hi and sum_s n_s u_s = 0 (lo <= 0 <= hi).  By the KKT
+    conditions u_s = clamp(v_s - lam, lo, hi) for the streams with tokens; the
+    sum is non-increasing in lam, and lam is found by bisection in float64 (a
+    fixed number of halvings).  A stream without tokens is only clamped."""
+    v = np.asarray(v, dtype=np.float64)
+    n = np.asarray(counts, dtype=np.float64)
+    live = n > 0
+    if not live.any():
+        return np.clip(v, lo, hi)
+
+    def f(lam):
+        return float(np.sum(n[live] * np.clip(v[live] - lam, lo, hi)))
+
+    a = float(v[live].min()) - hi   # f(a) = N * hi >= 0
+    b = float(v[live].max()) - lo   # f(b) = N * lo <= 0
+    for _ in range(iters):
+        mid = 0.5 * (a + b)
+        if f(mid) > 0:
+            a = mid
+        else:
+            b = mid
+    lam = 0.5 * (a + b)
+    return np.where(live, np.clip(v - lam, lo, hi), np.clip(v, lo, hi))
+
+
+def compass_candidates(u, v_clip, h, counts, bounds):
+    """The trial points of one round around the incumbent (u = log gains,
+    v_clip = log c): for every coordinate d (the S gains, then the threshold)
+    a step of +h, then -h.  A gain step is projected with project_log_gains; a
+    threshold step is clamped to [log c_min, log c_max].  Returns the fp32
+    gains [2(S+1), S] and thresholds [2(S+1)], the values that are evaluated
+    (clamped to the bounds after exponentiation), and their log coordinates."""
+    g_min, g_max, c_min, c_max = (float(b) for b in bounds)
+    lo, hi = np.log(g_min), np.log(g_max)
+    S = len(u)
+    gam, clip, us, vs = [], [], [], []
+    for d in range(S + 1):
+        for sign in (1.0, -1.0):
+            if d < S:
+                w = np.array(u, dtype=np.float64)
+                w[d] += sign * h
+                w = project_log_gains(w, counts, lo, hi)
+                vc = v_clip
+            else:
+                w = np.array(u, dtype=np.float64)
+                vc = min(max(v_clip + sign * h, np.log(c_min)), np.log(c_max))
+            gam.append(np.clip(np.exp(w).astype(F32), F32(g_min), F32(g_max)))
+            clip.append(np.clip(F32(np.exp(vc)), F32(c_min), F32(c_max)))
+            us.append(w)
+            vs.append(vc)
+    return np.stack(gam), np.array(clip, dtype=F32), np.stack(us), np.array(vs)
+
+
+def calib_search(objective, counts, bounds, clip_init, log_step, rounds):
+    """Compass search for Eq. (9)'s (gamma*, c*).  objective(gammas [C, S],
+    clips [C]) -> float64 [C].  Starts from gamma = 1 (which meets every
+    constraint) and c = clip_init clamped to [c_min, c_max], with step
+    log_step.  Each round evaluates compass_candidates; the first candidate
+    with the smallest objective replaces the incumbent if it is strictly
+    better, else the step halves.  Returns (gamma fp32 [S], c fp32, L, step,
+    trace); trace holds per round the candidates' objectives and the
+    incumbent's before the round."""
+    g_min, g_max, c_min, c_max = (float(b) for b in bounds)
+    S = len(counts)
+    u = np.zeros(S)
+    gam = np.ones(S, dtype=F32)
+    c = np.clip(F32(clip_init), F32(c_min), F32(c_max))
+    vc = float(np.log(np.float64(c)))
+    L = float(objective(gam[None, :], np.array([c], dtype=F32))[0])
+    h = float(log_step)
+    trace = []
+    for _ in range(rounds):
+        G, C, U, V = compass_candidates(u, vc, h, counts, bounds)
+        obj = np.asarray(objective(G, C), dtype=np.float64)
+        trace.append((L, obj))
+        j = int(np.argmin(obj))
+        if obj[j] < L:
+            L, u, vc, gam, c = float(obj[j]), U[j], float(V[j]), G[j], C[j]
+        else:
+            h = 0.5 * h
+    return gam, F32(c), L, h, trace

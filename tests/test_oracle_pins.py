@@ -370,3 +370,103 @@ def test_calib_objective_streams_separate():
     on1 = O.calib_objective(L_.x_bits, L_.tok2stream, 3, pw["codes"], pw["w_scale"], 128, g, c, [0, 1, 0],
                             dinv=L_.dinv)
     assert on0[0] == on0[1] and on1[0] != on1[1]
+
+
+# ---------------------------------------------------------------- constrained (gamma, c) search, Eq. (9)
+def test_projection_closed_form_inside_bounds():
+    """With no bound active the token-weighted projection onto
+    sum_s n_s u_s = 0 subtracts the token-weighted mean: u = v - sum(n v) / sum(n)."""
+    rng = np.random.default_rng(20)
+    for S in (1, 2, 3, 9):
+        n = rng.integers(1, 5000, S)
+        v = rng.normal(0, 0.2, S)
+        u = O.project_log_gains(v, n, -5.0, 5.0)
+        assert np.allclose(u, v - (n * v).sum() / n.sum(), rtol=0, atol=1e-12)
+
+
+def test_projection_matches_active_set_enumeration():
+    """App. C.1 constraint set with bounds that bind: the projection equals
+    the best feasible point over every active set (each coordinate free, at
+    its lower or at its upper bound; the free ones then have the closed form
+    v - mu), i.e. brute force on the convex problem min sum n (u - v)^2; a
+    stream without tokens is only clamped."""
+    import itertools
+    rng = np.random.default_rng(21)
+    lo, hi = np.log(0.5), np.log(2.0)
+    for trial in range(8):
+        S = 4
+        n = rng.integers(1, 200, S).astype(float)
+        v = rng.normal(0, 1.0, S)
+        u = O.project_log_gains(v, n, lo, hi)
+        assert np.all(u >= lo) and np.all(u <= hi)
+        assert abs((n * u).sum()) <= 1e-9 * n.sum()
+        best, best_u = np.inf, None
+        for act in itertools.product((0, 1, 2), repeat=S):
+            z = np.where(np.array(act) == 1, lo, hi).astype(float)
+            free = np.array(act) == 0
+            if free.any():
+                mu = ((n * v)[free].sum() + (n * z)[~free].sum()) / n[free].sum()
+                z[free] = v[free] - mu
+            if abs((n * z).sum()) > 1e-9 * n.sum() or np.any(z < lo - 1e-12) or np.any(z > hi + 1e-12):
+                continue
+            val = float((n * (z - v) ** 2).sum())
+            if val < best:
+                best, best_u = val, z
+        assert np.allclose(u, best_u, atol=1e-9)
+    u = O.project_log_gains(np.array([3.0, 0.4, -0.2]), np.array([0, 10, 10]), lo, hi)
+    assert u[0] == hi and abs(u[1] + u[2]) < 1e-12 and abs(u[1] - 0.3) < 1e-12
+
+
+def test_compass_search_finds_the_constrained_minimum_of_a_quadratic():
+    """The search procedure on an objective with a known constrained
+    minimizer: f = sum_s n_s (log gamma_s - a_s)^2 + (log c - b)^2, whose
+    minimizer on the constraint set (bounds inactive) is log gamma =
+    a - weighted mean of a, c = e^b."""
+    n = np.array([4096, 32, 64])
+    a = np.array([0.1, -0.4, 0.7])
+    b = np.log(3.0)
+
+    def f(G, C):
+        return ((n[None, :] * (np.log(G.astype(np.float64)) - a[None, :]) ** 2).sum(1)
+                + (np.log(C.astype(np.float64)) - b) ** 2)
+
+    gam, c, L, h, trace = O.calib_search(f, n, (0.25, 4.0, 0.5, 20.0), 1.0, 0.5, 80)
+    u_star = a - (n * a).sum() / n.sum()
+    assert np.allclose(np.log(gam.astype(np.float64)), u_star, atol=2e-3)
+    assert abs(np.log(float(c)) - b) < 2e-3
+    assert abs((n * np.log(gam.astype(np.float64))).sum()) < 1e-3 * n.sum()
+    # the incumbent's objective never rises
+    inc = [t[0] for t in trace] + [L]
+    assert all(x >= y for x, y in zip(inc, inc[1:]))
+
+
+def test_calib_search_on_a_layer():
+    """The search on Eq. (9) itself (three streams, uniform weights): every
+    constraint holds at the result, the objective does not rise from the
+    start (gamma = 1, c = clip_init), and the returned L is the objective of
+    the returned point."""
+    L_ = _layer(K=256, N=64, counts=(40, 6, 10), seed=22)
+    pw = O.pack_weights(L_.w, L_.d, 128)
+    n = np.bincount(L_.tok2stream, minlength=3)
+    om = np.full(3, 1 / 3)
+    ref = O.calib_reference(L_.x_bits, pw["codes"], pw["w_scale"], 128, L_.dinv)
+
+    def f(G, C):
+        return O.calib_objective(L_.x_bits, L_.tok2stream, 3, pw["codes"], pw["w_scale"], 128, G, C, om,
+                                 dinv=L_.dinv, act_bits=4, ref=ref)
+
+    bounds = (0.5, 2.0, 0.1, 50.0)
+    gam, c, L, h, trace = O.calib_search(f, n, bounds, float(L_.clip[0]), 0.5, 10)
+    assert np.all(gam >= F32(0.5)) and np.all(gam <= F32(2.0)) and F32(0.1) <= c <= F32(50.0)
+    assert abs((n * np.log(gam.astype(np.float64))).sum()) < 1e-5 * n.sum()
+    assert L <= trace[0][0]
+    assert f(gam[None, :], np.array([c]))[0] == L
+
+
+def test_calib_search_single_stream_keeps_unit_gain():
+    """One stream: sum n log gamma = 0 forces gamma = 1 exactly (only the
+    threshold moves)."""
+    n = np.array([50])
+    gam, c, L, h, _ = O.calib_search(lambda G, C: (np.log(C.astype(np.float64)) - 1.0) ** 2
+                                     + (G[:, 0].astype(np.float64) - 3.0) ** 2, n, (0.5, 2.0, 0.1, 10.0), 1.0, 0.5, 30)
+    assert gam[0] == F32(1.0) and abs(np.log(float(c)) - 1.0) < 1e-3
