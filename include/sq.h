@@ -247,6 +247,46 @@ sq_status sq_calib_objective(const uint16_t* x, int32_t M, const int32_t* tok2st
                              const double* omega, double* objective, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/* Constrained search for (gamma*, c*) of Eq. 9 under the constraints of
+ * Sec. 4.3 and App. C.1: gamma_min <= gamma_s <= gamma_max for every stream,
+ * clip_min <= c <= clip_max and sum_s n_s log gamma_s = 0.  The paper names
+ * no optimizer; this one is a compass search in log coordinates
+ * (log gamma_1 .. log gamma_S, log c) started at gamma = 1 (which meets every
+ * constraint) and c = clip_init clamped to its bounds, with step log_step.
+ * Each round tries, for every coordinate in turn (the S gains, then c), a
+ * step of +h and of -h: 2 (S + 1) candidates.  A gain step is mapped back
+ * onto the constraint set by the nearest point in the token-weighted norm
+ * sum_s n_s (u_s - v_s)^2 (u_s = clamp(v_s - lambda), lambda found by 64
+ * bisection halvings in fp64; a stream without tokens is only clamped); a
+ * threshold step is clamped.  Gains and thresholds are evaluated as fp32
+ * values exp(.) clamped to the bounds.  The first candidate with the smallest
+ * objective replaces the incumbent when strictly better; otherwise h halves.
+ * Everything, including the search state, stays on the device: the call
+ * enqueues `rounds` rounds and returns without synchronizing. */
+typedef struct sq_calib_search_params {
+  float gamma_min, gamma_max; /* 0 < gamma_min <= 1 <= gamma_max */
+  float clip_min, clip_max;   /* 0 < clip_min <= clip_max */
+  float clip_init;            /* start threshold (finite) */
+  float log_step;             /* initial step h > 0 in log space */
+  int32_t rounds;             /* 0 .. 1024 (0: evaluate the start only) */
+} sq_calib_search_params;
+
+/* Workspace bytes for sq_calib_search (1 <= num_streams <= 64); 0 for
+ * invalid arguments.  Host-only. */
+size_t sq_calib_search_workspace_bytes(int32_t M, int32_t K, int32_t N, int32_t act_bits, int32_t num_streams);
+
+/* Arguments as for sq_calib_objective; params is a host struct.  Outputs
+ * (device): gamma_out fp32 [num_streams], clip_out fp32 [1] and
+ * objective_out fp64 [1], the best point found and its objective, which is
+ * bit-identical to what sq_calib_objective returns for that point.  The
+ * outputs also hold the incumbent during the search.  Non-finite or
+ * inconsistent bounds return SQ_ERR_UNSUPPORTED. */
+sq_status sq_calib_search(const uint16_t* x, int32_t M, const int32_t* tok2stream, int32_t num_streams,
+                          const float* dinv, int32_t act_bits, const sq_weight* w, const double* y_ref,
+                          const double* omega, const sq_calib_search_params* params, float* gamma_out,
+                          float* clip_out, double* objective_out, void* workspace, size_t workspace_bytes,
+                          hipStream_t stream);
+
 /* Measurement hook: the int8 matrix-core rate the GPU sustains, as a
  * ceiling beside the published peak.  Launches sq_probe_mfma_i8_sink_bytes()
  * / 1024 workgroups (two per CU) whose waves each issue iters * 16

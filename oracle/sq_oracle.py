@@ -381,8 +381,11 @@ def project_log_gains(v, counts, lo, hi, iters=64):
     if not live.any():
         return np.clip(v, lo, hi)
 
-    def f(lam):
-        return float(np.sum(n[live] * np.clip(v[live] - lam, lo, hi)))
+    def f(lam):   # summed stream by stream, in order
+        t = 0.0
+        for s in np.flatnonzero(live):
+            t += float(n[s]) * min(max(float(v[s]) - lam, lo), hi)
+        return t
 
     a = float(v[live].min()) - hi   # f(a) = N * hi >= 0
     b = float(v[live].max()) - lo   # f(b) = N * lo <= 0

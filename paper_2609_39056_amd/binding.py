@@ -62,6 +62,18 @@ class sq_weight(ctypes.Structure):
     ]
 
 
+class sq_calib_search_params(ctypes.Structure):
+    _fields_ = [
+        ("gamma_min", ctypes.c_float),
+        ("gamma_max", ctypes.c_float),
+        ("clip_min", ctypes.c_float),
+        ("clip_max", ctypes.c_float),
+        ("clip_init", ctypes.c_float),
+        ("log_step", ctypes.c_float),
+        ("rounds", ctypes.c_int32),
+    ]
+
+
 _P = ctypes.c_void_p
 _I = ctypes.c_int32
 _S = ctypes.c_size_t
@@ -81,6 +93,9 @@ _SIGS = {
     "sq_calib_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
     "sq_calib_objective": (_I, [_P, _I, _P, _I, _P, _I, ctypes.POINTER(sq_weight), _P, _I, _P, _P, _P, _P, _P, _S,
                                 _P]),
+    "sq_calib_search_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
+    "sq_calib_search": (_I, [_P, _I, _P, _I, _P, _I, ctypes.POINTER(sq_weight), _P, _P,
+                             ctypes.POINTER(sq_calib_search_params), _P, _P, _P, _P, _S, _P]),
     "sq_probe_mfma_i8_sink_bytes": (_S, []),
     "sq_probe_mfma_i8": (_I, [_I, _I, _I, _P, _S, _P]),
 }
@@ -265,6 +280,23 @@ def sq_calib_objective(x: torch.Tensor, tok2stream: torch.Tensor, num_streams: i
     _check(lib().sq_calib_objective(_ptr(x), M, _ptr(tok2stream), num_streams, _ptr(dinv), act_bits,
                                     ctypes.byref(ws), _ptr(y_ref), C, _ptr(cand_gamma), _ptr(cand_clip),
                                     _ptr(omega), _ptr(objective), wp, wb, _stream(stream)), "sq_calib_objective")
+
+
+def sq_calib_search_workspace_bytes(M: int, K: int, N: int, act_bits: int, num_streams: int) -> int:
+    return int(lib().sq_calib_search_workspace_bytes(M, K, N, act_bits, num_streams))
+
+
+def sq_calib_search(x: torch.Tensor, tok2stream: torch.Tensor, num_streams: int, dinv: Optional[torch.Tensor],
+                    act_bits: int, w: Weight, y_ref: torch.Tensor, omega: torch.Tensor,
+                    params: sq_calib_search_params, gamma_out: torch.Tensor, clip_out: torch.Tensor,
+                    objective_out: torch.Tensor, workspace: torch.Tensor, stream=None) -> None:
+    """Constrained compass search for Eq. (9)'s (gamma*, c*) (include/sq.h)."""
+    M = x.shape[0]
+    ws = w.struct()
+    wp, wb = _ws(workspace)
+    _check(lib().sq_calib_search(_ptr(x), M, _ptr(tok2stream), num_streams, _ptr(dinv), act_bits, ctypes.byref(ws),
+                                 _ptr(y_ref), _ptr(omega), ctypes.byref(params), _ptr(gamma_out), _ptr(clip_out),
+                                 _ptr(objective_out), wp, wb, _stream(stream)), "sq_calib_search")
 
 
 # ------------------------------------------------------------------ helpers

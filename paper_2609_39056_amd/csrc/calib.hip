@@ -181,7 +181,140 @@ __global__ __launch_bounds__(256) void calib_sum_kernel(const double* __restrict
   if (threadIdx.x == 0) *out = (part[0] + part[1]) + (part[2] + part[3]);
 }
 
+// ---------------------------------------------------------------- constrained search
+// Compass search over (log gamma_1 .. log gamma_S, log c).  State in device
+// memory: st = {unused, h, log c}, u = the incumbent's log gains, and the
+// caller's gamma / clip / objective outputs hold the incumbent's evaluated
+// values.  Candidate j of a round moves coordinate j/2 (the gains, then the
+// threshold) by +h (j even) or -h (j odd).
+
+__device__ __forceinline__ double clampd(double v, double lo, double hi) { return fmin(fmax(v, lo), hi); }
+__device__ __forceinline__ float clampf_(float v, float lo, float hi) { return fminf(fmaxf(v, lo), hi); }
+
+__global__ __launch_bounds__(64) void calib_search_init_kernel(SearchBounds b, int32_t S, double* st, double* u,
+                                                               float* gamma, float* clip) {
+  for (int32_t s = threadIdx.x; s < S; s += 64) {
+    u[s] = 0.0;
+    gamma[s] = 1.0f;
+  }
+  if (threadIdx.x == 0) {
+    const float c = clampf_(b.clip_init, b.clip_min, b.clip_max);
+    clip[0] = c;
+    st[0] = 0.0;
+    st[1] = static_cast<double>(b.log_step);
+    st[2] = log(static_cast<double>(c));
+  }
+}
+
+// One thread per candidate (C = 2 (S + 1) <= 256).  A gain step is projected
+// onto lo <= u_s <= hi, sum_s n_s u_s = 0 (nearest point in the token-
+// weighted norm: u_s = clamp(w_s - lam) for streams with tokens, lam by 64
+// bisection halvings in fp64); a threshold step is clamped to the log bounds.
+__global__ __launch_bounds__(256) void calib_propose_kernel(SearchBounds b, int32_t S, const int32_t* counts,
+                                                            const double* st, const double* u, double* cand_u,
+                                                            double* cand_v, float* cand_gamma, float* cand_clip) {
+  const int32_t C = 2 * (S + 1);
+  const int32_t j = threadIdx.x;
+  if (j >= C) return;
+  const int32_t d = j >> 1;
+  const double step = (j & 1) ? -st[1] : st[1];
+  const double lo = log(static_cast<double>(b.gamma_min)), hi = log(static_cast<double>(b.gamma_max));
+  double* uj = cand_u + static_cast<size_t>(j) * S;
+  double vc = st[2];
+  if (d < S) {
+    bool any = false;
+    double wmin = 0.0, wmax = 0.0;
+    for (int32_t s = 0; s < S; ++s) {
+      const double w = u[s] + (s == d ? step : 0.0);
+      if (counts[s] > 0) {
+        wmin = any ? fmin(wmin, w) : w;
+        wmax = any ? fmax(wmax, w) : w;
+        any = true;
+      }
+    }
+    double lam = 0.0;
+    if (any) {
+      double a = wmin - hi, c = wmax - lo;
+      for (int it = 0; it < 64; ++it) {
+        const double mid = 0.5 * (a + c);
+        double f = 0.0;
+        for (int32_t s = 0; s < S; ++s) {
+          if (counts[s] <= 0) continue;
+          const double w = u[s] + (s == d ? step : 0.0);
+          f += static_cast<double>(counts[s]) * clampd(w - mid, lo, hi);
+        }
+        if (f > 0.0)
+          a = mid;
+        else
+          c = mid;
+      }
+      lam = 0.5 * (a + c);
+    }
+    for (int32_t s = 0; s < S; ++s) {
+      const double w = u[s] + (s == d ? step : 0.0);
+      uj[s] = counts[s] > 0 ? clampd(w - lam, lo, hi) : clampd(w, lo, hi);
+    }
+  } else {
+    for (int32_t s = 0; s < S; ++s) uj[s] = u[s];
+    vc = clampd(vc + step, log(static_cast<double>(b.clip_min)), log(static_cast<double>(b.clip_max)));
+  }
+  for (int32_t s = 0; s < S; ++s)
+    cand_gamma[static_cast<size_t>(j) * S + s] =
+        clampf_(static_cast<float>(exp(uj[s])), b.gamma_min, b.gamma_max);
+  cand_v[j] = vc;
+  cand_clip[j] = clampf_(static_cast<float>(exp(vc)), b.clip_min, b.clip_max);
+}
+
+// The first candidate with the smallest objective replaces the incumbent if
+// strictly better; otherwise the step halves.
+__global__ __launch_bounds__(64) void calib_select_kernel(int32_t S, const double* cand_obj, const double* cand_u,
+                                                          const double* cand_v, const float* cand_gamma,
+                                                          const float* cand_clip, double* st, double* u,
+                                                          float* gamma, float* clip, double* objective) {
+  const int32_t C = 2 * (S + 1);
+  int32_t best = 0;
+  for (int32_t j = 1; j < C; ++j)
+    if (cand_obj[j] < cand_obj[best]) best = j;
+  const bool better = cand_obj[best] < objective[0];
+  __syncthreads();  // every thread has read objective[0] before it changes
+  if (better) {
+    for (int32_t s = threadIdx.x; s < S; s += 64) {
+      u[s] = cand_u[static_cast<size_t>(best) * S + s];
+      gamma[s] = cand_gamma[static_cast<size_t>(best) * S + s];
+    }
+    if (threadIdx.x == 0) {
+      st[2] = cand_v[best];
+      clip[0] = cand_clip[best];
+      objective[0] = cand_obj[best];
+    }
+  } else if (threadIdx.x == 0) {
+    st[1] = 0.5 * st[1];
+  }
+}
+
 }  // namespace
+
+hipError_t launch_calib_search_init(const SearchBounds& b, int32_t S, double* st, double* u, float* gamma,
+                                    float* clip, hipStream_t s) {
+  hipLaunchKernelGGL(calib_search_init_kernel, dim3(1), dim3(64), 0, s, b, S, st, u, gamma, clip);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_propose(const SearchBounds& b, int32_t S, const int32_t* counts, const double* st,
+                                const double* u, double* cand_u, double* cand_v, float* cand_gamma,
+                                float* cand_clip, hipStream_t s) {
+  hipLaunchKernelGGL(calib_propose_kernel, dim3(1), dim3(256), 0, s, b, S, counts, st, u, cand_u, cand_v,
+                     cand_gamma, cand_clip);
+  return hipGetLastError();
+}
+
+hipError_t launch_calib_select(int32_t S, const double* cand_obj, const double* cand_u, const double* cand_v,
+                               const float* cand_gamma, const float* cand_clip, double* st, double* u,
+                               float* gamma, float* clip, double* objective, hipStream_t s) {
+  hipLaunchKernelGGL(calib_select_kernel, dim3(1), dim3(64), 0, s, S, cand_obj, cand_u, cand_v, cand_gamma,
+                     cand_clip, st, u, gamma, clip, objective);
+  return hipGetLastError();
+}
 
 hipError_t launch_calib_reference(const CalibRefArgs& a, hipStream_t s) {
   const int32_t tiles_n = (a.N + kRefTile - 1) / kRefTile;

@@ -3,6 +3,7 @@
 #include <stdint.h>
 
 #include <algorithm>
+#include <cmath>
 
 #include "sq_internal.h"
 
@@ -104,9 +105,38 @@ size_t fused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
 // calibration workspace: the fused linear's | y of one candidate fp32 [M][N] |
 // per-row errors fp64 [M] | stream counts int32 [S]
 constexpr int32_t kCalibMaxCandidates = 1 << 16;
+constexpr int32_t kCalibSearchMaxRounds = 1024;
 size_t calib_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits, int32_t S) {
   return fused_ws_bytes(M, K, N, bits) + round_up(static_cast<size_t>(M) * N * 4) +
          round_up(static_cast<size_t>(M) * 8) + round_up(static_cast<size_t>(S) * 4);
+}
+
+// search state after the calibration workspace: st fp64 [4] | u fp64 [S] |
+// candidates' log gains fp64 [C][S] | log thresholds fp64 [C] | objectives
+// fp64 [C] | gains fp32 [C][S] | thresholds fp32 [C], C = 2 (S + 1)
+struct SearchWs {
+  double *st, *u, *cand_u, *cand_v, *cand_obj;
+  float *cand_gamma, *cand_clip;
+};
+size_t search_extra_bytes(int32_t S, SearchWs* out = nullptr, uint8_t* base = nullptr) {
+  const size_t C = 2 * (static_cast<size_t>(S) + 1);
+  const size_t parts[7] = {4 * 8, S * 8ull, C * S * 8, C * 8, C * 8, C * S * 4, C * 4};
+  size_t off = 0;
+  void* ptr[7];
+  for (int i = 0; i < 7; ++i) {
+    ptr[i] = base + off;
+    off += round_up(parts[i]);
+  }
+  if (out != nullptr) {
+    out->st = static_cast<double*>(ptr[0]);
+    out->u = static_cast<double*>(ptr[1]);
+    out->cand_u = static_cast<double*>(ptr[2]);
+    out->cand_v = static_cast<double*>(ptr[3]);
+    out->cand_obj = static_cast<double*>(ptr[4]);
+    out->cand_gamma = static_cast<float*>(ptr[5]);
+    out->cand_clip = static_cast<float*>(ptr[6]);
+  }
+  return off;
 }
 
 size_t unfused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
@@ -179,6 +209,64 @@ sq_status linear_fused(int32_t bits, const uint16_t* x, int32_t M, const sq_act_
   GemmArgs g = gemm_args(f.qx, f.scale, M, act, w, y, out_dtype);
   g.kc = f.kc;
   return hip_status(launch_gemm(bits, kEpiOut, g, stream, f.partial, f.partial_bytes));
+}
+
+// One candidate of Eq. 9: the fused linear in STATIC mode with one-step
+// tables (gamma [S], clip [1], both device pointers) and no bias into fp32,
+// then the weighted squared error against y_ref into *out.
+struct CalibEval {
+  const uint16_t* x;
+  int32_t M, S, act_bits;
+  const int32_t* tok2stream;
+  const float* dinv;
+  sq_weight wt;
+  const double* y_ref;
+  const double* omega;
+  void* fused_ws;
+  size_t fused_bytes;
+  float* yq;
+  double* err;
+  int32_t* counts;
+};
+
+CalibEval calib_eval_setup(const uint16_t* x, int32_t M, const int32_t* tok2stream, int32_t S, const float* dinv,
+                           int32_t act_bits, const sq_weight* w, const double* y_ref, const double* omega,
+                           void* workspace) {
+  CalibEval e;
+  e.x = x;
+  e.M = M;
+  e.S = S;
+  e.act_bits = act_bits;
+  e.tok2stream = tok2stream;
+  e.dinv = dinv;
+  e.wt = *w;
+  e.wt.bias = nullptr;  // the bias is on both sides of Eq. 9 and cancels
+  e.y_ref = y_ref;
+  e.omega = omega;
+  uint8_t* p = static_cast<uint8_t*>(workspace);
+  e.fused_ws = p;
+  e.fused_bytes = fused_ws_bytes(M, w->K, w->N, act_bits);
+  e.yq = reinterpret_cast<float*>(p + e.fused_bytes);
+  e.err = reinterpret_cast<double*>(p + e.fused_bytes + round_up(static_cast<size_t>(M) * w->N * 4));
+  e.counts = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(e.err) + round_up(static_cast<size_t>(M) * 8));
+  return e;
+}
+
+sq_status calib_eval(const CalibEval& e, const float* gamma, const float* clip, double* out, hipStream_t stream) {
+  sq_act_params a{};
+  a.tok2stream = e.tok2stream;
+  a.gamma = gamma;
+  a.clip = clip;
+  a.dinv = e.dinv;
+  a.num_streams = e.S;
+  a.num_steps = 1;
+  a.step = 0;
+  a.range_mode = SQ_RANGE_STATIC;
+  a.act_bits = e.act_bits;
+  sq_status st = linear_fused(e.act_bits, e.x, e.M, &a, &e.wt, e.yq, SQ_OUT_F32, e.fused_ws, e.fused_bytes, stream);
+  if (st != SQ_OK) return st;
+  return hip_status(launch_calib_error(e.yq, e.y_ref, e.tok2stream, e.counts, e.omega, e.M, e.wt.N, e.S, e.err,
+                                       out, stream));
 }
 
 }  // namespace
@@ -364,32 +452,74 @@ sq_status sq_calib_objective(const uint16_t* x, int32_t M, const int32_t* tok2st
   const int32_t K = w->K, N = w->N, S = num_streams;
   if (ws_bytes < calib_ws_bytes(M, K, N, act_bits, S)) return SQ_ERR_WORKSPACE;
 
-  const size_t fused_bytes = fused_ws_bytes(M, K, N, act_bits);
-  uint8_t* p = static_cast<uint8_t*>(workspace);
-  float* yq = reinterpret_cast<float*>(p + fused_bytes);
-  double* err = reinterpret_cast<double*>(p + fused_bytes + round_up(static_cast<size_t>(M) * N * 4));
-  int32_t* counts = reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(err) + round_up(static_cast<size_t>(M) * 8));
-  sq_weight wt = *w;
-  wt.bias = nullptr;  // the bias is on both sides of Eq. 9 and cancels
-  st = hip_status(launch_calib_counts(tok2stream, M, S, counts, stream));
+  CalibEval e = calib_eval_setup(x, M, tok2stream, S, dinv, act_bits, w, y_ref, omega, workspace);
+  st = hip_status(launch_calib_counts(tok2stream, M, S, e.counts, stream));
   if (st != SQ_OK) return st;
   for (int32_t c = 0; c < num_candidates; ++c) {
-    sq_act_params a{};
-    a.tok2stream = tok2stream;
-    a.gamma = cand_gamma + static_cast<size_t>(c) * S;
-    a.clip = cand_clip + c;
-    a.dinv = dinv;
-    a.num_streams = S;
-    a.num_steps = 1;
-    a.step = 0;
-    a.range_mode = SQ_RANGE_STATIC;
-    a.act_bits = act_bits;
-    st = linear_fused(act_bits, x, M, &a, &wt, yq, SQ_OUT_F32, workspace, fused_bytes, stream);
-    if (st != SQ_OK) return st;
-    st = hip_status(launch_calib_error(yq, y_ref, tok2stream, counts, omega, M, N, S, err, objective + c, stream));
+    st = calib_eval(e, cand_gamma + static_cast<size_t>(c) * S, cand_clip + c, objective + c, stream);
     if (st != SQ_OK) return st;
   }
   return SQ_OK;
+}
+
+sq_status sq_calib_search(const uint16_t* x, int32_t M, const int32_t* tok2stream, int32_t num_streams,
+                          const float* dinv, int32_t act_bits, const sq_weight* w, const double* y_ref,
+                          const double* omega, const sq_calib_search_params* params, float* gamma_out,
+                          float* clip_out, double* objective_out, void* workspace, size_t ws_bytes,
+                          hipStream_t stream) {
+  if (x == nullptr || tok2stream == nullptr || y_ref == nullptr || omega == nullptr || params == nullptr ||
+      gamma_out == nullptr || clip_out == nullptr || objective_out == nullptr || workspace == nullptr)
+    return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  if (act_bits != 8 && act_bits != 4) return SQ_ERR_UNSUPPORTED;
+  const sq_calib_search_params& p = *params;
+  if (!valid_m(M) || num_streams < 1 || num_streams > kCalibSearchMaxStreams || p.rounds < 0 ||
+      p.rounds > kCalibSearchMaxRounds)
+    return SQ_ERR_SHAPE;
+  const bool ok_bounds = std::isfinite(p.gamma_min) && std::isfinite(p.gamma_max) && std::isfinite(p.clip_min) &&
+                         std::isfinite(p.clip_max) && std::isfinite(p.clip_init) && std::isfinite(p.log_step) &&
+                         p.gamma_min > 0.0f && p.gamma_min <= 1.0f && p.gamma_max >= 1.0f && p.clip_min > 0.0f &&
+                         p.clip_min <= p.clip_max && p.log_step > 0.0f;
+  if (!ok_bounds) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(y_ref, 16) || !aligned(workspace, 16) || !aligned(tok2stream, 4) ||
+      !aligned(omega, 8) || !aligned(gamma_out, 4) || !aligned(clip_out, 4) || !aligned(objective_out, 8))
+    return SQ_ERR_ALIGN;
+  if (dinv != nullptr && !aligned(dinv, 16)) return SQ_ERR_ALIGN;
+  const int32_t S = num_streams;
+  const size_t base = calib_ws_bytes(M, w->K, w->N, act_bits, S);
+  if (ws_bytes < base + search_extra_bytes(S)) return SQ_ERR_WORKSPACE;
+
+  CalibEval e = calib_eval_setup(x, M, tok2stream, S, dinv, act_bits, w, y_ref, omega, workspace);
+  SearchWs sw;
+  search_extra_bytes(S, &sw, static_cast<uint8_t*>(workspace) + base);
+  const SearchBounds b{p.gamma_min, p.gamma_max, p.clip_min, p.clip_max, p.clip_init, p.log_step};
+  const int32_t C = 2 * (S + 1);
+  st = hip_status(launch_calib_counts(tok2stream, M, S, e.counts, stream));
+  if (st != SQ_OK) return st;
+  st = hip_status(launch_calib_search_init(b, S, sw.st, sw.u, gamma_out, clip_out, stream));
+  if (st != SQ_OK) return st;
+  st = calib_eval(e, gamma_out, clip_out, objective_out, stream);
+  if (st != SQ_OK) return st;
+  for (int32_t r = 0; r < p.rounds; ++r) {
+    st = hip_status(launch_calib_propose(b, S, e.counts, sw.st, sw.u, sw.cand_u, sw.cand_v, sw.cand_gamma,
+                                         sw.cand_clip, stream));
+    if (st != SQ_OK) return st;
+    for (int32_t c = 0; c < C; ++c) {
+      st = calib_eval(e, sw.cand_gamma + static_cast<size_t>(c) * S, sw.cand_clip + c, sw.cand_obj + c, stream);
+      if (st != SQ_OK) return st;
+    }
+    st = hip_status(launch_calib_select(S, sw.cand_obj, sw.cand_u, sw.cand_v, sw.cand_gamma, sw.cand_clip, sw.st,
+                                        sw.u, gamma_out, clip_out, objective_out, stream));
+    if (st != SQ_OK) return st;
+  }
+  return SQ_OK;
+}
+
+size_t sq_calib_search_workspace_bytes(int32_t M, int32_t K, int32_t N, int32_t act_bits, int32_t num_streams) {
+  if (num_streams > kCalibSearchMaxStreams) return 0;
+  const size_t base = sq_calib_workspace_bytes(M, K, N, act_bits, num_streams);
+  return base == 0 ? 0 : base + search_extra_bytes(num_streams);
 }
 
 size_t sq_probe_mfma_i8_sink_bytes(void) { return static_cast<size_t>(mfma_probe_workgroups()) * 256 * 4; }

@@ -183,6 +183,21 @@ hipError_t launch_calib_error(const float* yq, const double* ref, const int32_t*
                               const int32_t* counts, const double* omega, int32_t M, int32_t N, int32_t S,
                               double* err, double* out, hipStream_t s);
 
+// constrained compass search for Eq. 9 (at most kCalibSearchMaxStreams
+// streams: one thread per candidate, 2 (S + 1) of them)
+constexpr int32_t kCalibSearchMaxStreams = 64;
+struct SearchBounds {
+  float gamma_min, gamma_max, clip_min, clip_max, clip_init, log_step;
+};
+hipError_t launch_calib_search_init(const SearchBounds& b, int32_t S, double* st, double* u, float* gamma,
+                                    float* clip, hipStream_t s);
+hipError_t launch_calib_propose(const SearchBounds& b, int32_t S, const int32_t* counts, const double* st,
+                                const double* u, double* cand_u, double* cand_v, float* cand_gamma,
+                                float* cand_clip, hipStream_t s);
+hipError_t launch_calib_select(int32_t S, const double* cand_obj, const double* cand_u, const double* cand_v,
+                               const float* cand_gamma, const float* cand_clip, double* st, double* u,
+                               float* gamma, float* clip, double* objective, hipStream_t s);
+
 // matrix-core rate probe (measurement hook)
 int mfma_probe_workgroups();
 hipError_t launch_mfma_probe(int32_t* sink, int32_t iters, int32_t random, int32_t fold, hipStream_t s);

@@ -200,3 +200,42 @@ def test_calib_reference_rejects_and_sizes(L):
     assert B.sq_calib_workspace_bytes(M, K, N, 8, 4097) == 0
     assert B.sq_calib_workspace_bytes(M, K, 100, 8, 3) == 0
     assert B.sq_calib_workspace_bytes(M, K, N, 6, 3) == 0
+
+
+def search(L, x=A, M=88, t2s=A, S=3, dinv=None, bits=8, w=None, ref=A, om=A, p=None, g=A, c=A, obj=A, ws=A,
+           nbytes=1 << 30):
+    w = wt() if w is None else w
+    if p is None:
+        p = B.sq_calib_search_params(0.5, 2.0, 0.1, 10.0, 1.0, 0.5, 4)
+    return L.sq_calib_search(x, M, t2s, S, dinv, bits, ctypes.byref(w), ref, om, ctypes.byref(p) if p else None,
+                             g, c, obj, ws, nbytes, None)
+
+
+def _sp(**kw):
+    d = dict(gamma_min=0.5, gamma_max=2.0, clip_min=0.1, clip_max=10.0, clip_init=1.0, log_step=0.5, rounds=4)
+    d.update(kw)
+    return B.sq_calib_search_params(**d)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(x=None), NULL), (dict(t2s=None), NULL), (dict(ref=None), NULL), (dict(om=None), NULL), (dict(p=False), NULL),
+    (dict(g=None), NULL), (dict(c=None), NULL), (dict(obj=None), NULL), (dict(ws=None), NULL), (dict(bits=6), UNSUP),
+    (dict(M=0), SHAPE), (dict(S=0), SHAPE), (dict(S=65), SHAPE), (dict(p=_sp(rounds=-1)), SHAPE),
+    (dict(p=_sp(rounds=1025)), SHAPE), (dict(p=_sp(gamma_min=0.0)), UNSUP), (dict(p=_sp(gamma_min=1.5)), UNSUP),
+    (dict(p=_sp(gamma_max=0.9)), UNSUP), (dict(p=_sp(clip_min=0.0)), UNSUP), (dict(p=_sp(clip_max=0.05)), UNSUP),
+    (dict(p=_sp(log_step=0.0)), UNSUP), (dict(p=_sp(clip_init=float("inf"))), UNSUP),
+    (dict(p=_sp(gamma_max=float("nan"))), UNSUP), (dict(x=A + 2), ALIGN), (dict(ref=A + 8), ALIGN),
+    (dict(om=A + 4), ALIGN), (dict(g=A + 2), ALIGN), (dict(obj=A + 4), ALIGN), (dict(nbytes=4096), WS),
+    (dict(w=wt(K=200)), SHAPE),
+])
+def test_calib_search_rejects(L, kw, code):
+    assert search(L, **kw) == code
+
+
+def test_calib_search_workspace(L):
+    M, K, N = 1000, 2048, 4096
+    for S in (1, 3, 64):
+        n = B.sq_calib_search_workspace_bytes(M, K, N, 8, S)
+        assert n > B.sq_calib_workspace_bytes(M, K, N, 8, S) and n % 256 == 0
+    assert B.sq_calib_search_workspace_bytes(M, K, N, 8, 65) == 0
+    assert B.sq_calib_search_workspace_bytes(M, K, N, 8, 0) == 0

@@ -185,3 +185,118 @@ def test_calib_objective_larger(bits):
                              dinv=L.dinv, act_bits=bits, ref=ref)
     bound = objective_bound(L, pw, G, bits, gammas, clips, omega, ref, abs_reference(L, pw, G), 3)
     check_objectives(got, want, bound)
+
+
+# ---------------------------------------------------------------- constrained search
+def gpu_search(L, W, bits, omega, ref, bounds, clip_init, log_step, rounds, S=None):
+    M, K, N = L.x_bits.shape[0], W.K, W.N
+    S = L.gamma.shape[1] if S is None else S
+    ws = torch.empty(B.sq_calib_search_workspace_bytes(M, K, N, bits, S), dtype=torch.uint8, device="cuda")
+    g = torch.full((S,), float("nan"), dtype=torch.float32, device="cuda")
+    c = torch.full((1,), float("nan"), dtype=torch.float32, device="cuda")
+    obj = torch.full((1,), float("nan"), dtype=torch.float64, device="cuda")
+    p = B.sq_calib_search_params(*[float(b) for b in bounds], float(clip_init), float(log_step), rounds)
+    B.sq_calib_search(u16_to_dev(L.x_bits, torch.bfloat16), i32_to_dev(L.tok2stream), S, f32_to_dev(L.dinv), bits,
+                      W, ref, torch.as_tensor(np.asarray(omega, dtype=np.float64), device="cuda"), p, g, c, obj, ws)
+    torch.cuda.synchronize()
+    return g.cpu().numpy(), F32(c.cpu().numpy()[0]), float(obj.cpu().numpy()[0])
+
+
+def check_constraints(gam, c, counts, bounds):
+    g_min, g_max, c_min, c_max = (F32(b) for b in bounds)
+    assert np.all(gam >= g_min) and np.all(gam <= g_max) and c_min <= c <= c_max
+    lg = np.log(gam.astype(np.float64))
+    # each fp32 gain carries a rounding of 2^-24 relative: |log| moves by <= 2^-24
+    assert abs((counts * lg).sum()) <= counts.sum() * (2.0**-23 + 1e-12)
+
+
+@pytest.mark.parametrize("bits,M,counts", [(8, 200, (140, 20, 40)), (4, 200, (140, 20, 40)),
+                                           (8, 37, (25, 4, 8)), (4, 96, (60, 0, 20, 16))])
+def test_calib_search_matches_oracle(bits, M, counts):
+    """The GPU search against the oracle's compass search on the same layer:
+    when every decision of the oracle's run (which candidate is smallest,
+    whether it beats the incumbent) is separated by more than the objective's
+    error bound, the GPU takes the same path and returns the same fp32 point;
+    in every case the result meets the constraints, its objective is the
+    GPU's sq_calib_objective of that point, and the oracle's objective of it
+    is no worse than the start's.  Includes a stream without tokens."""
+    K, N, G = 256, 128, 128
+    L = synth.make_layer(K=K, N=N, stream_counts=counts, T=2, seed=[50, bits, M], permute=True)
+    S = L.gamma.shape[1]
+    n = np.bincount(L.tok2stream, minlength=S)
+    pw, W = weight(L, G)
+    ref_dev = gpu_reference(L, W)
+    ref = O.calib_reference(L.x_bits, pw["codes"], pw["w_scale"], G, L.dinv)
+    ref_abs = abs_reference(L, pw, G)
+    omega = np.full(S, 1.0 / S)
+    bounds = (0.5, 2.0, float(L.clip[0]) / 8, float(L.clip[0]) * 2)
+    bounds = tuple(float(F32(b)) for b in bounds)
+    rounds = 6
+
+    def f(Gm, Cm):
+        return O.calib_objective(L.x_bits, L.tok2stream, S, pw["codes"], pw["w_scale"], G, Gm, Cm, omega,
+                                 dinv=L.dinv, act_bits=bits, ref=ref)
+
+    g_or, c_or, L_or, h_or, trace = O.calib_search(f, n, bounds, L.clip[0], 0.5, rounds)
+    g_gpu, c_gpu, L_gpu = gpu_search(L, W, bits, omega, ref_dev, bounds, L.clip[0], 0.5, rounds)
+    check_constraints(g_gpu, c_gpu, n, bounds)
+    # the returned objective is the evaluator's for the returned point
+    again = gpu_objective(L, W, bits, g_gpu[None, :], np.array([c_gpu]), omega, ref_dev)
+    assert again.view(np.uint64)[0] == np.float64(L_gpu).view(np.uint64)
+    start = f(np.ones((1, S), F32), np.array([np.clip(F32(L.clip[0]), F32(bounds[2]), F32(bounds[3]))]))[0]
+    got_or = f(g_gpu[None, :], np.array([c_gpu]))[0]
+    b_pt = objective_bound(L, pw, G, bits, g_gpu[None, :], np.array([c_gpu]), omega, ref, ref_abs, S)[0]
+    assert got_or <= start + b_pt
+    assert abs(L_gpu - got_or) <= b_pt + 1e-12 * got_or
+
+    # separated decisions: replay the oracle's rounds with the bound of every candidate
+    c0 = np.clip(F32(L.clip[0]), F32(bounds[2]), F32(bounds[3]))
+    u, vc, h = np.zeros(S), float(np.log(np.float64(c0))), 0.5
+    inc_b = objective_bound(L, pw, G, bits, np.ones((1, S), F32), np.array([c0]), omega, ref, ref_abs, S)[0]
+    separated = True
+    inc_g, inc_c = np.ones(S, F32), c0
+    for L_inc, obj in trace:
+        Gm, Cm, U, V = O.compass_candidates(u, vc, h, n, bounds)
+        bd = objective_bound(L, pw, G, bits, Gm, Cm, omega, ref, ref_abs, S)
+        j = int(np.argmin(obj))
+        # points that differ only in the gains of streams without tokens give
+        # bit-identical outputs, hence equal objectives, on both sides
+        live = n > 0
+        for k in range(len(obj)):
+            same = np.array_equal(Gm[k][live], Gm[j][live]) and Cm[k] == Cm[j]
+            if k != j and not same and obj[k] - obj[j] <= bd[k] + bd[j]:
+                separated = False
+        same_as_inc = np.array_equal(Gm[j][live], inc_g[live]) and Cm[j] == inc_c
+        if not same_as_inc and abs(obj[j] - L_inc) <= bd[j] + inc_b:
+            separated = False
+        if obj[j] < L_inc:
+            u, vc, inc_b, inc_g, inc_c = U[j], float(V[j]), bd[j], Gm[j], Cm[j]
+        else:
+            h = 0.5 * h
+    if separated:
+        assert np.array_equal(g_gpu, g_or) and c_gpu == c_or, (g_gpu, g_or, c_gpu, c_or)
+        assert abs(L_gpu - L_or) <= inc_b + 1e-12 * L_or
+    print(f"separated={separated} L_gpu={L_gpu} L_or={L_or} start={start}")
+
+
+def test_calib_search_start_and_single_stream():
+    """rounds = 0 evaluates the start (gamma = 1, c = clip_init clamped); with
+    one stream the constraint pins gamma to 1 and only c moves."""
+    K, N, G, bits = 256, 64, 128, 8
+    L = synth.make_layer(K=K, N=N, stream_counts=(48, 16, 8), T=1, seed=51, permute=True)
+    pw, W = weight(L, G)
+    ref_dev = gpu_reference(L, W)
+    bounds = (0.5, 2.0, 0.25, 4.0)
+    g, c, obj = gpu_search(L, W, bits, np.full(3, 1 / 3), ref_dev, bounds, 100.0, 0.5, 0)
+    assert np.all(g == 1.0) and c == F32(4.0)
+    want = gpu_objective(L, W, bits, np.ones((1, 3), F32), np.array([4.0], F32), np.full(3, 1 / 3), ref_dev)[0]
+    assert np.float64(obj).view(np.uint64) == want.view(np.uint64)
+    L1 = synth.make_layer(K=K, N=N, stream_counts=(64,), T=1, seed=52)
+    pw1, W1 = weight(L1, G)
+    ref1 = gpu_reference(L1, W1)
+    g1, c1, o1 = gpu_search(L1, W1, bits, np.ones(1), ref1, (0.5, 2.0, float(L1.clip[0]) / 4, float(L1.clip[0]) * 2),
+                            L1.clip[0], 0.5, 5)
+    assert g1[0] == F32(1.0)
+    start = gpu_objective(L1, W1, bits, np.ones((1, 1), F32),
+                          np.array([np.clip(L1.clip[0], F32(L1.clip[0] / 4), F32(L1.clip[0] * 2))]), np.ones(1), ref1)
+    assert o1 <= start[0]
