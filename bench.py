@@ -315,6 +315,103 @@ def run_suite(args):
     fout.close()
 
 
+PEAK_FP64_TFLOPS = 78.6     # MI355X fp64 (vector and matrix), 78.6 TFLOP/s
+CALIB_CANDIDATES = 16
+CALIB_ROUNDS = 8
+
+
+def calibration_figures(torch, B, ly, stream, dev, cpu_rows):
+    """The calibration path of Eq. (9) on the up projection (2048 -> 8192,
+    one weight step per output channel as in the paper's calibration setup)
+    over one batch of M tokens: the fp64 target X~ W^ (once per linear), the
+    objective of a batch of candidates (each: the fused linear in STATIC mode,
+    fp32 out, then the weighted squared error), the fused linear alone on the
+    same tables, and the constrained search.  HIP events on the stream the
+    kernels run on."""
+    L, W = ly["L"], ly["W_pc"]
+    M, K, N = L.M, ly["K"], ly["N"]
+    S = L.gamma.shape[1]
+    x, t2s, dinv = ly["x"], ly["acts"][8].tok2stream, ly["acts"][8].dinv
+    rng = np.random.default_rng(7)
+    gam = (L.gamma[rng.integers(0, L.gamma.shape[0], CALIB_CANDIDATES)]
+           * rng.lognormal(0.0, 0.2, (CALIB_CANDIDATES, S))).astype(np.float32)
+    clip = (L.clip[0] * rng.lognormal(0.0, 0.3, CALIB_CANDIDATES)).astype(np.float32)
+    gam_d, clip_d = torch.from_numpy(gam).to(dev), torch.from_numpy(clip).to(dev)
+    omega = torch.full((S,), 1.0 / S, dtype=torch.float64, device=dev)
+    ref = torch.empty((M, N), dtype=torch.float64, device=dev)
+    obj = torch.empty((CALIB_CANDIDATES,), dtype=torch.float64, device=dev)
+    ws = torch.empty(B.sq_calib_search_workspace_bytes(M, K, N, 8, S), dtype=torch.uint8, device=dev)
+
+    def timed(fn, reps):
+        fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps  # ms
+
+    ms_ref = timed(lambda: B.sq_calib_reference(x, dinv, W, ref, stream), 3)
+    ms_obj = timed(lambda: B.sq_calib_objective(x, t2s, S, dinv, 8, W, ref, gam_d, clip_d, omega, obj, ws, stream),
+                   3) / CALIB_CANDIDATES
+    y32 = torch.empty((M, N), dtype=torch.float32, device=dev)
+    wsf = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, K, N, 8, dev)
+    Wnb = B.Weight(qw=W.qw, w_scale=W.w_scale, w_group=W.w_group, bias=None)
+    act1 = B.ActParams(tok2stream=t2s, gamma=gam_d[:1], step=0, act_bits=8, range_mode=B.SQ_RANGE_STATIC,
+                       clip=clip_d[:1], dinv=dinv)
+    ms_lin = timed(lambda: B.sq_linear_w4a8(x, act1, Wnb, y32, B.SQ_OUT_F32, wsf, stream), 3 * CALIB_CANDIDATES)
+    del y32, wsf
+    params = B.sq_calib_search_params(0.25, 4.0, float(L.clip[0]) / 8, float(L.clip[0]) * 4, float(L.clip[0]), 0.5,
+                                      CALIB_ROUNDS)
+    g_out = torch.empty((S,), dtype=torch.float32, device=dev)
+    c_out = torch.empty((1,), dtype=torch.float32, device=dev)
+    o_out = torch.empty((1,), dtype=torch.float64, device=dev)
+    ms_search = timed(lambda: B.sq_calib_search(x, t2s, S, dinv, 8, W, ref, omega, params, g_out, c_out, o_out, ws,
+                                                stream), 1)
+    n_search = 1 + CALIB_ROUNDS * 2 * (S + 1)
+    start = obj.new_empty((1,))
+    B.sq_calib_objective(x, t2s, S, dinv, 8, W, ref, torch.ones((1, S), dtype=torch.float32, device=dev),
+                         torch.tensor([float(L.clip[0])], dtype=torch.float32, device=dev), omega, start, ws, stream)
+    torch.cuda.synchronize()
+    err_bytes = M * N * (4 + 8)  # the candidate's fp32 output and the fp64 target, read once
+    us_err = (ms_obj - ms_lin) * 1e3
+    out = {
+        "workload": f"up projection {K}->{N}, per-channel int4 weights, M={M} tokens in {S} streams, A8 STATIC",
+        "reference_ms": round(ms_ref, 3),
+        "reference_fp64_tflops": round(2.0 * M * K * N / (ms_ref * 1e-3) / 1e12, 2),
+        "reference_frac_fp64_peak": round(2.0 * M * K * N / (ms_ref * 1e-3) / 1e12 / PEAK_FP64_TFLOPS, 4),
+        "objective_us_per_candidate": round(ms_obj * 1e3, 1),
+        "fused_linear_f32_us": round(ms_lin * 1e3, 1),
+        "error_kernels_us": round(us_err, 1),
+        "error_kernels_gbs": round(err_bytes / max(us_err, 1e-3) / 1e3, 1),
+        "search_ms": round(ms_search, 2), "search_rounds": CALIB_ROUNDS, "search_candidates": n_search,
+        "search_objective_start": float(start.item()), "search_objective_end": float(o_out.item()),
+        "search_gamma": [round(float(v), 5) for v in g_out.cpu()], "search_clip": round(float(c_out.item()), 5),
+    }
+    if cpu_rows is not None:
+        out["cpu_oracle"] = calibration_cpu(L, K, cpu_rows)
+        out["cpu_oracle"]["gpu_over_cpu"] = round(
+            (M / (ms_obj * 1e-3)) / out["cpu_oracle"]["tokens_per_s_per_candidate"], 1)
+    return out
+
+
+def calibration_cpu(L, K, rows):
+    """The oracle's Eq. (9) objective for one candidate on a row sample of
+    the same layer (its target X~ W^ included, as the GPU's per-linear
+    reference is amortized only over candidates)."""
+    from oracle import sq_oracle as O
+
+    idx = np.sort(np.random.default_rng(1).choice(L.M, size=rows, replace=False))
+    pw = O.pack_weights(L.w, L.d, K)
+    S = L.gamma.shape[1]
+    t0 = time.perf_counter()
+    O.calib_objective(L.x_bits[idx], L.tok2stream[idx], S, pw["codes"], pw["w_scale"], K, L.gamma[:1], L.clip[:1],
+                      np.full(S, 1.0 / S), dinv=L.dinv, act_bits=8)
+    dt = time.perf_counter() - t0
+    return dict(tokens_per_s_per_candidate=round(rows / dt, 1), seconds=round(dt, 3), rows=rows)
+
+
 def main():
     args = parse()
     if args.suite:
@@ -452,6 +549,9 @@ def main():
     ms_w4a4 = time_variant(B.sq_linear_w4a4, 4, "ws_fused", vsteps)
     ms_pc = time_variant(B.sq_linear_w4a8, 8, "ws_fused", vsteps, "W_pc")
 
+    # ---- the calibration path of Eq. (9) on the up projection
+    calib = calibration_figures(torch, B, layers[0], stream, dev, None if args.no_cpu else 256)
+
     # ---- the int8 matrix-core rate this GPU sustains (sq_probe_mfma_i8: back
     # to back MFMAs on register operands at the GEMM's occupancy), as a
     # measured ceiling beside the published peak: zero operands, random
@@ -524,6 +624,7 @@ def main():
                        "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2)},
         "fused_w4a8_per_channel_steps": {"ms_per_step": round(ms_pc, 5),
                                          "tops": round(ops_step / (ms_pc * 1e-3) / 1e12, 2)},
+        "calibration": calib,
         "hbm_copy": {"bytes": 2 * (COPY_MIB << 20), "us": round(copy_us, 1),
                      "gbs": round(2 * (COPY_MIB << 20) / (copy_us * 1e-6) / 1e9, 1)},
     }

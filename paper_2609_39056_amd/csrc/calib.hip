@@ -151,6 +151,7 @@ __global__ __launch_bounds__(256) void calib_row_error_kernel(const float* __res
   const float4* yr = reinterpret_cast<const float4*>(yq + i * N);
   const double2* rr = reinterpret_cast<const double2*>(ref + i * N);
   double acc = 0.0;
+#pragma unroll 4
   for (int32_t j = lane; j < N / 4; j += 64) {
     const float4 a = yr[j];
     const double2 b0 = rr[2 * j], b1 = rr[2 * j + 1];
