@@ -57,6 +57,10 @@ def parse():
                    help="instead of the one-line benchmark, measure every layer configuration (per-layer "
                         "kernels, the unfused path, and the 28-layer x 10-step sweep as one HIP graph) and "
                         "write one JSON record per line to PATH")
+    p.add_argument("--action-only", type=int, default=0, metavar="TOKENS",
+                   help="time the 2B-class linears on TOKENS action tokens only (the weight-streaming regime): "
+                        "28 layers x {qkv, out, up, down} with distinct weights, W4A8 and W4A4, eager calls; "
+                        "one JSON line per width (for HBM-traffic counters)")
     p.add_argument("--cpu-rows", type=int, default=0,
                    help="rows of each layer the oracle times (0 = all: one whole step)")
     return p.parse_args()
@@ -412,8 +416,80 @@ def calibration_cpu(L, K, rows):
     return dict(tokens_per_s_per_candidate=round(rows / dt, 1), seconds=round(dt, 3), rows=rows)
 
 
+def run_action_only(args):
+    """The few-token regime: every call streams a distinct weight (28 layers x
+    4 linears, 0.7 GB packed: more than the 256 MB last-level cache), one pass
+    of eager fused calls per width, HIP events around the pass, then a plain
+    512 MiB copy (the reference for the HBM byte counters)."""
+    import torch
+
+    from paper_2609_39056_amd import binding as B
+    from paper_2609_39056_amd import synth
+
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    B.lib()
+    stream = torch.cuda.current_stream()
+    tokens = (0, 0, args.action_only)
+    lin = synth.LINEARS_2B
+    NL = 28
+    inputs = {name: synth.device_layer(K, N, tokens, T=T_STEPS, seed=4000 + i, device=dev, with_weight=False)
+              for i, (name, (K, N)) in enumerate(lin.items())}
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    weights = []
+    for _ in range(NL):
+        ws = {}
+        for name, (K, N) in lin.items():
+            w = torch.randn((N, K), generator=g, device=dev) * 0.02
+            ws[name] = B.prepare_weight(w, inputs[name]["d"], W_GROUP, bias=inputs[name]["bias"])
+            del w
+        weights.append(ws)
+    M = args.action_only
+    for bits in (8, 4):
+        fused = B.sq_linear_w4a8 if bits == 8 else B.sq_linear_w4a4
+        bufs = {name: dict(y=torch.empty((M, N), dtype=torch.bfloat16, device=dev),
+                           ws=B.alloc_workspace(B.SQ_VARIANT_FUSED, M, K, N, bits, dev),
+                           act=B.ActParams(tok2stream=inputs[name]["tok2stream"], gamma=inputs[name]["gamma"],
+                                           step=1, act_bits=bits, dinv=inputs[name]["dinv"]))
+                for name, (K, N) in lin.items()}
+
+        def one_pass():
+            for layer in range(NL):
+                for name in lin:
+                    b = bufs[name]
+                    fused(inputs[name]["x"], b["act"], weights[layer][name], b["y"], B.SQ_OUT_BF16, b["ws"], stream)
+
+        for _ in range(max(1, args.warmup // 10)):
+            one_pass()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        one_pass()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3
+        calls = NL * len(lin)
+        ab = NL * sum(M * K * 2 + N * K // 2 + N * K // W_GROUP * 2 + M * N * 2 + 2 * N + 4 * M
+                      for K, N in lin.values())
+        print(json.dumps(dict(group="action-only linears, 2B class, eager fused calls", tokens=M, act_bits=bits,
+                              calls=calls, us_per_call=round(us / calls, 2), alg_mb_per_pass=round(ab / 1e6, 1),
+                              gbs=round(ab / us / 1e3, 1), frac_hbm=round(ab / us / 1e3 / PEAK_HBM_GBS, 4))),
+              flush=True)
+        del bufs
+    src = torch.empty(COPY_MIB << 20, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+
+
 def main():
     args = parse()
+    if args.action_only:
+        if args.gpus != 1:
+            print("bench.py runs on one GPU only", file=sys.stderr)
+            sys.exit(2)
+        run_action_only(args)
+        return
     if args.suite:
         if args.gpus != 1:
             print("bench.py runs on one GPU only", file=sys.stderr)
