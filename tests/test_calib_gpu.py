@@ -300,3 +300,43 @@ def test_calib_search_start_and_single_stream():
     start = gpu_objective(L1, W1, bits, np.ones((1, 1), F32),
                           np.array([np.clip(L1.clip[0], F32(L1.clip[0] / 4), F32(L1.clip[0] * 2))]), np.ones(1), ref1)
     assert o1 <= start[0]
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_calib_objective_max_rows(bits):
+    """M = 2^24 calibration tokens (the C ABI's maximum; row offsets of the
+    fp64 target pass 2^31 bytes): a 256-token block tiled 65536 times, so
+    every stream's error sum and token count grow by the same factor and the
+    objective must equal the block's.  Compared with the oracle on the block
+    (within its bound) and with the GPU's own objective of the block."""
+    K, N, G, R = 128, 64, 128, 1 << 16
+    L = synth.make_layer(K=K, N=N, stream_counts=(192, 24, 40), T=2, seed=60, permute=True)
+    pw, W = weight(L, G)
+    gammas, clips = candidates(L, 1, seed=61)
+    omega = np.array([0.5, 0.3, 0.2])
+    ref_small = gpu_reference(L, W)
+    small = gpu_objective(L, W, bits, gammas, clips, omega, ref_small)
+    ref = O.calib_reference(L.x_bits, pw["codes"], pw["w_scale"], G, L.dinv)
+    want = O.calib_objective(L.x_bits, L.tok2stream, 3, pw["codes"], pw["w_scale"], G, gammas, clips, omega,
+                             dinv=L.dinv, act_bits=bits, ref=ref)
+    bound = objective_bound(L, pw, G, bits, gammas, clips, omega, ref, abs_reference(L, pw, G), 3)
+    check_objectives(small, want, bound)
+    del ref_small
+    x = u16_to_dev(L.x_bits, torch.bfloat16).repeat(R, 1)
+    t2s = i32_to_dev(L.tok2stream).repeat(R)
+    M = x.shape[0]
+    assert M == 1 << 24
+    ref_big = torch.empty((M, N), dtype=torch.float64, device="cuda")
+    dinv = f32_to_dev(L.dinv)
+    B.sq_calib_reference(x, dinv, W, ref_big)
+    ws = torch.empty(B.sq_calib_workspace_bytes(M, K, N, bits, 3), dtype=torch.uint8, device="cuda")
+    obj = torch.full((len(clips),), float("nan"), dtype=torch.float64, device="cuda")
+    B.sq_calib_objective(x, t2s, 3, dinv, bits, W, ref_big, f32_to_dev(gammas), f32_to_dev(clips),
+                         torch.as_tensor(omega, device="cuda"), obj, ws)
+    torch.cuda.synchronize()
+    big = obj.cpu().numpy()
+    # identical rows give identical per-row errors; only the order of the fp64 sums differs
+    assert np.allclose(big, small, rtol=1e-9, atol=0), (big, small)
+    # the last tiled copy of the target equals the block's
+    tail = ref_big[M - L.x_bits.shape[0]:].cpu().numpy()
+    assert np.all(np.abs(tail - ref) <= K * 2.0**-52 * abs_reference(L, pw, G))
