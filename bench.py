@@ -252,6 +252,8 @@ def run_suite(args):
     layer_group("14B-class linears, 8384 tokens (8192+64+128)", synth.LINEARS_14B, synth.TOKENS_14B, (8, 4), 0.02, 12)
     layer_group("2B-class linears, W4A8, one weight step per output channel (the paper's weight format)",
                 synth.LINEARS_2B, synth.TOKENS_2B, (8,), 0.02, 60, per_channel=True)
+    layer_group("14B-class column shards at 8-way tensor parallelism (one GPU's share: N / 8)",
+                {"qkv/8": (5120, 1920), "up/8": (5120, 1728)}, synth.TOKENS_14B, (8, 4), 0.02, 24)
     layer_group("14B-class linears, W4A8, one weight step per output channel", synth.LINEARS_14B, synth.TOKENS_14B,
                 (8,), 0.02, 12, per_channel=True)
 

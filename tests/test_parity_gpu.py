@@ -313,6 +313,9 @@ FULL = [
     ("2B qkv W4A4", 4, synth.TOKENS_2B, 2048, 6144, (0.01, 0.02, 0.05)),
     ("2B down W4A4", 4, synth.TOKENS_2B, 8192, 2048, (0.01, 0.02, 0.05)),
     ("14B out W4A8", 8, synth.TOKENS_14B, 5120, 5120, 0.02),
+    # one GPU's column shard of the 14B up projection at 8-way tensor parallelism
+    ("14B up TP8 shard W4A8", 8, synth.TOKENS_14B, 5120, 1728, 0.02),
+    ("14B up TP8 shard W4A4", 4, synth.TOKENS_14B, 5120, 1728, 0.02),
 ]
 
 
