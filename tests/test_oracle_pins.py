@@ -415,6 +415,8 @@ def test_projection_matches_active_set_enumeration():
         assert np.allclose(u, best_u, atol=1e-9)
     u = O.project_log_gains(np.array([3.0, 0.4, -0.2]), np.array([0, 10, 10]), lo, hi)
     assert u[0] == hi and abs(u[1] + u[2]) < 1e-12 and abs(u[1] - 0.3) < 1e-12
+    u = O.project_log_gains(np.array([0.3, 0.4, -0.2]), np.array([0, 10, 10]), lo, hi)
+    assert u[0] == 0.3 and abs(u[1] - 0.3) < 1e-12
 
 
 def test_compass_search_finds_the_constrained_minimum_of_a_quadratic():
@@ -470,3 +472,68 @@ def test_calib_search_single_stream_keeps_unit_gain():
     gam, c, L, h, _ = O.calib_search(lambda G, C: (np.log(C.astype(np.float64)) - 1.0) ** 2
                                      + (G[:, 0].astype(np.float64) - 3.0) ** 2, n, (0.5, 2.0, 0.1, 10.0), 1.0, 0.5, 30)
     assert gam[0] == F32(1.0) and abs(np.log(float(c)) - 1.0) < 1e-3
+
+
+def test_calib_objective_token_mean_per_stream():
+    """Eq. (9) divides each stream's squared error by its token count: the
+    same calibration batch given twice (every row duplicated) leaves the
+    objective unchanged, and so does doubling one stream's rows alone."""
+    L_ = _layer(K=256, N=64, counts=(20, 6, 8), seed=14)
+    pw = O.pack_weights(L_.w, L_.d, 128)
+    g = np.array([[1.0, 1.5, 0.75], [0.8, 1.0, 1.3]], F32)
+    c = np.array([4.0, 3.0], F32)
+    om = np.array([0.5, 0.3, 0.2])
+
+    def obj(xb, t2s):
+        return O.calib_objective(xb, t2s, 3, pw["codes"], pw["w_scale"], 128, g, c, om, dinv=L_.dinv)
+
+    base = obj(L_.x_bits, L_.tok2stream)
+    twice = obj(np.concatenate([L_.x_bits, L_.x_bits]), np.concatenate([L_.tok2stream, L_.tok2stream]))
+    assert np.allclose(twice, base, rtol=1e-12, atol=0)
+    s1 = L_.tok2stream == 1
+    more = obj(np.concatenate([L_.x_bits, L_.x_bits[s1]]), np.concatenate([L_.tok2stream, L_.tok2stream[s1]]))
+    assert np.allclose(more, base, rtol=1e-12, atol=0)
+
+
+def test_calib_objective_zero_with_channel_scaling():
+    """The target of Eq. (9) is X D^-1 W^: with power-of-two D^-1 and inputs
+    whose gamma_s x D^-1 are representable codes, the modulated output equals
+    X D^-1 W^ exactly and the objective is 0; dropping D^-1 from either side
+    would leave a nonzero error."""
+    rng = np.random.default_rng(15)
+    M, K, N, S = 12, 256, 64, 3
+    delta = 2.0 ** -4
+    c = np.float32(127 * delta)
+    gam = np.array([1.0, 2.0, 0.5], F32)
+    dinv = (2.0 ** rng.integers(-2, 3, K)).astype(F32)
+    t2s = (np.arange(M) % S).astype(np.int32)
+    k = rng.integers(-127, 128, size=(M, K))
+    x = (k * delta / gam[t2s][:, None] / dinv[None, :]).astype(F32)
+    x_bits = _bits(x)
+    assert np.array_equal(O.bf16_bits_to_f32(x_bits), x)
+    w = rng.standard_normal((N, K)).astype(F32) * 0.05
+    pw = O.pack_weights(w, None, 128)
+    ref = O.calib_reference(x_bits, pw["codes"], pw["w_scale"], 128, dinv)
+    L = O.calib_objective(x_bits, t2s, S, pw["codes"], pw["w_scale"], 128, gam[None, :], [c], np.ones(S) / S,
+                          dinv=dinv, ref=ref)
+    assert L[0] <= 1e-24 * float((ref ** 2).mean())
+    ref_nod = O.calib_reference(x_bits, pw["codes"], pw["w_scale"], 128)
+    assert float(((ref - ref_nod) ** 2).mean()) > 1e-6 * float((ref ** 2).mean())
+
+
+def test_compass_candidates_respect_the_bounds():
+    """Every trial point of a round lies in the constraint set (App. C.1) in
+    its log coordinates as well as in its evaluated fp32 values, also when the
+    incumbent sits on a bound: a threshold step past c_max stays at log c_max."""
+    n = np.array([100, 10, 0])
+    bounds = (0.5, 2.0, 0.25, 4.0)
+    u = np.array([np.log(2.0), -np.log(2.0) * 10 / 10, 0.0])
+    u = O.project_log_gains(u, n, np.log(0.5), np.log(2.0))
+    G, C, U, V = O.compass_candidates(u, np.log(4.0), 0.7, n, bounds)
+    assert G.shape == (8, 3) and C.shape == (8,)
+    assert np.all(U >= np.log(0.5) - 1e-15) and np.all(U <= np.log(2.0) + 1e-15)
+    assert np.all(V >= np.log(0.25) - 1e-15) and np.all(V <= np.log(4.0) + 1e-15)
+    assert np.all(G >= F32(0.5)) and np.all(G <= F32(2.0)) and np.all(C >= F32(0.25)) and np.all(C <= F32(4.0))
+    assert np.all(np.abs((n * U).sum(axis=1)) <= 1e-9 * n.sum())
+    # the threshold's +h step is clamped to the bound, its -h step moves down by h
+    assert V[6] == np.log(4.0) and abs(V[7] - (np.log(4.0) - 0.7)) < 1e-15
