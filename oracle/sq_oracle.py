@@ -43,6 +43,10 @@ Readings where the paper leaves a choice:
   coordinates with every trial point projected onto the constraint set (the
   token-weighted nearest point) and the step halved after a round without
   progress.
+* Shared scaling, Sec. 4.2 Eq. (7): the paper gives the objective but no
+  family for D and no optimizer; the family here is d_k = amax|X_k|^alpha /
+  amax|W_k|^(1-alpha) (clamped to [2^-6, 2^6]) over a list of exponents, with
+  the per-token / per-group absmax activation quantizer and unit gains.
 * int4 packing (both weights and A4 activations): for every 8 consecutive
   codes k = 8g..8g+7 the four bytes 4g..4g+3 hold code 8g+b in the low nibble
   and code 8g+b+4 in the high nibble of byte 4g+b.
@@ -350,15 +354,23 @@ def calib_objective(x_bits, tok2stream, num_streams, qw_codes, w_scale_bits, w_g
     for g, c in zip(np.asarray(gammas, dtype=F32), np.asarray(clips, dtype=F32)):
         res = linear(x_bits, t2s, g[None, :], 0, qw_codes, w_scale_bits, w_group, dinv=dinv,
                      clip=np.array([c], dtype=F32), bias_bits=None, range_mode=RANGE_STATIC, act_bits=act_bits)
-        d2 = ((res["y64"] - ref) ** 2).sum(axis=1)
-        L = 0.0
-        for s in range(num_streams):
-            rows = t2s == s
-            n = int(rows.sum())
-            if n:
-                L += float(omega[s]) / n * float(d2[rows].sum())
-        out.append(L)
+        out.append(weighted_stream_error(res["y64"], ref, t2s, num_streams, omega))
     return np.array(out, dtype=np.float64)
+
+
+def weighted_stream_error(y, ref, ids, num_ids, omega):
+    """sum_s omega_s / n_s * sum_{i : ids_i = s} || y_i - ref_i ||^2 (float64):
+    each stream's (or region's) mean squared row error, weighted; a stream
+    with no rows adds 0 (Eq. (7) and (9))."""
+    d2 = ((np.asarray(y, np.float64) - ref) ** 2).sum(axis=1)
+    ids = np.asarray(ids)
+    L = 0.0
+    for s in range(num_ids):
+        rows = ids == s
+        n = int(rows.sum())
+        if n:
+            L += float(omega[s]) / n * float(d2[rows].sum())
+    return L
 
 
 # ---------------------------------------------------------------- constrained search, Eq. (9)
@@ -455,3 +467,51 @@ def calib_search(objective, counts, bounds, clip_init, log_step, rounds):
         else:
             h = 0.5 * h
     return gam, F32(c), L, h, trace
+
+
+
+# ---------------------------------------------------------------- shared channel scaling, Eq. (7)
+# Eq. (7) chooses the shared scaling D* by the reconstruction error of
+# Q(X D^-1) Q(D W) against the full-precision X W, weighted per region
+# (tau, s); the paper names neither a family for D nor an optimizer.  The
+# reading here: the one-parameter family below, searched over a list of
+# exponents; the activation quantizer of the objective is the per-token (8-bit)
+# or per-64-group (4-bit) absmax quantizer with unit gains (Eq. (7) has none).
+
+def smooth_scales(x_bits, w, alpha):
+    """d_k = amax_i |x_ik|^alpha / amax_j |w_jk|^(1 - alpha), evaluated in
+    float64 (alpha taken as the fp32 value given), clamped to [2^-6, 2^6] and
+    rounded to fp32; a channel whose amax is 0 on either side gets d = 1.
+    Also returns dinv = fp32(1 / d).  x_bits: bf16 [M, K]; w: fp32 [N, K]."""
+    ax = np.abs(bf16_bits_to_f32(np.asarray(x_bits, np.uint16))).max(axis=0).astype(np.float64)
+    aw = np.abs(np.asarray(w, F32)).max(axis=0).astype(np.float64)
+    a = float(F32(alpha))
+    d = np.ones(ax.shape, dtype=np.float64)
+    for k in range(ax.size):
+        if ax[k] > 0 and aw[k] > 0:
+            d[k] = ax[k] ** a / aw[k] ** (1.0 - a)
+    d = np.minimum(np.maximum(d, 2.0 ** -6), 2.0 ** 6).astype(F32)
+    return d, (F32(1.0) / d).astype(F32)
+
+
+def scaling_objective(x_bits, region, num_regions, region_weight, w, w_group, alphas, act_bits=8, ref=None):
+    """Eq. (7) for each exponent of the family (smooth_scales):
+
+        L(D) = sum_r weight_r / n_r * || Q(X_r D^-1) Q(D W) - X_r W ||_F^2
+
+    over regions r (an id per row, e.g. step x stream; weight_r = pi_tau
+    omega^D_{tau,s}).  Q(D W) is pack_weights(w, d); Q(X D^-1) Q(D W) is the
+    fused linear with DYNAMIC ranges, unit gains and no bias at its float64
+    value; X W is full_precision_linear.  Returns float64 [len(alphas)]."""
+    if ref is None:
+        ref = full_precision_linear(x_bits, w)
+    region = np.asarray(region, np.int32)
+    ones = np.ones((1, num_regions), dtype=F32)
+    out = []
+    for alpha in np.asarray(alphas, dtype=F32):
+        d, dinv = smooth_scales(x_bits, w, alpha)
+        pw = pack_weights(w, d, w_group)
+        res = linear(x_bits, region, ones, 0, pw["codes"], pw["w_scale"], w_group, dinv=dinv, bias_bits=None,
+                     range_mode=RANGE_DYNAMIC, act_bits=act_bits)
+        out.append(weighted_stream_error(res["y64"], ref, region, num_regions, region_weight))
+    return np.array(out, dtype=np.float64)

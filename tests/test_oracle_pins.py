@@ -537,3 +537,74 @@ def test_compass_candidates_respect_the_bounds():
     assert np.all(np.abs((n * U).sum(axis=1)) <= 1e-9 * n.sum())
     # the threshold's +h step is clamped to the bound, its -h step moves down by h
     assert V[6] == np.log(4.0) and abs(V[7] - (np.log(4.0) - 0.7)) < 1e-15
+
+
+# ---------------------------------------------------------------- shared channel scaling, Eq. (7)
+def test_smooth_scales_closed_forms():
+    """The family at its ends and middle: alpha = 1 gives d = amax|X| and
+    alpha = 0 gives 1 / amax|W| exactly (within the clamp), alpha = 1/2 the
+    square root of their ratio to within fp32 rounding; zero channels give 1."""
+    rng = np.random.default_rng(30)
+    K = 64
+    x = (rng.standard_normal((16, K)) * 2.0 ** rng.integers(-3, 4, K)).astype(F32)
+    x[:, 5] = 0.0
+    x[:, 7] *= 400.0  # amax above 2^6: the clamp binds at alpha = 1
+    xb = _bits(x)
+    xf = O.bf16_bits_to_f32(xb).astype(np.float64)
+    w = (rng.standard_normal((8, K)) * 0.05).astype(F32)
+    w[:, 9] = 0.0
+    ax, aw = np.abs(xf).max(0), np.abs(w.astype(np.float64)).max(0)
+    clamp = lambda v: np.minimum(np.maximum(v, 2.0 ** -6), 2.0 ** 6)
+    live = (ax > 0) & (aw > 0)
+    d1, _ = O.smooth_scales(xb, w, 1.0)
+    assert np.array_equal(d1[live], clamp(ax[live]).astype(F32))
+    d0, _ = O.smooth_scales(xb, w, 0.0)
+    assert np.array_equal(d0[live], clamp(1.0 / aw[live]).astype(F32))
+    dh, dinv = O.smooth_scales(xb, w, 0.5)
+    want = clamp(np.sqrt(ax[live] / aw[live]))
+    assert np.all(np.abs(dh[live] - want) <= 2.0 ** -23 * want)
+    assert dh[5] == 1.0 and dh[9] == 1.0 and d0[5] == 1.0 and d1[7] == 64.0
+    assert np.array_equal(dinv, (F32(1.0) / dh).astype(F32))
+
+
+@pytest.mark.parametrize("act_bits", [8, 4])
+def test_scaling_objective_homogeneous(act_bits):
+    """Eq. (7) with the family's ends: at alpha = 1 doubling X doubles d, so
+    X D^-1 and the codes stay and only the weight steps double; at alpha = 0
+    doubling W halves d, so D W stays and the activation steps double.  Either
+    way both the quantized and the full-precision outputs double exactly and
+    the objective grows by exactly 4."""
+    L_ = _layer(K=256, N=64, counts=(20, 4, 8), seed=31)
+    reg = L_.tok2stream
+    om = np.array([0.5, 0.3, 0.2])
+    # X scaled by 2^-5 (exact) so that d = amax|X| stays inside the clamp [2^-6, 2^6] when doubled
+    x1 = O.f32_to_bf16_bits(O.bf16_bits_to_f32(L_.x_bits) * F32(2.0 ** -5))
+    assert np.abs(O.bf16_bits_to_f32(x1)).max() < 32
+    x2 = O.f32_to_bf16_bits(2 * O.bf16_bits_to_f32(x1))
+    a = O.scaling_objective(x1, reg, 3, om, L_.w, 128, [1.0], act_bits=act_bits)
+    b = O.scaling_objective(x2, reg, 3, om, L_.w, 128, [1.0], act_bits=act_bits)
+    assert b[0] == 4 * a[0] and a[0] > 0
+    assert 1 / np.abs(L_.w).max(0).min() < 32
+    a0 = O.scaling_objective(L_.x_bits, reg, 3, om, L_.w, 128, [0.0], act_bits=act_bits)
+    b0 = O.scaling_objective(L_.x_bits, reg, 3, om, 2 * L_.w, 128, [0.0], act_bits=act_bits)
+    assert b0[0] == 4 * a0[0] and a0[0] > 0
+
+
+def test_scaling_objective_regions_and_scaling_matter():
+    """The region weights average per region (the batch given twice leaves
+    the objective unchanged); D matters: the exponents give different
+    objectives on a layer with outlier channels, and at alpha = 1/2 the
+    objective is below that of D = I (alpha chosen so d = 1 is not in the
+    family) for this outlier-heavy input."""
+    L_ = _layer(K=256, N=64, counts=(30, 6, 10), seed=32)
+    reg, om = L_.tok2stream, np.full(3, 1 / 3)
+    al = [0.0, 0.5, 1.0]
+    a = O.scaling_objective(L_.x_bits, reg, 3, om, L_.w, 128, al)
+    b = O.scaling_objective(np.concatenate([L_.x_bits, L_.x_bits]), np.concatenate([reg, reg]), 3, om, L_.w, 128, al)
+    assert np.allclose(a, b, rtol=1e-12, atol=0)
+    assert len(set(a.tolist())) == 3
+    pw = O.pack_weights(L_.w, None, 128)
+    ones = np.ones((1, 3), F32)
+    res = O.linear(L_.x_bits, reg, ones, 0, pw["codes"], pw["w_scale"], 128, bias_bits=None)
+    plain = O.weighted_stream_error(res["y64"], O.full_precision_linear(L_.x_bits, L_.w), reg, 3, om)
+    assert a[1] < plain
