@@ -247,6 +247,53 @@ sq_status sq_calib_objective(const uint16_t* x, int32_t M, const int32_t* tok2st
                              const double* omega, double* objective, void* workspace, size_t workspace_bytes,
                              hipStream_t stream);
 
+/* Shared channel scaling, Sec. 4.2 Eq. 7.  The paper chooses D* by
+ *
+ *     L(D) = sum_r weight_r / n_r * || Q(X_r D^-1) Q(D W) - X_r W ||_F^2
+ *
+ * over regions r (per step and stream; weight_r = pi_tau omega^D_{tau,s})
+ * but names no family for D and no optimizer.  This library evaluates the
+ * one-parameter family d_k = amax_i |x_ik|^alpha / amax_j |w_jk|^(1 - alpha)
+ * (fp64, clamped to [2^-6, 2^6], then fp32; 1 where either amax is 0) for a
+ * list of exponents; the caller keeps the best and folds it with
+ * sq_pack_weights.
+ *
+ * sq_calib_fp_reference writes the full-precision target Y = X W^T in fp64:
+ * x bf16 [M, K], w fp32 [N, K] (16-byte aligned), y_ref fp64 [M, N]. */
+sq_status sq_calib_fp_reference(const uint16_t* x, int32_t M, const float* w, int32_t N, int32_t K, double* y_ref,
+                                hipStream_t stream);
+
+/* d fp32 [K] and dinv = fp32(1 / d) [K] of the family above for one alpha
+ * (finite), from the per-channel maxima of |x| over the M rows of x (bf16
+ * [M, K]) and of |w| over the N rows of w (fp32 [N, K], 1 <= N <= 2^20).
+ * d and dinv must be distinct; they also serve as scratch.  x and w 16-byte
+ * aligned. */
+sq_status sq_smooth_scales(const uint16_t* x, int32_t M, const float* w, int32_t N, int32_t K, float alpha, float* d,
+                           float* dinv, hipStream_t stream);
+
+/* Workspace bytes for sq_calib_scaling_objective (1 <= num_regions <= 4096);
+ * 0 for invalid arguments.  Host-only. */
+size_t sq_calib_scaling_workspace_bytes(int32_t M, int32_t K, int32_t N, int32_t w_group, int32_t act_bits,
+                                        int32_t num_regions);
+
+/* L(D) of Eq. 7 for each exponent alphas[i] (a HOST array of num_alphas
+ * finite values, 1 .. 65536) into objective[i] (device fp64):
+ *   region         int32 [M], the region of every row; each must lie in
+ *                  [0, num_regions) (device data, not checked, as tok2stream)
+ *   region_weight  fp64 [num_regions] (device)
+ *   w              fp32 [N, K] the unquantized weight; y_ref its target from
+ *                  sq_calib_fp_reference
+ * Per exponent: d and dinv as sq_smooth_scales, Q(D W) packed with w_group,
+ * then the fused linear with DYNAMIC ranges (per token for act_bits 8, per 64
+ * channels for 4), unit gains and no bias into fp32, and the weighted squared
+ * error in fp64 in a fixed order.  Alignment: x, w, y_ref and workspace 16
+ * bytes, region_weight and objective 8, region 4. */
+sq_status sq_calib_scaling_objective(const uint16_t* x, int32_t M, const int32_t* region, int32_t num_regions,
+                                     const double* region_weight, const float* w, int32_t N, int32_t K,
+                                     int32_t w_group, int32_t act_bits, const double* y_ref, int32_t num_alphas,
+                                     const float* alphas, double* objective, void* workspace, size_t workspace_bytes,
+                                     hipStream_t stream);
+
 /* Constrained search for (gamma*, c*) of Eq. 9 under the constraints of
  * Sec. 4.3 and App. C.1: gamma_min <= gamma_s <= gamma_max for every stream,
  * clip_min <= c <= clip_max and sum_s n_s log gamma_s = 0.  The paper names

@@ -93,6 +93,11 @@ _SIGS = {
     "sq_calib_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
     "sq_calib_objective": (_I, [_P, _I, _P, _I, _P, _I, ctypes.POINTER(sq_weight), _P, _I, _P, _P, _P, _P, _P, _S,
                                 _P]),
+    "sq_calib_fp_reference": (_I, [_P, _I, _P, _I, _I, _P, _P]),
+    "sq_smooth_scales": (_I, [_P, _I, _P, _I, _I, ctypes.c_float, _P, _P, _P]),
+    "sq_calib_scaling_workspace_bytes": (_S, [_I, _I, _I, _I, _I, _I]),
+    "sq_calib_scaling_objective": (_I, [_P, _I, _P, _I, _P, _P, _I, _I, _I, _I, _P, _I,
+                                        ctypes.POINTER(ctypes.c_float), _P, _P, _S, _P]),
     "sq_calib_search_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
     "sq_calib_search": (_I, [_P, _I, _P, _I, _P, _I, ctypes.POINTER(sq_weight), _P, _P,
                              ctypes.POINTER(sq_calib_search_params), _P, _P, _P, _P, _S, _P]),
@@ -280,6 +285,40 @@ def sq_calib_objective(x: torch.Tensor, tok2stream: torch.Tensor, num_streams: i
     _check(lib().sq_calib_objective(_ptr(x), M, _ptr(tok2stream), num_streams, _ptr(dinv), act_bits,
                                     ctypes.byref(ws), _ptr(y_ref), C, _ptr(cand_gamma), _ptr(cand_clip),
                                     _ptr(omega), _ptr(objective), wp, wb, _stream(stream)), "sq_calib_objective")
+
+
+def sq_calib_fp_reference(x: torch.Tensor, w: torch.Tensor, y_ref: torch.Tensor, stream=None) -> None:
+    """The full-precision target X W^T of Eq. (7) into fp64 y_ref [M, N]."""
+    M, K = x.shape
+    N = w.shape[0]
+    _check(lib().sq_calib_fp_reference(_ptr(x), M, _ptr(w), N, K, _ptr(y_ref), _stream(stream)),
+           "sq_calib_fp_reference")
+
+
+def sq_smooth_scales(x: torch.Tensor, w: torch.Tensor, alpha: float, d: torch.Tensor, dinv: torch.Tensor,
+                     stream=None) -> None:
+    """d = amax|X|^alpha / amax|W|^(1 - alpha) per channel (clamped) and 1 / d."""
+    M, K = x.shape
+    N = w.shape[0]
+    _check(lib().sq_smooth_scales(_ptr(x), M, _ptr(w), N, K, float(alpha), _ptr(d), _ptr(dinv), _stream(stream)),
+           "sq_smooth_scales")
+
+
+def sq_calib_scaling_workspace_bytes(M: int, K: int, N: int, w_group: int, act_bits: int, num_regions: int) -> int:
+    return int(lib().sq_calib_scaling_workspace_bytes(M, K, N, w_group, act_bits, num_regions))
+
+
+def sq_calib_scaling_objective(x: torch.Tensor, region: torch.Tensor, num_regions: int, region_weight: torch.Tensor,
+                               w: torch.Tensor, w_group: int, act_bits: int, y_ref: torch.Tensor, alphas,
+                               objective: torch.Tensor, workspace: torch.Tensor, stream=None) -> None:
+    """Eq. (7) for each exponent in `alphas` (a host sequence) into fp64 objective."""
+    M, K = x.shape
+    N = w.shape[0]
+    a = (ctypes.c_float * len(alphas))(*[float(v) for v in alphas])
+    wp, wb = _ws(workspace)
+    _check(lib().sq_calib_scaling_objective(_ptr(x), M, _ptr(region), num_regions, _ptr(region_weight), _ptr(w), N,
+                                            K, w_group, act_bits, _ptr(y_ref), len(alphas), a, _ptr(objective), wp,
+                                            wb, _stream(stream)), "sq_calib_scaling_objective")
 
 
 def sq_calib_search_workspace_bytes(M: int, K: int, N: int, act_bits: int, num_streams: int) -> int:

@@ -23,10 +23,14 @@ namespace {
 constexpr int kRefTile = 128;  // output rows and columns per workgroup
 constexpr int kRefKc = 16;     // K per LDS stage
 
+// FPW: the weight operand is fp32 W [N][K] itself (the full-precision target
+// of Eq. 7, no D^-1); otherwise packed codes times their fp16 steps.
+template <bool FPW>
 __global__ __launch_bounds__(256) void calib_reference_kernel(const uint16_t* __restrict__ x,
                                                               const float* __restrict__ dinv,
                                                               const uint8_t* __restrict__ qw,
                                                               const uint16_t* __restrict__ w_scale,
+                                                              const float* __restrict__ wf,
                                                               double* __restrict__ y, int32_t M, int32_t N,
                                                               int32_t K, int32_t w_group, int32_t tiles_n,
                                                               size_t n_tiles) {
@@ -46,7 +50,8 @@ __global__ __launch_bounds__(256) void calib_reference_kernel(const uint16_t* __
   const int32_t wn = n0 + sr;
   const bool win = wn < N;
   const uint16_t* xrow = x + (xin ? xm : 0) * static_cast<int64_t>(K);
-  const uint8_t* wrow = qw + static_cast<size_t>(win ? wn : 0) * (K / 2);
+  const uint8_t* wrow = FPW ? nullptr : qw + static_cast<size_t>(win ? wn : 0) * (K / 2);
+  const float* wfrow = FPW ? wf + static_cast<size_t>(win ? wn : 0) * K : nullptr;
 
   double acc[8][8];
 #pragma unroll
@@ -71,20 +76,31 @@ __global__ __launch_bounds__(256) void calib_reference_kernel(const uint16_t* __
       const float xf = bf16_to_f32((xw[j >> 1] >> (16 * (j & 1))) & 0xFFFFu);
       xs[sh * 8 + j][sr] = static_cast<double>(dinv != nullptr ? xf * d[j] : xf);
     }
-    // 8 codes kb .. kb+7 sit in one dword: byte b holds code kb+b (low nibble)
-    // and code kb+b+4 (high nibble)
-    uint32_t p = 0u;
-    double step = 0.0;
-    if (win) {
-      p = *reinterpret_cast<const uint32_t*>(wrow + kb / 2);
-      step = static_cast<double>(f16_to_f32(w_scale[static_cast<size_t>(kb / w_group) * N + wn]));
-    }
+    if constexpr (FPW) {
+      float4 w0 = make_float4(0.f, 0.f, 0.f, 0.f), w1 = w0;
+      if (win) {
+        w0 = *reinterpret_cast<const float4*>(wfrow + kb);
+        w1 = *reinterpret_cast<const float4*>(wfrow + kb + 4);
+      }
+      const float wv[8] = {w0.x, w0.y, w0.z, w0.w, w1.x, w1.y, w1.z, w1.w};
 #pragma unroll
-    for (int b = 0; b < 4; ++b) {
-      const int lo = static_cast<int32_t>(p << (28 - 8 * b)) >> 28;
-      const int hi = static_cast<int32_t>(p << (24 - 8 * b)) >> 28;
-      ws[sh * 8 + b][sr] = static_cast<double>(lo) * step;
-      ws[sh * 8 + b + 4][sr] = static_cast<double>(hi) * step;
+      for (int j = 0; j < 8; ++j) ws[sh * 8 + j][sr] = static_cast<double>(wv[j]);
+    } else {
+      // 8 codes kb .. kb+7 sit in one dword: byte b holds code kb+b (low
+      // nibble) and code kb+b+4 (high nibble)
+      uint32_t p = 0u;
+      double step = 0.0;
+      if (win) {
+        p = *reinterpret_cast<const uint32_t*>(wrow + kb / 2);
+        step = static_cast<double>(f16_to_f32(w_scale[static_cast<size_t>(kb / w_group) * N + wn]));
+      }
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int lo = static_cast<int32_t>(p << (28 - 8 * b)) >> 28;
+        const int hi = static_cast<int32_t>(p << (24 - 8 * b)) >> 28;
+        ws[sh * 8 + b][sr] = static_cast<double>(lo) * step;
+        ws[sh * 8 + b + 4][sr] = static_cast<double>(hi) * step;
+      }
     }
     __syncthreads();
 #pragma unroll 4
@@ -180,6 +196,53 @@ __global__ __launch_bounds__(256) void calib_sum_kernel(const double* __restrict
   if ((threadIdx.x & 63) == 0) part[threadIdx.x >> 6] = acc;
   __syncthreads();
   if (threadIdx.x == 0) *out = (part[0] + part[1]) + (part[2] + part[3]);
+}
+
+// ---------------------------------------------------------------- shared channel scaling (Eq. 7)
+// Per-channel absolute maxima by atomic max on the bits of |v| (non-negative
+// floats order like their bit patterns; the result does not depend on the
+// order), then d_k = amax|X_k|^alpha / amax|W_k|^(1 - alpha) in fp64, clamped
+// to [2^-6, 2^6], and dinv = 1 / d in fp32.
+__global__ __launch_bounds__(256) void calib_fill_kernel(float* __restrict__ p, int32_t n, float v) {
+  for (int32_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = v;
+}
+
+__global__ __launch_bounds__(256) void calib_zero_u32_kernel(uint32_t* __restrict__ p, int32_t n) {
+  for (int32_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
+}
+
+// One thread per channel; grid.y splits the rows.  BF16: x is bf16 bits,
+// otherwise fp32.
+template <bool BF16>
+__global__ __launch_bounds__(256) void channel_amax_kernel(const void* __restrict__ src, int64_t rows, int32_t K,
+                                                           int64_t rows_per_block, uint32_t* __restrict__ amax) {
+  const int32_t k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= K) return;
+  const int64_t r0 = static_cast<int64_t>(blockIdx.y) * rows_per_block;
+  const int64_t r1 = min(rows, r0 + rows_per_block);
+  uint32_t m = 0u;
+  for (int64_t r = r0; r < r1; ++r) {
+    const uint32_t b = BF16 ? (static_cast<uint32_t>(static_cast<const uint16_t*>(src)[r * K + k] & 0x7FFFu) << 16)
+                            : (static_cast<const uint32_t*>(src)[r * K + k] & 0x7FFFFFFFu);
+    m = max(m, b);
+  }
+  if (m != 0u) atomicMax(&amax[k], m);
+}
+
+__global__ __launch_bounds__(256) void smooth_scale_kernel(const uint32_t* __restrict__ ax_bits,
+                                                           const uint32_t* __restrict__ aw_bits, int32_t K,
+                                                           float alpha, float* __restrict__ d,
+                                                           float* __restrict__ dinv) {
+  const int32_t k = blockIdx.x * 256 + threadIdx.x;
+  if (k >= K) return;
+  const double ax = static_cast<double>(__uint_as_float(ax_bits[k]));
+  const double aw = static_cast<double>(__uint_as_float(aw_bits[k]));
+  const double a = static_cast<double>(alpha);
+  double v = 1.0;
+  if (ax > 0.0 && aw > 0.0) v = pow(ax, a) / pow(aw, 1.0 - a);
+  const float dk = static_cast<float>(fmin(fmax(v, 0.015625), 64.0));
+  d[k] = dk;
+  dinv[k] = 1.0f / dk;
 }
 
 // ---------------------------------------------------------------- constrained search
@@ -320,8 +383,47 @@ hipError_t launch_calib_select(int32_t S, const double* cand_obj, const double* 
 hipError_t launch_calib_reference(const CalibRefArgs& a, hipStream_t s) {
   const int32_t tiles_n = (a.N + kRefTile - 1) / kRefTile;
   const size_t n_tiles = static_cast<size_t>((a.M + kRefTile - 1) / kRefTile) * tiles_n;
-  hipLaunchKernelGGL(calib_reference_kernel, wg_grid(n_tiles), dim3(256), 0, s, a.x, a.dinv, a.qw, a.w_scale,
-                     a.y, a.M, a.N, a.K, a.w_group, tiles_n, n_tiles);
+  if (a.wf != nullptr)
+    hipLaunchKernelGGL(calib_reference_kernel<true>, wg_grid(n_tiles), dim3(256), 0, s, a.x, nullptr, nullptr,
+                       nullptr, a.wf, a.y, a.M, a.N, a.K, 0, tiles_n, n_tiles);
+  else
+    hipLaunchKernelGGL(calib_reference_kernel<false>, wg_grid(n_tiles), dim3(256), 0, s, a.x, a.dinv, a.qw,
+                       a.w_scale, nullptr, a.y, a.M, a.N, a.K, a.w_group, tiles_n, n_tiles);
+  return hipGetLastError();
+}
+
+namespace {
+void launch_amax(bool bf16, const void* src, int64_t rows, int32_t K, uint32_t* amax, hipStream_t s) {
+  const int64_t rpb = 64;  // rows per workgroup: one atomic per channel per 64 rows
+  const int64_t yb = (rows + rpb - 1) / rpb;
+  const int64_t ybc = yb < 65535 ? yb : 65535;
+  const int64_t per = (rows + ybc - 1) / ybc;
+  const dim3 grid((K + 255) / 256, static_cast<unsigned>(ybc));
+  if (bf16)
+    hipLaunchKernelGGL(channel_amax_kernel<true>, grid, dim3(256), 0, s, src, rows, K, per, amax);
+  else
+    hipLaunchKernelGGL(channel_amax_kernel<false>, grid, dim3(256), 0, s, src, rows, K, per, amax);
+}
+}  // namespace
+
+hipError_t launch_channel_amax(const uint16_t* x, int32_t M, const float* w, int32_t N, int32_t K,
+                               uint32_t* ax_bits, uint32_t* aw_bits, hipStream_t s) {
+  hipLaunchKernelGGL(calib_zero_u32_kernel, dim3((K + 255) / 256), dim3(256), 0, s, ax_bits, K);
+  hipLaunchKernelGGL(calib_zero_u32_kernel, dim3((K + 255) / 256), dim3(256), 0, s, aw_bits, K);
+  launch_amax(true, x, M, K, ax_bits, s);
+  launch_amax(false, w, N, K, aw_bits, s);
+  return hipGetLastError();
+}
+
+hipError_t launch_smooth_scales(const uint32_t* ax_bits, const uint32_t* aw_bits, int32_t K, float alpha, float* d,
+                                float* dinv, hipStream_t s) {
+  hipLaunchKernelGGL(smooth_scale_kernel, dim3((K + 255) / 256), dim3(256), 0, s, ax_bits, aw_bits, K, alpha, d,
+                     dinv);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_f32(float* p, int32_t n, float v, hipStream_t s) {
+  hipLaunchKernelGGL(calib_fill_kernel, dim3((n + 255) / 256), dim3(256), 0, s, p, n, v);
   return hipGetLastError();
 }
 

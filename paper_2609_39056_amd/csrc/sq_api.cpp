@@ -139,6 +139,37 @@ size_t search_extra_bytes(int32_t S, SearchWs* out = nullptr, uint8_t* base = nu
   return off;
 }
 
+// scaling-objective area after the calibration workspace: amax bits of X and
+// W [K] | d [K] | dinv [K] | packed Q(D W) [N][K/2] | fp16 steps [K/w_group][N]
+// | a one-step gain table of ones [R]
+struct ScalingWs {
+  uint32_t *ax, *aw;
+  float *d, *dinv, *ones;
+  uint8_t* qw;
+  uint16_t* w_scale;
+};
+size_t scaling_extra_bytes(int32_t K, int32_t N, int32_t w_group, int32_t R, ScalingWs* out = nullptr,
+                           uint8_t* base = nullptr) {
+  const size_t parts[7] = {4ull * K, 4ull * K, 4ull * K, 4ull * K, static_cast<size_t>(N) * K / 2,
+                           static_cast<size_t>(K / w_group) * N * 2, 4ull * R};
+  size_t off = 0;
+  void* ptr[7];
+  for (int i = 0; i < 7; ++i) {
+    ptr[i] = base + off;
+    off += round_up(parts[i]);
+  }
+  if (out != nullptr) {
+    out->ax = static_cast<uint32_t*>(ptr[0]);
+    out->aw = static_cast<uint32_t*>(ptr[1]);
+    out->d = static_cast<float*>(ptr[2]);
+    out->dinv = static_cast<float*>(ptr[3]);
+    out->qw = static_cast<uint8_t*>(ptr[4]);
+    out->w_scale = static_cast<uint16_t*>(ptr[5]);
+    out->ones = static_cast<float*>(ptr[6]);
+  }
+  return off;
+}
+
 size_t unfused_ws_bytes(int32_t M, int32_t K, int32_t N, int32_t bits) {
   const size_t mk4 = round_up(static_cast<size_t>(M) * K * 4);
   const size_t mn4 = round_up(static_cast<size_t>(M) * N * 4);
@@ -252,7 +283,8 @@ CalibEval calib_eval_setup(const uint16_t* x, int32_t M, const int32_t* tok2stre
   return e;
 }
 
-sq_status calib_eval(const CalibEval& e, const float* gamma, const float* clip, double* out, hipStream_t stream) {
+sq_status calib_eval_range(const CalibEval& e, const float* gamma, const float* clip, int32_t range_mode, double* out,
+                           hipStream_t stream) {
   sq_act_params a{};
   a.tok2stream = e.tok2stream;
   a.gamma = gamma;
@@ -261,12 +293,16 @@ sq_status calib_eval(const CalibEval& e, const float* gamma, const float* clip, 
   a.num_streams = e.S;
   a.num_steps = 1;
   a.step = 0;
-  a.range_mode = SQ_RANGE_STATIC;
+  a.range_mode = range_mode;
   a.act_bits = e.act_bits;
   sq_status st = linear_fused(e.act_bits, e.x, e.M, &a, &e.wt, e.yq, SQ_OUT_F32, e.fused_ws, e.fused_bytes, stream);
   if (st != SQ_OK) return st;
   return hip_status(launch_calib_error(e.yq, e.y_ref, e.tok2stream, e.counts, e.omega, e.M, e.wt.N, e.S, e.err,
                                        out, stream));
+}
+
+sq_status calib_eval(const CalibEval& e, const float* gamma, const float* clip, double* out, hipStream_t stream) {
+  return calib_eval_range(e, gamma, clip, SQ_RANGE_STATIC, out, stream);
 }
 
 }  // namespace
@@ -421,8 +457,32 @@ sq_status sq_calib_reference(const uint16_t* x, int32_t M, const float* dinv, co
   if (!valid_m(M)) return SQ_ERR_SHAPE;
   if (!aligned(x, 16) || !aligned(y_ref, 16)) return SQ_ERR_ALIGN;
   if (dinv != nullptr && !aligned(dinv, 16)) return SQ_ERR_ALIGN;
-  CalibRefArgs a{x, dinv, w->qw, w->w_scale, y_ref, M, w->N, w->K, w->w_group};
+  CalibRefArgs a{x, dinv, w->qw, w->w_scale, nullptr, y_ref, M, w->N, w->K, w->w_group};
   return hip_status(launch_calib_reference(a, stream));
+}
+
+sq_status sq_calib_fp_reference(const uint16_t* x, int32_t M, const float* w, int32_t N, int32_t K, double* y_ref,
+                                hipStream_t stream) {
+  if (x == nullptr || w == nullptr || y_ref == nullptr) return SQ_ERR_NULL;
+  if (!valid_m(M) || !valid_k(K) || !valid_n(N)) return SQ_ERR_SHAPE;
+  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y_ref, 16)) return SQ_ERR_ALIGN;
+  CalibRefArgs a{x, nullptr, nullptr, nullptr, w, y_ref, M, N, K, 0};
+  return hip_status(launch_calib_reference(a, stream));
+}
+
+sq_status sq_smooth_scales(const uint16_t* x, int32_t M, const float* w, int32_t N, int32_t K, float alpha, float* d,
+                           float* dinv, hipStream_t stream) {
+  if (x == nullptr || w == nullptr || d == nullptr || dinv == nullptr) return SQ_ERR_NULL;
+  if (!valid_m(M) || !valid_k(K) || N < 1 || N > kMaxN) return SQ_ERR_SHAPE;
+  if (!std::isfinite(alpha)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(d, 4) || !aligned(dinv, 4)) return SQ_ERR_ALIGN;
+  if (d == dinv) return SQ_ERR_UNSUPPORTED;
+  // the amaxes land in the output buffers, which the last kernel overwrites in place
+  sq_status st = hip_status(launch_channel_amax(x, M, w, N, K, reinterpret_cast<uint32_t*>(d),
+                                                reinterpret_cast<uint32_t*>(dinv), stream));
+  if (st != SQ_OK) return st;
+  return hip_status(launch_smooth_scales(reinterpret_cast<const uint32_t*>(d), reinterpret_cast<const uint32_t*>(dinv),
+                                         K, alpha, d, dinv, stream));
 }
 
 size_t sq_calib_workspace_bytes(int32_t M, int32_t K, int32_t N, int32_t act_bits, int32_t num_streams) {
@@ -511,6 +571,57 @@ sq_status sq_calib_search(const uint16_t* x, int32_t M, const int32_t* tok2strea
     }
     st = hip_status(launch_calib_select(S, sw.cand_obj, sw.cand_u, sw.cand_v, sw.cand_gamma, sw.cand_clip, sw.st,
                                         sw.u, gamma_out, clip_out, objective_out, stream));
+    if (st != SQ_OK) return st;
+  }
+  return SQ_OK;
+}
+
+size_t sq_calib_scaling_workspace_bytes(int32_t M, int32_t K, int32_t N, int32_t w_group, int32_t act_bits,
+                                        int32_t num_regions) {
+  if (w_group < kKTile || w_group % kKTile != 0 || !valid_k(K) || K % w_group != 0) return 0;
+  const size_t base = sq_calib_workspace_bytes(M, K, N, act_bits, num_regions);
+  return base == 0 ? 0 : base + scaling_extra_bytes(K, N, w_group, num_regions);
+}
+
+sq_status sq_calib_scaling_objective(const uint16_t* x, int32_t M, const int32_t* region, int32_t num_regions,
+                                     const double* region_weight, const float* w, int32_t N, int32_t K,
+                                     int32_t w_group, int32_t act_bits, const double* y_ref, int32_t num_alphas,
+                                     const float* alphas, double* objective, void* workspace, size_t ws_bytes,
+                                     hipStream_t stream) {
+  if (x == nullptr || region == nullptr || region_weight == nullptr || w == nullptr || y_ref == nullptr ||
+      alphas == nullptr || objective == nullptr || workspace == nullptr)
+    return SQ_ERR_NULL;
+  if (act_bits != 8 && act_bits != 4) return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M) || !valid_k(K) || !valid_n(N) || num_regions < 1 || num_regions > kCalibMaxStreams ||
+      num_alphas < 1 || num_alphas > kCalibMaxCandidates)
+    return SQ_ERR_SHAPE;
+  if (w_group < kKTile || w_group % kKTile != 0 || K % w_group != 0) return SQ_ERR_UNSUPPORTED;
+  for (int32_t i = 0; i < num_alphas; ++i)
+    if (!std::isfinite(alphas[i])) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(w, 16) || !aligned(y_ref, 16) || !aligned(workspace, 16) || !aligned(region, 4) ||
+      !aligned(region_weight, 8) || !aligned(objective, 8))
+    return SQ_ERR_ALIGN;
+  const int32_t R = num_regions;
+  const size_t base = calib_ws_bytes(M, K, N, act_bits, R);
+  if (ws_bytes < base + scaling_extra_bytes(K, N, w_group, R)) return SQ_ERR_WORKSPACE;
+  ScalingWs sw;
+  scaling_extra_bytes(K, N, w_group, R, &sw, static_cast<uint8_t*>(workspace) + base);
+  // Q(D W) lands in the workspace; Eq. 7 has no gain: a one-step table of ones
+  sq_weight wt{sw.qw, sw.w_scale, nullptr, N, K, w_group};
+  CalibEval e = calib_eval_setup(x, M, region, R, sw.dinv, act_bits, &wt, y_ref, region_weight, workspace);
+  sq_status st = hip_status(launch_calib_counts(region, M, R, e.counts, stream));
+  if (st != SQ_OK) return st;
+  st = hip_status(launch_fill_f32(sw.ones, R, 1.0f, stream));
+  if (st != SQ_OK) return st;
+  st = hip_status(launch_channel_amax(x, M, w, N, K, sw.ax, sw.aw, stream));
+  if (st != SQ_OK) return st;
+  for (int32_t i = 0; i < num_alphas; ++i) {
+    st = hip_status(launch_smooth_scales(sw.ax, sw.aw, K, alphas[i], sw.d, sw.dinv, stream));
+    if (st != SQ_OK) return st;
+    PackArgs pk{w, sw.d, sw.qw, sw.w_scale, N, K, w_group};
+    st = hip_status(launch_pack_weights(pk, stream));
+    if (st != SQ_OK) return st;
+    st = calib_eval_range(e, sw.ones, nullptr, SQ_RANGE_DYNAMIC, objective + i, stream);
     if (st != SQ_OK) return st;
   }
   return SQ_OK;

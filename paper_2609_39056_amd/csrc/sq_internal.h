@@ -172,9 +172,17 @@ struct CalibRefArgs {
   const float* dinv;
   const uint8_t* qw;
   const uint16_t* w_scale;
-  double* y;  // [M][N] X~ W^
+  const float* wf;  // fp32 W [N][K]: the target is X W (no D^-1, no codes); NULL: X~ W^ from qw / w_scale
+  double* y;        // [M][N]
   int32_t M, N, K, w_group;
 };
+// per-channel amax of |x| (bf16 [M][K]) and |w| (fp32 [N][K]) as fp32 bits
+hipError_t launch_channel_amax(const uint16_t* x, int32_t M, const float* w, int32_t N, int32_t K,
+                               uint32_t* ax_bits, uint32_t* aw_bits, hipStream_t s);
+// d = clamp(ax^alpha / aw^(1 - alpha), 2^-6, 2^6) (fp64, 1 where an amax is 0), dinv = 1 / d
+hipError_t launch_smooth_scales(const uint32_t* ax_bits, const uint32_t* aw_bits, int32_t K, float alpha, float* d,
+                                float* dinv, hipStream_t s);
+hipError_t launch_fill_f32(float* p, int32_t n, float v, hipStream_t s);
 hipError_t launch_calib_reference(const CalibRefArgs& a, hipStream_t s);
 // counts[s] = tokens of stream s (ids outside [0, S) are not counted)
 hipError_t launch_calib_counts(const int32_t* tok2stream, int32_t M, int32_t S, int32_t* counts, hipStream_t s);

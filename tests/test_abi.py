@@ -239,3 +239,34 @@ def test_calib_search_workspace(L):
         assert n > B.sq_calib_workspace_bytes(M, K, N, 8, S) and n % 256 == 0
     assert B.sq_calib_search_workspace_bytes(M, K, N, 8, 65) == 0
     assert B.sq_calib_search_workspace_bytes(M, K, N, 8, 0) == 0
+
+
+def test_scaling_entry_points_reject(L):
+    """Eq. (7) entry points validate before launching."""
+    F = ctypes.c_float
+    assert L.sq_calib_fp_reference(None, 88, A, 256, 256, A, None) == NULL
+    assert L.sq_calib_fp_reference(A, 0, A, 256, 256, A, None) == SHAPE
+    assert L.sq_calib_fp_reference(A, 88, A, 100, 256, A, None) == SHAPE
+    assert L.sq_calib_fp_reference(A, 88, A + 4, 256, 256, A, None) == ALIGN
+    assert L.sq_smooth_scales(A, 88, A, 256, 256, F(0.5), None, A + 1024, None) == NULL
+    assert L.sq_smooth_scales(A, 88, A, 0, 256, F(0.5), A, A + 1024, None) == SHAPE
+    assert L.sq_smooth_scales(A, 88, A, 256, 200, F(0.5), A, A + 1024, None) == SHAPE
+    assert L.sq_smooth_scales(A, 88, A, 256, 256, F(float("nan")), A, A + 1024, None) == UNSUP
+    assert L.sq_smooth_scales(A, 88, A, 256, 256, F(0.5), A, A, None) == UNSUP
+    assert L.sq_smooth_scales(A + 2, 88, A, 256, 256, F(0.5), A, A + 1024, None) == ALIGN
+    assert B.sq_calib_scaling_workspace_bytes(1000, 2048, 4096, 128, 8, 6) > B.sq_calib_workspace_bytes(1000, 2048,
+                                                                                                        4096, 8, 6)
+    assert B.sq_calib_scaling_workspace_bytes(1000, 2048, 4096, 96, 8, 6) == 0
+    assert B.sq_calib_scaling_workspace_bytes(1000, 2048, 4096, 128, 8, 0) == 0
+    al = (F * 3)(0.0, 0.5, 1.0)
+    bad = (F * 2)(0.5, float("inf"))
+
+    def so(x=A, M=88, reg=A, R=3, rw=A, w=A, N=256, K=256, G=128, bits=8, ref=A, n=3, alphas=al, obj=A, ws=A,
+           nbytes=1 << 30):
+        return L.sq_calib_scaling_objective(x, M, reg, R, rw, w, N, K, G, bits, ref, n, alphas, obj, ws, nbytes, None)
+
+    for kw, code in [(dict(x=None), NULL), (dict(alphas=None), NULL), (dict(obj=None), NULL), (dict(bits=6), UNSUP),
+                     (dict(M=0), SHAPE), (dict(R=0), SHAPE), (dict(R=4097), SHAPE), (dict(n=0), SHAPE),
+                     (dict(G=96), UNSUP), (dict(alphas=bad, n=2), UNSUP), (dict(ref=A + 8), ALIGN),
+                     (dict(rw=A + 4), ALIGN), (dict(nbytes=4096), WS), (dict(N=100), SHAPE)]:
+        assert so(**kw) == code, kw

@@ -340,3 +340,93 @@ def test_calib_objective_max_rows(bits):
     # the last tiled copy of the target equals the block's
     tail = ref_big[M - L.x_bits.shape[0]:].cpu().numpy()
     assert np.all(np.abs(tail - ref) <= K * 2.0**-52 * abs_reference(L, pw, G))
+
+
+# ---------------------------------------------------------------- shared channel scaling, Eq. (7)
+@pytest.mark.parametrize("M,N", [(200, 192), (4500, 64)])
+def test_smooth_scales(M, N):
+    """d and 1/d of the family, bit-exact against the oracle for five
+    exponents, on a layer with x20 outlier channels (the clamp binds at alpha
+    = 1) and an all-zero channel (d = 1); 4500 rows span 71 row blocks of the
+    amax kernel."""
+    K = 256
+    L = synth.make_layer(K=K, N=N, stream_counts=(M - 30, 10, 20), T=1, seed=[70, M])
+    xb = L.x_bits.copy()
+    xb[:, 3] = 0
+    x = u16_to_dev(xb, torch.bfloat16)
+    w = f32_to_dev(L.w)
+    d = torch.empty(K, dtype=torch.float32, device="cuda")
+    dinv = torch.empty_like(d)
+    for alpha in (0.0, 0.25, 0.5, 0.75, 1.0):
+        B.sq_smooth_scales(x, w, alpha, d, dinv)
+        torch.cuda.synchronize()
+        want_d, want_dinv = O.smooth_scales(xb, L.w, alpha)
+        got_d, got_dinv = d.cpu().numpy(), dinv.cpu().numpy()
+        assert np.array_equal(got_d.view(np.uint32), want_d.view(np.uint32)), alpha
+        assert np.array_equal(got_dinv.view(np.uint32), want_dinv.view(np.uint32)), alpha
+        assert got_d[3] == 1.0
+    assert want_d.max() == 64.0  # alpha = 1: the clamp binds on the outlier channels
+
+
+@pytest.mark.parametrize("M,N", [(200, 192), (1, 64)])
+def test_calib_fp_reference(M, N):
+    """X W^T in fp64 against the oracle's full-precision product."""
+    K = 384
+    L = synth.make_layer(K=K, N=N, stream_counts=(M, 0, 0), T=1, seed=[71, M])
+    ref = torch.full((M, N), float("nan"), dtype=torch.float64, device="cuda")
+    B.sq_calib_fp_reference(u16_to_dev(L.x_bits, torch.bfloat16), f32_to_dev(L.w), ref)
+    want = O.full_precision_linear(L.x_bits, L.w)
+    scale = np.abs(O.bf16_bits_to_f32(L.x_bits).astype(np.float64)) @ np.abs(L.w.astype(np.float64)).T
+    assert np.all(np.abs(ref.cpu().numpy() - want) <= K * 2.0**-52 * scale)
+
+
+def scaling_bound(L, G, bits, region, R, weights, alphas, ref, ref_abs):
+    """As objective_bound, for Eq. (7)'s candidates (DYNAMIC ranges, unit
+    gains, the fp64 full-precision target)."""
+    K = L.x_bits.shape[1]
+    out = []
+    for alpha in alphas:
+        d, dinv = O.smooth_scales(L.x_bits, L.w, alpha)
+        pw = O.pack_weights(L.w, d, G)
+        res = O.linear(L.x_bits, region, np.ones((1, R), F32), 0, pw["codes"], pw["w_scale"], G, dinv=dinv,
+                       bias_bits=None, act_bits=bits)
+        e = np.abs(res["y64"] - ref)
+        t = 1e-5 * res["A"] + 2.0**-23 * np.abs(res["y64"]) + K * 2.0**-52 * ref_abs
+        row = (2 * e * t + t * t).sum(axis=1)
+        b = 0.0
+        for r in range(R):
+            n = int((region == r).sum())
+            if n:
+                b += float(weights[r]) / n * float(row[region == r].sum())
+        out.append(b)
+    return np.array(out)
+
+
+@pytest.mark.parametrize("G", [128, 256])
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("M", [37, 200])
+def test_calib_scaling_objective(M, bits, G):
+    """Eq. (7) for five exponents against the oracle within the derived bound,
+    with six regions (three streams x two step halves, uneven weights); the
+    GPU's best exponent is the oracle's within that bound."""
+    K, N = 256, 128
+    L = synth.make_layer(K=K, N=N, stream_counts=(M - M // 4 - M // 8, M // 8, M // 4), T=1, seed=[72, M, bits],
+                         permute=True)
+    R = 6
+    region = (L.tok2stream + 3 * (np.arange(M) % 2)).astype(np.int32)
+    weights = np.array([0.3, 0.1, 0.1, 0.3, 0.1, 0.1])
+    alphas = [0.0, 0.25, 0.5, 0.75, 1.0]
+    x, w = u16_to_dev(L.x_bits, torch.bfloat16), f32_to_dev(L.w)
+    ref_dev = torch.empty((M, N), dtype=torch.float64, device="cuda")
+    B.sq_calib_fp_reference(x, w, ref_dev)
+    ws = torch.empty(B.sq_calib_scaling_workspace_bytes(M, K, N, G, bits, R), dtype=torch.uint8, device="cuda")
+    obj = torch.full((len(alphas),), float("nan"), dtype=torch.float64, device="cuda")
+    B.sq_calib_scaling_objective(x, i32_to_dev(region), R, torch.as_tensor(weights, device="cuda"), w, G, bits,
+                                 ref_dev, alphas, obj, ws)
+    torch.cuda.synchronize()
+    got = obj.cpu().numpy()
+    ref = O.full_precision_linear(L.x_bits, L.w)
+    want = O.scaling_objective(L.x_bits, region, R, weights, L.w, G, alphas, act_bits=bits, ref=ref)
+    ref_abs = np.abs(O.bf16_bits_to_f32(L.x_bits).astype(np.float64)) @ np.abs(L.w.astype(np.float64)).T
+    bound = scaling_bound(L, G, bits, region, R, weights, alphas, ref, ref_abs)
+    check_objectives(got, want, bound)
