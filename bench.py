@@ -332,7 +332,8 @@ def calibration_figures(torch, B, ly, stream, dev, cpu_rows):
     over one batch of M tokens: the fp64 target X~ W^ (once per linear), the
     objective of a batch of candidates (each: the fused linear in STATIC mode,
     fp32 out, then the weighted squared error), the fused linear alone on the
-    same tables, and the constrained search.  HIP events on the stream the
+    same tables, the constrained search, and the shared-scaling objective of
+    Eq. (7) over 11 exponents of the D family.  HIP events on the stream the
     kernels run on."""
     L, W = ly["L"], ly["W_pc"]
     M, K, N = L.M, ly["K"], ly["N"]
@@ -380,6 +381,19 @@ def calibration_figures(torch, B, ly, stream, dev, cpu_rows):
     B.sq_calib_objective(x, t2s, S, dinv, 8, W, ref, torch.ones((1, S), dtype=torch.float32, device=dev),
                          torch.tensor([float(L.clip[0])], dtype=torch.float32, device=dev), omega, start, ws, stream)
     torch.cuda.synchronize()
+    # the shared scaling of Eq. 7 over 11 exponents: full-precision fp64 target,
+    # then per exponent D, Q(D W) packed on the GPU, the fused linear (DYNAMIC,
+    # unit gains) and the error weighted per stream (uniform)
+    alphas = [i / 10 for i in range(11)]
+    w32 = torch.from_numpy(L.w).to(dev)
+    ref_fp = torch.empty((M, N), dtype=torch.float64, device=dev)
+    ms_fp_ref = timed(lambda: B.sq_calib_fp_reference(x, w32, ref_fp, stream), 1)
+    ws_s = torch.empty(B.sq_calib_scaling_workspace_bytes(M, K, N, K, 8, S), dtype=torch.uint8, device=dev)
+    obj_s = torch.empty((len(alphas),), dtype=torch.float64, device=dev)
+    ms_scaling = timed(lambda: B.sq_calib_scaling_objective(x, t2s, S, omega, w32, K, 8, ref_fp, alphas, obj_s, ws_s,
+                                                            stream), 1)
+    scal = obj_s.cpu().numpy()
+    del ws_s, ref_fp, w32
     err_bytes = M * N * (4 + 8)  # the candidate's fp32 output and the fp64 target, read once
     us_err = (ms_obj - ms_lin) * 1e3
     out = {
@@ -394,6 +408,11 @@ def calibration_figures(torch, B, ly, stream, dev, cpu_rows):
         "search_ms": round(ms_search, 2), "search_rounds": CALIB_ROUNDS, "search_candidates": n_search,
         "search_objective_start": float(start.item()), "search_objective_end": float(o_out.item()),
         "search_gamma": [round(float(v), 5) for v in g_out.cpu()], "search_clip": round(float(c_out.item()), 5),
+        "scaling_fp_reference_ms": round(ms_fp_ref, 3),
+        "scaling_objective_us_per_exponent": round(ms_scaling * 1e3 / len(alphas), 1),
+        "scaling_exponents": len(alphas),
+        "scaling_best_alpha": alphas[int(np.argmin(scal))],
+        "scaling_objective_best": float(scal.min()), "scaling_objective_alpha0": float(scal[0]),
     }
     if cpu_rows is not None:
         out["cpu_oracle"] = calibration_cpu(L, K, cpu_rows)
