@@ -211,22 +211,48 @@ __global__ __launch_bounds__(256) void calib_zero_u32_kernel(uint32_t* __restric
   for (int32_t i = blockIdx.x * 256 + threadIdx.x; i < n; i += gridDim.x * 256) p[i] = 0u;
 }
 
-// One thread per channel; grid.y splits the rows.  BF16: x is bf16 bits,
-// otherwise fp32.
+// A workgroup covers 32 x CH channels (CH = 8 bf16 or 4 fp32: one 16-byte
+// load per row) and a range of rows (grid.y); its eight row lanes take every
+// eighth row, meet in LDS, and one atomic max per channel leaves the
+// workgroup.
+constexpr int kAmaxLanes = 32;
 template <bool BF16>
 __global__ __launch_bounds__(256) void channel_amax_kernel(const void* __restrict__ src, int64_t rows, int32_t K,
                                                            int64_t rows_per_block, uint32_t* __restrict__ amax) {
-  const int32_t k = blockIdx.x * 256 + threadIdx.x;
-  if (k >= K) return;
+  constexpr int CH = BF16 ? 8 : 4;
+  constexpr int WCH = kAmaxLanes * CH;  // channels per workgroup
+  __shared__ uint32_t red[8][WCH];
+  const int cl = threadIdx.x % kAmaxLanes, rl = threadIdx.x / kAmaxLanes;
+  const int32_t k0 = blockIdx.x * WCH + cl * CH;
   const int64_t r0 = static_cast<int64_t>(blockIdx.y) * rows_per_block;
   const int64_t r1 = min(rows, r0 + rows_per_block);
-  uint32_t m = 0u;
-  for (int64_t r = r0; r < r1; ++r) {
-    const uint32_t b = BF16 ? (static_cast<uint32_t>(static_cast<const uint16_t*>(src)[r * K + k] & 0x7FFFu) << 16)
-                            : (static_cast<const uint32_t*>(src)[r * K + k] & 0x7FFFFFFFu);
-    m = max(m, b);
+  const size_t row_bytes = static_cast<size_t>(K) * (BF16 ? 2 : 4);
+  uint32_t m[CH];
+#pragma unroll
+  for (int c = 0; c < CH; ++c) m[c] = 0u;
+  if (k0 < K) {
+    const uint8_t* base = static_cast<const uint8_t*>(src) + static_cast<size_t>(k0) * (BF16 ? 2 : 4);
+#pragma unroll 4
+    for (int64_t r = r0 + rl; r < r1; r += 8) {
+      const uint4 v = *reinterpret_cast<const uint4*>(base + static_cast<size_t>(r) * row_bytes);
+      const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+      for (int c = 0; c < CH; ++c) {
+        const uint32_t b = BF16 ? ((w[c >> 1] >> (16 * (c & 1))) & 0x7FFFu) << 16 : w[c] & 0x7FFFFFFFu;
+        m[c] = max(m[c], b);
+      }
+    }
   }
-  if (m != 0u) atomicMax(&amax[k], m);
+#pragma unroll
+  for (int c = 0; c < CH; ++c) red[rl][cl * CH + c] = m[c];
+  __syncthreads();
+  if (threadIdx.x < WCH) {
+    uint32_t v = red[0][threadIdx.x];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) v = max(v, red[i][threadIdx.x]);
+    const int32_t k = blockIdx.x * WCH + threadIdx.x;
+    if (k < K && v != 0u) atomicMax(&amax[k], v);
+  }
 }
 
 __global__ __launch_bounds__(256) void smooth_scale_kernel(const uint32_t* __restrict__ ax_bits,
@@ -394,11 +420,12 @@ hipError_t launch_calib_reference(const CalibRefArgs& a, hipStream_t s) {
 
 namespace {
 void launch_amax(bool bf16, const void* src, int64_t rows, int32_t K, uint32_t* amax, hipStream_t s) {
-  const int64_t rpb = 64;  // rows per workgroup: one atomic per channel per 64 rows
+  const int64_t rpb = 256;  // rows per workgroup: one atomic per channel per 256 rows
   const int64_t yb = (rows + rpb - 1) / rpb;
   const int64_t ybc = yb < 65535 ? yb : 65535;
   const int64_t per = (rows + ybc - 1) / ybc;
-  const dim3 grid((K + 255) / 256, static_cast<unsigned>(ybc));
+  const int wch = kAmaxLanes * (bf16 ? 8 : 4);
+  const dim3 grid((K + wch - 1) / wch, static_cast<unsigned>(ybc));
   if (bf16)
     hipLaunchKernelGGL(channel_amax_kernel<true>, grid, dim3(256), 0, s, src, rows, K, per, amax);
   else
