@@ -76,3 +76,65 @@ def test_graph_replays_match_eager(bits, M, K, N, per_channel):
         assert torch.equal(y.view(torch.int16), ref.view(torch.int16)), f"replay {rep}"
         assert torch.equal(y_gemm.view(torch.int32), ref_gemm.view(torch.int32)), f"replay {rep}"
     del g
+
+
+@pytest.mark.parametrize("bits", [8, 4])
+def test_graph_calibration_replays_match_eager(bits):
+    """The calibration calls captured as one HIP graph: the Eq. (9) objective
+    of four candidates and a three-round constrained search (its state stays
+    on the device between rounds), and the Eq. (7) objective over three
+    exponents.  Every replay equals the eager results bit for bit, with eager
+    calls on another layer's inputs overwriting the same workspaces between
+    replays."""
+    import numpy as np
+
+    from gpu_util import f32_to_dev, i32_to_dev
+
+    M, K, N, S = 200, 256, 128, 3
+    L1 = synth.make_layer(K=K, N=N, stream_counts=split(M), T=2, seed=[13, bits])
+    L2 = synth.make_layer(K=K, N=N, stream_counts=split(M), T=2, seed=[14, bits])
+    _, W = oracle_weight(L1, 128)
+    dev = lambda L: dict(x=u16_to_dev(L.x_bits, torch.bfloat16), t2s=i32_to_dev(L.tok2stream),
+                         dinv=f32_to_dev(L.dinv), w=f32_to_dev(L.w),
+                         ref=torch.empty((M, N), dtype=torch.float64, device="cuda"),
+                         fp=torch.empty((M, N), dtype=torch.float64, device="cuda"))
+    d1, d2 = dev(L1), dev(L2)
+    gam = f32_to_dev(np.concatenate([L1.gamma, L1.gamma[::-1] * 1.1]).astype(np.float32))
+    clip = f32_to_dev(np.array([L1.clip[0], L1.clip[1], L1.clip[0] * 0.8, L1.clip[1] * 1.2], np.float32))
+    om = torch.full((S,), 1.0 / S, dtype=torch.float64, device="cuda")
+    ws = torch.empty(max(B.sq_calib_search_workspace_bytes(M, K, N, bits, S),
+                         B.sq_calib_scaling_workspace_bytes(M, K, N, 128, bits, S)), dtype=torch.uint8, device="cuda")
+    obj = torch.empty(4, dtype=torch.float64, device="cuda")
+    g_out = torch.empty(S, dtype=torch.float32, device="cuda")
+    c_out = torch.empty(1, dtype=torch.float32, device="cuda")
+    o_out = torch.empty(1, dtype=torch.float64, device="cuda")
+    sobj = torch.empty(3, dtype=torch.float64, device="cuda")
+    p = B.sq_calib_search_params(0.5, 2.0, float(L1.clip[0]) / 4, float(L1.clip[0]) * 4, float(L1.clip[0]), 0.5, 3)
+
+    def call(d):
+        B.sq_calib_reference(d["x"], d["dinv"], W, d["ref"])
+        B.sq_calib_objective(d["x"], d["t2s"], S, d["dinv"], bits, W, d["ref"], gam, clip, om, obj, ws)
+        B.sq_calib_search(d["x"], d["t2s"], S, d["dinv"], bits, W, d["ref"], om, p, g_out, c_out, o_out, ws)
+        B.sq_calib_fp_reference(d["x"], d["w"], d["fp"])
+        B.sq_calib_scaling_objective(d["x"], d["t2s"], S, om, d["w"], 128, bits, d["fp"], [0.25, 0.5, 0.75], sobj, ws)
+
+    outs = lambda: [t.clone() for t in (obj, g_out, c_out, o_out, sobj)]
+    call(d1)
+    torch.cuda.synchronize()
+    ref = outs()
+    call(d2)
+    torch.cuda.synchronize()
+    other = outs()
+    assert not torch.equal(other[0], ref[0])
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(d1)
+    for rep in range(3):
+        call(d2)
+        torch.cuda.synchronize()
+        assert all(torch.equal(a, b) for a, b in zip(outs(), other))
+        g.replay()
+        torch.cuda.synchronize()
+        for a, b in zip(outs(), ref):
+            assert torch.equal(a, b), f"replay {rep}"
+    del g
