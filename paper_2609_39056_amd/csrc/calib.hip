@@ -1,13 +1,19 @@
-// Activation calibration (Sec. 4.3, Eq. 9): the reconstruction error of one
-// linear under a candidate (gain per stream, shared threshold), weighted per
-// stream by omega_s / n_s.
+// Calibration.  Activation calibration (Sec. 4.3, Eq. 9): the reconstruction
+// error of one linear under a candidate (gain per stream, shared threshold),
+// weighted per stream by omega_s / n_s, and a constrained search over
+// candidates.  Shared scaling (Sec. 4.2, Eq. 7): the same error against the
+// full-precision product for a family of channel scalings D.
 //
-//   - calib_reference_kernel: the target X~ W^ in fp64, X~ = fp32(x) * dinv
-//     (the quantizer's first step) and W^ = code * Delta_W.  Every product is
-//     exact in fp64 (24 x 15 significant bits), so the kernel differs from any
-//     other fp64 evaluation only in the order of its K sums.  128 x 128 output
-//     tiles, each thread 8 x 8 of them, K staged 16 at a time through LDS
-//     already widened to fp64.  Computed once per linear.
+//   - calib_reference_kernel<false>: the target X~ W^ in fp64, X~ = fp32(x) *
+//     dinv (the quantizer's first step) and W^ = code * Delta_W.  Every
+//     product is exact in fp64 (24 x 15 significant bits), so the kernel
+//     differs from any other fp64 evaluation only in the order of its K sums.
+//     128 x 128 output tiles, each thread 8 x 8 of them, K staged 16 at a time
+//     through LDS already widened to fp64.  Computed once per linear.
+//     calib_reference_kernel<true>: the same with fp32 W (the target X W of
+//     Eq. 7; products of 8 x 24 significant bits, exact).
+//   - channel_amax_kernel, smooth_scale_kernel: the per-channel maxima of |X|
+//     and |W| and the family d = amax|X|^alpha / amax|W|^(1 - alpha) of Eq. 7.
 //   - calib_count_kernel: n_s, the tokens of every stream (LDS histogram per
 //     workgroup, one global add per non-empty bin).
 //   - calib_row_error_kernel: e_i = omega_s(i) / n_s(i) * sum_j (y_ij - ref_ij)^2
