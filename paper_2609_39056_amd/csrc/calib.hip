@@ -19,8 +19,9 @@
 //   - calib_row_error_kernel: e_i = omega_s(i) / n_s(i) * sum_j (y_ij - ref_ij)^2
 //     for the candidate's fp32 output y, one wave per row, fixed order.
 //   - calib_sum_kernel: L = sum_i e_i in one workgroup, fixed order.
-// The candidate's output itself comes from the fused linear (STATIC range,
-// one step, no bias), so the objective measures the arithmetic that runs.
+// The candidate's output itself comes from the fused linear (no bias; STATIC
+// with the candidate's one-step table for Eq. 9, DYNAMIC with unit gains for
+// Eq. 7), so the objective measures the arithmetic that runs.
 #include "sq_internal.h"
 
 namespace sq {
