@@ -430,3 +430,56 @@ def test_calib_scaling_objective(M, bits, G):
     ref_abs = np.abs(O.bf16_bits_to_f32(L.x_bits).astype(np.float64)) @ np.abs(L.w.astype(np.float64)).T
     bound = scaling_bound(L, G, bits, region, R, weights, alphas, ref, ref_abs)
     check_objectives(got, want, bound)
+
+
+@pytest.mark.parametrize("bits,G", [(8, 2048), (4, 128)])
+def test_calib_objective_benchmark_shape(bits, G):
+    """The benchmark's calibration configuration: the 2B up projection
+    (2048 -> 8192) over 4192 tokens, in the launch configuration the
+    benchmark times (the tiled GEMM with its split tail; one weight step per
+    output channel for A8).  The 4192 rows are a 262-token block repeated 16
+    times, so the objective must equal the oracle's objective of the block
+    (within its bound); the search over the full batch is checked for its
+    constraints and its returned objective."""
+    K, N, R = 2048, 8192, 16
+    L = synth.make_layer(K=K, N=N, stream_counts=(256, 2, 4), T=2, seed=80, permute=True)
+    pw, W = weight(L, G)
+    gammas, clips = candidates(L, 1, seed=81)
+    omega = np.full(3, 1 / 3)
+    ref = O.calib_reference(L.x_bits, pw["codes"], pw["w_scale"], G, L.dinv)
+    want = O.calib_objective(L.x_bits, L.tok2stream, 3, pw["codes"], pw["w_scale"], G, gammas, clips, omega,
+                             dinv=L.dinv, act_bits=bits, ref=ref)
+    bound = objective_bound(L, pw, G, bits, gammas, clips, omega, ref, abs_reference(L, pw, G), 3)
+    x = u16_to_dev(L.x_bits, torch.bfloat16).repeat(R, 1)
+    t2s = i32_to_dev(L.tok2stream).repeat(R)
+    M = x.shape[0]
+    assert M == 4192
+    dinv = f32_to_dev(L.dinv)
+    ref_big = torch.empty((M, N), dtype=torch.float64, device="cuda")
+    B.sq_calib_reference(x, dinv, W, ref_big)
+    ws = torch.empty(B.sq_calib_search_workspace_bytes(M, K, N, bits, 3), dtype=torch.uint8, device="cuda")
+    obj = torch.full((len(clips),), float("nan"), dtype=torch.float64, device="cuda")
+    om = torch.as_tensor(omega, device="cuda")
+    B.sq_calib_objective(x, t2s, 3, dinv, bits, W, ref_big, f32_to_dev(gammas), f32_to_dev(clips), om, obj, ws)
+    torch.cuda.synchronize()
+    check_objectives(obj.cpu().numpy(), want, bound)
+    g = torch.empty(3, dtype=torch.float32, device="cuda")
+    c = torch.empty(1, dtype=torch.float32, device="cuda")
+    o = torch.empty(1, dtype=torch.float64, device="cuda")
+    bnds = (0.25, 4.0, float(F32(L.clip[0] / 8)), float(F32(L.clip[0] * 4)))
+    p = B.sq_calib_search_params(*bnds, float(L.clip[0]), 0.5, 4)
+    B.sq_calib_search(x, t2s, 3, dinv, bits, W, ref_big, om, p, g, c, o, ws)
+    torch.cuda.synchronize()
+    gam_np, c_np = g.cpu().numpy(), F32(c.cpu().numpy()[0])
+    n = np.bincount(L.tok2stream, minlength=3) * R
+    check_constraints(gam_np, c_np, n, bnds)
+    again = gpu_objective_dev(x, t2s, dinv, W, bits, ref_big, gam_np[None, :], np.array([c_np]), omega, ws)
+    assert again.view(np.uint64)[0] == np.float64(o.cpu().numpy()[0]).view(np.uint64)
+
+
+def gpu_objective_dev(x, t2s, dinv, W, bits, ref, gammas, clips, omega, ws):
+    obj = torch.full((len(clips),), float("nan"), dtype=torch.float64, device="cuda")
+    B.sq_calib_objective(x, t2s, len(omega), dinv, bits, W, ref, f32_to_dev(gammas), f32_to_dev(clips),
+                         torch.as_tensor(np.asarray(omega, np.float64), device="cuda"), obj, ws)
+    torch.cuda.synchronize()
+    return obj.cpu().numpy()
