@@ -483,3 +483,29 @@ def gpu_objective_dev(x, t2s, dinv, W, bits, ref, gammas, clips, omega, ws):
                          torch.as_tensor(np.asarray(omega, np.float64), device="cuda"), obj, ws)
     torch.cuda.synchronize()
     return obj.cpu().numpy()
+
+
+def test_calib_search_max_streams():
+    """The search at its stream limit (64 streams, a third of them without
+    tokens; 130 candidates a round): every constraint holds, streams without
+    tokens keep gamma = 1 (a step on them never improves the objective), the
+    returned objective is the evaluator's for the returned point, and it is no
+    worse than the start."""
+    K, N, G, bits, S = 256, 64, 128, 8, 64
+    rng = np.random.default_rng(90)
+    counts = [int(v) if i % 3 else 0 for i, v in enumerate(rng.integers(1, 9, S))]
+    L = synth.make_layer(K=K, N=N, stream_counts=tuple(counts), T=1, seed=91, permute=True)
+    assert L.gamma.shape[1] == S
+    n = np.bincount(L.tok2stream, minlength=S)
+    pw, W = weight(L, G)
+    ref_dev = gpu_reference(L, W)
+    omega = np.full(S, 1.0 / S)
+    bounds = (0.5, 2.0, float(F32(L.clip[0] / 4)), float(F32(L.clip[0] * 2)))
+    g, c, obj = gpu_search(L, W, bits, omega, ref_dev, bounds, L.clip[0], 0.5, 3)
+    check_constraints(g, c, n, bounds)
+    assert np.all(g[n == 0] == 1.0)
+    again = gpu_objective(L, W, bits, g[None, :], np.array([c]), omega, ref_dev)
+    assert again.view(np.uint64)[0] == np.float64(obj).view(np.uint64)
+    c0 = np.clip(F32(L.clip[0]), F32(bounds[2]), F32(bounds[3]))
+    start = gpu_objective(L, W, bits, np.ones((1, S), F32), np.array([c0]), omega, ref_dev)[0]
+    assert obj <= start
