@@ -14,8 +14,13 @@ kernels, for the per-kernel figures and the roofline of the GEMM.
 
 Prints one JSON line.  Besides the contract fields it carries the roofline of
 the dominant kernel (the GEMM, against the int8 MFMA peak), the unfused
-variant and the W4A4 variant on the same layers, and the CPU oracle timed on a
-bounded row sample.
+variant and the W4A4 variant on the same layers, the calibration path
+(Eq. (9) objective and search, Eq. (7) scaling objective) on the up
+projection, and the CPU oracle timed on a bounded row sample.
+
+Other modes: --suite PATH (every layer configuration and the denoising-loop
+sweeps, one JSON record per line) and --action-only TOKENS (the few-token,
+weight-streaming regime alone).
 """
 from __future__ import annotations
 
