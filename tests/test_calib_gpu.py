@@ -122,7 +122,7 @@ def test_calib_reference(M, N, G, use_dinv):
 
 @pytest.mark.parametrize("G", [128, 256])
 @pytest.mark.parametrize("bits", [8, 4])
-@pytest.mark.parametrize("M", [37, 200])
+@pytest.mark.parametrize("M", [1, 37, 200])
 def test_calib_objective(M, bits, G):
     """Seven candidates on a three-stream layer (permuted rows), uniform and
     uneven stream weights: 37 tokens (weight-streaming GEMM) and 200 (tiled;
@@ -404,7 +404,7 @@ def scaling_bound(L, G, bits, region, R, weights, alphas, ref, ref_abs):
 
 @pytest.mark.parametrize("G", [128, 256])
 @pytest.mark.parametrize("bits", [8, 4])
-@pytest.mark.parametrize("M", [37, 200])
+@pytest.mark.parametrize("M", [1, 37, 200])
 def test_calib_scaling_objective(M, bits, G):
     """Eq. (7) for five exponents against the oracle within the derived bound,
     with six regions (three streams x two step halves, uneven weights); the
