@@ -314,7 +314,8 @@ typedef struct sq_calib_search_params {
   float gamma_min, gamma_max; /* 0 < gamma_min <= 1 <= gamma_max */
   float clip_min, clip_max;   /* 0 < clip_min <= clip_max */
   float clip_init;            /* start threshold (finite) */
-  float log_step;             /* initial step h > 0 in log space */
+  float log_step;             /* initial step h in log space, 0 < h <= 64 (the projection's 64
+                                 bisection halvings then resolve lambda to fp64 precision) */
   int32_t rounds;             /* 0 .. 1024 (0: evaluate the start only) */
 } sq_calib_search_params;
 

@@ -540,7 +540,7 @@ sq_status sq_calib_search(const uint16_t* x, int32_t M, const int32_t* tok2strea
   const bool ok_bounds = std::isfinite(p.gamma_min) && std::isfinite(p.gamma_max) && std::isfinite(p.clip_min) &&
                          std::isfinite(p.clip_max) && std::isfinite(p.clip_init) && std::isfinite(p.log_step) &&
                          p.gamma_min > 0.0f && p.gamma_min <= 1.0f && p.gamma_max >= 1.0f && p.clip_min > 0.0f &&
-                         p.clip_min <= p.clip_max && p.log_step > 0.0f;
+                         p.clip_min <= p.clip_max && p.log_step > 0.0f && p.log_step <= 64.0f;
   if (!ok_bounds) return SQ_ERR_UNSUPPORTED;
   if (!aligned(x, 16) || !aligned(y_ref, 16) || !aligned(workspace, 16) || !aligned(tok2stream, 4) ||
       !aligned(omega, 8) || !aligned(gamma_out, 4) || !aligned(clip_out, 4) || !aligned(objective_out, 8))

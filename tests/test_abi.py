@@ -223,7 +223,7 @@ def _sp(**kw):
     (dict(M=0), SHAPE), (dict(S=0), SHAPE), (dict(S=65), SHAPE), (dict(p=_sp(rounds=-1)), SHAPE),
     (dict(p=_sp(rounds=1025)), SHAPE), (dict(p=_sp(gamma_min=0.0)), UNSUP), (dict(p=_sp(gamma_min=1.5)), UNSUP),
     (dict(p=_sp(gamma_max=0.9)), UNSUP), (dict(p=_sp(clip_min=0.0)), UNSUP), (dict(p=_sp(clip_max=0.05)), UNSUP),
-    (dict(p=_sp(log_step=0.0)), UNSUP), (dict(p=_sp(clip_init=float("inf"))), UNSUP),
+    (dict(p=_sp(log_step=0.0)), UNSUP), (dict(p=_sp(log_step=65.0)), UNSUP), (dict(p=_sp(clip_init=float("inf"))), UNSUP),
     (dict(p=_sp(gamma_max=float("nan"))), UNSUP), (dict(x=A + 2), ALIGN), (dict(ref=A + 8), ALIGN),
     (dict(om=A + 4), ALIGN), (dict(g=A + 2), ALIGN), (dict(obj=A + 4), ALIGN), (dict(nbytes=4096), WS),
     (dict(w=wt(K=200)), SHAPE),
