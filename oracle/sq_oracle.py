@@ -374,9 +374,10 @@ def weighted_stream_error(y, ref, ids, num_ids, omega):
 
 
 # ---------------------------------------------------------------- constrained search, Eq. (9)
-# The paper fixes the constraints of the joint (gamma, c) calibration (bounds
-# on c and on every gamma_s, and sum_s n_s log gamma_s = 0) but names no
-# search procedure.  The reading here: a compass (pattern) search in the log
+# Sec. 4.3 (the constraints under Eq. (9)) and App. C.1 fix the constraints of
+# the joint (gamma, c) calibration (bounds on c and on every gamma_s, and
+# sum_s n_s log gamma_s = 0, which makes c the token-weighted geometric mean
+# of the effective thresholds c / gamma_s) but name no search procedure.  The reading here: a compass (pattern) search in the log
 # coordinates (log gamma_1 .. log gamma_S, log c), each trial point projected
 # back onto the constraint set, with the step halved after a round that finds
 # no better point.
