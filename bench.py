@@ -708,7 +708,7 @@ def main():
             "act_bits": 8, "w_group": W_GROUP,
         },
         "roofline": {
-            "bound": "mfma", "kernel": "gemm_pipe_kernel<8,0,false> + gemm_tail_kernel<8,0,false> (sq_gemm_w4a8)",
+            "bound": "mfma", "kernel": "gemm_pipe16_kernel<0> + gemm_tail_kernel<8,0,false> (sq_gemm_w4a8)",
             "launches": 2 * len(evs),
             "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",
             "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": measured_traffic(),

@@ -46,6 +46,7 @@ constexpr int TM = 2;        // 32-row MFMA tiles per wave
 constexpr int TN = 2;        // 32-col MFMA tiles per wave
 constexpr int GROUP_M = 8;   // m-tiles per supertile (L2 reuse)
 constexpr bool kPipeWide = false;  // tile shape of the pipelined kernel (see Cfg)
+constexpr bool kPipe16 = true;     // 8-bit, 128-wide groups: the GEMM on 16 x 16 x 64 MFMAs (gemm_pipe16_kernel)
 
 // Workgroup shape: NWM x NWN waves of 64 x 64 outputs (the most a wave's
 // registers hold: an int32 accumulator and an fp32 sum per output); a
@@ -687,6 +688,279 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
+// ---------------------------------------------------------------- 8-bit activations on 16 x 16 MFMA tiles
+// The pipelined 8-bit GEMM with 128-wide weight groups on
+// v_mfma_i32_16x16x64_i8: the same tiles, work list, loads, LDS layout, stage
+// barrier and split tail as gemm_pipe_kernel, with each wave's 64 x 64
+// outputs as 4 x 4 tiles of 16 x 16 (two MFMAs of 64 channels per 128-channel
+// stage, each block's fold on four registers per tile).  In a register-only
+// loop with random int8 operands and the per-block fold this instruction
+// sustains about 1.5x the rate of the 32 x 32 x 32 one under the board's power
+// limit; in the GEMM it gains 0-5 % (2B up about equal, 2B and 14B down 2-5 %
+// faster).  With one weight step per channel (no fold) the 32 x 32 kernel
+// stays, which was as fast or faster there.
+//
+// Lane (row or column lane & 15, g = lane >> 4) feeds k-step s (0, 1) of a
+// stage with the channels [32 g + 16 s, +16): for 8-bit activations the
+// 16-byte chunk 2 g + s of the row, for packed weights the low (s = 0) or high
+// (s = 1) half of chunk g of the column, so one 16-byte read serves both
+// k-steps.  Both operands use the same assignment.  An accumulator lane holds
+// column lane & 15 and rows 4 (lane >> 4) + j, j < 4.
+constexpr int TM16 = 4, TN16 = 4;  // 16 x 16 tiles per wave
+
+struct FragOffsets16 {
+  int a0[2];
+  int b0;
+  __device__ __forceinline__ FragOffsets16(int wm, int wn, int lane) {
+    using LY = Layout<8, false>;
+    const int g = lane >> 4;
+    const int arow0 = wm * 64 + (lane & 15);
+    const int bcol0 = wn * 64 + (lane & 15);
+#pragma unroll
+    for (int s = 0; s < 2; ++s) a0[s] = arow0 * KT + 16 * ((2 * g + s) ^ ((arow0 >> 1) & 7));
+    b0 = LY::A_BYTES + bcol0 * (KT / 2) + 16 * (g ^ ((bcol0 >> 2) & 3));
+  }
+  // a 16-row step keeps the swizzle term ((row >> 1) & 7 and (col >> 2) & 3)
+  __device__ __forceinline__ int a(int tm, int s) const { return a0[s] + tm * 16 * KT; }
+  __device__ __forceinline__ int b(int tn) const { return b0 + tn * 16 * (KT / 2); }
+};
+
+__device__ __forceinline__ void fold8_biased4(const v4i& c, float w, float (&yt)[4]) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) yt[r] = __builtin_fmaf(__int_as_float(c[r]) - 12582912.0f, w, yt[r]);
+}
+
+// the weight steps of a stage for the lane's column of each 16-wide tile
+__device__ __forceinline__ void read_wscale16(const uint8_t* st, int wave, int lane, float (&w)[TN16]) {
+  using LY = Layout<8, false>;
+  const uint32_t* Wst = reinterpret_cast<const uint32_t*>(st + LY::A_BYTES + LY::B_BYTES + wave * 256);
+#pragma unroll
+  for (int tn = 0; tn < TN16; ++tn) {
+    const int c = tn * 16 + (lane & 15);  // column within the wave's 64
+    const uint32_t pair = Wst[c >> 1];
+    w[tn] = f16_to_f32((c & 1) ? (pair >> 16) : (pair & 0xFFFFu)) * 0.0625f;  // widened codes: factor 16
+  }
+}
+
+// Row factor of row m0 + wm * 64 + lane and the bias of the lane's column in
+// each 16-wide tile, loaded when a tile starts.
+template <int EPI>
+struct EpiInputs16 {
+  float rowf;
+  float bias[TN16];
+  __device__ __forceinline__ void load(const GemmArgs& a, int m0, int n0, int wm, int wn, int lane) {
+    const int m = min(m0 + wm * 64 + lane, a.M - 1);
+    rowf = EPI == kEpiOut ? static_cast<const float*>(a.act_scale)[m] : 1.0f;
+#pragma unroll
+    for (int tn = 0; tn < TN16; ++tn) {
+      const int n = min(n0 + wn * 64 + tn * 16 + (lane & 15), a.N - 1);
+      bias[tn] = (EPI == kEpiOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
+    }
+  }
+};
+
+// Epilogue of one 128 x 128 tile from the 16 x 16 accumulator layout: row
+// factor and bias per lane (one column, four rows), a quad transpose to one
+// row and four consecutive columns, then 16-byte (fp32) or 8-byte stores.
+template <int EPI>
+__device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16][TN16][4], int m0, int n0, int wm,
+                                             int wn, int lane_in, const EpiInputs16<EPI>& in) {
+  int lane = lane_in;
+  asm volatile("" : "+v"(lane));
+  const int M = a.M, N = a.N;
+  if (n0 + wn * 64 >= N) return;  // N % 64 == 0: a wave's 64 columns are all in or all out
+  const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
+  const int rf_bits = __float_as_int(in.rowf);
+  const int q4 = (lane >> 4) * 4;
+#pragma unroll
+  for (int tm = 0; tm < TM16; ++tm) {
+    float rowf[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      rowf[j] = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 16 + q4 + j) * 4, rf_bits));
+#pragma unroll
+    for (int tn = 0; tn < TN16; ++tn) {
+      float v[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        v[j] = EPI == kEpiPartial ? y[tm][tn][j] : __builtin_fmaf(y[tm][tn][j], rowf[j], in.bias[tn]);
+      quad_transpose(v, lane);
+      const int m = m0 + wm * 64 + tm * 16 + q4 + (lane & 3);
+      const int n = n0 + wn * 64 + tn * 16 + (lane & 12);
+      if (m < M) {
+        if (f32out) {
+          *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * N + n) =
+              make_float4(v[0], v[1], v[2], v[3]);
+        } else {
+          uint2 w;
+          if (a.out_dtype == SQ_OUT_BF16) {
+            const bf16x2 lo = __builtin_convertvector((float2v){v[0], v[1]}, bf16x2);
+            const bf16x2 hi = __builtin_convertvector((float2v){v[2], v[3]}, bf16x2);
+            w = make_uint2(__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi));
+          } else {
+            w = make_uint2(f32_to_f16(v[0]) | (f32_to_f16(v[1]) << 16), f32_to_f16(v[2]) | (f32_to_f16(v[3]) << 16));
+          }
+          *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + static_cast<size_t>(m) * N + n) = w;
+        }
+      }
+    }
+  }
+}
+
+// A split range's sums of one 128 x 128 tile in the layout of
+// gemm_tail_kernel's partial buffer (row-major tile, rows past M not written).
+__device__ __forceinline__ void write_partial16(const GemmArgs& a, const float (&y)[TM16][TN16][4], int unit, int m0,
+                                                int wm, int wn, int lane_in) {
+  constexpr int BM = Cfg<8, false>::BM, BN = Cfg<8, false>::BN;
+  int ln = lane_in;
+  asm volatile("" : "+v"(ln));
+  float* P = a.partial + static_cast<size_t>(unit) * BM * BN;
+#pragma unroll
+  for (int tm = 0; tm < TM16; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN16; ++tn)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = wm * 64 + tm * 16 + (ln >> 4) * 4 + j;
+        if (m0 + row < a.M) P[row * BN + wn * 64 + tn * 16 + (ln & 15)] = y[tm][tn][j];
+      }
+}
+
+template <int EPI>
+__global__ __launch_bounds__(256, 2) void gemm_pipe16_kernel(GemmArgs a) {
+  using LY = Layout<8, false>;
+  using CF = Cfg<8, false>;
+  static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
+  constexpr int BM = CF::BM, BN = CF::BN;
+  constexpr int NDMA = LY::A_DMA + LY::B_DMA + 1;
+  constexpr int AHEAD = (CF::DIST - 1) * NDMA;
+  constexpr uint32_t RING = CF::STAGES * LY::STAGE;
+
+  __shared__ __align__(1024) uint8_t smem[RING];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm = wave / CF::NWN, wn = wave % CF::NWN;
+  const int M = a.M, N = a.N, K = a.K;
+  const int ntm = (M + BM - 1) / BM, ntn = (N + BN - 1) / BN, nkt = K / KT;
+  const int nitems = a.ndp + (ntm * ntn - a.ndp) * a.split;
+  const int G = gridDim.x;
+  if (static_cast<int>(blockIdx.x) >= nitems) return;
+  const uint32_t smem_lds = lds_offset(smem);
+
+  auto item_of = [&](int it) { return pipe_item(a, it, ntm, ntn, nkt, BM, BN); };
+
+  // the load cursor: (item, stage) two stages ahead of the computation
+  int d_it = blockIdx.x;
+  PipeItem d = item_of(d_it);
+  int d_kt = d.kt0;
+  uint32_t d_slot = 0;
+  StageLoads<8, false> ld;
+  ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
+  auto issue = [&]() {
+    ld.template issue<false, true>(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
+    d_slot = d_slot + LY::STAGE == RING ? 0 : d_slot + LY::STAGE;
+  };
+  // past the last stage of the last item the same stage is loaded again (in
+  // bounds, into a free slot), so every iteration issues the same loads
+  auto advance = [&]() {
+    if (d_kt + 1 < d.kt1) {
+      ++d_kt;
+    } else if (d_it + G < nitems) {
+      d_it += G;
+      d = item_of(d_it);
+      d_kt = d.kt0;
+      ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
+    }
+  };
+
+  const FragOffsets16 off(wm, wn, lane);
+#pragma unroll
+  for (int i = 0; i < CF::DIST; ++i) {
+    issue();
+    advance();
+  }
+  wait_vm_and_barrier<AHEAD>();
+
+  uint32_t c_slot = 0;
+  auto next_slot = [&](uint32_t s) { return s + LY::STAGE == RING ? 0u : s + LY::STAGE; };
+
+  // the accumulators are set once: each tile's first fold scales whatever
+  // they hold (finite values) by a zero step
+  v4i acc[TM16][TN16];
+#pragma unroll
+  for (int tm = 0; tm < TM16; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN16; ++tn) acc[tm][tn] = (v4i)(0);
+  // each block's sum starts from the bits of 1.5 * 2^23 (fold8_biased4); |16 C|
+  // <= 128 * 128 * 128 = 2^21 for any int8 codes, inside the exact range
+  const v4i magic = (v4i)(kMagicAcc);
+  for (int it = blockIdx.x;;) {
+    const PipeItem c = item_of(it);
+    EpiInputs16<EPI> ein;
+    ein.load(a, c.m0, c.n0, wm, wn, lane);
+    float y[TM16][TN16][4];
+    {
+      float wsv_prev[TN16], wsv[TN16];
+#pragma unroll
+      for (int tm = 0; tm < TM16; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN16; ++tn)
+#pragma unroll
+          for (int j = 0; j < 4; ++j) y[tm][tn][j] = 0.0f;
+#pragma unroll
+      for (int tn = 0; tn < TN16; ++tn) wsv_prev[tn] = 0.0f;  // the fold before the first block adds 0
+      for (int kt = c.kt0; kt < c.kt1; ++kt) {
+        issue();
+        advance();
+        const uint8_t* st = smem + c_slot;
+        read_wscale16(st, wave, lane, wsv);
+        v4i bq[TN16][2];
+#pragma unroll
+        for (int tn = 0; tn < TN16; ++tn) {
+          const uint4 pb = *reinterpret_cast<const uint4*>(st + off.b(tn));
+          bq[tn][0] = unpack_frag(pb.x, pb.y);
+          bq[tn][1] = unpack_frag(pb.z, pb.w);
+        }
+#pragma unroll
+        for (int tm = 0; tm < TM16; ++tm) {
+          const v4i a0 = *reinterpret_cast<const v4i*>(st + off.a(tm, 0));
+          const v4i a1 = *reinterpret_cast<const v4i*>(st + off.a(tm, 1));
+#pragma unroll
+          for (int tn = 0; tn < TN16; ++tn) {
+            fold8_biased4(acc[tm][tn], wsv_prev[tn], y[tm][tn]);
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0, bq[tn][0], magic, 0, 0, 0);
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1, bq[tn][1], acc[tm][tn], 0, 0, 0);
+          }
+        }
+        // issue order: each MFMA followed by a share of the VALU work (folds,
+        // unpacking), so the VALU runs under the matrix cores
+#pragma unroll
+        for (int i = 0; i < TM16 * TN16 * 2; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // up to five VALU
+        }
+#pragma unroll
+        for (int tn = 0; tn < TN16; ++tn) wsv_prev[tn] = wsv[tn];
+        wait_vm_and_barrier<AHEAD>();
+        c_slot = next_slot(c_slot);
+      }
+#pragma unroll
+      for (int t = 0; t < TM16 * TN16; ++t)
+        fold8_biased4(acc[t / TN16][t % TN16], wsv_prev[t % TN16], y[t / TN16][t % TN16]);
+    }
+
+    if (c.unit >= 0) {
+      write_partial16(a, y, c.unit, c.m0, wm, wn, lane);
+    } else {
+      store_tile16<EPI>(a, y, c.m0, c.n0, wm, wn, lane, ein);
+    }
+    it += G;
+    if (it >= nitems) break;
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
 // ---------------------------------------------------------------- 4-bit activations on the fp8 matrix cores
 // The fused linear's 4-bit path for the tiled kernel.  The first kernel wrote
 // each activation code as the fp8 e4m3 byte of code * 2^-9 (sign and
@@ -1200,7 +1474,10 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
     const int rest = p.ntiles - p.ndp;
     const int nitems = p.ndp + rest * p.split;
     const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
-    hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI, PC>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
+    if constexpr (ABITS == 8 && !PC && kPipe16)
+      hipLaunchKernelGGL((gemm_pipe16_kernel<EPI>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
+    else
+      hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI, PC>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || rest == 0 || p.split == 1) return e;
     constexpr int per_tile_blocks = CF::BM * CF::BN / 4 / 256;
