@@ -698,7 +698,8 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
 // sustains about 1.5x the rate of the 32 x 32 x 32 one under the board's power
 // limit; in the GEMM it gains 0-5 % (2B up about equal, 2B and 14B down 2-5 %
 // faster).  With one weight step per channel (no fold) the 32 x 32 kernel
-// stays, which was as fast or faster there.
+// stays, which was as fast or faster there, and so it does for the fp32
+// partial sums of the unfused path, whose 16 x 16 stores cover half a line.
 //
 // Lane (row or column lane & 15, g = lane >> 4) feeds k-step s (0, 1) of a
 // stage with the channels [32 g + 16 s, +16): for 8-bit activations the
@@ -1474,7 +1475,7 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
     const int rest = p.ntiles - p.ndp;
     const int nitems = p.ndp + rest * p.split;
     const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
-    if constexpr (ABITS == 8 && !PC && kPipe16)
+    if constexpr (ABITS == 8 && !PC && EPI == kEpiOut && kPipe16)
       hipLaunchKernelGGL((gemm_pipe16_kernel<EPI>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
     else
       hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI, PC>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
