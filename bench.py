@@ -1,22 +1,31 @@
-"""Benchmark of the fused W4A8 linear on one MI355X.
+"""Benchmark of the fused W4A8 / W4A4 linear on one MI355X.
 
-Workload: the 2B-class world-action DiT MLP pair at W4A8, hidden 2048 -> 8192
--> 2048, 4096 video + 32 proprio + 64 action tokens (M = 4192), per-step
-per-stream gain tables for 10 denoising steps, int4 weights with fp16 steps
-per 128-wide group.  One step = one pass of the hot path over the batch: for
-the up and the down projection, the first kernel (channel scaling, stream
-gain, per-token int8 quantization) and the second (int8-MFMA GEMM against the
-int4 weight with the dequantization / compensation / bias epilogue), bf16
-output, as one fused C-ABI call per layer (sq_linear_w4a8).  The denoising
-step index tau cycles through the table.  A second pass issues the same work
-as separate sq_quantize_act / sq_gemm_w4a8 calls with HIP events around the
-kernels, for the per-kernel figures and the roofline of the GEMM.
+Workload of the headline line: the linears of one 14B-class world-action DiT
+block at W4A8 -- qkv 5120->15360, out 5120->5120, up 5120->13824, down
+13824->5120 -- over 8384 tokens (8192 video + 64 proprio + 128 action), per-step
+per-stream gain tables for 10 denoising steps, int4 weights with fp16 steps per
+128-wide group, per-token int8 activations (DYNAMIC range), bf16 output.  This
+is the largest layer configuration that runs on one GPU.  One step = one pass
+of the hot path over the batch: for each of the four linears, the first kernel
+(channel scaling, stream gain, per-token int8 quantization) and the second
+(int8-MFMA GEMM against the int4 weight with the dequantization /
+compensation / bias epilogue), as one fused C-ABI call per linear
+(sq_linear_w4a8).  The denoising step index tau cycles through the table.
+Inputs are drawn on the GPU and resident in HBM before the timed region.
+
+A second pass issues the same work as separate sq_quantize_act / sq_gemm_w4a8
+calls (the fused call's two launches) with HIP events around every kernel of
+every step, on the stream the kernels run on: the per-kernel figures and the
+roofline of the GEMM.
 
 Prints one JSON line.  Besides the contract fields it carries the roofline of
-the dominant kernel (the GEMM, against the int8 MFMA peak), the unfused
-variant and the W4A4 variant on the same layers, the calibration path
-(Eq. (9) objective and search, Eq. (7) scaling objective) on the up
-projection, and the CPU oracle timed on a bounded row sample.
+the dominant kernel (the GEMM, against the int8 MFMA peak and the matrix-core
+rate measured with the same instruction and fold), the fused W4A4 linear, the
+unfused variant and the per-output-channel weight steps on the same block, the
+2B-class MLP pair (4192 tokens) and the 2B-class block at batch 4 (16768
+tokens) as extra records, the calibration path (Eq. (9) objective and search,
+Eq. (7) scaling objective) on the 2B up projection, and the CPU oracle timed on
+a stratified row sample of the 14B block.
 
 Other modes: --suite PATH (every layer configuration and the denoising-loop
 sweeps, one JSON record per line) and --action-only TOKENS (the few-token,
@@ -41,22 +50,19 @@ if ROOT not in sys.path:
 PEAK_INT8_TOPS = 5000.0      # MI355X dense int8 MFMA, 5.0 POP/s
 PEAK_HBM_GBS = 8000.0        # MI355X HBM3E, 8 TB/s
 COPY_MIB = 512               # plain device copy run after the timed region (counter calibration)
-TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_w4a8_2B_mlp_M4192_hbm_traffic.md")
+TRAFFIC_SUMMARY = os.path.join(ROOT, "profiles", "gemm_w4a8_14B_block_M8384_hbm_traffic.md")
 GEMM_SOURCES = ("paper_2609_39056_amd/csrc/gemm_w4.hip", "paper_2609_39056_amd/csrc/gemm_frag.h",
                 "paper_2609_39056_amd/csrc/sq_internal.h")
-TOKENS = (4096, 32, 64)
-LINEARS = (("up", 2048, 8192), ("down", 8192, 2048))
 T_STEPS = 10
 W_GROUP = 128
+MLP_2B = (("up", 2048, 8192), ("down", 8192, 2048))
 
 
 def parse():
     p = argparse.ArgumentParser()
     p.add_argument("--gpus", type=int, default=1)
-    p.add_argument("--steps", type=int, default=200)
-    p.add_argument("--warmup", type=int, default=20)
-    p.add_argument("--sample-every", type=int, default=4,
-                   help="per-kernel HIP events on steps/n steps of the per-kernel pass (events cost host time)")
+    p.add_argument("--steps", type=int, default=100)
+    p.add_argument("--warmup", type=int, default=10)
     p.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     p.add_argument("--suite", metavar="PATH", default=None,
                    help="instead of the one-line benchmark, measure every layer configuration (per-layer "
@@ -66,27 +72,47 @@ def parse():
                    help="time the 2B-class linears on TOKENS action tokens only (the weight-streaming regime): "
                         "28 layers x {qkv, out, up, down} with distinct weights, W4A8 and W4A4, eager calls; "
                         "one JSON line per width (for HBM-traffic counters)")
-    p.add_argument("--cpu-rows", type=int, default=0,
-                   help="rows of each layer the oracle times (0 = all: one whole step)")
+    p.add_argument("--cpu-video-rows", type=int, default=256,
+                   help="video rows per layer in the oracle's stratified sample (all proprio / action rows too)")
     return p.parse_args()
 
 
-def make_layers(torch, B, synth, dev):
+def device_block(torch, B, synth, dev, linears, tokens, seed, batch=1, per_channel=False):
+    """The linears of one block, drawn on the GPU (synth.device_layer), with
+    weights prepared on the GPU (sq_pack_weights).  Keeps each fp32 weight on
+    the host for the oracle's baseline leg."""
     layers = []
-    for li, (name, K, N) in enumerate(LINEARS):
-        L = synth.make_layer(K=K, N=N, stream_counts=TOKENS, T=T_STEPS, seed=[0, 2, li])
+    for li, (name, (K, N)) in enumerate(linears.items()):
+        L = synth.device_layer(K, N, tokens, T=T_STEPS, seed=seed + li, batch=batch, device=dev)
+        w = L.pop("w")
+        ly = dict(name=name, K=K, N=N, M=int(L["x"].shape[0]), x=L["x"], dev=L,
+                  W=B.prepare_weight(w, L["d"], W_GROUP, bias=L["bias"]))
+        if per_channel:
+            ly["W_pc"] = B.prepare_weight(w, L["d"], K, bias=L["bias"])
+        ly["w_host"] = w.cpu().numpy()
+        del w
+        ly["acts"] = {bits: B.ActParams(tok2stream=L["tok2stream"], gamma=L["gamma"], step=0, act_bits=bits,
+                                        dinv=L["dinv"]) for bits in (8, 4)}
+        layers.append(ly)
+    return layers
+
+
+def host_layers(torch, B, synth, dev):
+    """The 2B-class MLP pair drawn on the host (synth.make_layer), for the
+    calibration figures, which need the host inputs."""
+    layers = []
+    for li, (name, K, N) in enumerate(MLP_2B):
+        L = synth.make_layer(K=K, N=N, stream_counts=synth.TOKENS_2B, T=T_STEPS, seed=[0, 2, li])
         x = torch.from_numpy(L.x_bits.view(np.int16)).view(torch.bfloat16).to(dev)
         w, d = torch.from_numpy(L.w).to(dev), torch.from_numpy(L.d).to(dev)
         bias = torch.from_numpy(L.bias_bits.view(np.int16)).view(torch.bfloat16).to(dev)
         W = B.prepare_weight(w, d, W_GROUP, bias=bias)
-        W_pc = B.prepare_weight(w, d, K, bias=bias)  # one step per output channel (context line)
+        W_pc = B.prepare_weight(w, d, K, bias=bias)
         del w
-        acts = {}
-        for bits in (8, 4):
-            acts[bits] = B.ActParams(tok2stream=torch.from_numpy(L.tok2stream).to(dev),
-                                     gamma=torch.from_numpy(L.gamma).to(dev), step=0, act_bits=bits,
-                                     dinv=torch.from_numpy(L.dinv).to(dev))
-        layers.append(dict(name=name, K=K, N=N, L=L, x=x, W=W, W_pc=W_pc, acts=acts))
+        acts = {bits: B.ActParams(tok2stream=torch.from_numpy(L.tok2stream).to(dev),
+                                  gamma=torch.from_numpy(L.gamma).to(dev), step=0, act_bits=bits,
+                                  dinv=torch.from_numpy(L.dinv).to(dev)) for bits in (8, 4)}
+        layers.append(dict(name=name, K=K, N=N, M=L.M, L=L, x=x, W=W, W_pc=W_pc, acts=acts))
     return layers
 
 
@@ -99,49 +125,61 @@ def gemm_source_sha256():
 
 
 def measured_traffic():
-    """HBM bytes per GEMM launch from the committed counter summary, or None
-    when there is none or it was taken on a different GEMM source."""
+    """HBM bytes of one step's four GEMM calls from the committed counter
+    summary, or None when there is none or it was taken on a different GEMM
+    source."""
     try:
         with open(TRAFFIC_SUMMARY) as f:
             text = f.read()
     except OSError:
         return None
     sha = re.search(r"^source_sha256:\s*([0-9a-f]{64})\s*$", text, re.M)
-    val = re.search(r"^traffic_bytes_per_launch:\s*([0-9]+)\s*$", text, re.M)
+    val = re.search(r"^traffic_bytes_per_step:\s*([0-9]+)\s*$", text, re.M)
     if not sha or not val or sha.group(1) != gemm_source_sha256():
         return None
     return int(val.group(1))
 
 
-def cpu_baseline(layers, rows_per_layer):
-    """The oracle, as it stands, on a row sample of each layer (all the same
-    arithmetic per row as the full layer); throughput scaled to TOPS."""
-    from oracle import sq_oracle as O
+def cpu_baseline(layers, video_rows):
+    """The oracle, as it stands, on a stratified row sample of each linear of
+    the block (every proprio and action row plus `video_rows` random video
+    rows; each row costs the same arithmetic as in the full layer), W4A8 at
+    tau = 3; throughput scaled to TOPS (2 * rows * K * N per second)."""
+    import torch
 
-    rng = np.random.default_rng(0)
+    from oracle import sq_oracle as O
+    from paper_2609_39056_amd import synth
+
     prepared = []
-    for ly in layers:  # offline weight preparation: not part of the timed sample
-        L = ly["L"]
-        n = L.M if rows_per_layer <= 0 else min(rows_per_layer, L.M)
-        prepared.append((L, O.pack_weights(L.w, L.d, W_GROUP),
-                         np.sort(rng.choice(L.M, size=n, replace=False))))
+    for ly in layers:  # offline weight preparation and the host copy of the sample: not timed
+        d = ly["dev"]
+        t2s = d["tok2stream"].cpu().numpy()
+        rows = synth.stratified_rows(t2s, video_rows, seed=0)
+        xr = ly["x"][torch.as_tensor(rows, device=ly["x"].device)].view(torch.int16).cpu().numpy().view(np.uint16)
+        prepared.append(dict(x=xr, t2s=t2s[rows], gamma=d["gamma"].cpu().numpy(), dinv=d["dinv"].cpu().numpy(),
+                             bias=d["bias"].view(torch.int16).cpu().numpy().view(np.uint16),
+                             pw=O.pack_weights(ly["w_host"], d["d"].cpu().numpy(), W_GROUP), K=ly["K"], N=ly["N"],
+                             M=ly["M"]))
     ops = 0
     t0 = time.perf_counter()
-    for L, pw, rows in prepared:
-        O.linear(L.x_bits[rows], L.tok2stream[rows], L.gamma, 3, pw["codes"], pw["w_scale"], W_GROUP,
-                 dinv=L.dinv, bias_bits=L.bias_bits, act_bits=8)
-        ops += 2 * len(rows) * L.K * L.N
+    for p in prepared:
+        O.linear(p["x"], p["t2s"], p["gamma"], 3, p["pw"]["codes"], p["pw"]["w_scale"], W_GROUP, dinv=p["dinv"],
+                 bias_bits=p["bias"], act_bits=8)
+        ops += 2 * p["x"].shape[0] * p["K"] * p["N"]
     dt = time.perf_counter() - t0
     try:
         cores = len(os.sched_getaffinity(0))
     except AttributeError:
         cores = os.cpu_count()
     threads = int(os.environ.get("OMP_NUM_THREADS", cores))
+    n = prepared[0]["x"].shape[0]
     return dict(value=ops / dt / 1e12, unit="TOPS", cores=min(cores, threads), kind="oracle",
                 seconds=round(dt, 3),
-                sample=f"{len(prepared[0][2])} of {prepared[0][0].M} rows of each of the up (2048->8192) and "
-                       f"down (8192->2048) W4A8 layers, one step at tau=3 (quantize, exact block "
-                       f"accumulation, fp32 epilogue); weights packed beforehand; TOPS = 2*rows*K*N / time")
+                sample=f"stratified rows: {n} of {prepared[0]['M']} per linear (every proprio and action row plus "
+                       f"{video_rows} random video rows) of each of the four 14B-block linears (qkv, out, up, "
+                       f"down), W4A8 DYNAMIC at tau=3 (quantize, exact block accumulation, fp32 epilogue); "
+                       f"weights packed beforehand; throughput extrapolated linearly in rows: "
+                       f"TOPS = sum 2*rows*K*N / time")
 
 
 def run_suite(args):
@@ -510,22 +548,16 @@ def run_action_only(args):
 
 def main():
     args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported (every step of the layer is "
+              f"row-independent: several GPUs would each take their own slice of the tokens)", file=sys.stderr)
+        sys.exit(2)
     if args.action_only:
-        if args.gpus != 1:
-            print("bench.py runs on one GPU only", file=sys.stderr)
-            sys.exit(2)
         run_action_only(args)
         return
     if args.suite:
-        if args.gpus != 1:
-            print("bench.py runs on one GPU only", file=sys.stderr)
-            sys.exit(2)
         run_suite(args)
         return
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only; --gpus {args.gpus} is not supported "
-              f"(the layer is row-parallel: each GPU would take its own slice of the tokens)", file=sys.stderr)
-        sys.exit(2)
 
     import torch
 
@@ -538,141 +570,184 @@ def main():
     dev = "cuda:0"
     torch.cuda.set_device(0)
     B.lib()
-    M = sum(TOKENS)
-    layers = make_layers(torch, B, synth, dev)
     stream = torch.cuda.current_stream()
+    BF16 = B.SQ_OUT_BF16
+    FUSED = {8: B.sq_linear_w4a8, 4: B.sq_linear_w4a4}
 
-    # per-layer buffers
-    for ly in layers:
-        ly["qx8"], ly["r8"] = B.act_buffers(M, ly["K"], 8, dev)
-        ly["y"] = torch.empty((M, ly["N"]), dtype=torch.bfloat16, device=dev)
-        ly["ws_unf"] = {b: B.alloc_workspace(B.SQ_VARIANT_UNFUSED, M, ly["K"], ly["N"], b, dev) for b in (8, 4)}
-        ly["ws_fused"] = {b: B.alloc_workspace(B.SQ_VARIANT_FUSED, M, ly["K"], ly["N"], b, dev) for b in (8, 4)}
-        ly["ws_gemm"] = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, ly["K"], ly["N"], 8, dev)
+    def buffers(layers, with_split=False, unfused=False):
+        for ly in layers:
+            M, K, N = ly["M"], ly["K"], ly["N"]
+            ly["y"] = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            ly["ws_fused"] = {b: B.alloc_workspace(B.SQ_VARIANT_FUSED, M, K, N, b, dev) for b in (8, 4)}
+            if with_split:
+                ly["qx8"], ly["r8"] = B.act_buffers(M, K, 8, dev)
+                ly["ws_gemm"] = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, K, N, 8, dev)
+            if unfused:
+                ly["ws_unf"] = B.alloc_workspace(B.SQ_VARIANT_UNFUSED, M, K, N, 8, dev)
 
-    def variant_step(tau, fn, bits, ws_key, w_key="W"):
+    def fused_step(layers, tau, bits=8, wkey="W"):
         for ly in layers:
             act = ly["acts"][bits]
             act.step = tau
-            fn(ly["x"], act, ly[w_key], ly["y"], B.SQ_OUT_BF16, ly[ws_key][bits], stream)
+            FUSED[bits](ly["x"], act, ly[wkey], ly["y"], BF16, ly["ws_fused"][bits], stream)
 
-    def fused_step(tau, events=None):
-        for i, ly in enumerate(layers):
+    def unfused_step(layers, tau):
+        for ly in layers:
             act = ly["acts"][8]
             act.step = tau
-            if events is not None:
-                events[2 * i].record(stream)
-            B.sq_quantize_act(ly["x"], act, ly["qx8"], ly["r8"], stream)
-            if events is not None:
-                events[2 * i + 1].record(stream)
-            B.sq_gemm_w4a8(ly["qx8"], ly["r8"], ly["W"], ly["y"], B.SQ_OUT_BF16, workspace=ly["ws_gemm"],
-                           stream=stream)
-        if events is not None:
-            events[4].record(stream)
+            B.sq_linear_unfused(ly["x"], act, ly["W"], ly["y"], BF16, ly["ws_unf"], stream)
 
-    # ---- per-kernel breakdown: the same step as its two C-ABI calls per
-    # layer (sq_quantize_act, sq_gemm_w4a8), HIP events around every kernel of
-    # the sampled steps, on the stream the kernels run on.  The samples are
-    # taken in the pass's second half (clocks settle over the first), as many
-    # as steps / sample_every.
-    for s in range(args.warmup):
-        fused_step(s % T_STEPS)
-    torch.cuda.synchronize()
-    every = max(1, args.sample_every)
-    sampled = list(range(args.steps // 2, args.steps, max(1, every // 2)))[: max(1, args.steps // every)]
-    evs = {s: [torch.cuda.Event(enable_timing=True) for _ in range(5)] for s in sampled}
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for s in range(args.steps):
-        fused_step(s % T_STEPS, evs.get(s))
-    torch.cuda.synchronize()
-    ms_split = (time.perf_counter() - t1) * 1e3 / args.steps
+    def timed_steps(step_fn, steps, warmup):
+        """Wall time per step (ms) of `steps` steps after `warmup` untimed ones,
+        synchronized on both sides."""
+        for s in range(warmup):
+            step_fn(s % T_STEPS)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(steps):
+            step_fn(s % T_STEPS)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / steps
 
-    # ---- main timed region: the fused W4A8 linear (sq_linear_w4a8, the
-    # product's entry point) for both layers, K steps; after the per-kernel
-    # pass, so that the GPU runs at its steady-state clocks
-    for s in range(args.warmup):
-        variant_step(s % T_STEPS, B.sq_linear_w4a8, 8, "ws_fused")
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for s in range(args.steps):
-        variant_step(s % T_STEPS, B.sq_linear_w4a8, 8, "ws_fused")
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms_per_step = wall * 1e3 / args.steps
+    def event_pass(layers, calls, steps):
+        """Per-call device time: HIP events on the kernels' stream around
+        every call of every step; calls(ly, tau) issues one layer's calls in
+        order and returns their count.  Returns (ms per call [layer][call],
+        wall ms per step)."""
+        ncall = None
+        evs = []
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for s in range(steps):
+            e = []
+            for ly in layers:
+                e.append(torch.cuda.Event(enable_timing=True))
+                e[-1].record(stream)
+                n = calls(ly, s % T_STEPS, e)
+                ncall = n if ncall is None else ncall
+            e.append(torch.cuda.Event(enable_timing=True))
+            e[-1].record(stream)
+            evs.append(e)
+        torch.cuda.synchronize()
+        wall = (time.perf_counter() - t0) * 1e3 / steps
+        per = np.zeros((len(layers), ncall))
+        for e in evs:
+            for i in range(len(layers)):
+                for c in range(ncall):
+                    k = i * ncall + c
+                    per[i, c] += e[k].elapsed_time(e[k + 1])
+        return per / steps, wall
 
+    def split_calls(ly, tau, e):
+        act = ly["acts"][8]
+        act.step = tau
+        B.sq_quantize_act(ly["x"], act, ly["qx8"], ly["r8"], stream)
+        e.append(torch.cuda.Event(enable_timing=True))
+        e[-1].record(stream)
+        B.sq_gemm_w4a8(ly["qx8"], ly["r8"], ly["W"], ly["y"], BF16, workspace=ly["ws_gemm"], stream=stream)
+        return 2
 
-    k1 = np.zeros(2)
-    k2 = np.zeros(2)
-    for e in evs.values():
-        for i in range(2):
-            k1[i] += e[2 * i].elapsed_time(e[2 * i + 1])
-            k2[i] += e[2 * i + 1].elapsed_time(e[2 * i + 2])
-    k1 /= len(evs)
-    k2 /= len(evs)  # ms per launch, per layer
+    def fused_calls(bits):
+        def calls(ly, tau, e):
+            act = ly["acts"][bits]
+            act.step = tau
+            FUSED[bits](ly["x"], act, ly["W"], ly["y"], BF16, ly["ws_fused"][bits], stream)
+            return 1
+        return calls
 
-    ops = [2.0 * M * ly["K"] * ly["N"] for ly in layers]
-    ops_step = sum(ops)
+    def ops_of(layers):
+        return sum(2.0 * ly["M"] * ly["K"] * ly["N"] for ly in layers)
+
+    # ---- the 14B-class block (configuration 4), drawn on the GPU
+    blk = device_block(torch, B, synth, dev, synth.LINEARS_14B, synth.TOKENS_14B, seed=5000, per_channel=True)
+    buffers(blk, with_split=True, unfused=True)
+    M = blk[0]["M"]
+    ops_step = ops_of(blk)
+
+    # ---- headline timed region: the fused W4A8 linear (sq_linear_w4a8, the
+    # product's entry point) for the four linears, K steps
+    ms_per_step = timed_steps(lambda t: fused_step(blk, t), args.steps, args.warmup)
     value = ops_step / (ms_per_step * 1e-3) / 1e12
+
+    # ---- per-kernel pass: the same steps as the fused call's two launches,
+    # events around every kernel of every step
+    for s in range(max(2, args.warmup // 2)):
+        for ly in blk:
+            split_calls(ly, s % T_STEPS, [])
+    per_k, ms_split = event_pass(blk, split_calls, args.steps)
+    k1, k2 = per_k[:, 0], per_k[:, 1]  # ms per launch, per linear
+    ops = [2.0 * M * ly["K"] * ly["N"] for ly in blk]
     gemm_tops = sum(ops) / (k2.sum() * 1e-3) / 1e12
-    # algorithmic bytes of the first kernel: bf16 X in, int8 Q_X + fp32 r out
-    k1_bytes = [M * ly["K"] * 2 + M * ly["K"] + 4 * M for ly in layers]
-    k1_gbs = sum(k1_bytes) / (k1.sum() * 1e-3) / 1e9
-    # algorithmic bytes of the whole layer (bf16 X, int4 W, fp16 steps, bf16 Y, stream map)
-    alg_bytes = [M * ly["K"] * 2 + ly["N"] * ly["K"] // 2 + ly["N"] * ly["K"] // W_GROUP * 2 + M * ly["N"] * 2
-                 + 4 * M for ly in layers]
-    serial = [b1 / (PEAK_HBM_GBS * 1e9) + max(o / (PEAK_INT8_TOPS * 1e12), 0.0)
-              for b1, o in zip(k1_bytes, ops)]
-    per_layer = {
-        ly["name"]: dict(
-            us_quant=round(k1[i] * 1e3, 2), us_gemm=round(k2[i] * 1e3, 2),
-            us_layer=round((k1[i] + k2[i]) * 1e3, 2),
-            tops_layer=round(ops[i] / ((k1[i] + k2[i]) * 1e-3) / 1e12, 1),
-            frac_layer_int8=round(ops[i] / ((k1[i] + k2[i]) * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4),
+    # algorithmic bytes: first kernel bf16 X in, int8 Q_X + fp32 r out (+ the
+    # stream map); GEMM Q_X + r in, int4 W + fp16 steps + bf16 bias, bf16 Y out;
+    # layer bf16 X, int4 W, fp16 steps, bias, bf16 Y, stream map
+    k1_bytes = [M * ly["K"] * 3 + 8 * M for ly in blk]
+    k2_bytes = [M * ly["K"] + 4 * M + ly["N"] * ly["K"] // 2 + ly["N"] * ly["K"] // W_GROUP * 2 + 2 * ly["N"]
+                + 2 * M * ly["N"] for ly in blk]
+    alg_bytes = [M * ly["K"] * 2 + ly["N"] * ly["K"] // 2 + ly["N"] * ly["K"] // W_GROUP * 2 + 2 * ly["N"]
+                 + M * ly["N"] * 2 + 4 * M for ly in blk]
+    serial = [b1 / (PEAK_HBM_GBS * 1e9) + max(o / (PEAK_INT8_TOPS * 1e12), b2 / (PEAK_HBM_GBS * 1e9))
+              for b1, b2, o in zip(k1_bytes, k2_bytes, ops)]
+    per_layer = {}
+    for i, ly in enumerate(blk):
+        t = (k1[i] + k2[i]) * 1e-3
+        per_layer[ly["name"]] = dict(
+            K=ly["K"], N=ly["N"], us_quant=round(k1[i] * 1e3, 2), us_gemm=round(k2[i] * 1e3, 2),
+            us_layer=round(t * 1e6, 2), tops_layer=round(ops[i] / t / 1e12, 1),
+            tops_gemm=round(ops[i] / (k2[i] * 1e-3) / 1e12, 1),
+            frac_layer_int8=round(ops[i] / t / 1e12 / PEAK_INT8_TOPS, 4),
             frac_gemm_int8=round(ops[i] / (k2[i] * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4),
             frac_quant_hbm=round(k1_bytes[i] / (k1[i] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            frac_serial_roofline=round(serial[i] / ((k1[i] + k2[i]) * 1e-3), 4),
-            alg_mb=round(alg_bytes[i] / 1e6, 2))
-        for i, ly in enumerate(layers)}
+            frac_serial_roofline=round(serial[i] / t, 4), alg_mb=round(alg_bytes[i] / 1e6, 2))
 
-    # ---- unfused W4A8 and fused W4A4 on the same layers (context)
-    def time_variant(fn, bits, ws_key, steps, w_key="W"):
-        for s in range(max(3, args.warmup // 4)):
-            variant_step(s % T_STEPS, fn, bits, ws_key, w_key)
-        torch.cuda.synchronize()
-        t = time.perf_counter()
-        for s in range(steps):
-            variant_step(s % T_STEPS, fn, bits, ws_key, w_key)
-        torch.cuda.synchronize()
-        return (time.perf_counter() - t) * 1e3 / steps
+    # ---- fused W4A4 on the same block, with per-linear call times
+    ms_w4a4 = timed_steps(lambda t: fused_step(blk, t, bits=4), args.steps, max(2, args.warmup // 2))
+    per4, _ = event_pass(blk, fused_calls(4), max(5, args.steps // 4))
+    per8, _ = event_pass(blk, fused_calls(8), max(5, args.steps // 4))
+    # ---- unfused W4A8 and per-output-channel weight steps on the same block
+    ms_unfused = timed_steps(lambda t: unfused_step(blk, t), max(5, args.steps // 4), 2)
+    ms_pc = timed_steps(lambda t: fused_step(blk, t, wkey="W_pc"), args.steps, 2)
+    for ly in blk:
+        del ly["ws_unf"], ly["W_pc"], ly["ws_gemm"], ly["qx8"], ly["r8"]
+    torch.cuda.empty_cache()
 
-    vsteps = max(10, args.steps // 4)
-    ms_unfused = time_variant(B.sq_linear_unfused, 8, "ws_unf", vsteps)
-    ms_w4a4 = time_variant(B.sq_linear_w4a4, 4, "ws_fused", vsteps)
-    ms_pc = time_variant(B.sq_linear_w4a8, 8, "ws_fused", vsteps, "W_pc")
+    # ---- the 2B-class MLP pair (configuration 2) and the 2B-class block at
+    # batch 4 (configuration 5's batch-4 row count)
+    mlp = host_layers(torch, B, synth, dev)
+    buffers(mlp)
+    ms_mlp8 = timed_steps(lambda t: fused_step(mlp, t), args.steps, args.warmup)
+    ms_mlp4 = timed_steps(lambda t: fused_step(mlp, t, bits=4), args.steps, 2)
+    b4 = device_block(torch, B, synth, dev, synth.LINEARS_2B, synth.TOKENS_2B, seed=6000, batch=4)
+    buffers(b4)
+    ms_b4 = {bits: timed_steps(lambda t, b=bits: fused_step(b4, t, bits=b), max(10, args.steps // 2), 3)
+             for bits in (8, 4)}
+    del b4
+    torch.cuda.empty_cache()
 
-    # ---- the calibration path of Eq. (9) on the up projection
-    calib = calibration_figures(torch, B, layers[0], stream, dev, None if args.no_cpu else 256)
+    # ---- the calibration path of Eq. (9) on the 2B up projection
+    calib = calibration_figures(torch, B, mlp[0], stream, dev, None if args.no_cpu else 256)
 
     # ---- the int8 matrix-core rate this GPU sustains (sq_probe_mfma_i8: back
-    # to back MFMAs on register operands at the GEMM's occupancy), as a
-    # measured ceiling beside the published peak: zero operands, random
-    # operands, and random operands with the 128-group fold's VALU work
+    # to back MFMAs on register operands at the GEMM's occupancy) in both MFMA
+    # forms: zero operands, random operands, and random operands with the
+    # 128-wide block fold of the GEMM kernel that issues that form
     sink = B.probe_sink(dev)
     n_wg = sink.numel() // 256
     probe_iters = 20000
     ceiling = {}
-    for label, rnd, fold in (("zero_operands", 0, 0), ("random_operands", 1, 0),
-                             ("random_operands_with_128_group_fold", 1, 1)):
-        B.sq_probe_mfma_i8(200, rnd, fold, sink, stream)
-        p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        p0.record(stream)
-        B.sq_probe_mfma_i8(probe_iters, rnd, fold, sink, stream)
-        p1.record(stream)
-        torch.cuda.synchronize()
-        probe_ops = n_wg * 4 * probe_iters * 16 * 2.0 * 32 ** 3
-        ceiling[label] = round(probe_ops / (p0.elapsed_time(p1) * 1e-3) / 1e12, 1)
+    for shape, name in ((16, "16x16x64"), (32, "32x32x32")):
+        for label, rnd, fold in (("zero_operands", 0, 0), ("random_operands", 1, 0),
+                                 ("random_operands_with_fold", 1, 1)):
+            B.sq_probe_mfma_i8(200, rnd, fold, sink, stream, shape=shape)
+            p0, p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            p0.record(stream)
+            B.sq_probe_mfma_i8(probe_iters, rnd, fold, sink, stream, shape=shape)
+            p1.record(stream)
+            torch.cuda.synchronize()
+            probe_ops = n_wg * 4 * probe_iters * 2.0 ** 20
+            ceiling[f"{name}_{label}"] = round(probe_ops / (p0.elapsed_time(p1) * 1e-3) / 1e12, 1)
     del sink
+    ceil_gemm = ceiling["16x16x64_random_operands_with_fold"]
 
     # ---- a plain device copy of known size: the reference for the HBM byte
     # counters (FETCH_SIZE / WRITE_SIZE) of the profiled GEMM launches
@@ -687,6 +762,8 @@ def main():
     copy_us = c0.elapsed_time(c1) * 1e3
     del src, dst
 
+    mlp_ops = ops_of(mlp)
+    b4_ops = sum(2.0 * 4 * sum(synth.TOKENS_2B) * K * N for K, N in synth.LINEARS_2B.values())
     out = {
         "metric": "fused W4A8/W4A4 linear TOPS + % int8-MFMA (or HBM) roofline per layer",
         "value": round(value, 2),
@@ -701,37 +778,53 @@ def main():
         "dtype": "int8",
         "data": "synthetic",
         "config": {
-            "workload": "2B-class WAM DiT MLP pair, W4A8: up 2048->8192 and down 8192->2048, "
-                        "M=4192 tokens (4096 video + 32 proprio + 64 action), 10-step gain tables, "
-                        "int4 weight groups of 128 (fp16 steps), per-token int8 activations (DYNAMIC), bf16 out",
-            "M": M, "linears": [[ly["name"], ly["K"], ly["N"]] for ly in layers],
-            "act_bits": 8, "w_group": W_GROUP,
+            "workload": "14B-class WAM DiT block linears, W4A8: qkv 5120->15360, out 5120->5120, "
+                        "up 5120->13824, down 13824->5120; M=8384 tokens (8192 video + 64 proprio + 128 action), "
+                        "10-step gain tables, int4 weight groups of 128 (fp16 steps), per-token int8 activations "
+                        "(DYNAMIC), bf16 out",
+            "M": M, "linears": [[ly["name"], ly["K"], ly["N"]] for ly in blk], "act_bits": 8, "w_group": W_GROUP,
         },
         "roofline": {
-            "bound": "mfma", "kernel": "gemm_pipe16_kernel<0> + gemm_tail_kernel<8,0,false> (sq_gemm_w4a8)",
-            "launches": 2 * len(evs),
+            "bound": "mfma",
+            "kernel": "sq_gemm_w4a8: gemm_pipe16_kernel<0> (+ gemm_tail_kernel<8,0,false> where tiles split)",
+            "per": "the four GEMM calls of one step (qkv, out, up, down)",
+            "launches": int(args.steps * len(blk)),
             "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",
             "frac": round(gemm_tops / PEAK_INT8_TOPS, 4), "traffic": measured_traffic(),
-            "measured_ceiling": ceiling["random_operands_with_128_group_fold"],
-            "frac_of_measured_ceiling": round(gemm_tops / ceiling["random_operands_with_128_group_fold"], 4),
+            "ops_per_step": ops_step, "us_gemm_per_step": round(k2.sum() * 1e3, 2),
+            "measured_ceiling": ceil_gemm,
+            "measured_ceiling_what": "v_mfma_i32_16x16x64_i8 with the biased 128-block fold, random operands",
+            "frac_of_measured_ceiling": round(gemm_tops / ceil_gemm, 4),
         },
         "mfma_i8_ceiling_tops": ceiling,
         "per_layer": per_layer,
-        "quant_kernel_gbs": round(k1_gbs, 1),
+        "quant_kernel_gbs": round(sum(k1_bytes) / (k1.sum() * 1e-3) / 1e9, 1),
+        "w4a8_as_k1_k2_calls": {"ms_per_step": round(ms_split, 5),
+                                "gemm_tops": round(gemm_tops, 1)},
+        "fused_w4a8_per_call_us": {ly["name"]: round(per8[i, 0] * 1e3, 2) for i, ly in enumerate(blk)},
+        "fused_w4a4": {"ms_per_step": round(ms_w4a4, 5), "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2),
+                       "per_call_us": {ly["name"]: round(per4[i, 0] * 1e3, 2) for i, ly in enumerate(blk)},
+                       "frac_int8": round(ops_step / (ms_w4a4 * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)},
         "unfused_w4a8": {"ms_per_step": round(ms_unfused, 5),
                          "tops": round(ops_step / (ms_unfused * 1e-3) / 1e12, 2),
                          "fused_speedup": round(ms_unfused / ms_per_step, 3)},
-        "w4a8_as_k1_k2_calls": {"ms_per_step": round(ms_split, 5)},
-        "fused_w4a4": {"ms_per_step": round(ms_w4a4, 5),
-                       "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2)},
         "fused_w4a8_per_channel_steps": {"ms_per_step": round(ms_pc, 5),
                                          "tops": round(ops_step / (ms_pc * 1e-3) / 1e12, 2)},
+        "mlp_2B_M4192": {"workload": "2B-class MLP pair up 2048->8192, down 8192->2048, M=4192 (4096+32+64)",
+                         "w4a8": {"ms_per_step": round(ms_mlp8, 5),
+                                  "tops": round(mlp_ops / (ms_mlp8 * 1e-3) / 1e12, 2)},
+                         "w4a4": {"ms_per_step": round(ms_mlp4, 5),
+                                  "tops": round(mlp_ops / (ms_mlp4 * 1e-3) / 1e12, 2)}},
+        "block_2B_batch4_M16768": {"workload": "2B-class block qkv/out/up/down, batch 4: M=16768",
+                                   **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
+                                                  "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}
+                                      for b in (8, 4)}},
         "calibration": calib,
         "hbm_copy": {"bytes": 2 * (COPY_MIB << 20), "us": round(copy_us, 1),
                      "gbs": round(2 * (COPY_MIB << 20) / (copy_us * 1e-6) / 1e9, 1)},
     }
     if not args.no_cpu:
-        out["cpu_baseline"] = cpu_baseline(layers, args.cpu_rows)
+        out["cpu_baseline"] = cpu_baseline(blk, args.cpu_video_rows)
     print(json.dumps(out), flush=True)
 
 

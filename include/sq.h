@@ -337,22 +337,33 @@ sq_status sq_calib_search(const uint16_t* x, int32_t M, const int32_t* tok2strea
 
 /* Measurement hook: the int8 matrix-core rate the GPU sustains, as a
  * ceiling beside the published peak.  Launches sq_probe_mfma_i8_sink_bytes()
- * / 1024 workgroups (two per CU) whose waves each issue iters * 16
- * v_mfma_i32_32x32x32_i8 back to back on register operands (2 * 32^3 int8
- * ops each), with no memory traffic: operands all zero (random_operands ==
- * 0) or pseudo-random; with fold != 0 each 32x32 accumulator is also
- * converted and fma'd into fp32 once per four MFMAs, as the dequantization of
- * one 128-channel block.  The caller times the call (e.g. with HIP events);
- * sink is int32 scratch of at least sq_probe_mfma_i8_sink_bytes() bytes that
- * keeps the work live.  iters in [1, 2^24]. */
+ * / 1024 workgroups (two per CU) whose waves each issue back-to-back int8
+ * MFMAs on register operands, with no memory traffic, 2^20 int8 operations
+ * per wave and iteration:
+ *   shape 32: iters * 16 v_mfma_i32_32x32x32_i8 (four 32 x 32 tiles); with
+ *             fold != 0 each tile's accumulator is also converted and fma'd
+ *             into fp32 once per four MFMAs (one 128-channel block);
+ *   shape 16: iters * 32 v_mfma_i32_16x16x64_i8 (sixteen 16 x 16 tiles of
+ *             two MFMAs); with fold != 0 each block starts from the integer
+ *             bits of 1.5 * 2^23 and is folded by a subtraction and an fma
+ *             per output, as the 16 x 16 tiled GEMM does.
+ * Operands all zero (random_operands == 0) or pseudo-random.  The caller
+ * times the call (e.g. with HIP events); sink is int32 scratch of at least
+ * sq_probe_mfma_i8_sink_bytes() bytes that keeps the work live.
+ * iters in [1, 2^24]; another shape returns SQ_ERR_UNSUPPORTED. */
 size_t sq_probe_mfma_i8_sink_bytes(void);
-sq_status sq_probe_mfma_i8(int32_t iters, int32_t random_operands, int32_t fold, int32_t* sink, size_t sink_bytes,
-                           hipStream_t stream);
+sq_status sq_probe_mfma_i8(int32_t shape, int32_t iters, int32_t random_operands, int32_t fold, int32_t* sink,
+                           size_t sink_bytes, hipStream_t stream);
 
-/* Test hook: runs the fused GEMM main loop on already-quantized activations
- * and writes every int32 block accumulator instead of the epilogue:
- * acc_out[b][i][j] = sum over K-block b of q_ik * w_jk, with blocks of
- * w_group (8-bit) or 64 (4-bit).  qx as for sq_gemm_w4a8 / sq_gemm_w4a4.
+/* Test hook: writes every int32 block accumulator of Q_X Q_W instead of an
+ * epilogue: acc_out[b][i][j] = sum over K-block b of q_ik * w_jk, with blocks
+ * of w_group (8-bit) or 64 (4-bit).  It runs the library's non-pipelined GEMM
+ * kernel (the one that serves 8-bit activations with 128 < w_group < K and
+ * the unfused path's int32 C), NOT the kernels the fused linear normally
+ * dispatches to (the pipelined int8 and fp8 kernels and the weight-streaming
+ * kernel); those have no dump epilogue, and their block sums are checked
+ * through outputs computed in exact arithmetic instead (integer activations,
+ * power-of-two steps).  qx as for sq_gemm_w4a8 / sq_gemm_w4a4.
  * acc_out is int32 [K/block][M][N]. */
 sq_status sq_debug_block_acc_i32(const void* qx, int32_t M, int32_t act_bits, const sq_weight* w,
                                  int32_t* acc_out, hipStream_t stream);

@@ -192,7 +192,8 @@ def quantize_act(x_bits, tok2stream, gamma, step, dinv=None, clip=None,
 
 # --------------------------------------------------------------------------
 # Offline weight preparation: fold D, quantize per group to int4, pack
-# (Sec. 4.2, "we fold D* into the weights ... stored as packed integers")
+# (Sec. 4.2: the channel scaling is folded into the weights, which are then
+# kept as packed integers)
 # --------------------------------------------------------------------------
 def pack_weights(w, d=None, w_group=128):
     """w: fp32 [N, K] (W^T), d: fp32 [K] or None.

@@ -102,7 +102,7 @@ _SIGS = {
     "sq_calib_search": (_I, [_P, _I, _P, _I, _P, _I, ctypes.POINTER(sq_weight), _P, _P,
                              ctypes.POINTER(sq_calib_search_params), _P, _P, _P, _P, _S, _P]),
     "sq_probe_mfma_i8_sink_bytes": (_S, []),
-    "sq_probe_mfma_i8": (_I, [_I, _I, _I, _P, _S, _P]),
+    "sq_probe_mfma_i8": (_I, [_I, _I, _I, _I, _P, _S, _P]),
 }
 
 _lib = None
@@ -365,11 +365,13 @@ def act_buffers(M: int, K: int, act_bits: int, device="cuda"):
             torch.empty((M, K // A4_GROUP), dtype=torch.float16, device=device))
 
 
-def sq_probe_mfma_i8(iters: int, random_operands: bool, fold: bool, sink: torch.Tensor, stream=None) -> None:
-    """Matrix-core rate probe (include/sq.h): iters * 16 int8 MFMAs per wave
-    of a full-occupancy grid, register operands only; sink is int32 scratch of
-    sq_probe_mfma_i8_sink_bytes() bytes."""
-    _check(lib().sq_probe_mfma_i8(iters, int(random_operands), int(fold), _ptr(sink), sink.numel() * 4,
+def sq_probe_mfma_i8(iters: int, random_operands: bool, fold: bool, sink: torch.Tensor, stream=None,
+                     shape: int = 32) -> None:
+    """Matrix-core rate probe (include/sq.h): iters * 2^20 int8 MFMA operations
+    per wave of a full-occupancy grid, register operands only, on
+    v_mfma_i32_32x32x32_i8 (shape 32) or v_mfma_i32_16x16x64_i8 (shape 16);
+    sink is int32 scratch of sq_probe_mfma_i8_sink_bytes() bytes."""
+    _check(lib().sq_probe_mfma_i8(shape, iters, int(random_operands), int(fold), _ptr(sink), sink.numel() * 4,
                                   _stream(stream)), "sq_probe_mfma_i8")
 
 

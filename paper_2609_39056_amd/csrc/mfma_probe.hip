@@ -1,11 +1,20 @@
 // Measurement hook: the int8 matrix-core rate this GPU sustains, as a ceiling
 // to set beside the published peak.  Every wave of a full-occupancy grid (two
 // 256-thread workgroups per CU, as the tiled GEMM runs) issues back-to-back
-// v_mfma_i32_32x32x32_i8 on register operands, with no memory traffic in the
-// loop.  Operands all zero or pseudo-random: the rate depends on the data
-// (random operands draw more power).  With `fold`, each 32x32 tile's
-// accumulator is also converted and multiply-added into fp32 once per four
-// MFMAs, the dequantization work per 128-channel block of the GEMM.
+// int8 MFMAs on register operands, with no memory traffic in the loop, in
+// either of the two forms the GEMM kernels use:
+//  - v_mfma_i32_32x32x32_i8, four 32 x 32 tiles of four MFMAs per iteration;
+//    with `fold`, each tile's accumulator is converted (v_cvt_f32_i32) and
+//    multiply-added into fp32 once per four MFMAs, the dequantization of one
+//    128-channel block;
+//  - v_mfma_i32_16x16x64_i8, sixteen 16 x 16 tiles of two MFMAs per
+//    iteration (a wave's 64 x 64 outputs over one 128-channel stage); with
+//    `fold`, each block starts from the integer bits of 1.5 * 2^23 and is
+//    folded by a subtraction and an fma per output, the tiled 16 x 16 kernel's
+//    biased fold.
+// Both issue 2^20 int8 operations per wave and iteration.  Operands all zero
+// or pseudo-random: the rate depends on the data (random operands draw more
+// power).
 #include "sq_internal.h"
 
 namespace sq {
@@ -61,16 +70,75 @@ __global__ __launch_bounds__(256, 2) void mfma_probe_kernel(int32_t* sink, int32
   sink[blockIdx.x * 256 + threadIdx.x] = s;  // keeps the work live
 }
 
+template <bool FOLD>
+__global__ __launch_bounds__(256, 2) void mfma_probe16_kernel(int32_t* sink, int32_t iters, int32_t random) {
+  const int l = threadIdx.x & 63;
+  v4i_p a[2], b[4][2];
+  {
+    uint32_t h = static_cast<uint32_t>(l) * 2654435761u + blockIdx.x * 97u;
+    const int m = random ? -1 : 0;
+    auto next = [&]() {
+      h ^= h >> 13;
+      h *= 2246822519u;
+      h ^= h >> 16;
+      h += 0x9E3779B9u;
+      return static_cast<int>(h) & m;
+    };
+#pragma unroll
+    for (int i = 0; i < 2; ++i) a[i] = (v4i_p){next(), next(), next(), next()};
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int i = 0; i < 2; ++i) b[t][i] = (v4i_p){next(), next(), next(), next()};
+  }
+  constexpr int kMagic = 0x4B400000;  // the bits of 1.5 * 2^23
+  const v4i_p magic = (v4i_p)(FOLD ? kMagic : 0);
+  v4i_p acc[16];
+  float y[16][4];
+#pragma unroll
+  for (int t = 0; t < 16; ++t) {
+    acc[t] = magic;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) y[t][r] = 0.0f;
+  }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      if constexpr (FOLD) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[t][r] = __builtin_fmaf(__int_as_float(acc[t][r]) - 12582912.0f, 0.001f, y[t][r]);
+        acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], b[t & 3][0], magic, 0, 0, 0);
+      } else {
+        acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[0], b[t & 3][0], acc[t], 0, 0, 0);
+      }
+      acc[t] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a[1], b[(t >> 2) & 3][1], acc[t], 0, 0, 0);
+    }
+  }
+  int s = 0;
+#pragma unroll
+  for (int t = 0; t < 16; ++t)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) s += acc[t][r] + static_cast<int>(y[t][r]);
+  sink[blockIdx.x * 256 + threadIdx.x] = s;  // keeps the work live
+}
+
 }  // namespace
 
 int mfma_probe_workgroups() { return device_cus() * 2; }
 
-hipError_t launch_mfma_probe(int32_t* sink, int32_t iters, int32_t random, int32_t fold, hipStream_t s) {
+hipError_t launch_mfma_probe(int32_t* sink, int32_t shape, int32_t iters, int32_t random, int32_t fold,
+                             hipStream_t s) {
   const dim3 grid(static_cast<unsigned>(mfma_probe_workgroups()));
-  if (fold)
+  if (shape == 16) {
+    if (fold)
+      hipLaunchKernelGGL((mfma_probe16_kernel<true>), grid, dim3(256), 0, s, sink, iters, random);
+    else
+      hipLaunchKernelGGL((mfma_probe16_kernel<false>), grid, dim3(256), 0, s, sink, iters, random);
+  } else if (fold) {
     hipLaunchKernelGGL((mfma_probe_kernel<true>), grid, dim3(256), 0, s, sink, iters, random);
-  else
+  } else {
     hipLaunchKernelGGL((mfma_probe_kernel<false>), grid, dim3(256), 0, s, sink, iters, random);
+  }
   return hipGetLastError();
 }
 

@@ -307,42 +307,62 @@ def test_deterministic(bits):
 
 
 # ------------------------------------------------------------------ full-size layers, sampled rows
+# (name, bit widths, tokens per sample, batch, K, N, outlier fraction(s)):
+# every linear of the 2B (4192 tokens) and 14B (8384 tokens) configurations,
+# the 4-bit 2B linears with per-stream outliers of 1 / 2 / 5 %, the batch-4
+# sweep's row count (16768 tokens), and one GPU's column shard of the 14B up
+# projection at 8-way tensor parallelism.
 FULL = [
-    ("2B up W4A8", 8, synth.TOKENS_2B, 2048, 8192, 0.02),
-    ("2B down W4A8", 8, synth.TOKENS_2B, 8192, 2048, 0.02),
-    ("2B qkv W4A4", 4, synth.TOKENS_2B, 2048, 6144, (0.01, 0.02, 0.05)),
-    ("2B down W4A4", 4, synth.TOKENS_2B, 8192, 2048, (0.01, 0.02, 0.05)),
-    ("14B out W4A8", 8, synth.TOKENS_14B, 5120, 5120, 0.02),
-    # one GPU's column shard of the 14B up projection at 8-way tensor parallelism
-    ("14B up TP8 shard W4A8", 8, synth.TOKENS_14B, 5120, 1728, 0.02),
-    ("14B up TP8 shard W4A4", 4, synth.TOKENS_14B, 5120, 1728, 0.02),
+    ("2B up", (8, 4), synth.TOKENS_2B, 1, 2048, 8192, 0.02),
+    ("2B down", (8,), synth.TOKENS_2B, 1, 8192, 2048, 0.02),
+    ("2B qkv outliers 1/2/5%", (4,), synth.TOKENS_2B, 1, 2048, 6144, (0.01, 0.02, 0.05)),
+    ("2B out outliers 1/2/5%", (4,), synth.TOKENS_2B, 1, 2048, 2048, (0.01, 0.02, 0.05)),
+    ("2B up outliers 1/2/5%", (4,), synth.TOKENS_2B, 1, 2048, 8192, (0.01, 0.02, 0.05)),
+    ("2B down outliers 1/2/5%", (4,), synth.TOKENS_2B, 1, 8192, 2048, (0.01, 0.02, 0.05)),
+    ("2B up batch 4", (8, 4), synth.TOKENS_2B, 4, 2048, 8192, 0.02),
+    ("14B qkv", (8, 4), synth.TOKENS_14B, 1, 5120, 15360, 0.02),
+    ("14B out", (8, 4), synth.TOKENS_14B, 1, 5120, 5120, 0.02),
+    ("14B up", (8, 4), synth.TOKENS_14B, 1, 5120, 13824, 0.02),
+    ("14B down", (8, 4), synth.TOKENS_14B, 1, 13824, 5120, 0.02),
+    ("14B up TP8 shard", (8, 4), synth.TOKENS_14B, 1, 5120, 1728, 0.02),
 ]
 
 
-@pytest.mark.parametrize("name,bits,tokens,K,N,outl", FULL, ids=[f[0] for f in FULL])
-def test_full_size_sampled_rows(name, bits, tokens, K, N, outl):
-    """Full-size layers in the launch configuration the benchmark times; the
-    oracle checks every proprio / action row and 256 random video rows."""
-    L = synth.make_layer(K=K, N=N, stream_counts=tokens, T=10, seed=[8, K, N], outlier_frac=outl)
+@pytest.mark.parametrize("name,bits_list,tokens,batch,K,N,outl", FULL, ids=[f[0] for f in FULL])
+def test_full_size_sampled_rows(name, bits_list, tokens, batch, K, N, outl):
+    """Full-size layers in the launch configuration the benchmark times, with
+    fp32 and bf16 outputs; the oracle checks every proprio / action row and
+    256 random video rows, and the first kernel's codes and scales of those
+    rows are read back from the workspace."""
+    L = synth.make_layer(K=K, N=N, stream_counts=tokens, T=10, seed=[8, K, N, batch], outlier_frac=outl,
+                         batch=batch)
     pw, W = oracle_weight(L, 128)
     step = 7
-    act = act_params(L, step, bits, 0)
-    y, ws = run_linear(FUSED[bits], L, act, W, BF16)
     rows = synth.stratified_rows(L.tok2stream, 256, seed=0)
-    res = oracle_linear(L, step, bits, 0, pw, 128, rows=rows)
-    check_output(y, res, BF16, rows=rows)
-    # codes and scales of the sampled rows, read back from the workspace
-    check_first_kernel_output(ws, L.M, L.K, bits, 128, res, rows=rows)
+    x = xdev(L)
+    for bits in bits_list:
+        act = act_params(L, step, bits, 0)
+        res = oracle_linear(L, step, bits, 0, pw, 128, rows=rows)
+        ws = B.alloc_workspace(B.SQ_VARIANT_FUSED, L.M, K, N, bits)
+        for out in (F32, BF16):
+            y = torch.full((L.M, N), float("nan"), dtype=TORCH_OUT[out], device="cuda")
+            FUSED[bits](x, act, W, y, out, ws)
+            check_output(y, res, out, rows=rows)
+            check_first_kernel_output(ws, L.M, L.K, bits, 128, res, rows=rows)
+            del y
+        del ws
 
 
-def test_mfma_probe_runs():
+@pytest.mark.parametrize("shape", [32, 16])
+def test_mfma_probe_runs(shape):
     """The matrix-core probe (a measurement hook) runs on the GPU and writes
-    its sink; zero operands leave every accumulator zero."""
+    its sink; zero operands leave every accumulator zero (without the fold)."""
     sink = B.probe_sink()
     sink.fill_(7)
-    B.sq_probe_mfma_i8(3, False, False, sink)
+    B.sq_probe_mfma_i8(3, False, False, sink, shape=shape)
     torch.cuda.synchronize()
     assert int(sink.abs().max()) == 0
-    B.sq_probe_mfma_i8(3, True, True, sink)
-    torch.cuda.synchronize()
-    assert int(sink.abs().max()) > 0
+    for fold in (False, True):
+        B.sq_probe_mfma_i8(3, True, fold, sink, shape=shape)
+        torch.cuda.synchronize()
+        assert int(sink.abs().max()) > 0
