@@ -74,6 +74,12 @@ __device__ __forceinline__ void fold8_biased(const v16i& c, float w, float (&yt)
   for (int r = 0; r < 16; ++r) yt[r] = __builtin_fmaf(__int_as_float(c[r]) - 12582912.0f, w, yt[r]);
 }
 
+// The same for the four registers of a 16 x 16 accumulator tile.
+__device__ __forceinline__ void fold8_biased4(const v4i& c, float w, float (&yt)[4]) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) yt[r] = __builtin_fmaf(__int_as_float(c[r]) - 12582912.0f, w, yt[r]);
+}
+
 // LDS byte offset of a __shared__ object.
 __device__ __forceinline__ uint32_t lds_offset(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const lds_u8_t*)p));

@@ -726,11 +726,6 @@ struct FragOffsets16 {
   __device__ __forceinline__ int b(int tn) const { return b0 + tn * 16 * (KT / 2); }
 };
 
-__device__ __forceinline__ void fold8_biased4(const v4i& c, float w, float (&yt)[4]) {
-#pragma unroll
-  for (int r = 0; r < 4; ++r) yt[r] = __builtin_fmaf(__int_as_float(c[r]) - 12582912.0f, w, yt[r]);
-}
-
 // the weight steps of a stage for the lane's column of each 16-wide tile
 __device__ __forceinline__ void read_wscale16(const uint8_t* st, int wave, int lane, float (&w)[TN16]) {
   using LY = Layout<8, false>;
