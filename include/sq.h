@@ -192,6 +192,23 @@ sq_status sq_linear_w4a4(const uint16_t* x, int32_t M, const sq_act_params* act,
                          void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
                          hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the fused
+ * W4A8 linear of sq_linear_w4a8 (same validation, kernels and results) with
+ * no workspace argument.  Q_X, r and the GEMM's partial sums live in a device
+ * array of SQ_NOALLOC_SCRATCH_BYTES inside this library, one per GPU, held
+ * until the process ends; the call allocates and frees nothing.  Layers whose
+ * sq_workspace_bytes(SQ_VARIANT_FUSED, M, K, N, 8) exceeds the array return
+ * SQ_ERR_WORKSPACE and launch nothing.  Every call on a GPU shares that GPU's
+ * array and leaves its contents behind (nothing in it needs to start at
+ * zero): calls that overlap on one GPU (concurrent streams, or host threads
+ * without ordering) race and must be serialized by the caller.  The first
+ * call on each device looks the array's device address up (SQ_ERR_HIP if
+ * that fails). */
+#define SQ_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+sq_status sq_linear_w4a8_noalloc(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                                 void* y, int32_t out_dtype, hipStream_t stream);
+
 /* The same layer without fusion, as the execution that Sec. 4.4 replaces:
  * channel scaling, gain, quantization, GEMM, dequantization, inverse-gain
  * compensation and bias each run as their own kernel, passing fp32 (or

@@ -88,6 +88,7 @@ _SIGS = {
     "sq_linear_w4a8": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_w4a4": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_unfused": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
+    "sq_linear_w4a8_noalloc": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P]),
     "sq_debug_block_acc_i32": (_I, [_P, _I, _I, ctypes.POINTER(sq_weight), _P, _P]),
     "sq_calib_reference": (_I, [_P, _I, _P, ctypes.POINTER(sq_weight), _P, _P]),
     "sq_calib_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
@@ -249,6 +250,17 @@ def sq_linear_w4a4(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, s
 
 def sq_linear_unfused(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, stream=None) -> None:
     _linear("sq_linear_unfused", x, act, w, y, out_dtype, workspace, stream)
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20  # SQ_NOALLOC_SCRATCH_BYTES
+
+
+def sq_linear_w4a8_noalloc(x, act: ActParams, w: Weight, y, out_dtype: int, stream=None) -> None:
+    """sq_linear_w4a8 without a workspace argument: the library's own device
+    scratch array holds Q_X, r and the partial sums (include/sq.h)."""
+    s, ws = act.struct(), w.struct()
+    _check(lib().sq_linear_w4a8_noalloc(_ptr(x), x.shape[0], ctypes.byref(s), ctypes.byref(ws), _ptr(y), out_dtype,
+                                        _stream(stream)), "sq_linear_w4a8_noalloc")
 
 
 def sq_debug_block_acc_i32(qx: torch.Tensor, act_bits: int, w: Weight, acc_out: torch.Tensor,

@@ -242,6 +242,18 @@ sq_status linear_fused(int32_t bits, const uint16_t* x, int32_t M, const sq_act_
   return hip_status(launch_gemm(bits, kEpiOut, g, stream, f.partial, f.partial_bytes));
 }
 
+}  // namespace
+
+// The fused linear on a caller-chosen workspace (the library's static scratch
+// for the allocation-free entry point).
+sq_status sq::linear_fused_on(int32_t bits, const uint16_t* x, int32_t M, const sq_act_params* act,
+                              const sq_weight* w, void* y, int32_t out_dtype, void* ws, size_t ws_bytes,
+                              hipStream_t stream) {
+  return linear_fused(bits, x, M, act, w, y, out_dtype, ws, ws_bytes, stream);
+}
+
+namespace {
+
 // One candidate of Eq. 9: the fused linear in STATIC mode with one-step
 // tables (gamma [S], clip [1], both device pointers) and no bias into fp32,
 // then the weighted squared error against y_ref into *out.

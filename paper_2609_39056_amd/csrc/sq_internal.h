@@ -133,6 +133,11 @@ struct PackArgs {
   int32_t N, K, w_group;
 };
 
+// The fused linear (8- or 4-bit activations) with its workspace given: the
+// same validation and kernels as sq_linear_w4a8 / sq_linear_w4a4.
+sq_status linear_fused_on(int32_t bits, const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                          void* y, int32_t out_dtype, void* ws, size_t ws_bytes, hipStream_t stream);
+
 // ---------------------------------------------------------------- launchers (return hipError_t)
 hipError_t launch_quantize_act(int act_bits, const QuantArgs& a, hipStream_t s);
 hipError_t launch_pack_weights(const PackArgs& a, hipStream_t s);
