@@ -480,6 +480,50 @@ def calibration_cpu(L, K, rows):
     return dict(tokens_per_s_per_candidate=round(rows / dt, 1), seconds=round(dt, 3), rows=rows)
 
 
+def graph_us(torch, fn, reps, warm=3):
+    """Device time per call: `reps` calls captured as one HIP graph, one warm
+    replay, then one timed replay (HIP events)."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(reps):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    g.replay()
+    e1.record()
+    torch.cuda.synchronize()
+    del g
+    return e0.elapsed_time(e1) * 1e3 / reps
+
+
+def static_single_kernel_figures(torch, B, synth, dev, reps=50):
+    """The STATIC single-kernel W4A8 linear (sq_linear_w4a8_static1) against
+    the two-kernel fused call in STATIC mode (sq_linear_w4a8), at 64 and 128
+    action tokens on the 2B-class linears: us per call, graph-replayed."""
+    out = {}
+    for M in (64, 128):
+        for i, (name, (K, N)) in enumerate(synth.LINEARS_2B.items()):
+            L = synth.device_layer(K, N, (0, 0, M), T=T_STEPS, seed=7000 + i, device=dev)
+            W = B.prepare_weight(L["w"], L["d"], W_GROUP, bias=L["bias"])
+            clip = torch.full((T_STEPS,), 4.0, dtype=torch.float32, device=dev)
+            act = B.ActParams(tok2stream=L["tok2stream"], gamma=L["gamma"], step=1, act_bits=8,
+                              range_mode=B.SQ_RANGE_STATIC, clip=clip, dinv=L["dinv"])
+            y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+            wsf = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, K, N, 8, dev)
+            wsg = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, K, N, 8, dev)
+            two = graph_us(torch, lambda: B.sq_linear_w4a8(L["x"], act, W, y, B.SQ_OUT_BF16, wsf), reps)
+            one = graph_us(torch, lambda: B.sq_linear_w4a8_static1(L["x"], act, W, y, B.SQ_OUT_BF16, wsg), reps)
+            out[f"{name}_M{M}"] = dict(us_two_kernels=round(two, 2), us_single_kernel=round(one, 2),
+                                       single_over_two=round(one / two, 3))
+            del L, W, y, wsf, wsg
+    return out
+
+
 def run_action_only(args):
     """The few-token regime: every call streams a distinct weight (28 layers x
     4 linears, 0.7 GB packed: more than the 256 MB last-level cache), one pass
@@ -724,6 +768,9 @@ def main():
     del b4
     torch.cuda.empty_cache()
 
+    # ---- the STATIC single-kernel linear at few tokens, against the two kernels
+    single = static_single_kernel_figures(torch, B, synth, dev)
+
     # ---- the calibration path of Eq. (9) on the 2B up projection
     calib = calibration_figures(torch, B, mlp[0], stream, dev, None if args.no_cpu else 256)
 
@@ -819,6 +866,7 @@ def main():
                                    **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
                                                   "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}
                                       for b in (8, 4)}},
+        "static_single_kernel_few_tokens": single,
         "calibration": calib,
         "hbm_copy": {"bytes": 2 * (COPY_MIB << 20), "us": round(copy_us, 1),
                      "gbs": round(2 * (COPY_MIB << 20) / (copy_us * 1e-6) / 1e9, 1)},

@@ -209,6 +209,25 @@ sq_status sq_linear_w4a4(const uint16_t* x, int32_t M, const sq_act_params* act,
 sq_status sq_linear_w4a8_noalloc(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                                  void* y, int32_t out_dtype, hipStream_t stream);
 
+/* The fused W4A8 linear as ONE kernel, for the paper's static activation
+ * ranges (App. D: an offline threshold per layer and step) and few tokens:
+ * the weight-streaming GEMM reads X itself and quantizes each 128-channel
+ * stage in LDS with the first kernel's arithmetic (the quantization block of
+ * this header, STATIC), so neither the first kernel's launch nor Q_X in HBM
+ * remain (Sec. 4.4 on removing launches and intermediate traffic).  The
+ * outputs equal those of sq_linear_w4a8 with the same arguments bit for bit.
+ * Requires act->act_bits == 8, act->range_mode == SQ_RANGE_STATIC,
+ * M <= 128 and w->w_group 128 or K (else SQ_ERR_UNSUPPORTED).
+ *   workspace: NULL (K is never split across workgroups) or a device buffer
+ *   of ws_bytes >= sq_workspace_bytes(SQ_VARIANT_GEMM, M, K, N, 8), 16-byte
+ *   aligned, for the partial sums of a K split (contents need no
+ *   initialization).
+ * Every workgroup quantizes the activations it reads (M x its K range), so
+ * the quantization work is repeated once per 32 output channels; with the
+ * first kernel it is done once.  Which of the two is faster is measured. */
+sq_status sq_linear_w4a8_static1(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                                 void* y, int32_t out_dtype, void* workspace, size_t ws_bytes, hipStream_t stream);
+
 /* The same layer without fusion, as the execution that Sec. 4.4 replaces:
  * channel scaling, gain, quantization, GEMM, dequantization, inverse-gain
  * compensation and bias each run as their own kernel, passing fp32 (or

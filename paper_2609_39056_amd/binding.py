@@ -89,6 +89,8 @@ _SIGS = {
     "sq_linear_w4a4": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_unfused": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S, _P]),
     "sq_linear_w4a8_noalloc": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P]),
+    "sq_linear_w4a8_static1": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S,
+                                    _P]),
     "sq_debug_block_acc_i32": (_I, [_P, _I, _I, ctypes.POINTER(sq_weight), _P, _P]),
     "sq_calib_reference": (_I, [_P, _I, _P, ctypes.POINTER(sq_weight), _P, _P]),
     "sq_calib_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
@@ -246,6 +248,16 @@ def sq_linear_w4a8(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, s
 
 def sq_linear_w4a4(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, stream=None) -> None:
     _linear("sq_linear_w4a4", x, act, w, y, out_dtype, workspace, stream)
+
+
+def sq_linear_w4a8_static1(x, act: ActParams, w: Weight, y, out_dtype: int, workspace=None, stream=None) -> None:
+    """The STATIC single-kernel W4A8 linear for at most 128 tokens (include/sq.h);
+    workspace None (no K split) or a SQ_VARIANT_GEMM workspace."""
+    M = x.shape[0]
+    s, ws = act.struct(), w.struct()
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(lib().sq_linear_w4a8_static1(_ptr(x), M, ctypes.byref(s), ctypes.byref(ws), _ptr(y), out_dtype,
+                                        _ptr(workspace), nbytes, _stream(stream)), "sq_linear_w4a8_static1")
 
 
 def sq_linear_unfused(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, stream=None) -> None:

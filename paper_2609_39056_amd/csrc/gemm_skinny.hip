@@ -27,10 +27,19 @@ constexpr int TM = 2;  // 32-row MFMA tiles per wave
 // activations) there is no fold in the loop: each wave keeps int32 sums over
 // its stages, the four are added in integers, and the total is converted and
 // scaled once (split ranges hand int32 sums to the second kernel).
+// t rounded to the nearest integer, ties to even (abs(t) <= 2^22): the low
+// byte of t + 1.5 * 2^23 is the two's-complement code.
+__device__ __forceinline__ uint32_t rne_code_bits8(float t) { return __float_as_uint(t + 12582912.0f); }
+// The low bytes of four words, in order, as one word.
+__device__ __forceinline__ uint32_t pack_bytes8(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3) {
+  const uint32_t lo = __builtin_amdgcn_perm(w1, w0, 0x0c0c0400u);
+  const uint32_t hi = __builtin_amdgcn_perm(w3, w2, 0x0c0c0400u);
+  return __builtin_amdgcn_perm(hi, lo, 0x05040100u);
+}
+
 constexpr int SK_BM = 64;  // rows per workgroup
 constexpr int SK_BN = 32;  // output channels per workgroup
-constexpr int SK_DIST = 2;             // stages loaded ahead
-constexpr int SK_SLOTS = SK_DIST + 1;  // ring slots per wave
+constexpr int SK_DIST = 2;  // stages loaded ahead (the codes kernels)
 
 // LDS layout of a slot (16-byte chunks XOR-swizzled, as in the tiled kernel,
 // so that fragment reads are free of bank conflicts):
@@ -42,23 +51,32 @@ constexpr int SK_SLOTS = SK_DIST + 1;  // ring slots per wave
 // Lane (column n = lane & 31, h = lane >> 5) feeds k-step s of a stage with the
 // channels [64 (s >> 1) + 32 h + 16 (s & 1), +16) of both operands; 64-wide
 // blocks are k-steps {0, 1} and {2, 3}.
-template <int ABITS>
+// QX (the single-kernel linear, 8-bit STATIC ranges): the slot's activation
+// area holds the stage's bf16 rows (row r, 256 B, chunk c at position
+// c ^ (r & 15)), which the wave quantizes in place into the 8-bit layout
+// above (the first 8 KB) before its MFMAs; one stage is loaded ahead.
+template <int ABITS, bool QX = false>
 struct Sk {
-  static constexpr int A = SK_BM * (ABITS == 8 ? KT : KT / 2);  // activation codes (8 / 4 KB)
+  static constexpr int DIST = QX ? 1 : SK_DIST;  // stages loaded ahead
+  static constexpr int SLOTS = DIST + 1;         // ring slots per wave
+  static constexpr int A = SK_BM * (QX ? 2 * KT : (ABITS == 8 ? KT : KT / 2));  // bf16 rows, or codes (8 / 4 KB)
   static constexpr int B = SK_BN * (KT / 2);                    // packed weights (2 KB)
   static constexpr int SIG = ABITS == 4 ? 256 : 0;              // 4-bit group steps
   static constexpr int B_OFF = A, S_OFF = A + B, W_OFF = A + B + SIG;
-  static constexpr int SLOT = W_OFF + 256;                      // + one 256 B load of weight steps
+  static constexpr int D_OFF = W_OFF + 256;                     // QX: the stage's 128 D^-1 values
+  static constexpr int SLOT = D_OFF + (QX ? 512 : 0);           // + one 256 B load of weight steps
   static constexpr int NDMA = A / 1024 + B / 1024 + (ABITS == 4 ? 1 : 0) + 1;  // loads per stage and wave
-  static constexpr int WGS_PER_CU = 4 * SK_SLOTS * SLOT * 2 <= 160 * 1024 ? 2 : 1;
-  static_assert(4 * SK_BM * SK_BN * 4 <= 4 * SK_SLOTS * SLOT, "the wave sums fit in the ring");
+  static constexpr int WGS_PER_CU = 4 * SLOTS * SLOT * 2 <= 160 * 1024 ? 2 : 1;
+  static_assert(4 * SK_BM * SK_BN * 4 <= 4 * SLOTS * SLOT, "the wave sums fit in the ring");
+  static_assert(!QX || ABITS == 8, "in-kernel quantization: 8-bit codes");
 };
 
-template <int ABITS, int EPI, bool PC>
-__global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel(GemmArgs a) {
-  using L = Sk<ABITS>;
+template <int ABITS, int EPI, bool PC, bool QX = false>
+__global__ __launch_bounds__(256, (Sk<ABITS, QX>::WGS_PER_CU)) void gemm_skinny_kernel(GemmArgs a) {
+  using L = Sk<ABITS, QX>;
   static_assert(!PC || ABITS == 8, "one weight step per channel: 8-bit activations");
-  __shared__ __attribute__((aligned(16))) uint8_t ring[4][SK_SLOTS][L::SLOT];
+  static_assert(!QX || EPI == kEpiOut, "the single-kernel linear finishes its outputs");
+  __shared__ __attribute__((aligned(16))) uint8_t ring[4][L::SLOTS][L::SLOT];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int M = a.M, N = a.N, K = a.K;
@@ -69,13 +87,16 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
   const int kt0 = range * nkt / S, kt1 = (range + 1) * nkt / S;
   const int h = lane >> 5, col = lane & 31;
   const int rows = min(M - m0, SK_BM);
-  const int arow = ABITS == 8 ? K : K / 2;  // bytes of an activation row
+  const int arow = QX ? 2 * K : (ABITS == 8 ? K : K / 2);  // bytes of an activation row (QX: bf16)
 
   // direct-load sources: rows past the matrix read its last row
   uint32_t voffA[L::A / 1024];
 #pragma unroll
   for (int i = 0; i < L::A / 1024; ++i) {
-    if constexpr (ABITS == 8) {
+    if constexpr (QX) {
+      const int r = 4 * i + (lane >> 4);
+      voffA[i] = static_cast<uint32_t>(min(r, rows - 1) * arow + 16 * ((lane & 15) ^ (r & 15)));
+    } else if constexpr (ABITS == 8) {
       const int r = 8 * i + (lane >> 3);
       voffA[i] = static_cast<uint32_t>(min(r, rows - 1) * arow + 16 * ((lane & 7) ^ ((r >> 1) & 7)));
     } else {
@@ -104,6 +125,12 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
     if constexpr (ABITS == 4) dma<4>(sig + 2 * kt, voffS, st + L::S_OFF);  // the stage's two groups
     // group-major steps of the stage's weight group
     dma<4>(a.w_scale + static_cast<size_t>((kt * KT) / a.w_group) * N + n0, voffW, st + L::W_OFF);
+    if constexpr (QX) {  // D^-1 of the stage's channels (one stage ahead: the wait is for all loads)
+      if (a.dinv != nullptr) {
+        dma<4>(a.dinv + kt * KT, 4 * lane, st + L::D_OFF);
+        dma<4>(a.dinv + kt * KT + 64, 4 * lane, st + L::D_OFF + 256);
+      }
+    }
   };
 
   // fragment offsets within a slot: activations per (row tile, k-step) for
@@ -217,17 +244,71 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
     }
   };
 
+  // QX: the STATIC quantization of Eq. 1 with the channel scaling of Eq. 6
+  // and the gain of Eq. 8, with the first kernel's fp32 chain
+  // (q = rint(clamp((x * dinv) * g * (1 / Delta))), Delta = c / 127): lane l
+  // quantizes row l of the stage (rows past M repeat the last row)
+  float qg = 0.0f, qinv = 0.0f, qdelta = 0.0f;
+  if constexpr (QX) {
+    qg = a.gamma[a.step * a.S + a.tok2stream[m0 + min(lane, rows - 1)]];
+    qdelta = a.clip[a.step] / 127.0f;
+    qinv = 1.0f / qdelta;
+    if (__builtin_isinf(qinv)) qinv = 0.0f;
+  }
+  auto quantize = [&](int slot, int kt) {
+    uint8_t* st = &ring[wave][slot][0];
+    const int r = lane;
+    uint4 xv[16];  // the row's 128 bf16 values of the stage, chunk c at position c ^ (r & 15)
+#pragma unroll
+    for (int c = 0; c < 16; ++c) xv[c] = *reinterpret_cast<const uint4*>(st + r * 256 + 16 * (c ^ (r & 15)));
+    const bool has_d = a.dinv != nullptr;
+    uint4 out[8];
+#pragma unroll
+    for (int c16 = 0; c16 < 8; ++c16) {
+      // D^-1 of the 16 channels (the same for every lane: broadcast reads);
+      // without D, 1 (x * 1 = x exactly)
+      float dvv[16];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 d4 = *reinterpret_cast<const float4*>(st + L::D_OFF + 64 * c16 + 16 * q);
+        dvv[4 * q] = has_d ? d4.x : 1.0f;
+        dvv[4 * q + 1] = has_d ? d4.y : 1.0f;
+        dvv[4 * q + 2] = has_d ? d4.z : 1.0f;
+        dvv[4 * q + 3] = has_d ? d4.w : 1.0f;
+      }
+      uint32_t b[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int k = 16 * c16 + e;
+        const uint32_t w = (k & 7) < 2 ? xv[k >> 3].x : (k & 7) < 4 ? xv[k >> 3].y : (k & 7) < 6 ? xv[k >> 3].z
+                                                                                                 : xv[k >> 3].w;
+        const float x = __uint_as_float((k & 1) ? (w & 0xFFFF0000u) : (w << 16)) * dvv[e];
+        float t = (x * qg) * qinv;
+        t = fminf(fmaxf(t, -127.0f), 127.0f);
+        b[e] = rne_code_bits8(t);
+      }
+      out[c16] = make_uint4(pack_bytes8(b[0], b[1], b[2], b[3]), pack_bytes8(b[4], b[5], b[6], b[7]),
+                            pack_bytes8(b[8], b[9], b[10], b[11]), pack_bytes8(b[12], b[13], b[14], b[15]));
+    }
+    // in place: every read of the wave was issued before these writes, and
+    // the LDS executes a wave's operations in order
+#pragma unroll
+    for (int c16 = 0; c16 < 8; ++c16)
+      *reinterpret_cast<uint4*>(st + r * KT + 16 * (c16 ^ ((r >> 1) & 7))) = out[c16];
+  };
+
   // this wave's stages kt0 + wave + 4j, j < nst; past the end the last stage
   // is loaded again, so every wait leaves the same number of loads in flight
   const int nst = kt1 - kt0 > wave ? (kt1 - kt0 - wave + 3) / 4 : 0;
   auto stage = [&](int j) { return kt0 + wave + 4 * min(j, nst - 1); };
   if (nst > 0) {
 #pragma unroll
-    for (int p = 0; p < SK_DIST; ++p) issue(stage(p), p);
+    for (int p = 0; p < L::DIST; ++p) issue(stage(p), p);
     for (int j = 0; j < nst; ++j) {
-      wait_vm<L::NDMA * (SK_DIST - 1)>();                  // stage j has landed
-      issue(stage(j + SK_DIST), (j + SK_DIST) % SK_SLOTS);  // into the slot read last iteration
-      compute(j % SK_SLOTS);
+      wait_vm<L::NDMA * (L::DIST - 1)>();                     // stage j has landed
+      issue(stage(j + L::DIST), (j + L::DIST) % L::SLOTS);  // into the slot read last iteration
+      if constexpr (QX) quantize(j % L::SLOTS, stage(j));
+      compute(j % L::SLOTS);
     }
   }
   if constexpr (ABITS == 8 && !PC) {
@@ -291,7 +372,9 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
   float rowf = 1.0f, bias = 0.0f;
   if constexpr (EPI == kEpiOut) {
     const int m = m0 + min(lane, rows - 1);
-    if constexpr (ABITS == 8)
+    if constexpr (QX)
+      rowf = qdelta / a.gamma[a.step * a.S + a.tok2stream[m]];  // r_i = Delta / gamma_s(i), as the first kernel
+    else if constexpr (ABITS == 8)
       rowf = static_cast<const float*>(a.act_scale)[m];
     else
       rowf = 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
@@ -333,7 +416,7 @@ __global__ __launch_bounds__(256, Sk<ABITS>::WGS_PER_CU) void gemm_skinny_kernel
 // output in range order (int32 sums with one step per channel, then the one
 // conversion) and finishes it as the skinny epilogue does.  Four adjacent
 // outputs per thread.
-template <int ABITS, int EPI, bool PC>
+template <int ABITS, int EPI, bool PC, bool QX = false>
 __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   const int strips = a.N / SK_BN;
   const int g = blockIdx.x * 256 + threadIdx.x;  // one thread per 4 outputs of a 64 x 32 block
@@ -372,8 +455,9 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
     y[3] = acc.w;
   }
   if constexpr (EPI == kEpiOut) {
-    const float rowf = ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
-                                  : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
+    const float rowf = QX ? (a.clip[a.step] / 127.0f) / a.gamma[a.step * a.S + a.tok2stream[m]]
+                          : ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
+                                       : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
       const float b = a.bias != nullptr ? bf16_to_f32(a.bias[n + j]) : 0.0f;
@@ -419,7 +503,7 @@ int skinny_split(int act_bits, int32_t M, int32_t N, int32_t K) {
   return act_bits == 8 ? split_t<8>(M, N, K) : split_t<4>(M, N, K);
 }
 
-template <int ABITS, int EPI, bool PC>
+template <int ABITS, int EPI, bool PC, bool QX = false>
 hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
   GemmArgs a = a0;
   int S = skinny_split(ABITS, a.M, a.N, a.K);
@@ -427,11 +511,16 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
   a.split = S;
   a.partial = S > 1 ? partial : nullptr;
   const int strips = a.N / SK_BN, mblocks = (a.M + SK_BM - 1) / SK_BM;
-  hipLaunchKernelGGL((gemm_skinny_kernel<ABITS, EPI, PC>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((gemm_skinny_kernel<ABITS, EPI, PC, QX>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || S == 1) return e;
   const int threads = strips * mblocks * (SK_BM * SK_BN / 4);
-  hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI, PC>), dim3((threads + 255) / 256), dim3(256), 0, s, a);
+  if constexpr (QX) {  // the second kernel takes r_i from the row-scale array: the row factor is computed there too
+    hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI, PC, true>), dim3((threads + 255) / 256), dim3(256), 0, s,
+                       a);
+  } else {
+    hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI, PC>), dim3((threads + 255) / 256), dim3(256), 0, s, a);
+  }
   return hipGetLastError();
 }
 
@@ -441,6 +530,11 @@ size_t skinny_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K) {
   const int S = skinny_split(act_bits, M, N, K);
   if (S <= 1) return 0;
   return static_cast<size_t>(N / SK_BN) * ((M + SK_BM - 1) / SK_BM) * S * (SK_BM * SK_BN) * sizeof(float);
+}
+
+hipError_t launch_skinny_static1(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
+  return a.w_group != KT ? launch_t<8, kEpiOut, true, true>(a, s, partial, partial_bytes)
+                         : launch_t<8, kEpiOut, false, true>(a, s, partial, partial_bytes);
 }
 
 hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,

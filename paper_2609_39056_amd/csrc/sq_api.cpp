@@ -406,6 +406,25 @@ sq_status sq_linear_w4a4(const uint16_t* x, int32_t M, const sq_act_params* act,
   return linear_fused(4, x, M, act, w, y, out_dtype, workspace, ws_bytes, stream);
 }
 
+sq_status sq_linear_w4a8_static1(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                                 void* y, int32_t out_dtype, void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (x == nullptr || y == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  st = check_act(act, w->K);
+  if (st != SQ_OK) return st;
+  if (act->act_bits != 8 || act->range_mode != SQ_RANGE_STATIC) return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!skinny_applies(8, M, w->K, w->w_group)) return SQ_ERR_UNSUPPORTED;
+  if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(y, 16)) return SQ_ERR_ALIGN;
+  if (workspace != nullptr && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  GemmArgs g = gemm_args(x, nullptr, M, act, w, y, out_dtype);
+  g.dinv = act->dinv;
+  g.clip = act->clip;
+  return hip_status(launch_skinny_static1(g, stream, static_cast<float*>(workspace), workspace ? ws_bytes : 0));
+}
+
 sq_status sq_linear_unfused(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                             void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
                             hipStream_t stream) {

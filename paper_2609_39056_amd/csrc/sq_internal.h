@@ -100,6 +100,10 @@ struct GemmArgs {
   // sums in `partial`, and one more kernel adds them up and finishes the tile.
   int32_t ndp, split;
   float* partial;
+  // the single-kernel linear (launch_skinny_static1): qx holds X (bf16 [M][K])
+  // and the kernel quantizes it with STATIC thresholds, D^-1 and the gains
+  const float* dinv;
+  const float* clip;
 };
 
 // Bytes of the partial-sum buffer the split-K tail may use for a GEMM of this
@@ -122,6 +126,11 @@ inline bool skinny_applies(int act_bits, int32_t M, int32_t K, int32_t w_group) 
 // the weight-streaming kernel does not apply (more than 128 tokens).
 inline bool a4_fp8_path(int32_t M, int32_t K, int32_t w_group) { return !skinny_applies(4, M, K, w_group); }
 size_t skinny_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K);
+// The STATIC single-kernel W4A8 linear for few tokens (skinny_applies(8, ...)):
+// the weight-streaming GEMM with the first kernel's quantization done on each
+// stage in LDS; a.qx = X, a.dinv, a.clip, a.gamma, a.tok2stream, a.step, a.S
+// set; EPI kEpiOut.  Splits K like launch_skinny (8-bit).
+hipError_t launch_skinny_static1(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes);
 hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,
                          size_t partial_bytes);
 

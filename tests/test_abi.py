@@ -273,3 +273,26 @@ def test_scaling_entry_points_reject(L):
                      (dict(G=96), UNSUP), (dict(alphas=bad, n=2), UNSUP), (dict(ref=A + 8), ALIGN),
                      (dict(rw=A + 4), ALIGN), (dict(nbytes=4096), WS), (dict(N=100), SHAPE)]:
         assert so(**kw) == code, kw
+
+
+def test_static1_rejects(L):
+    """The single-kernel STATIC linear validates before launching: it needs
+    STATIC 8-bit ranges, at most 128 tokens and weight groups of 128 or K."""
+    st = dict(range_mode=1)
+
+    def s1(x=A, M=88, a=None, w=None, y=A, out=0, ws=None, nbytes=0):
+        a = act(**st) if a is None else a
+        w = wt() if w is None else w
+        return L.sq_linear_w4a8_static1(x, M, ctypes.byref(a), ctypes.byref(w), y, out, ws, nbytes, None)
+
+    assert s1(x=None) == NULL
+    assert s1(y=None) == NULL
+    assert s1(a=act()) == UNSUP                       # DYNAMIC ranges
+    assert s1(a=act(range_mode=1, act_bits=4)) == UNSUP
+    assert s1(a=act(range_mode=1, clip=None)) == NULL
+    assert s1(M=129) == UNSUP                         # more than 128 tokens
+    assert s1(M=0) == SHAPE
+    assert s1(w=wt(K=512, w_group=256)) == UNSUP      # neither 128 nor K
+    assert s1(out=3) == UNSUP
+    assert s1(x=A + 2) == ALIGN
+    assert s1(ws=A + 8, nbytes=1 << 20) == ALIGN
