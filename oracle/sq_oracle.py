@@ -47,6 +47,15 @@ Readings where the paper leaves a choice:
   family for D and no optimizer; the family here is d_k = amax|X_k|^alpha /
   amax|W_k|^(1-alpha) (clamped to [2^-6, 2^6]) over a list of exponents, with
   the per-token / per-group absmax activation quantizer and unit gains.
+* MLP chain (producer-side fusion of the up projection into the down
+  projection's quantizer): the up output is cast to bf16 as the layer's output
+  would be, GELU is evaluated on that bf16 value and rounded to bf16 (GELU
+  stays in BF16, App. D), and the result is the down projection's input,
+  quantized with its STATIC thresholds.  GELU(x) = x Phi(x) =
+  0.5 x (1 + erf(x / sqrt 2)); the paper does not say how erf is evaluated,
+  so erf here is the rational approximation 7.1.28 of Abramowitz & Stegun
+  (erf z ~ 1 - (1 + a1 z + ... + a6 z^6)^-16, |error| <= 3e-7), written as a
+  fixed sequence of fp32 operations.
 * int4 packing (both weights and A4 activations): for every 8 consecutive
   codes k = 8g..8g+7 the four bytes 4g..4g+3 hold code 8g+b in the low nibble
   and code 8g+b+4 in the high nibble of byte 4g+b.
@@ -317,6 +326,61 @@ def full_precision_linear(x_bits, w, bias_bits=None):
     if bias_bits is not None:
         y = y + bf16_bits_to_f32(bias_bits).astype(np.float64)[None, :]
     return y
+
+
+# --------------------------------------------------------------------------
+# GELU between the up and down projections of the MLP, in bf16 (App. D), and
+# the chain into the down projection's STATIC quantizer (Sec. 4.4, the
+# producer-side fusion of the intermediate activation)
+# --------------------------------------------------------------------------
+# Abramowitz & Stegun 7.1.28: erf z ~ 1 - (1 + a1 z + a2 z^2 + ... + a6 z^6)^-16
+AS_ERF_COEFFS = (0.0705230784, 0.0422820123, 0.0092705272, 0.0001520143, 0.0002765672, 0.0000430638)
+INV_SQRT2 = F32(0.70710677)  # fp32(1 / sqrt 2)
+
+
+def erf_as(z):
+    """erf of z >= 0 (fp32 array) by 7.1.28, one IEEE fp32 operation at a
+    time: the polynomial by Horner's rule from a6 down, the 16th power by four
+    squarings, then 1 - 1 / p^16 (0 where p^16 overflows to infinity)."""
+    z = np.asarray(z, dtype=F32)
+    a = [F32(c) for c in AS_ERF_COEFFS]
+    p = np.full(z.shape, a[5], dtype=F32)
+    with np.errstate(over="ignore", divide="ignore"):  # large z: p overflows to +inf and 1 / p to 0
+        for c in (a[4], a[3], a[2], a[1], a[0], F32(1.0)):
+            p = ((p * z).astype(F32) + c).astype(F32)
+        for _ in range(4):
+            p = (p * p).astype(F32)
+        inv = (F32(1.0) / p).astype(F32)
+    return (F32(1.0) - inv).astype(F32)
+
+
+def gelu_f32(x):
+    """GELU of fp32 x: 0.5 x (1 + erf(x / sqrt 2)) with the erf above, as
+    z = |x| * fp32(1/sqrt 2), e = erf(z), s = 1 + e (x >= 0) or 1 - e
+    (x < 0), then x * (s * 0.5) (the halving is exact, and taken first so
+    that x * s cannot overflow)."""
+    x = np.asarray(x, dtype=F32)
+    e = erf_as((np.abs(x) * INV_SQRT2).astype(F32))
+    s = np.where(x >= 0, (F32(1.0) + e).astype(F32), (F32(1.0) - e).astype(F32)).astype(F32)
+    return (x * (s * F32(0.5)).astype(F32)).astype(F32)
+
+
+def gelu_bf16(h_bits):
+    """GELU on bf16 values (bit patterns), rounded to bf16 (RNE)."""
+    return f32_to_bf16_bits(gelu_f32(bf16_bits_to_f32(h_bits)))
+
+
+def mlp_chain_codes(y_up, tok2stream, gamma_down, step, dinv_down, clip_down):
+    """The down projection's 8-bit codes and row scales from the up
+    projection's fp32 output y_up [M, N_up]: cast to bf16 (the layer's output
+    format), GELU in bf16, then the STATIC quantizer of the down layer (its
+    gains, thresholds and D^-1; Eq. 1, 6, 8).  Returns (h, g, qa): the up
+    output in bf16, the GELU output in bf16 and quantize_act's result."""
+    h = f32_to_bf16_bits(np.asarray(y_up, dtype=F32))
+    g = gelu_bf16(h)
+    qa = quantize_act(g, tok2stream, gamma_down, step, dinv=dinv_down, clip=clip_down,
+                      range_mode=RANGE_STATIC, act_bits=8)
+    return h, g, qa
 
 
 # --------------------------------------------------------------------------
