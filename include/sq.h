@@ -228,6 +228,36 @@ sq_status sq_linear_w4a8_noalloc(const uint16_t* x, int32_t M, const sq_act_para
 sq_status sq_linear_w4a8_static1(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                                  void* y, int32_t out_dtype, void* workspace, size_t ws_bytes, hipStream_t stream);
 
+/* Producer-side fusion of the MLP's one direct chain, up projection -> GELU
+ * -> down projection (the DiT block keeps GELU in bf16, App. D; Sec. 4.4 on
+ * intermediate traffic): the fused W4A8 linear of the up projection (x, act,
+ * w, workspace as for sq_linear_w4a8) whose GEMM epilogue does not store Y
+ * but, per output, rounds Y to bf16, evaluates GELU with the sequence of
+ * sq_gelu_bf16, rounds to bf16 and quantizes the result with the DOWN
+ * projection's STATIC 8-bit quantizer (act_next: its stream ids, gains,
+ * per-step thresholds, D^-1 and step; Eq. 1, 6 and 8).  Writes
+ *   qx_next  int8 [M][N] (N = w->N = the down projection's K), 4-byte aligned
+ *   r_next   fp32 [M], r_i = Delta / gamma_s(i) of the down layer,
+ * exactly what sq_quantize_act(act_next) writes for the bf16 output of
+ * sq_gelu_bf16 applied to sq_linear_w4a8's bf16 output; they feed
+ * sq_gemm_w4a8 with the down projection's weights.  The down layer's
+ * channel scaling act_next->dinv must be NULL or 16-byte aligned.
+ * Requires act->act_bits == 8, w->w_group == 128, M > 128 (the tiled GEMM;
+ * fewer tokens take the weight-streaming kernel, which has no such
+ * epilogue), act_next->act_bits == 8 and act_next->range_mode ==
+ * SQ_RANGE_STATIC (a dynamic range needs the whole row before any code):
+ * else SQ_ERR_UNSUPPORTED. */
+sq_status sq_linear_w4a8_gelu_quant(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                                    const sq_act_params* act_next, int8_t* qx_next, float* r_next, void* workspace,
+                                    size_t ws_bytes, hipStream_t stream);
+
+/* GELU of n bf16 values (x, y device buffers of n uint16 bit patterns,
+ * 16-byte aligned, y may equal x; n may be 0): y = bf16(0.5 x (1 + erf(x /
+ * sqrt 2))) with erf by Abramowitz and Stegun 7.1.28 as one fixed sequence of
+ * fp32 operations (Horner's rule from a6, four squarings, 1 - 1/p), rounded
+ * to nearest even; the op the quantized DiT keeps in bf16 (App. D). */
+sq_status sq_gelu_bf16(const uint16_t* x, size_t n, uint16_t* y, hipStream_t stream);
+
 /* The same layer without fusion, as the execution that Sec. 4.4 replaces:
  * channel scaling, gain, quantization, GEMM, dequantization, inverse-gain
  * compensation and bias each run as their own kernel, passing fp32 (or

@@ -360,9 +360,10 @@ def gelu_f32(x):
     (x < 0), then x * (s * 0.5) (the halving is exact, and taken first so
     that x * s cannot overflow)."""
     x = np.asarray(x, dtype=F32)
-    e = erf_as((np.abs(x) * INV_SQRT2).astype(F32))
-    s = np.where(x >= 0, (F32(1.0) + e).astype(F32), (F32(1.0) - e).astype(F32)).astype(F32)
-    return (x * (s * F32(0.5)).astype(F32)).astype(F32)
+    with np.errstate(invalid="ignore"):  # NaN inputs, and -inf * 0, give NaN
+        e = erf_as((np.abs(x) * INV_SQRT2).astype(F32))
+        s = np.where(x >= 0, (F32(1.0) + e).astype(F32), (F32(1.0) - e).astype(F32)).astype(F32)
+        return (x * (s * F32(0.5)).astype(F32)).astype(F32)
 
 
 def gelu_bf16(h_bits):

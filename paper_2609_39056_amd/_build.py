@@ -36,7 +36,7 @@ FLAGS = [
 ]
 
 SOURCES = ["sq_api.cpp", "quant_act.hip", "pack_weights.hip", "gemm_w4.hip", "gemm_skinny.hip", "unfused.hip",
-           "mfma_probe.hip", "calib.hip", "noalloc.hip"]
+           "mfma_probe.hip", "calib.hip", "noalloc.hip", "gelu.hip"]
 
 
 _REMARK = re.compile(r"remark: Function Name: (\S+)|remark:\s+(ScratchSize \[bytes/lane\]|VGPRs Spill): (\d+)")

@@ -91,6 +91,9 @@ _SIGS = {
     "sq_linear_w4a8_noalloc": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P]),
     "sq_linear_w4a8_static1": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P, _S,
                                     _P]),
+    "sq_linear_w4a8_gelu_quant": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight),
+                                       ctypes.POINTER(sq_act_params), _P, _P, _P, _S, _P]),
+    "sq_gelu_bf16": (_I, [_P, _S, _P, _P]),
     "sq_debug_block_acc_i32": (_I, [_P, _I, _I, ctypes.POINTER(sq_weight), _P, _P]),
     "sq_calib_reference": (_I, [_P, _I, _P, ctypes.POINTER(sq_weight), _P, _P]),
     "sq_calib_workspace_bytes": (_S, [_I, _I, _I, _I, _I]),
@@ -258,6 +261,26 @@ def sq_linear_w4a8_static1(x, act: ActParams, w: Weight, y, out_dtype: int, work
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(lib().sq_linear_w4a8_static1(_ptr(x), M, ctypes.byref(s), ctypes.byref(ws), _ptr(y), out_dtype,
                                         _ptr(workspace), nbytes, _stream(stream)), "sq_linear_w4a8_static1")
+
+
+def sq_linear_w4a8_gelu_quant(x, act: ActParams, w: Weight, act_next: ActParams, qx_next, r_next, workspace,
+                              stream=None) -> None:
+    """The up projection with the GELU epilogue that writes the down
+    projection's STATIC codes qx_next (int8 [M, N]) and row scales r_next
+    (fp32 [M]) (include/sq.h); workspace as for sq_linear_w4a8."""
+    M = x.shape[0]
+    s, ws, sn = act.struct(), w.struct(), act_next.struct()
+    _check(lib().sq_linear_w4a8_gelu_quant(_ptr(x), M, ctypes.byref(s), ctypes.byref(ws), ctypes.byref(sn),
+                                           _ptr(qx_next), _ptr(r_next), _ptr(workspace),
+                                           workspace.numel() * workspace.element_size(), _stream(stream)),
+           "sq_linear_w4a8_gelu_quant")
+
+
+def sq_gelu_bf16(x, y, stream=None) -> None:
+    """y = bf16 GELU of the bf16 tensor x (same number of elements; y may be x)."""
+    n = x.numel()
+    assert y.numel() == n
+    _check(lib().sq_gelu_bf16(_ptr(x), n, _ptr(y), _stream(stream)), "sq_gelu_bf16")
 
 
 def sq_linear_unfused(x, act: ActParams, w: Weight, y, out_dtype: int, workspace, stream=None) -> None:

@@ -37,6 +37,7 @@
 #include <type_traits>
 
 #include "gemm_frag.h"
+#include "gelu.h"
 #include "sq_internal.h"
 
 namespace sq {
@@ -739,25 +740,50 @@ __device__ __forceinline__ void read_wscale16(const uint8_t* st, int wave, int l
 }
 
 // Row factor of row m0 + wm * 64 + lane and the bias of the lane's column in
-// each 16-wide tile, loaded when a tile starts.
+// each 16-wide tile, loaded when a tile starts.  The GELU epilogue also loads
+// the next layer's gain of that row, its 1 / Delta and the D^-1 of the four
+// columns the lane holds after the quad transpose in each 16-wide tile.
 template <int EPI>
 struct EpiInputs16 {
+  static constexpr bool kOut = EPI == kEpiOut || EPI == kEpiGelu;
+  static constexpr bool kGelu = EPI == kEpiGelu;
   float rowf;
   float bias[TN16];
+  float gain;
+  float inv;
+  float dinv[kGelu ? TN16 : 1][4];
   __device__ __forceinline__ void load(const GemmArgs& a, int m0, int n0, int wm, int wn, int lane) {
     const int m = min(m0 + wm * 64 + lane, a.M - 1);
-    rowf = EPI == kEpiOut ? static_cast<const float*>(a.act_scale)[m] : 1.0f;
+    rowf = kOut ? static_cast<const float*>(a.act_scale)[m] : 1.0f;
 #pragma unroll
     for (int tn = 0; tn < TN16; ++tn) {
       const int n = min(n0 + wn * 64 + tn * 16 + (lane & 15), a.N - 1);
-      bias[tn] = (EPI == kEpiOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
+      bias[tn] = (kOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
+    }
+    if constexpr (kGelu) {
+      const NextQuant& q = a.nq;
+      gain = q.gamma[q.step * q.S + q.tok2stream[m]];
+      inv = 1.0f / (q.clip[q.step] / 127.0f);
+      if (__builtin_isinf(inv)) inv = 0.0f;
+#pragma unroll
+      for (int tn = 0; tn < TN16; ++tn) {
+        const int n = min(n0 + wn * 64 + tn * 16 + (lane & 12), a.N - 4);
+        const float4 d = q.dinv != nullptr ? *reinterpret_cast<const float4*>(q.dinv + n)
+                                           : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+        dinv[tn][0] = d.x;
+        dinv[tn][1] = d.y;
+        dinv[tn][2] = d.z;
+        dinv[tn][3] = d.w;
+      }
     }
   }
 };
 
 // Epilogue of one 128 x 128 tile from the 16 x 16 accumulator layout: row
 // factor and bias per lane (one column, four rows), a quad transpose to one
-// row and four consecutive columns, then 16-byte (fp32) or 8-byte stores.
+// row and four consecutive columns, then 16-byte (fp32) or 8-byte stores; or,
+// for the GELU epilogue, four code bytes of the next layer (4-byte stores)
+// and, from the waves of the first column tile, the next layer's row scales.
 template <int EPI>
 __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16][TN16][4], int m0, int n0, int wm,
                                              int wn, int lane_in, const EpiInputs16<EPI>& in) {
@@ -768,12 +794,19 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16]
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
   const int rf_bits = __float_as_int(in.rowf);
   const int q4 = (lane >> 4) * 4;
+  if constexpr (EPI == kEpiGelu) {
+    const int m = m0 + wm * 64 + lane;
+    if (n0 + wn * 64 == 0 && m < M) a.nq.r[m] = (a.nq.clip[a.nq.step] / 127.0f) / in.gain;
+  }
 #pragma unroll
   for (int tm = 0; tm < TM16; ++tm) {
     float rowf[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
       rowf[j] = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 16 + q4 + j) * 4, rf_bits));
+    float gain = 0.0f;
+    if constexpr (EPI == kEpiGelu)
+      gain = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 16 + q4 + (lane & 3)) * 4, __float_as_int(in.gain)));
 #pragma unroll
     for (int tn = 0; tn < TN16; ++tn) {
       float v[4];
@@ -784,7 +817,10 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16]
       const int m = m0 + wm * 64 + tm * 16 + q4 + (lane & 3);
       const int n = n0 + wn * 64 + tn * 16 + (lane & 12);
       if (m < M) {
-        if (f32out) {
+        if constexpr (EPI == kEpiGelu) {
+          *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(a.out) + static_cast<size_t>(m) * N + n) =
+              gelu_codes4(v, in.dinv[tn], gain, in.inv);
+        } else if (f32out) {
           *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * N + n) =
               make_float4(v[0], v[1], v[2], v[3]);
         } else {
@@ -826,7 +862,8 @@ template <int EPI>
 __global__ __launch_bounds__(256, 2) void gemm_pipe16_kernel(GemmArgs a) {
   using LY = Layout<8, false>;
   using CF = Cfg<8, false>;
-  static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
+  static_assert(EPI == kEpiOut || EPI == kEpiPartial || EPI == kEpiGelu,
+                "the pipelined path applies the weight steps");
   constexpr int BM = CF::BM, BN = CF::BN;
   constexpr int NDMA = LY::A_DMA + LY::B_DMA + 1;
   constexpr int AHEAD = (CF::DIST - 1) * NDMA;
@@ -1393,7 +1430,7 @@ __global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
     y[2] = acc.z;
     y[3] = acc.w;
   }
-  if constexpr (EPI == kEpiOut) {
+  if constexpr (EPI == kEpiOut || EPI == kEpiGelu) {
     const float rowf = ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
                                   : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
 #pragma unroll
@@ -1401,6 +1438,25 @@ __global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
       const float b = a.bias != nullptr ? bf16_to_f32(a.bias[n + j]) : 0.0f;
       y[j] = __builtin_fmaf(y[j], rowf, b);
     }
+  }
+  if constexpr (EPI == kEpiGelu) {
+    const NextQuant& q = a.nq;
+    const float gain = q.gamma[q.step * q.S + q.tok2stream[m]];
+    const float delta = q.clip[q.step] / 127.0f;
+    float inv = 1.0f / delta;
+    if (__builtin_isinf(inv)) inv = 0.0f;
+    float d[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+    if (q.dinv != nullptr) {
+      const float4 dv = *reinterpret_cast<const float4*>(q.dinv + n);
+      d[0] = dv.x;
+      d[1] = dv.y;
+      d[2] = dv.z;
+      d[3] = dv.w;
+    }
+    *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(a.out) + static_cast<size_t>(m) * a.N + n) =
+        gelu_codes4(y, d, gain, inv);
+    if (n == 0) q.r[m] = delta / gain;
+    return;
   }
   if (EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32) {
     *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * a.N + n) =
@@ -1470,7 +1526,7 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
     const int rest = p.ntiles - p.ndp;
     const int nitems = p.ndp + rest * p.split;
     const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
-    if constexpr (ABITS == 8 && !PC && EPI == kEpiOut && kPipe16)
+    if constexpr (ABITS == 8 && !PC && (EPI == kEpiOut || EPI == kEpiGelu) && kPipe16)
       hipLaunchKernelGGL((gemm_pipe16_kernel<EPI>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
     else
       hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI, PC>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
@@ -1548,6 +1604,11 @@ size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t
                                : pipe_plan<4>(M, N, K, ~static_cast<size_t>(0));
   const size_t unit = static_cast<size_t>(Cfg<8, kPipeWide>::BM) * Cfg<8, kPipeWide>::BN * sizeof(float);
   return static_cast<size_t>(p.ntiles - p.ndp) * (p.split > 1 ? p.split : 0) * unit;
+}
+
+hipError_t launch_gemm_gelu_quant(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
+  if (skinny_applies(8, a.M, a.K, a.w_group) || a.w_group != KT) return hipErrorInvalidValue;
+  return launch_t<8, kEpiGelu, true>(a, s, partial, partial_bytes);
 }
 
 hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,

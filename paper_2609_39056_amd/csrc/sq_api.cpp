@@ -425,6 +425,42 @@ sq_status sq_linear_w4a8_static1(const uint16_t* x, int32_t M, const sq_act_para
   return hip_status(launch_skinny_static1(g, stream, static_cast<float*>(workspace), workspace ? ws_bytes : 0));
 }
 
+sq_status sq_linear_w4a8_gelu_quant(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                                    const sq_act_params* act_next, int8_t* qx_next, float* r_next, void* workspace,
+                                    size_t ws_bytes, hipStream_t stream) {
+  if (x == nullptr || qx_next == nullptr || r_next == nullptr || workspace == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  st = check_act(act, w->K);
+  if (st != SQ_OK) return st;
+  st = check_act(act_next, w->N);  // the next layer's input channels are this layer's outputs
+  if (st != SQ_OK) return st;
+  if (act->act_bits != 8 || act_next->act_bits != 8 || act_next->range_mode != SQ_RANGE_STATIC)
+    return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (w->w_group != kKTile || skinny_applies(8, M, w->K, w->w_group)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(x, 16) || !aligned(workspace, 16) || !aligned(qx_next, 4) || !aligned(r_next, 4)) return SQ_ERR_ALIGN;
+  if (ws_bytes < fused_ws_bytes(M, w->K, w->N, 8)) return SQ_ERR_WORKSPACE;
+  FusedWs f = fused_ws(workspace, ws_bytes, M, w->K, 8, false);
+  st = quantize(x, M, w->K, act, f.qx, f.scale, stream);
+  if (st != SQ_OK) return st;
+  GemmArgs g = gemm_args(f.qx, f.scale, M, act, w, qx_next, SQ_OUT_BF16);
+  g.nq.tok2stream = act_next->tok2stream;
+  g.nq.gamma = act_next->gamma;
+  g.nq.dinv = act_next->dinv;
+  g.nq.clip = act_next->clip;
+  g.nq.S = act_next->num_streams;
+  g.nq.step = act_next->step;
+  g.nq.r = r_next;
+  return hip_status(launch_gemm_gelu_quant(g, stream, f.partial, f.partial_bytes));
+}
+
+sq_status sq_gelu_bf16(const uint16_t* x, size_t n, uint16_t* y, hipStream_t stream) {
+  if (n > 0 && (x == nullptr || y == nullptr)) return SQ_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(y, 16)) return SQ_ERR_ALIGN;
+  return hip_status(launch_gelu_bf16(x, n, y, stream));
+}
+
 sq_status sq_linear_unfused(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                             void* y, int32_t out_dtype, void* workspace, size_t ws_bytes,
                             hipStream_t stream) {

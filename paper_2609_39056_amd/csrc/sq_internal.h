@@ -79,6 +79,19 @@ enum EpiMode : int {
   kEpiPartial = 1,  // fp32 sum_b fp32(C^b) * s_b * Delta_W (no row factor / bias)
   kEpiInt32 = 2,    // int32 C (one block spanning K)
   kEpiDump = 3,     // int32 C^b of every block to acc_out[b][i][j]
+  kEpiGelu = 4,     // row factor, bias, bf16, GELU, bf16, the next layer's STATIC 8-bit codes to out
+};
+
+// The next linear's STATIC 8-bit quantizer, applied by the kEpiGelu epilogue
+// to GELU of this GEMM's bf16 output: codes int8 [M][N] go to GemmArgs::out,
+// the row scales r = Delta / gamma_s(i) to `r`.
+struct NextQuant {
+  const int32_t* tok2stream;
+  const float* gamma;  // [num_steps][S]
+  const float* dinv;   // D^-1 [N] or NULL
+  const float* clip;   // [num_steps]: Delta = clip[step] / 127
+  int32_t S, step;
+  float* r;            // [M]
 };
 
 struct GemmArgs {
@@ -104,6 +117,7 @@ struct GemmArgs {
   // and the kernel quantizes it with STATIC thresholds, D^-1 and the gains
   const float* dinv;
   const float* clip;
+  NextQuant nq;  // kEpiGelu only
 };
 
 // Bytes of the partial-sum buffer the split-K tail may use for a GEMM of this
@@ -154,6 +168,11 @@ hipError_t launch_pack_weights(const PackArgs& a, hipStream_t s);
 // every tile is then computed whole).
 hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial = nullptr,
                        size_t partial_bytes = 0);
+// The 8-bit GEMM with 128-wide weight groups on the pipelined kernel (more
+// than kSkinnyMaxM rows) and the kEpiGelu epilogue (a.nq set, a.out the codes).
+hipError_t launch_gemm_gelu_quant(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes);
+// GELU of n bf16 values to bf16 (the fp32 sequence of gelu.h).
+hipError_t launch_gelu_bf16(const uint16_t* x, size_t n, uint16_t* y, hipStream_t s);
 
 // unfused stages
 struct UnfusedArgs {

@@ -296,3 +296,45 @@ def test_static1_rejects(L):
     assert s1(out=3) == UNSUP
     assert s1(x=A + 2) == ALIGN
     assert s1(ws=A + 8, nbytes=1 << 20) == ALIGN
+
+
+def test_gelu_quant_rejects(L):
+    """The up projection with the GELU epilogue validates before launching:
+    8-bit activations, 128-wide weight groups, more than 128 tokens and a
+    STATIC 8-bit quantizer for the next layer, whose K is this layer's N."""
+    big = 1 << 30
+
+    def gq(x=A, M=300, a=None, w=None, an=None, qn=A, rn=A, ws=A, nbytes=big):
+        a = act() if a is None else a
+        w = wt() if w is None else w
+        an = act(range_mode=1) if an is None else an
+        return L.sq_linear_w4a8_gelu_quant(x, M, ctypes.byref(a), ctypes.byref(w), ctypes.byref(an), qn, rn, ws,
+                                           nbytes, None)
+
+    assert gq(x=None) == NULL
+    assert gq(qn=None) == NULL
+    assert gq(rn=None) == NULL
+    assert gq(ws=None) == NULL
+    assert gq(an=act()) == UNSUP                            # next layer DYNAMIC
+    assert gq(an=act(range_mode=1, act_bits=4)) == UNSUP
+    assert gq(an=act(range_mode=1, clip=None)) == NULL
+    assert gq(a=act(act_bits=4)) == UNSUP
+    assert gq(M=100) == UNSUP                               # few tokens: weight-streaming GEMM
+    assert gq(M=0) == SHAPE
+    assert gq(w=wt(K=512, w_group=256)) == UNSUP
+    assert gq(w=wt(K=512, w_group=512)) == UNSUP            # one step per channel
+    assert gq(w=wt(N=192)) == SHAPE                         # next layer's K must be a multiple of 128
+    assert gq(x=A + 2) == ALIGN
+    assert gq(qn=A + 2) == ALIGN
+    assert gq(rn=A + 2) == ALIGN
+    assert gq(ws=A + 8) == ALIGN
+    assert gq(an=act(range_mode=1, dinv=A + 4)) == ALIGN
+    assert gq(nbytes=1024) == WS
+
+
+def test_gelu_bf16_rejects(L):
+    assert L.sq_gelu_bf16(None, 8, A, None) == NULL
+    assert L.sq_gelu_bf16(A, 8, None, None) == NULL
+    assert L.sq_gelu_bf16(A + 2, 8, A, None) == ALIGN
+    assert L.sq_gelu_bf16(A, 8, A + 2, None) == ALIGN
+    assert L.sq_gelu_bf16(None, 0, None, None) == OK        # nothing to do: no launch

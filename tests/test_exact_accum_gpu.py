@@ -77,7 +77,7 @@ def tile_rows(M, seed):
 class ExactLayer:
     """Integer activations and power-of-two scales (see the module docstring)."""
 
-    def __init__(self, M, K, N, G, bits, seed, w_lo=-7):
+    def __init__(self, M, K, N, G, bits, seed, w_lo=-7, w_exp=(-2, 2)):
         rng = np.random.default_rng([21, M, K, N, G, bits] + list(np.atleast_1d(seed)))
         qa = 127 if bits == 8 else 7
         self.M, self.K, self.N, self.G, self.bits = M, K, N, G, bits
@@ -96,7 +96,7 @@ class ExactLayer:
         assert not np.any(u & 0xFFFF), "activation not exact in bf16"
         self.x_bits = (u >> 16).astype(np.uint16)
         self.cw = rng.integers(w_lo, 8, (N, K), dtype=np.int8)
-        self.ws_bits = pow2_f16_bits(rng.integers(-2, 2, (N, K // G)))  # [N][K/G]
+        self.ws_bits = pow2_f16_bits(rng.integers(w_exp[0], w_exp[1], (N, K // G)))  # [N][K/G]
 
     def device(self, range_mode=B.SQ_RANGE_STATIC):
         act = B.ActParams(tok2stream=i32_to_dev(self.t2s), gamma=f32_to_dev(self.gamma), step=self.step,
