@@ -23,7 +23,8 @@ the dominant kernel (the GEMM, against the int8 MFMA peak and the matrix-core
 rate measured with the same instruction and fold), the fused W4A4 linear, the
 unfused variant and the per-output-channel weight steps on the same block, the
 2B-class MLP pair (4192 tokens) and the 2B-class block at batch 4 (16768
-tokens) as extra records, the calibration path (Eq. (9) objective and search,
+tokens) as extra records, the MLP chain up -> GELU -> down with and without
+the producer-side fusion (14B- and 2B-class shapes), the calibration path (Eq. (9) objective and search,
 Eq. (7) scaling objective) on the 2B up projection, and the CPU oracle timed on
 a stratified row sample of the 14B block.
 
@@ -524,6 +525,54 @@ def static_single_kernel_figures(torch, B, synth, dev, reps=50):
     return out
 
 
+def mlp_chain_figures(torch, B, dev, up, down, reps=20):
+    """The MLP's direct chain, up projection -> GELU -> down projection, with
+    the down projection's STATIC quantizer (its per-step thresholds):
+    unfused as three calls (sq_linear_w4a8 to bf16, sq_gelu_bf16,
+    sq_linear_w4a8 of the down projection) against the producer-side fusion
+    (sq_linear_w4a8_gelu_quant writing the down projection's codes and row
+    scales, then sq_gemm_w4a8).  us per chain and per call, graph-replayed;
+    the same tokens feed both projections."""
+    M, N, K2 = up["M"], up["N"], down["N"]
+    ua, da = up["acts"][8], down["acts"][8]
+    ua.step = 1
+    clip = torch.full((T_STEPS,), 4.0, dtype=torch.float32, device=dev)
+    dact = B.ActParams(tok2stream=ua.tok2stream, gamma=da.gamma, step=1, act_bits=8, range_mode=B.SQ_RANGE_STATIC,
+                       clip=clip, dinv=da.dinv)
+    h = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    g = torch.empty_like(h)
+    yd = torch.empty((M, K2), dtype=torch.bfloat16, device=dev)
+    ws_up = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, up["K"], N, 8, dev)
+    ws_dn = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, N, K2, 8, dev)
+    ws_g = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, N, K2, 8, dev)
+    qn, rn = B.act_buffers(M, N, 8, dev)
+    BF = B.SQ_OUT_BF16
+    calls = {
+        "up_linear_bf16": lambda: B.sq_linear_w4a8(up["x"], ua, up["W"], h, BF, ws_up),
+        "gelu_bf16": lambda: B.sq_gelu_bf16(h, g),
+        "down_linear_static": lambda: B.sq_linear_w4a8(g, dact, down["W"], yd, BF, ws_dn),
+        "up_linear_gelu_quant": lambda: B.sq_linear_w4a8_gelu_quant(up["x"], ua, up["W"], dact, qn, rn, ws_up),
+        "down_gemm": lambda: B.sq_gemm_w4a8(qn, rn, down["W"], yd, BF, workspace=ws_g),
+    }
+    per = {k: round(graph_us(torch, f, reps), 2) for k, f in calls.items()}
+
+    def unfused():
+        for k in ("up_linear_bf16", "gelu_bf16", "down_linear_static"):
+            calls[k]()
+
+    def fused():
+        for k in ("up_linear_gelu_quant", "down_gemm"):
+            calls[k]()
+
+    us_u = graph_us(torch, unfused, reps)
+    us_f = graph_us(torch, fused, reps)
+    ops = 2.0 * M * up["K"] * N + 2.0 * M * N * K2
+    del h, g, yd, ws_up, ws_dn, ws_g, qn, rn
+    return {"M": M, "up": [up["K"], N], "down": [N, K2], "per_call_us": per,
+            "unfused_us": round(us_u, 2), "fused_us": round(us_f, 2), "fused_speedup": round(us_u / us_f, 3),
+            "fused_tops": round(ops / (us_f * 1e-6) / 1e12, 1), "unfused_tops": round(ops / (us_u * 1e-6) / 1e12, 1)}
+
+
 def run_action_only(args):
     """The few-token regime: every call streams a distinct weight (28 layers x
     4 linears, 0.7 GB packed: more than the 256 MB last-level cache), one pass
@@ -752,7 +801,11 @@ def main():
     ms_unfused = timed_steps(lambda t: unfused_step(blk, t), max(5, args.steps // 4), 2)
     ms_pc = timed_steps(lambda t: fused_step(blk, t, wkey="W_pc"), args.steps, 2)
     for ly in blk:
-        del ly["ws_unf"], ly["W_pc"], ly["ws_gemm"], ly["qx8"], ly["r8"]
+        del ly["ws_unf"]
+    torch.cuda.empty_cache()
+    chain14 = mlp_chain_figures(torch, B, dev, blk[2], blk[3])
+    for ly in blk:
+        del ly["W_pc"], ly["ws_gemm"], ly["qx8"], ly["r8"]
     torch.cuda.empty_cache()
 
     # ---- the 2B-class MLP pair (configuration 2) and the 2B-class block at
@@ -761,6 +814,7 @@ def main():
     buffers(mlp)
     ms_mlp8 = timed_steps(lambda t: fused_step(mlp, t), args.steps, args.warmup)
     ms_mlp4 = timed_steps(lambda t: fused_step(mlp, t, bits=4), args.steps, 2)
+    chain2 = mlp_chain_figures(torch, B, dev, mlp[0], mlp[1])
     b4 = device_block(torch, B, synth, dev, synth.LINEARS_2B, synth.TOKENS_2B, seed=6000, batch=4)
     buffers(b4)
     ms_b4 = {bits: timed_steps(lambda t, b=bits: fused_step(b4, t, bits=b), max(10, args.steps // 2), 3)
@@ -862,6 +916,7 @@ def main():
                                   "tops": round(mlp_ops / (ms_mlp8 * 1e-3) / 1e12, 2)},
                          "w4a4": {"ms_per_step": round(ms_mlp4, 5),
                                   "tops": round(mlp_ops / (ms_mlp4 * 1e-3) / 1e12, 2)}},
+        "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "2B_M4192": chain2},
         "block_2B_batch4_M16768": {"workload": "2B-class block qkv/out/up/down, batch 4: M=16768",
                                    **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
                                                   "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}
