@@ -708,16 +708,72 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
 // (s = 1) half of chunk g of the column, so one 16-byte read serves both
 // k-steps.  Both operands use the same assignment.  An accumulator lane holds
 // column lane & 15 and rows 4 (lane >> 4) + j, j < 4.
-constexpr int TM16 = 4, TN16 = 4;  // 16 x 16 tiles per wave
+//
+// Waves: two across a tile's 128 rows and P16_NWN across its 128 columns, each
+// computing 64 rows x P16_WCOLS columns as TM16 x TN16 tiles of 16 x 16.
+// P16_NWN = 4 (eight waves of 64 x 32, 121 VGPRs, four waves per SIMD)
+// measured the same speed as two waves per SIMD at 64 x 64.
+constexpr int P16_NWN = 2;
+constexpr int TM16 = 4, TN16 = 8 / P16_NWN;
+constexpr int P16_WCOLS = 16 * TN16;
+struct P16 {
+  static constexpr int NWM = 2, NWN = P16_NWN, NWAVE = NWM * NWN, NTHREADS = NWAVE * 64;
+  static constexpr int BM = 128, BN = 128;
+  static constexpr int DIST = 2, STAGES = 3, WGS_PER_CU = 2;
+  // one stage in LDS: A codes, packed weights, then each wave's 256-byte
+  // area of weight-step pairs (the Layout<8, false> arrangement)
+  static constexpr int A_BYTES = BM * KT, B_BYTES = BN * KT / 2, W_BYTES = NWAVE * 256;
+  static constexpr int STAGE = A_BYTES + B_BYTES + W_BYTES;
+  static constexpr int A_DMA = A_BYTES / 1024 / NWAVE, B_DMA = B_BYTES / 1024 / NWAVE;
+};
+static_assert(P16::BM == Cfg<8, kPipeWide>::BM && P16::BN == Cfg<8, kPipeWide>::BN,
+              "the split tail and the plan use the pipelined kernels' tile");
+
+// This wave's direct loads of one stage (StageLoads' arrangement for P16's
+// wave count; weight steps of 128-wide groups: stage kt is group kt).
+struct StageLoads16 {
+  uint32_t voffA[P16::A_DMA];
+  uint32_t voffB[P16::B_DMA];
+  uint32_t wcol2;  // first of the two output channels whose fp16 steps this lane's dword holds
+
+  __device__ __forceinline__ void set(int m0, int n0, int M, int N, int K, int wave, int wn, int lane) {
+#pragma unroll
+    for (int i = 0; i < P16::A_DMA; ++i) {
+      const int row = 8 * (P16::A_DMA * wave + i) + (lane >> 3);
+      const int c = (lane & 7) ^ ((row >> 1) & 7);
+      voffA[i] = static_cast<uint32_t>(min(m0 + row, M - 1) - m0) * static_cast<uint32_t>(K) + c * 16;
+    }
+#pragma unroll
+    for (int i = 0; i < P16::B_DMA; ++i) {
+      const int col = 16 * (P16::B_DMA * wave + i) + (lane >> 2);
+      const int c = (lane & 3) ^ ((col >> 2) & 3);
+      voffB[i] = static_cast<uint32_t>(min(n0 + col, N - 1) - n0) * static_cast<uint32_t>(K / 2) + c * 16;
+    }
+    // N is even, so the pair is clamped inside the row
+    wcol2 = static_cast<uint32_t>(min(n0 + wn * P16_WCOLS + 2 * (lane & (P16_WCOLS / 2 - 1)), N - 2));
+  }
+
+  __device__ __forceinline__ void issue(const GemmArgs& a, int m0, int n0, int kt, uint32_t st, int wave) const {
+    const int K = a.K;
+    const uint8_t* bA = static_cast<const uint8_t*>(a.qx) + static_cast<size_t>(m0) * K + kt * KT;
+    const uint8_t* bB = a.qw + static_cast<size_t>(n0) * (K / 2) + kt * (KT / 2);
+#pragma unroll
+    for (int i = 0; i < P16::A_DMA; ++i) dma<16>(bA, voffA[i], st + (P16::A_DMA * wave + i) * 1024);
+#pragma unroll
+    for (int i = 0; i < P16::B_DMA; ++i) dma<16>(bB, voffB[i], st + P16::A_BYTES + (P16::B_DMA * wave + i) * 1024);
+    const uint32_t e = static_cast<uint32_t>(kt) * static_cast<uint32_t>(a.N) + wcol2;
+    dma<4>(a.w_scale, e * 2, st + P16::A_BYTES + P16::B_BYTES + wave * 256);
+  }
+};
 
 struct FragOffsets16 {
   int a0[2];
   int b0;
   __device__ __forceinline__ FragOffsets16(int wm, int wn, int lane) {
-    using LY = Layout<8, false>;
+    using LY = P16;
     const int g = lane >> 4;
     const int arow0 = wm * 64 + (lane & 15);
-    const int bcol0 = wn * 64 + (lane & 15);
+    const int bcol0 = wn * P16_WCOLS + (lane & 15);
 #pragma unroll
     for (int s = 0; s < 2; ++s) a0[s] = arow0 * KT + 16 * ((2 * g + s) ^ ((arow0 >> 1) & 7));
     b0 = LY::A_BYTES + bcol0 * (KT / 2) + 16 * (g ^ ((bcol0 >> 2) & 3));
@@ -729,11 +785,10 @@ struct FragOffsets16 {
 
 // the weight steps of a stage for the lane's column of each 16-wide tile
 __device__ __forceinline__ void read_wscale16(const uint8_t* st, int wave, int lane, float (&w)[TN16]) {
-  using LY = Layout<8, false>;
-  const uint32_t* Wst = reinterpret_cast<const uint32_t*>(st + LY::A_BYTES + LY::B_BYTES + wave * 256);
+  const uint32_t* Wst = reinterpret_cast<const uint32_t*>(st + P16::A_BYTES + P16::B_BYTES + wave * 256);
 #pragma unroll
   for (int tn = 0; tn < TN16; ++tn) {
-    const int c = tn * 16 + (lane & 15);  // column within the wave's 64
+    const int c = tn * 16 + (lane & 15);  // column within the wave's P16_WCOLS
     const uint32_t pair = Wst[c >> 1];
     w[tn] = f16_to_f32((c & 1) ? (pair >> 16) : (pair & 0xFFFFu)) * 0.0625f;  // widened codes: factor 16
   }
@@ -757,7 +812,7 @@ struct EpiInputs16 {
     rowf = kOut ? static_cast<const float*>(a.act_scale)[m] : 1.0f;
 #pragma unroll
     for (int tn = 0; tn < TN16; ++tn) {
-      const int n = min(n0 + wn * 64 + tn * 16 + (lane & 15), a.N - 1);
+      const int n = min(n0 + wn * P16_WCOLS + tn * 16 + (lane & 15), a.N - 1);
       bias[tn] = (kOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
     }
     if constexpr (kGelu) {
@@ -767,7 +822,7 @@ struct EpiInputs16 {
       if (__builtin_isinf(inv)) inv = 0.0f;
 #pragma unroll
       for (int tn = 0; tn < TN16; ++tn) {
-        const int n = min(n0 + wn * 64 + tn * 16 + (lane & 12), a.N - 4);
+        const int n = min(n0 + wn * P16_WCOLS + tn * 16 + (lane & 12), a.N - 4);
         const float4 d = q.dinv != nullptr ? *reinterpret_cast<const float4*>(q.dinv + n)
                                            : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
         dinv[tn][0] = d.x;
@@ -790,13 +845,15 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16]
   int lane = lane_in;
   asm volatile("" : "+v"(lane));
   const int M = a.M, N = a.N;
-  if (n0 + wn * 64 >= N) return;  // N % 64 == 0: a wave's 64 columns are all in or all out
+  // N % 64 == 0 and the waves' column ranges are 64-aligned or nest in 64:
+  // a wave's columns are all in or all out
+  if (n0 + wn * P16_WCOLS >= N) return;
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
   const int rf_bits = __float_as_int(in.rowf);
   const int q4 = (lane >> 4) * 4;
   if constexpr (EPI == kEpiGelu) {
     const int m = m0 + wm * 64 + lane;
-    if (n0 + wn * 64 == 0 && m < M) a.nq.r[m] = (a.nq.clip[a.nq.step] / 127.0f) / in.gain;
+    if (n0 + wn * P16_WCOLS == 0 && m < M) a.nq.r[m] = (a.nq.clip[a.nq.step] / 127.0f) / in.gain;
   }
 #pragma unroll
   for (int tm = 0; tm < TM16; ++tm) {
@@ -815,7 +872,7 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16]
         v[j] = EPI == kEpiPartial ? y[tm][tn][j] : __builtin_fmaf(y[tm][tn][j], rowf[j], in.bias[tn]);
       quad_transpose(v, lane);
       const int m = m0 + wm * 64 + tm * 16 + q4 + (lane & 3);
-      const int n = n0 + wn * 64 + tn * 16 + (lane & 12);
+      const int n = n0 + wn * P16_WCOLS + tn * 16 + (lane & 12);
       if (m < M) {
         if constexpr (EPI == kEpiGelu) {
           *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(a.out) + static_cast<size_t>(m) * N + n) =
@@ -843,7 +900,7 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16]
 // gemm_tail_kernel's partial buffer (row-major tile, rows past M not written).
 __device__ __forceinline__ void write_partial16(const GemmArgs& a, const float (&y)[TM16][TN16][4], int unit, int m0,
                                                 int wm, int wn, int lane_in) {
-  constexpr int BM = Cfg<8, false>::BM, BN = Cfg<8, false>::BN;
+  constexpr int BM = P16::BM, BN = P16::BN;
   int ln = lane_in;
   asm volatile("" : "+v"(ln));
   float* P = a.partial + static_cast<size_t>(unit) * BM * BN;
@@ -854,14 +911,14 @@ __device__ __forceinline__ void write_partial16(const GemmArgs& a, const float (
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         const int row = wm * 64 + tm * 16 + (ln >> 4) * 4 + j;
-        if (m0 + row < a.M) P[row * BN + wn * 64 + tn * 16 + (ln & 15)] = y[tm][tn][j];
+        if (m0 + row < a.M) P[row * BN + wn * P16_WCOLS + tn * 16 + (ln & 15)] = y[tm][tn][j];
       }
 }
 
 template <int EPI>
-__global__ __launch_bounds__(256, 2) void gemm_pipe16_kernel(GemmArgs a) {
-  using LY = Layout<8, false>;
-  using CF = Cfg<8, false>;
+__global__ __launch_bounds__(P16::NTHREADS, P16::WGS_PER_CU) void gemm_pipe16_kernel(GemmArgs a) {
+  using LY = P16;
+  using CF = P16;
   static_assert(EPI == kEpiOut || EPI == kEpiPartial || EPI == kEpiGelu,
                 "the pipelined path applies the weight steps");
   constexpr int BM = CF::BM, BN = CF::BN;
@@ -888,10 +945,10 @@ __global__ __launch_bounds__(256, 2) void gemm_pipe16_kernel(GemmArgs a) {
   PipeItem d = item_of(d_it);
   int d_kt = d.kt0;
   uint32_t d_slot = 0;
-  StageLoads<8, false> ld;
+  StageLoads16 ld;
   ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
   auto issue = [&]() {
-    ld.template issue<false, true>(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
+    ld.issue(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
     d_slot = d_slot + LY::STAGE == RING ? 0 : d_slot + LY::STAGE;
   };
   // past the last stage of the last item the same stage is loaded again (in
@@ -1526,9 +1583,9 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
     const int rest = p.ntiles - p.ndp;
     const int nitems = p.ndp + rest * p.split;
     const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
-    if constexpr (ABITS == 8 && !PC && (EPI == kEpiOut || EPI == kEpiGelu) && kPipe16)
-      hipLaunchKernelGGL((gemm_pipe16_kernel<EPI>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
-    else
+    if constexpr (ABITS == 8 && !PC && (EPI == kEpiOut || EPI == kEpiGelu) && kPipe16) {
+      hipLaunchKernelGGL((gemm_pipe16_kernel<EPI>), dim3(grid), dim3(P16::NTHREADS), 0, s, a);
+    } else
       hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI, PC>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || rest == 0 || p.split == 1) return e;
