@@ -709,15 +709,17 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
 // k-steps.  Both operands use the same assignment.  An accumulator lane holds
 // column lane & 15 and rows 4 (lane >> 4) + j, j < 4.
 //
-// Waves: two across a tile's 128 rows and P16_NWN across its 128 columns, each
-// computing 64 rows x P16_WCOLS columns as TM16 x TN16 tiles of 16 x 16.
-// P16_NWN = 4 (eight waves of 64 x 32, 121 VGPRs, four waves per SIMD)
-// measured the same speed as two waves per SIMD at 64 x 64.
-constexpr int P16_NWN = 2;
-constexpr int TM16 = 4, TN16 = 8 / P16_NWN;
-constexpr int P16_WCOLS = 16 * TN16;
+// Waves: P16_NWM across a tile's 128 rows and P16_NWN across its 128
+// columns, each computing P16_WROWS x P16_WCOLS outputs as TM16 x TN16 tiles
+// of 16 x 16.  Measured alternatives to 2 x 2 waves of 64 x 64: 2 x 4 waves of
+// 64 x 32 (121 VGPRs, four waves per SIMD) the same speed, 1 x 4 waves of
+// 128 x 32 (each weight fragment widened once per workgroup) 1-2 % slower.
+constexpr int P16_NWM = 2, P16_NWN = 2;
+constexpr int TM16 = 8 / P16_NWM, TN16 = 8 / P16_NWN;
+constexpr int P16_WROWS = 16 * TM16, P16_WCOLS = 16 * TN16;
+constexpr int P16_RH = P16_WROWS / 64;  // 64-row halves of a wave's rows (one row per lane each)
 struct P16 {
-  static constexpr int NWM = 2, NWN = P16_NWN, NWAVE = NWM * NWN, NTHREADS = NWAVE * 64;
+  static constexpr int NWM = P16_NWM, NWN = P16_NWN, NWAVE = NWM * NWN, NTHREADS = NWAVE * 64;
   static constexpr int BM = 128, BN = 128;
   static constexpr int DIST = 2, STAGES = 3, WGS_PER_CU = 2;
   // one stage in LDS: A codes, packed weights, then each wave's 256-byte
@@ -772,7 +774,7 @@ struct FragOffsets16 {
   __device__ __forceinline__ FragOffsets16(int wm, int wn, int lane) {
     using LY = P16;
     const int g = lane >> 4;
-    const int arow0 = wm * 64 + (lane & 15);
+    const int arow0 = wm * P16_WROWS + (lane & 15);
     const int bcol0 = wn * P16_WCOLS + (lane & 15);
 #pragma unroll
     for (int s = 0; s < 2; ++s) a0[s] = arow0 * KT + 16 * ((2 * g + s) ^ ((arow0 >> 1) & 7));
@@ -794,22 +796,26 @@ __device__ __forceinline__ void read_wscale16(const uint8_t* st, int wave, int l
   }
 }
 
-// Row factor of row m0 + wm * 64 + lane and the bias of the lane's column in
-// each 16-wide tile, loaded when a tile starts.  The GELU epilogue also loads
+// Row factors of rows m0 + wm * P16_WROWS + 64 h + lane and the bias of the
+// lane's column in each 16-wide tile, loaded when a tile starts.  The GELU epilogue also loads
 // the next layer's gain of that row, its 1 / Delta and the D^-1 of the four
 // columns the lane holds after the quad transpose in each 16-wide tile.
 template <int EPI>
 struct EpiInputs16 {
   static constexpr bool kOut = EPI == kEpiOut || EPI == kEpiGelu;
   static constexpr bool kGelu = EPI == kEpiGelu;
-  float rowf;
+  float rowf[P16_RH];
   float bias[TN16];
-  float gain;
+  float gain[P16_RH];
   float inv;
   float dinv[kGelu ? TN16 : 1][4];
   __device__ __forceinline__ void load(const GemmArgs& a, int m0, int n0, int wm, int wn, int lane) {
-    const int m = min(m0 + wm * 64 + lane, a.M - 1);
-    rowf = kOut ? static_cast<const float*>(a.act_scale)[m] : 1.0f;
+#pragma unroll
+    for (int h = 0; h < P16_RH; ++h) {
+      const int m = min(m0 + wm * P16_WROWS + h * 64 + lane, a.M - 1);
+      rowf[h] = kOut ? static_cast<const float*>(a.act_scale)[m] : 1.0f;
+      if constexpr (kGelu) gain[h] = a.nq.gamma[a.nq.step * a.nq.S + a.nq.tok2stream[m]];
+    }
 #pragma unroll
     for (int tn = 0; tn < TN16; ++tn) {
       const int n = min(n0 + wn * P16_WCOLS + tn * 16 + (lane & 15), a.N - 1);
@@ -817,7 +823,6 @@ struct EpiInputs16 {
     }
     if constexpr (kGelu) {
       const NextQuant& q = a.nq;
-      gain = q.gamma[q.step * q.S + q.tok2stream[m]];
       inv = 1.0f / (q.clip[q.step] / 127.0f);
       if (__builtin_isinf(inv)) inv = 0.0f;
 #pragma unroll
@@ -849,21 +854,25 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16]
   // a wave's columns are all in or all out
   if (n0 + wn * P16_WCOLS >= N) return;
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
-  const int rf_bits = __float_as_int(in.rowf);
   const int q4 = (lane >> 4) * 4;
   if constexpr (EPI == kEpiGelu) {
-    const int m = m0 + wm * 64 + lane;
-    if (n0 + wn * P16_WCOLS == 0 && m < M) a.nq.r[m] = (a.nq.clip[a.nq.step] / 127.0f) / in.gain;
+#pragma unroll
+    for (int h = 0; h < P16_RH; ++h) {
+      const int m = m0 + wm * P16_WROWS + h * 64 + lane;
+      if (n0 + wn * P16_WCOLS == 0 && m < M) a.nq.r[m] = (a.nq.clip[a.nq.step] / 127.0f) / in.gain[h];
+    }
   }
 #pragma unroll
   for (int tm = 0; tm < TM16; ++tm) {
+    const int h = tm / 4, t4 = tm % 4;  // the 64-row half and the 16-row tile within it
+    const int rf_bits = __float_as_int(in.rowf[h]);
     float rowf[4];
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      rowf[j] = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 16 + q4 + j) * 4, rf_bits));
+      rowf[j] = __int_as_float(__builtin_amdgcn_ds_bpermute((t4 * 16 + q4 + j) * 4, rf_bits));
     float gain = 0.0f;
     if constexpr (EPI == kEpiGelu)
-      gain = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 16 + q4 + (lane & 3)) * 4, __float_as_int(in.gain)));
+      gain = __int_as_float(__builtin_amdgcn_ds_bpermute((t4 * 16 + q4 + (lane & 3)) * 4, __float_as_int(in.gain[h])));
 #pragma unroll
     for (int tn = 0; tn < TN16; ++tn) {
       float v[4];
@@ -871,7 +880,7 @@ __device__ __forceinline__ void store_tile16(const GemmArgs& a, float (&y)[TM16]
       for (int j = 0; j < 4; ++j)
         v[j] = EPI == kEpiPartial ? y[tm][tn][j] : __builtin_fmaf(y[tm][tn][j], rowf[j], in.bias[tn]);
       quad_transpose(v, lane);
-      const int m = m0 + wm * 64 + tm * 16 + q4 + (lane & 3);
+      const int m = m0 + wm * P16_WROWS + tm * 16 + q4 + (lane & 3);
       const int n = n0 + wn * P16_WCOLS + tn * 16 + (lane & 12);
       if (m < M) {
         if constexpr (EPI == kEpiGelu) {
@@ -910,7 +919,7 @@ __device__ __forceinline__ void write_partial16(const GemmArgs& a, const float (
     for (int tn = 0; tn < TN16; ++tn)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int row = wm * 64 + tm * 16 + (ln >> 4) * 4 + j;
+        const int row = wm * P16_WROWS + tm * 16 + (ln >> 4) * 4 + j;
         if (m0 + row < a.M) P[row * BN + wn * P16_WCOLS + tn * 16 + (ln & 15)] = y[tm][tn][j];
       }
 }
