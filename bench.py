@@ -73,6 +73,9 @@ def parse():
                    help="time the 2B-class linears on TOKENS action tokens only (the weight-streaming regime): "
                         "28 layers x {qkv, out, up, down} with distinct weights, W4A8 and W4A4, eager calls; "
                         "one JSON line per width (for HBM-traffic counters)")
+    p.add_argument("--headline-only", action="store_true",
+                   help="only the headline line's own measurements (the 14B block's timed steps, the per-kernel "
+                        "pass and the copy that calibrates the byte counters): for kernel traces and counters")
     p.add_argument("--cpu-video-rows", type=int, default=256,
                    help="video rows per layer in the oracle's stratified sample (all proprio / action rows too)")
     return p.parse_args()
@@ -525,6 +528,22 @@ def static_single_kernel_figures(torch, B, synth, dev, reps=50):
     return out
 
 
+def hbm_copy_figure(torch, dev, stream):
+    """A plain device copy of COPY_MIB MiB (a torch copy kernel): the reference
+    for the HBM byte counters (FETCH_SIZE / WRITE_SIZE) of profiled launches."""
+    src = torch.empty(COPY_MIB << 20, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(stream)
+    dst.copy_(src)
+    c1.record(stream)
+    torch.cuda.synchronize()
+    us = c0.elapsed_time(c1) * 1e3
+    del src, dst
+    return {"bytes": 2 * (COPY_MIB << 20), "us": round(us, 1), "gbs": round(2 * (COPY_MIB << 20) / (us * 1e-6) / 1e9, 1)}
+
+
 def mlp_chain_figures(torch, B, dev, up, down, reps=20):
     """The MLP's direct chain, up projection -> GELU -> down projection, with
     the down projection's STATIC quantizer (its per-step thresholds):
@@ -793,40 +812,41 @@ def main():
             frac_quant_hbm=round(k1_bytes[i] / (k1[i] * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             frac_serial_roofline=round(serial[i] / t, 4), alg_mb=round(alg_bytes[i] / 1e6, 2))
 
-    # ---- fused W4A4 on the same block, with per-linear call times
-    ms_w4a4 = timed_steps(lambda t: fused_step(blk, t, bits=4), args.steps, max(2, args.warmup // 2))
-    per4, _ = event_pass(blk, fused_calls(4), max(5, args.steps // 4))
-    per8, _ = event_pass(blk, fused_calls(8), max(5, args.steps // 4))
-    # ---- unfused W4A8 and per-output-channel weight steps on the same block
-    ms_unfused = timed_steps(lambda t: unfused_step(blk, t), max(5, args.steps // 4), 2)
-    ms_pc = timed_steps(lambda t: fused_step(blk, t, wkey="W_pc"), args.steps, 2)
-    for ly in blk:
-        del ly["ws_unf"]
-    torch.cuda.empty_cache()
-    chain14 = mlp_chain_figures(torch, B, dev, blk[2], blk[3])
-    for ly in blk:
-        del ly["W_pc"], ly["ws_gemm"], ly["qx8"], ly["r8"]
-    torch.cuda.empty_cache()
+    if not args.headline_only:
+        # ---- fused W4A4 on the same block, with per-linear call times
+        ms_w4a4 = timed_steps(lambda t: fused_step(blk, t, bits=4), args.steps, max(2, args.warmup // 2))
+        per4, _ = event_pass(blk, fused_calls(4), max(5, args.steps // 4))
+        per8, _ = event_pass(blk, fused_calls(8), max(5, args.steps // 4))
+        # ---- unfused W4A8 and per-output-channel weight steps on the same block
+        ms_unfused = timed_steps(lambda t: unfused_step(blk, t), max(5, args.steps // 4), 2)
+        ms_pc = timed_steps(lambda t: fused_step(blk, t, wkey="W_pc"), args.steps, 2)
+        for ly in blk:
+            del ly["ws_unf"]
+        torch.cuda.empty_cache()
+        chain14 = mlp_chain_figures(torch, B, dev, blk[2], blk[3])
+        for ly in blk:
+            del ly["W_pc"], ly["ws_gemm"], ly["qx8"], ly["r8"]
+        torch.cuda.empty_cache()
 
-    # ---- the 2B-class MLP pair (configuration 2) and the 2B-class block at
-    # batch 4 (configuration 5's batch-4 row count)
-    mlp = host_layers(torch, B, synth, dev)
-    buffers(mlp)
-    ms_mlp8 = timed_steps(lambda t: fused_step(mlp, t), args.steps, args.warmup)
-    ms_mlp4 = timed_steps(lambda t: fused_step(mlp, t, bits=4), args.steps, 2)
-    chain2 = mlp_chain_figures(torch, B, dev, mlp[0], mlp[1])
-    b4 = device_block(torch, B, synth, dev, synth.LINEARS_2B, synth.TOKENS_2B, seed=6000, batch=4)
-    buffers(b4)
-    ms_b4 = {bits: timed_steps(lambda t, b=bits: fused_step(b4, t, bits=b), max(10, args.steps // 2), 3)
-             for bits in (8, 4)}
-    del b4
-    torch.cuda.empty_cache()
+        # ---- the 2B-class MLP pair (configuration 2) and the 2B-class block at
+        # batch 4 (configuration 5's batch-4 row count)
+        mlp = host_layers(torch, B, synth, dev)
+        buffers(mlp)
+        ms_mlp8 = timed_steps(lambda t: fused_step(mlp, t), args.steps, args.warmup)
+        ms_mlp4 = timed_steps(lambda t: fused_step(mlp, t, bits=4), args.steps, 2)
+        chain2 = mlp_chain_figures(torch, B, dev, mlp[0], mlp[1])
+        b4 = device_block(torch, B, synth, dev, synth.LINEARS_2B, synth.TOKENS_2B, seed=6000, batch=4)
+        buffers(b4)
+        ms_b4 = {bits: timed_steps(lambda t, b=bits: fused_step(b4, t, bits=b), max(10, args.steps // 2), 3)
+                 for bits in (8, 4)}
+        del b4
+        torch.cuda.empty_cache()
 
-    # ---- the STATIC single-kernel linear at few tokens, against the two kernels
-    single = static_single_kernel_figures(torch, B, synth, dev)
+        # ---- the STATIC single-kernel linear at few tokens, against the two kernels
+        single = static_single_kernel_figures(torch, B, synth, dev)
 
-    # ---- the calibration path of Eq. (9) on the 2B up projection
-    calib = calibration_figures(torch, B, mlp[0], stream, dev, None if args.no_cpu else 256)
+        # ---- the calibration path of Eq. (9) on the 2B up projection
+        calib = calibration_figures(torch, B, mlp[0], stream, dev, None if args.no_cpu else 256)
 
     # ---- the int8 matrix-core rate this GPU sustains (sq_probe_mfma_i8: back
     # to back MFMAs on register operands at the GEMM's occupancy) in both MFMA
@@ -852,19 +872,8 @@ def main():
 
     # ---- a plain device copy of known size: the reference for the HBM byte
     # counters (FETCH_SIZE / WRITE_SIZE) of the profiled GEMM launches
-    src = torch.empty(COPY_MIB << 20, dtype=torch.uint8, device=dev).fill_(1)
-    dst = torch.empty_like(src)
-    dst.copy_(src)
-    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    c0.record(stream)
-    dst.copy_(src)
-    c1.record(stream)
-    torch.cuda.synchronize()
-    copy_us = c0.elapsed_time(c1) * 1e3
-    del src, dst
+    copy = hbm_copy_figure(torch, dev, stream)
 
-    mlp_ops = ops_of(mlp)
-    b4_ops = sum(2.0 * 4 * sum(synth.TOKENS_2B) * K * N for K, N in synth.LINEARS_2B.values())
     out = {
         "metric": "fused W4A8/W4A4 linear TOPS + % int8-MFMA (or HBM) roofline per layer",
         "value": round(value, 2),
@@ -902,30 +911,34 @@ def main():
         "quant_kernel_gbs": round(sum(k1_bytes) / (k1.sum() * 1e-3) / 1e9, 1),
         "w4a8_as_k1_k2_calls": {"ms_per_step": round(ms_split, 5),
                                 "gemm_tops": round(gemm_tops, 1)},
-        "fused_w4a8_per_call_us": {ly["name"]: round(per8[i, 0] * 1e3, 2) for i, ly in enumerate(blk)},
-        "fused_w4a4": {"ms_per_step": round(ms_w4a4, 5), "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2),
-                       "per_call_us": {ly["name"]: round(per4[i, 0] * 1e3, 2) for i, ly in enumerate(blk)},
-                       "frac_int8": round(ops_step / (ms_w4a4 * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)},
-        "unfused_w4a8": {"ms_per_step": round(ms_unfused, 5),
-                         "tops": round(ops_step / (ms_unfused * 1e-3) / 1e12, 2),
-                         "fused_speedup": round(ms_unfused / ms_per_step, 3)},
-        "fused_w4a8_per_channel_steps": {"ms_per_step": round(ms_pc, 5),
-                                         "tops": round(ops_step / (ms_pc * 1e-3) / 1e12, 2)},
-        "mlp_2B_M4192": {"workload": "2B-class MLP pair up 2048->8192, down 8192->2048, M=4192 (4096+32+64)",
-                         "w4a8": {"ms_per_step": round(ms_mlp8, 5),
-                                  "tops": round(mlp_ops / (ms_mlp8 * 1e-3) / 1e12, 2)},
-                         "w4a4": {"ms_per_step": round(ms_mlp4, 5),
-                                  "tops": round(mlp_ops / (ms_mlp4 * 1e-3) / 1e12, 2)}},
-        "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "2B_M4192": chain2},
-        "block_2B_batch4_M16768": {"workload": "2B-class block qkv/out/up/down, batch 4: M=16768",
-                                   **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
-                                                  "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}
-                                      for b in (8, 4)}},
-        "static_single_kernel_few_tokens": single,
-        "calibration": calib,
-        "hbm_copy": {"bytes": 2 * (COPY_MIB << 20), "us": round(copy_us, 1),
-                     "gbs": round(2 * (COPY_MIB << 20) / (copy_us * 1e-6) / 1e9, 1)},
+        "hbm_copy": copy,
     }
+    if not args.headline_only:
+        mlp_ops = ops_of(mlp)
+        b4_ops = sum(2.0 * 4 * sum(synth.TOKENS_2B) * K * N for K, N in synth.LINEARS_2B.values())
+        out.update({
+            "fused_w4a8_per_call_us": {ly["name"]: round(per8[i, 0] * 1e3, 2) for i, ly in enumerate(blk)},
+            "fused_w4a4": {"ms_per_step": round(ms_w4a4, 5), "tops": round(ops_step / (ms_w4a4 * 1e-3) / 1e12, 2),
+                           "per_call_us": {ly["name"]: round(per4[i, 0] * 1e3, 2) for i, ly in enumerate(blk)},
+                           "frac_int8": round(ops_step / (ms_w4a4 * 1e-3) / 1e12 / PEAK_INT8_TOPS, 4)},
+            "unfused_w4a8": {"ms_per_step": round(ms_unfused, 5),
+                             "tops": round(ops_step / (ms_unfused * 1e-3) / 1e12, 2),
+                             "fused_speedup": round(ms_unfused / ms_per_step, 3)},
+            "fused_w4a8_per_channel_steps": {"ms_per_step": round(ms_pc, 5),
+                                             "tops": round(ops_step / (ms_pc * 1e-3) / 1e12, 2)},
+            "mlp_2B_M4192": {"workload": "2B-class MLP pair up 2048->8192, down 8192->2048, M=4192 (4096+32+64)",
+                             "w4a8": {"ms_per_step": round(ms_mlp8, 5),
+                                      "tops": round(mlp_ops / (ms_mlp8 * 1e-3) / 1e12, 2)},
+                             "w4a4": {"ms_per_step": round(ms_mlp4, 5),
+                                      "tops": round(mlp_ops / (ms_mlp4 * 1e-3) / 1e12, 2)}},
+            "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "2B_M4192": chain2},
+            "block_2B_batch4_M16768": {"workload": "2B-class block qkv/out/up/down, batch 4: M=16768",
+                                       **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
+                                                      "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}
+                                          for b in (8, 4)}},
+            "static_single_kernel_few_tokens": single,
+            "calibration": calib,
+        })
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(blk, args.cpu_video_rows)
     print(json.dumps(out), flush=True)
