@@ -138,3 +138,78 @@ def test_graph_calibration_replays_match_eager(bits):
         for a, b in zip(outs(), ref):
             assert torch.equal(a, b), f"replay {rep}"
     del g
+
+
+def test_graph_chain_single_kernel_and_noalloc_replay():
+    """The MLP chain with the producer-side fusion (up projection with the GELU
+    epilogue, then the down projection's GEMM on its codes), the bf16 GELU,
+    the STATIC single-kernel linear (with and without a K split) and the
+    allocation-free linear, captured as one HIP graph: every replay equals the
+    eager calls bit for bit, with eager calls on other inputs in between."""
+    Mu, K, N, N2 = 300, 2048, 1024, 256
+    Lu1 = synth.make_layer(K=K, N=N, stream_counts=split(Mu), T=3, seed=[21, 1])
+    Lu2 = synth.make_layer(K=K, N=N, stream_counts=split(Mu), T=3, seed=[21, 2])
+    Ld = synth.make_layer(K=N, N=N2, stream_counts=split(Mu), T=3, seed=[21, 3])
+    _, Wu = oracle_weight(Lu1, 128)
+    _, Wd = oracle_weight(Ld, 128)
+    Ms, Ks, Ns = 64, 8192, 512  # few tokens: the single-kernel linear splits K with a workspace
+    Ls1 = synth.make_layer(K=Ks, N=Ns, stream_counts=(0, 0, Ms), T=3, seed=[21, 4])
+    Ls2 = synth.make_layer(K=Ks, N=Ns, stream_counts=(0, 0, Ms), T=3, seed=[21, 5])
+    _, Ws = oracle_weight(Ls1, 128)
+
+    def static_act(L, step, t2s=None):
+        a = act_params(L, step, 8, B.SQ_RANGE_STATIC)
+        if t2s is not None:
+            a.tok2stream = t2s
+        return a
+
+    xu = [u16_to_dev(L.x_bits, torch.bfloat16) for L in (Lu1, Lu2)]
+    xs = [u16_to_dev(L.x_bits, torch.bfloat16) for L in (Ls1, Ls2)]
+    au = [act_params(L, 1, 8, 0) for L in (Lu1, Lu2)]
+    ad = [static_act(Ld, 1, au[0].tok2stream), static_act(Ld, 2, au[1].tok2stream)]
+    as_ = [static_act(L, 1) for L in (Ls1, Ls2)]
+    ws_u = B.alloc_workspace(B.SQ_VARIANT_FUSED, Mu, K, N, 8)
+    ws_d = B.alloc_workspace(B.SQ_VARIANT_GEMM, Mu, N, N2, 8)
+    ws_s = B.alloc_workspace(B.SQ_VARIANT_GEMM, Ms, Ks, Ns, 8)
+    qn = torch.empty((Mu, N), dtype=torch.int8, device="cuda")
+    rn = torch.empty((Mu,), dtype=torch.float32, device="cuda")
+    yd = torch.empty((Mu, N2), dtype=torch.bfloat16, device="cuda")
+    g_out = torch.empty((Mu, K), dtype=torch.bfloat16, device="cuda")
+    ys1 = torch.empty((Ms, Ns), dtype=torch.bfloat16, device="cuda")
+    ys2 = torch.empty((Ms, Ns), dtype=torch.bfloat16, device="cuda")
+    yn = torch.empty((Mu, N), dtype=torch.bfloat16, device="cuda")
+
+    def call(i):
+        B.sq_linear_w4a8_gelu_quant(xu[i], au[i], Wu, ad[i], qn, rn, ws_u)
+        B.sq_gemm_w4a8(qn, rn, Wd, yd, B.SQ_OUT_BF16, workspace=ws_d)
+        B.sq_gelu_bf16(xu[i], g_out)
+        B.sq_linear_w4a8_static1(xs[i], as_[i], Ws, ys1, B.SQ_OUT_BF16)
+        B.sq_linear_w4a8_static1(xs[i], as_[i], Ws, ys2, B.SQ_OUT_BF16, workspace=ws_s)
+        B.sq_linear_w4a8_noalloc(xu[i], au[i], Wu, yn, B.SQ_OUT_BF16)
+
+    outs = (qn, rn, yd, g_out, ys1, ys2, yn)
+
+    def snap():
+        return [t.clone() for t in outs]
+
+    def same(a, b):
+        return all(torch.equal(u.view(torch.int8), v.view(torch.int8)) for u, v in zip(a, b))
+
+    call(0)
+    torch.cuda.synchronize()
+    ref = snap()
+    call(1)
+    torch.cuda.synchronize()
+    other = snap()
+    assert not any(torch.equal(u.view(torch.int8), v.view(torch.int8)) for u, v in zip(ref, other))
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        call(0)
+    for rep in range(3):
+        call(1)
+        torch.cuda.synchronize()
+        assert same(snap(), other)
+        g.replay()
+        torch.cuda.synchronize()
+        assert same(snap(), ref), f"replay {rep}"
+    del g
