@@ -76,7 +76,7 @@ def parse():
     p.add_argument("--headline-only", action="store_true",
                    help="only the headline line's own measurements (the 14B block's timed steps, the per-kernel "
                         "pass and the copy that calibrates the byte counters): for kernel traces and counters")
-    p.add_argument("--cpu-video-rows", type=int, default=256,
+    p.add_argument("--cpu-video-rows", type=int, default=640,
                    help="video rows per layer in the oracle's stratified sample (all proprio / action rows too)")
     return p.parse_args()
 
