@@ -40,45 +40,52 @@ __device__ __forceinline__ uint32_t pack_bytes8(uint32_t w0, uint32_t w1, uint32
 // 64-row blocks would leave CUs without a workgroup (few output channels,
 // e.g. the 2048-wide out and down projections): half the rows per workgroup
 // and half its LDS, so that twice as many workgroups run, two per CU.
+// Output channels per workgroup: 32, or 64 when 32-channel strips would need
+// more than one round of workgroups (the 128-token 2B projections, the 14B
+// ones at 64 tokens): each wave then computes two 32-channel tiles with the
+// same activation fragments.
 constexpr int SK_BM = 64;
-constexpr int SK_BN = 32;  // output channels per workgroup
+constexpr int SK_BN = 32;
 constexpr int SK_DIST = 2;  // stages loaded ahead (the codes kernels)
 
 // LDS layout of a slot (16-byte chunks XOR-swizzled, as in the tiled kernel,
 // so that fragment reads are free of bank conflicts):
 //   8-bit activation row r (128 B) at r * 128, chunk c at position c ^ ((r >> 1) & 7)
 //   4-bit activation row r (64 B) at r * 64, chunk c at position c ^ ((r >> 2) & 3)
-//   weight column n (64 B) at B_OFF + n * 64, chunk c at position c ^ ((n >> 2) & 3)
+//   weight column n (64 B, n < BN) at B_OFF + n * 64, chunk c at position c ^ ((n >> 2) & 3)
 //   4-bit group steps at S_OFF: row r's dword (the stage's two fp16 steps) at r * 4
 //   weight steps at W_OFF: dword i holds columns 2i, 2i + 1
-// Lane (column n = lane & 31, h = lane >> 5) feeds k-step s of a stage with the
-// channels [64 (s >> 1) + 32 h + 16 (s & 1), +16) of both operands; 64-wide
-// blocks are k-steps {0, 1} and {2, 3}.
+// Lane (column n = 32 tn + (lane & 31) of tile tn, h = lane >> 5) feeds k-step
+// s of a stage with the channels [64 (s >> 1) + 32 h + 16 (s & 1), +16) of both
+// operands; 64-wide blocks are k-steps {0, 1} and {2, 3}.
 // QX (the single-kernel linear, 8-bit STATIC ranges): the slot's activation
 // area holds the stage's bf16 rows (row r, 256 B, chunk c at position
 // c ^ (r & 15)), which the wave quantizes in place into the 8-bit layout
 // above (the first 8 KB) before its MFMAs; one stage is loaded ahead.
-template <int ABITS, bool QX = false, int BM = SK_BM>
+template <int ABITS, bool QX = false, int BM = SK_BM, int BN = SK_BN>
 struct Sk {
   static constexpr int DIST = QX ? 1 : SK_DIST;  // stages loaded ahead
   static constexpr int SLOTS = DIST + 1;         // ring slots per wave
   static constexpr int A = BM * (QX ? 2 * KT : (ABITS == 8 ? KT : KT / 2));  // bf16 rows, or codes (BM = 64: 8 / 4 KB)
-  static constexpr int B = SK_BN * (KT / 2);                    // packed weights (2 KB)
+  static constexpr int B = BN * (KT / 2);                       // packed weights (2 or 4 KB)
   static constexpr int SIG = ABITS == 4 ? 256 : 0;              // 4-bit group steps
   static constexpr int B_OFF = A, S_OFF = A + B, W_OFF = A + B + SIG;
   static constexpr int D_OFF = W_OFF + 256;                     // QX: the stage's 128 D^-1 values
   static constexpr int SLOT = D_OFF + (QX ? 512 : 0);           // + one 256 B load of weight steps
   static constexpr int NDMA = A / 1024 + B / 1024 + (ABITS == 4 ? 1 : 0) + 1;  // loads per stage and wave
   static constexpr int WGS_PER_CU = 4 * SLOTS * SLOT * 2 <= 160 * 1024 ? 2 : 1;
-  static_assert(4 * BM * SK_BN * 4 <= 4 * SLOTS * SLOT, "the wave sums fit in the ring");
+  static_assert(4 * SLOTS * SLOT <= 160 * 1024, "the ring fits in the LDS");
+  static_assert(4 * BM * BN * 4 <= 4 * SLOTS * SLOT, "the wave sums fit in the ring");
   static_assert(BM == 64 || (BM == 32 && !QX), "64-row blocks, or 32 without in-kernel quantization");
+  static_assert(BN == 32 || (BN == 64 && !QX), "64-channel strips without in-kernel quantization");
   static_assert(!QX || ABITS == 8, "in-kernel quantization: 8-bit codes");
 };
 
-template <int ABITS, int EPI, bool PC, bool QX = false, int BM = SK_BM>
-__global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_skinny_kernel(GemmArgs a) {
-  using L = Sk<ABITS, QX, BM>;
+template <int ABITS, int EPI, bool PC, bool QX = false, int BM = SK_BM, int BN = SK_BN>
+__global__ __launch_bounds__(256, (Sk<ABITS, QX, BM, BN>::WGS_PER_CU)) void gemm_skinny_kernel(GemmArgs a) {
+  using L = Sk<ABITS, QX, BM, BN>;
   constexpr int TM = BM / 32;  // 32-row MFMA tiles per wave
+  constexpr int TN = BN / 32;  // 32-channel MFMA tiles per wave
   static_assert(!PC || ABITS == 8, "one weight step per channel: 8-bit activations");
   static_assert(!QX || EPI == kEpiOut, "the single-kernel linear finishes its outputs");
   __shared__ __attribute__((aligned(16))) uint8_t ring[4][L::SLOTS][L::SLOT];
@@ -88,7 +95,7 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
   const int nkt = K / KT;
   const int S = a.split;
   const int strip = blockIdx.x / S, range = blockIdx.x % S;
-  const int m0 = blockIdx.y * BM, n0 = strip * SK_BN;
+  const int m0 = blockIdx.y * BM, n0 = strip * BN;
   const int kt0 = range * nkt / S, kt1 = (range + 1) * nkt / S;
   const int h = lane >> 5, col = lane & 31;
   const int rows = min(M - m0, BM);
@@ -116,7 +123,7 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
     voffB[i] = static_cast<uint32_t>(n * (K / 2) + 16 * ((lane & 3) ^ ((n >> 2) & 3)));
   }
   const uint32_t voffS = static_cast<uint32_t>(min(lane, rows - 1) * (K / kA4Group) * 2);  // row lane
-  const uint32_t voffW = 4 * (lane & 15);  // lanes 16..63 repeat the 16 dwords
+  const uint32_t voffW = 4 * (lane & (BN / 2 - 1));  // lanes past BN / 2 repeat the first dwords
   const uint32_t ring0 = lds_offset(&ring[wave][0][0]);
   const uint8_t* qx = static_cast<const uint8_t*>(a.qx) + static_cast<size_t>(m0) * arow;
   const uint8_t* qw = a.qw + static_cast<size_t>(n0) * (K / 2);
@@ -152,20 +159,28 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
         aoff[tm][ks] = r * 64 + 16 * ((2 * (ks >> 1) + h) ^ ((r >> 2) & 3));
     }
   }
-  int boff[2];
+  int boff[TN][2], woff[TN];
 #pragma unroll
-  for (int k2 = 0; k2 < 2; ++k2) boff[k2] = L::B_OFF + col * 64 + 16 * ((2 * k2 + h) ^ ((col >> 2) & 3));
-  const int woff = L::W_OFF + 4 * (col >> 1);
-
-  float y[TM][16];
-  v16i acc[TM];
+  for (int tn = 0; tn < TN; ++tn) {
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm) {
-    acc[tm] = (v16i)(0);
-#pragma unroll
-    for (int r = 0; r < 16; ++r) y[tm][r] = 0.0f;
+    for (int k2 = 0; k2 < 2; ++k2)
+      boff[tn][k2] = L::B_OFF + (32 * tn + col) * 64 + 16 * ((2 * k2 + h) ^ ((col >> 2) & 3));
+    woff[tn] = L::W_OFF + 4 * ((32 * tn + col) >> 1);
   }
-  float wprev = 0.0f;  // 8-bit: the fold before the first block adds 0
+
+  float y[TM][TN][16];
+  v16i acc[TM][TN];
+  float wprev[TN];  // 8-bit: the fold before the first block adds 0
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) {
+    wprev[tn] = 0.0f;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      acc[tm][tn] = (v16i)(0);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) y[tm][tn][r] = 0.0f;
+    }
+  }
 
   // 8-bit: y += fp32(C) * Delta_W of the previous block, then this block's
   // MFMAs.  4-bit: the MFMAs of both 64-blocks of the stage, then their folds
@@ -173,11 +188,15 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
   auto compute = [&](int slot) {
     const uint8_t* st = &ring[wave][slot][0];
     // every LDS read of the stage first: one latency per stage
-    uint4 pb[2];
+    uint4 pb[TN][2];
+    uint32_t wpair[TN];
     v4i af[TM][4];
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) pb[k2] = *reinterpret_cast<const uint4*>(st + boff[k2]);
-    const uint32_t wpair = *reinterpret_cast<const uint32_t*>(st + woff);
+    for (int tn = 0; tn < TN; ++tn) {
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) pb[tn][k2] = *reinterpret_cast<const uint4*>(st + boff[tn][k2]);
+      wpair[tn] = *reinterpret_cast<const uint32_t*>(st + woff[tn]);
+    }
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
@@ -198,54 +217,71 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
           sp[tm][g] = *reinterpret_cast<const uint4*>(st + L::S_OFF + (tm * 32 + 8 * g + 4 * h) * 4);
     }
     __builtin_amdgcn_sched_barrier(0);
-    v4i bf[4];
+    v4i bf[TN][4];
+    float wstep[TN];
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      bf[2 * k2] = unpack_frag(pb[k2].x, pb[k2].y);
-      bf[2 * k2 + 1] = unpack_frag(pb[k2].z, pb[k2].w);
+    for (int tn = 0; tn < TN; ++tn) {
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        bf[tn][2 * k2] = unpack_frag(pb[tn][k2].x, pb[tn][k2].y);
+        bf[tn][2 * k2 + 1] = unpack_frag(pb[tn][k2].z, pb[tn][k2].w);
+      }
+      wstep[tn] = f16_to_f32((col & 1) ? (wpair[tn] >> 16) : (wpair[tn] & 0xFFFFu));
     }
-    const float wstep = f16_to_f32((col & 1) ? (wpair >> 16) : (wpair & 0xFFFFu));
     if constexpr (PC) {
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-        for (int ks = 0; ks < 4; ++ks)
-          acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[ks], acc[tm], 0, 0, 0);
-      (void)wstep;
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int ks = 0; ks < 4; ++ks)
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[tn][ks], acc[tm][tn], 0, 0, 0);
     } else if constexpr (ABITS == 8) {
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm) {
-        fold8(acc[tm], wprev, y[tm]);
-        acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][0], bf[0], (v16i)(0), 0, 0, 0);
+      for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-        for (int ks = 1; ks < 4; ++ks)
-          acc[tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[ks], acc[tm], 0, 0, 0);
-      }
-      wprev = wstep * 0.0625f;  // widened weight codes carry a factor 16
+        for (int tn = 0; tn < TN; ++tn) {
+          fold8(acc[tm][tn], wprev[tn], y[tm][tn]);
+          acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][0], bf[tn][0], (v16i)(0), 0, 0, 0);
+#pragma unroll
+          for (int ks = 1; ks < 4; ++ks)
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[tm][ks], bf[tn][ks], acc[tm][tn], 0, 0, 0);
+        }
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) wprev[tn] = wstep[tn] * 0.0625f;  // widened weight codes carry a factor 16
     } else {
-      const float w = wstep * 0.00390625f;  // widened codes of both operands carry 16 * 16
-      v16i c[2][TM];
+      v16i c[2][TM][TN];
 #pragma unroll
       for (int hb = 0; hb < 2; ++hb)
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm) {
           const uint4 pa = __builtin_bit_cast(uint4, af[tm][2 * hb]);
-          c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.x, pa.y), bf[2 * hb], (v16i)(0), 0, 0, 0);
-          c[hb][tm] = __builtin_amdgcn_mfma_i32_32x32x32_i8(unpack_frag(pa.z, pa.w), bf[2 * hb + 1], c[hb][tm], 0, 0, 0);
+          const v4i a0 = unpack_frag(pa.x, pa.y), a1 = unpack_frag(pa.z, pa.w);
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn) {
+            c[hb][tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a0, bf[tn][2 * hb], (v16i)(0), 0, 0, 0);
+            c[hb][tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(a1, bf[tn][2 * hb + 1], c[hb][tm][tn], 0, 0, 0);
+          }
         }
       // block by block, as the tiled kernels: y += (fp32(C_b) sigma_b) * Delta_W
 #pragma unroll
-      for (int tm = 0; tm < TM; ++tm)
+      for (int tn = 0; tn < TN; ++tn) {
+        const float w = wstep[tn] * 0.00390625f;  // widened codes of both operands carry 16 * 16
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const uint32_t s4[4] = {sp[tm][g].x, sp[tm][g].y, sp[tm][g].z, sp[tm][g].w};
+        for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const int r = 4 * g + q;
-            y[tm][r] = __builtin_fmaf(mul_step16<0>(static_cast<float>(c[0][tm][r]), s4[q]), w, y[tm][r]);
-            y[tm][r] = __builtin_fmaf(mul_step16<1>(static_cast<float>(c[1][tm][r]), s4[q]), w, y[tm][r]);
+          for (int g = 0; g < 4; ++g) {
+            const uint32_t s4[4] = {sp[tm][g].x, sp[tm][g].y, sp[tm][g].z, sp[tm][g].w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const int r = 4 * g + q;
+              y[tm][tn][r] =
+                  __builtin_fmaf(mul_step16<0>(static_cast<float>(c[0][tm][tn][r]), s4[q]), w, y[tm][tn][r]);
+              y[tm][tn][r] =
+                  __builtin_fmaf(mul_step16<1>(static_cast<float>(c[1][tm][tn][r]), s4[q]), w, y[tm][tn][r]);
+            }
           }
-        }
+      }
     }
   };
 
@@ -318,63 +354,77 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
   }
   if constexpr (ABITS == 8 && !PC) {
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm) fold8(acc[tm], wprev, y[tm]);
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) fold8(acc[tm][tn], wprev[tn], y[tm][tn]);
   }
 
   // the four waves' sums, added in wave order; wave g then finishes register
-  // group g of both tiles: rows tm * 32 + 8 g + 4 h + q, q < 4
+  // group g of every tile: rows tm * 32 + 8 g + 4 h + q, q < 4
   wait_vm<0>();     // no direct load still writes the ring
   __syncthreads();  // and no wave still reads it
-  float* red = reinterpret_cast<float*>(&ring[0][0][0]);  // [wave][tm * 16 + r][lane]
+  constexpr int NT = TM * TN;
+  float* red = reinterpret_cast<float*>(&ring[0][0][0]);  // [wave][(tm * TN + tn) * 16 + r][lane]
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int r = 0; r < 16; ++r)
-      red[(wave * TM * 16 + tm * 16 + r) * 64 + lane] = PC ? __int_as_float(acc[tm][r]) : y[tm][r];
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        red[((wave * NT + tm * TN + tn) * 16 + r) * 64 + lane] = PC ? __int_as_float(acc[tm][tn][r]) : y[tm][tn][r];
   __syncthreads();
   const int g = wave;
-  float v[TM][4];
+  float v[TM][TN][4];
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int r = 4 * g + q;
-      if constexpr (PC) {  // int32 sums: exact in any order; raw bits while split
-        int t = __float_as_int(red[(tm * 16 + r) * 64 + lane]);
+    for (int tn = 0; tn < TN; ++tn)
 #pragma unroll
-        for (int w = 1; w < 4; ++w) t += __float_as_int(red[(w * TM * 16 + tm * 16 + r) * 64 + lane]);
-        v[tm][q] = __int_as_float(t);
-      } else {
-        float t = red[(tm * 16 + r) * 64 + lane];
+      for (int q = 0; q < 4; ++q) {
+        const int r = 4 * g + q, t = tm * TN + tn;
+        if constexpr (PC) {  // int32 sums: exact in any order; raw bits while split
+          int u = __float_as_int(red[(t * 16 + r) * 64 + lane]);
 #pragma unroll
-        for (int w = 1; w < 4; ++w) t += red[(w * TM * 16 + tm * 16 + r) * 64 + lane];
-        v[tm][q] = t;
+          for (int w = 1; w < 4; ++w) u += __float_as_int(red[((w * NT + t) * 16 + r) * 64 + lane]);
+          v[tm][tn][q] = __int_as_float(u);
+        } else {
+          float u = red[(t * 16 + r) * 64 + lane];
+#pragma unroll
+          for (int w = 1; w < 4; ++w) u += red[((w * NT + t) * 16 + r) * 64 + lane];
+          v[tm][tn][q] = u;
+        }
       }
-    }
 
   if (S > 1) {
-    // this K range's sums, [row][col] of the 64 x 32 block (rows < M)
-    float* P = a.partial + (static_cast<size_t>(blockIdx.y * (N / SK_BN) + strip) * S + range) * (BM * SK_BN);
+    // this K range's sums, [row][col] of the BM x BN block (rows < M)
+    float* P = a.partial + (static_cast<size_t>(blockIdx.y * (N / BN) + strip) * S + range) * (BM * BN);
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int row = tm * 32 + 8 * g + 4 * h + q;
-        if (row < rows) P[row * SK_BN + col] = v[tm][q];
-      }
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int row = tm * 32 + 8 * g + 4 * h + q;
+          if (row < rows) P[row * BN + 32 * tn + col] = v[tm][tn][q];
+        }
     return;
   }
   if constexpr (PC) {  // the one conversion, with the column's step (widened codes: factor 16)
-    const float wpc = f16_to_f32(a.w_scale[n0 + col]) * 0.0625f;
 #pragma unroll
-    for (int tm = 0; tm < TM; ++tm)
+    for (int tn = 0; tn < TN; ++tn) {
+      const float wpc = f16_to_f32(a.w_scale[n0 + 32 * tn + col]) * 0.0625f;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) v[tm][q] = static_cast<float>(__float_as_int(v[tm][q])) * wpc;
+      for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[tm][tn][q] = static_cast<float>(__float_as_int(v[tm][tn][q])) * wpc;
+    }
   }
   // epilogue: row factor (8-bit: r_i; 4-bit: kappa_i = 1 / gamma_s(i), the
   // compensation of Eq. 8), fetched from the lane that loaded it; bias; cast.
   // A quad transpose gives each lane four consecutive channels of one row.
-  float rowf = 1.0f, bias = 0.0f;
+  float rowf = 1.0f, bias[TN];
+#pragma unroll
+  for (int tn = 0; tn < TN; ++tn) bias[tn] = 0.0f;
   if constexpr (EPI == kEpiOut) {
     const int m = m0 + min(lane, rows - 1);
     if constexpr (QX)
@@ -383,21 +433,25 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
       rowf = static_cast<const float*>(a.act_scale)[m];
     else
       rowf = 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
-    if (a.bias != nullptr) bias = bf16_to_f32(a.bias[n0 + col]);
+    if (a.bias != nullptr) {
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) bias[tn] = bf16_to_f32(a.bias[n0 + 32 * tn + col]);
+    }
   }
   const int rf_bits = __float_as_int(rowf);
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
 #pragma unroll
-  for (int tm = 0; tm < TM; ++tm) {
+  for (int t = 0; t < TM * TN; ++t) {
+    const int tm = t / TN, tn = t % TN;
     float o[4];
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const float rf = __int_as_float(__builtin_amdgcn_ds_bpermute((tm * 32 + 8 * g + 4 * h + q) * 4, rf_bits));
-      o[q] = EPI == kEpiPartial ? v[tm][q] : __builtin_fmaf(v[tm][q], rf, bias);
+      o[q] = EPI == kEpiPartial ? v[tm][tn][q] : __builtin_fmaf(v[tm][tn][q], rf, bias[tn]);
     }
     quad_transpose(o, lane);
     const int row = tm * 32 + 8 * g + 4 * h + (lane & 3);
-    const int n = n0 + (lane & 28);
+    const int n = n0 + 32 * tn + (lane & 28);
     if (row < rows) {
       const size_t m = static_cast<size_t>(m0 + row);
       if (f32out) {
@@ -421,22 +475,22 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM>::WGS_PER_CU)) void gemm_ski
 // output in range order (int32 sums with one step per channel, then the one
 // conversion) and finishes it as the skinny epilogue does.  Four adjacent
 // outputs per thread.
-template <int ABITS, int EPI, bool PC, bool QX = false, int BM = SK_BM>
+template <int ABITS, int EPI, bool PC, bool QX = false, int BM = SK_BM, int BN = SK_BN>
 __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
-  const int strips = a.N / SK_BN;
-  const int g = blockIdx.x * 256 + threadIdx.x;  // one thread per 4 outputs of a BM x 32 block
-  const int blk = g / (BM * SK_BN / 4);
-  const int e = (g % (BM * SK_BN / 4)) * 4;
-  const int row = e / SK_BN, c = e % SK_BN;
+  const int strips = a.N / BN;
+  const int g = blockIdx.x * 256 + threadIdx.x;  // one thread per 4 outputs of a BM x BN block
+  const int blk = g / (BM * BN / 4);
+  const int e = (g % (BM * BN / 4)) * 4;
+  const int row = e / BN, c = e % BN;
   const int mb = blk / strips, strip = blk % strips;
-  const int m = mb * BM + row, n = strip * SK_BN + c;
+  const int m = mb * BM + row, n = strip * BN + c;
   if (mb * BM >= a.M || m >= a.M) return;
-  const float* P = a.partial + static_cast<size_t>(blk) * a.split * (BM * SK_BN) + row * SK_BN + c;
+  const float* P = a.partial + static_cast<size_t>(blk) * a.split * (BM * BN) + row * BN + c;
   float y[4];
   if constexpr (PC) {
     int4 acc = make_int4(0, 0, 0, 0);
     for (int sl = 0; sl < a.split; ++sl) {
-      const int4 v = *reinterpret_cast<const int4*>(P + static_cast<size_t>(sl) * (BM * SK_BN));
+      const int4 v = *reinterpret_cast<const int4*>(P + static_cast<size_t>(sl) * (BM * BN));
       acc.x += v.x;
       acc.y += v.y;
       acc.z += v.z;
@@ -448,7 +502,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   } else {
     float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
     for (int sl = 0; sl < a.split; ++sl) {
-      const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * (BM * SK_BN));
+      const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * (BM * BN));
       acc.x += v.x;
       acc.y += v.y;
       acc.z += v.z;
@@ -490,11 +544,11 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
 // MI355X: a stage costs a wave about 0.65 us, the second kernel and its
 // launch about 5 us, i.e. about 8 stages.  At most the workgroups that fit at
 // once (by LDS), and at least four stages (one per wave) in every range.
-template <int ABITS, int BM>
+template <int ABITS, int BM, int BN>
 int split_t(int32_t M, int32_t N, int32_t K) {
-  const int blocks = (N / SK_BN) * ((M + BM - 1) / BM);
+  const int blocks = (N / BN) * ((M + BM - 1) / BM);
   const int nkt = K / KT;
-  const int smax = std::max(1, std::min(device_cus() * Sk<ABITS, false, BM>::WGS_PER_CU / blocks, nkt / 4));
+  const int smax = std::max(1, std::min(device_cus() * Sk<ABITS, false, BM, BN>::WGS_PER_CU / blocks, nkt / 4));
   int best = 1;
   double best_cost = (nkt + 3) / 4;
   for (int S = 2; S <= smax; ++S) {
@@ -504,41 +558,58 @@ int split_t(int32_t M, int32_t N, int32_t K) {
   return best;
 }
 
-// Rows per workgroup for a layer (QX: always 64): 32 when 64-row blocks would
-// give fewer workgroups than CUs.  Measured at 64 and 128 tokens on the 2B
-// linears (fused call, graph-replayed): out 12-18 % faster, down up to 14 %,
-// qkv at 64 tokens within 3 %; up, with 256 strips, keeps 64-row blocks.
-int skinny_bm(int32_t M, int32_t N, bool qx) {
-  if (qx) return SK_BM;
-  return (N / SK_BN) * ((M + SK_BM - 1) / SK_BM) < device_cus() ? 32 : SK_BM;
+// Block shape for a layer (QX: always 64 x 32).  Rows: 32 when 64-row blocks
+// of 32 channels would give fewer workgroups than CUs (measured at 64 and 128
+// tokens on the 2B linears, fused call, graph-replayed: out 12-18 % faster,
+// down up to 14 %, qkv at 64 tokens within 3 %).  Channels: 64 when 64 x 32
+// blocks would not all run at once (one per CU with 8-bit codes, two with
+// 4-bit ones): the activations are then read once per 64 channels and half
+// as many workgroups remain.
+struct SkPlan {
+  int bm, bn;
+};
+SkPlan skinny_plan(int act_bits, int32_t M, int32_t N, bool qx) {
+  if (qx) return {SK_BM, SK_BN};
+  const int w = (N / SK_BN) * ((M + SK_BM - 1) / SK_BM);
+  const int slots = device_cus() * (act_bits == 8 ? Sk<8, false, SK_BM, SK_BN>::WGS_PER_CU
+                                                  : Sk<4, false, SK_BM, SK_BN>::WGS_PER_CU);
+  if (w < device_cus()) return {32, SK_BN};
+  if (w > slots) return {SK_BM, 64};
+  return {SK_BM, SK_BN};
+}
+
+template <int ABITS>
+int split_for(const SkPlan& p, int32_t M, int32_t N, int32_t K) {
+  if (p.bm == 32) return split_t<ABITS, 32, SK_BN>(M, N, K);
+  return p.bn == 64 ? split_t<ABITS, SK_BM, 64>(M, N, K) : split_t<ABITS, SK_BM, SK_BN>(M, N, K);
 }
 
 int skinny_split(int act_bits, int32_t M, int32_t N, int32_t K, bool qx = false) {
-  if (skinny_bm(M, N, qx) == 32) return act_bits == 8 ? split_t<8, 32>(M, N, K) : split_t<4, 32>(M, N, K);
-  return act_bits == 8 ? split_t<8, SK_BM>(M, N, K) : split_t<4, SK_BM>(M, N, K);
+  const SkPlan p = skinny_plan(act_bits, M, N, qx);
+  return act_bits == 8 ? split_for<8>(p, M, N, K) : split_for<4>(p, M, N, K);
 }
 
 size_t partial_bytes_for(int act_bits, int32_t M, int32_t N, int32_t K, bool qx) {
   const int S = skinny_split(act_bits, M, N, K, qx);
   if (S <= 1) return 0;
-  const int bm = skinny_bm(M, N, qx);
-  return static_cast<size_t>(N / SK_BN) * ((M + bm - 1) / bm) * S * (bm * SK_BN) * sizeof(float);
+  const SkPlan p = skinny_plan(act_bits, M, N, qx);
+  return static_cast<size_t>(N / p.bn) * ((M + p.bm - 1) / p.bm) * S * (p.bm * p.bn) * sizeof(float);
 }
 
-template <int ABITS, int EPI, bool PC, bool QX, int BM>
+template <int ABITS, int EPI, bool PC, bool QX, int BM, int BN>
 hipError_t launch_bm(const GemmArgs& a0, hipStream_t s, float* partial, size_t partial_bytes) {
   GemmArgs a = a0;
   int S = skinny_split(ABITS, a.M, a.N, a.K, QX);
   if (S > 1 && (partial == nullptr || partial_bytes < partial_bytes_for(ABITS, a.M, a.N, a.K, QX))) S = 1;
   a.split = S;
   a.partial = S > 1 ? partial : nullptr;
-  const int strips = a.N / SK_BN, mblocks = (a.M + BM - 1) / BM;
-  hipLaunchKernelGGL((gemm_skinny_kernel<ABITS, EPI, PC, QX, BM>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
+  const int strips = a.N / BN, mblocks = (a.M + BM - 1) / BM;
+  hipLaunchKernelGGL((gemm_skinny_kernel<ABITS, EPI, PC, QX, BM, BN>), dim3(strips * S, mblocks), dim3(256), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || S == 1) return e;
-  const int threads = strips * mblocks * (BM * SK_BN / 4);
+  const int threads = strips * mblocks * (BM * BN / 4);
   // with QX the second kernel computes r_i itself, as the first does
-  hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI, PC, QX, BM>), dim3((threads + 255) / 256), dim3(256), 0, s,
+  hipLaunchKernelGGL((gemm_skinny_tail_kernel<ABITS, EPI, PC, QX, BM, BN>), dim3((threads + 255) / 256), dim3(256), 0, s,
                      a);
   return hipGetLastError();
 }
@@ -546,9 +617,11 @@ hipError_t launch_bm(const GemmArgs& a0, hipStream_t s, float* partial, size_t p
 template <int ABITS, int EPI, bool PC, bool QX = false>
 hipError_t launch_t(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
   if constexpr (!QX) {
-    if (skinny_bm(a.M, a.N, false) == 32) return launch_bm<ABITS, EPI, PC, false, 32>(a, s, partial, partial_bytes);
+    const SkPlan p = skinny_plan(ABITS, a.M, a.N, false);
+    if (p.bm == 32) return launch_bm<ABITS, EPI, PC, false, 32, SK_BN>(a, s, partial, partial_bytes);
+    if (p.bn == 64) return launch_bm<ABITS, EPI, PC, false, SK_BM, 64>(a, s, partial, partial_bytes);
   }
-  return launch_bm<ABITS, EPI, PC, QX, SK_BM>(a, s, partial, partial_bytes);
+  return launch_bm<ABITS, EPI, PC, QX, SK_BM, SK_BN>(a, s, partial, partial_bytes);
 }
 
 }  // namespace

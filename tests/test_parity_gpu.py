@@ -209,7 +209,8 @@ def test_gemm_entry_points(bits, with_ws):
 
 @pytest.mark.parametrize("bits", [8, 4])
 @pytest.mark.parametrize("M,K,N", [(1, 2048, 2048), (2, 128, 64), (33, 8192, 2048), (64, 2048, 6144),
-                                   (65, 5120, 320), (128, 1024, 1024), (100, 13824, 128)])
+                                   (65, 5120, 320), (128, 1024, 1024), (100, 13824, 128), (128, 512, 8192),
+                                   (100, 1024, 8448)])
 @pytest.mark.parametrize("out", [F32, BF16])
 @pytest.mark.parametrize("per_channel", [False, True])
 def test_few_tokens(bits, M, K, N, out, per_channel):
@@ -218,7 +219,10 @@ def test_few_tokens(bits, M, K, N, out, per_channel):
     per output channel (8-bit: int32 sums over all of K, exact across the
     waves and split ranges).  Fused linear, and the second kernel alone
     without a workspace (K never split) and with one (K split across
-    workgroups when that is faster: 8192 and 13824 channels here)."""
+    workgroups when that is faster: 8192 and 13824 channels here).  Blocks of
+    32 rows (few output channels), 64 x 32, and 64 x 64 where 64 x 32 blocks
+    would not all run at once (8192 channels at 128 tokens with 8-bit codes,
+    8448 at 100 tokens with both widths)."""
     L = layer(M, K, N, seed=[9, M, K, N])
     G = K if per_channel else 128
     pw, W = oracle_weight(L, G)
