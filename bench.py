@@ -844,6 +844,15 @@ def main():
 
         # ---- the STATIC single-kernel linear at few tokens, against the two kernels
         single = static_single_kernel_figures(torch, B, synth, dev)
+        # ---- the MLP chain at few tokens (the weight-streaming GEMM with the GELU epilogue)
+        chain_few = {}
+        for tag, lins, M in (("2B_M64", synth.LINEARS_2B, 64), ("2B_M128", synth.LINEARS_2B, 128),
+                             ("14B_M64", synth.LINEARS_14B, 64)):
+            pair = device_block(torch, B, synth, dev, {"up": lins["up"], "down": lins["down"]}, (0, 0, M),
+                                seed=7100)
+            chain_few[tag] = mlp_chain_figures(torch, B, dev, pair[0], pair[1], reps=50)
+            del pair
+        torch.cuda.empty_cache()
 
         # ---- the calibration path of Eq. (9) on the 2B up projection
         calib = calibration_figures(torch, B, mlp[0], stream, dev, None if args.no_cpu else 256)
@@ -931,7 +940,7 @@ def main():
                                       "tops": round(mlp_ops / (ms_mlp8 * 1e-3) / 1e12, 2)},
                              "w4a4": {"ms_per_step": round(ms_mlp4, 5),
                                       "tops": round(mlp_ops / (ms_mlp4 * 1e-3) / 1e12, 2)}},
-            "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "2B_M4192": chain2},
+            "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "2B_M4192": chain2, **chain_few},
             "block_2B_batch4_M16768": {"workload": "2B-class block qkv/out/up/down, batch 4: M=16768",
                                        **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
                                                       "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}

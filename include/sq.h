@@ -242,11 +242,14 @@ sq_status sq_linear_w4a8_static1(const uint16_t* x, int32_t M, const sq_act_para
  * sq_gelu_bf16 applied to sq_linear_w4a8's bf16 output; they feed
  * sq_gemm_w4a8 with the down projection's weights.  The down layer's
  * channel scaling act_next->dinv must be NULL or 16-byte aligned.
- * Requires act->act_bits == 8, w->w_group == 128, M > 128 (the tiled GEMM;
- * fewer tokens take the weight-streaming kernel, which has no such
- * epilogue), act_next->act_bits == 8 and act_next->range_mode ==
- * SQ_RANGE_STATIC (a dynamic range needs the whole row before any code):
- * else SQ_ERR_UNSUPPORTED. */
+ * The epilogue runs in whichever GEMM the layer takes: the tiled one (more
+ * than 128 tokens) or the weight-streaming one (at most 128 tokens), and in
+ * the second kernel of a K split.
+ * Requires act->act_bits == 8, w->w_group == 128 (or, for at most 128
+ * tokens, w->w_group == K: one step per output channel),
+ * act_next->act_bits == 8 and act_next->range_mode == SQ_RANGE_STATIC (a
+ * dynamic range needs the whole row before any code): else
+ * SQ_ERR_UNSUPPORTED. */
 sq_status sq_linear_w4a8_gelu_quant(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
                                     const sq_act_params* act_next, int8_t* qx_next, float* r_next, void* workspace,
                                     size_t ws_bytes, hipStream_t stream);

@@ -3,6 +3,7 @@
 // tokens): the operands, block accumulation and epilogue of the tiled kernel.
 #include <algorithm>
 
+#include "gelu.h"
 #include "gemm_frag.h"
 #include "sq_internal.h"
 
@@ -422,10 +423,11 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM, BN>::WGS_PER_CU)) void gemm
   // epilogue: row factor (8-bit: r_i; 4-bit: kappa_i = 1 / gamma_s(i), the
   // compensation of Eq. 8), fetched from the lane that loaded it; bias; cast.
   // A quad transpose gives each lane four consecutive channels of one row.
+  constexpr bool kGelu = EPI == kEpiGelu;
   float rowf = 1.0f, bias[TN];
 #pragma unroll
   for (int tn = 0; tn < TN; ++tn) bias[tn] = 0.0f;
-  if constexpr (EPI == kEpiOut) {
+  if constexpr (EPI == kEpiOut || kGelu) {
     const int m = m0 + min(lane, rows - 1);
     if constexpr (QX)
       rowf = qdelta / a.gamma[a.step * a.S + a.tok2stream[m]];  // r_i = Delta / gamma_s(i), as the first kernel
@@ -437,6 +439,27 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM, BN>::WGS_PER_CU)) void gemm
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) bias[tn] = bf16_to_f32(a.bias[n0 + 32 * tn + col]);
     }
+  }
+  // GELU epilogue: the next layer's gain of the lane's row, its 1 / Delta,
+  // and the D^-1 of the four columns each lane holds after the transpose;
+  // the first strip's first wave writes the next layer's row scales
+  float gain = 0.0f, ninv = 0.0f, ndinv[TN][4];
+  if constexpr (kGelu) {
+    const NextQuant& q = a.nq;
+    gain = q.gamma[q.step * q.S + q.tok2stream[m0 + min(lane, rows - 1)]];
+    const float ndelta = q.clip[q.step] / 127.0f;
+    ninv = 1.0f / ndelta;
+    if (__builtin_isinf(ninv)) ninv = 0.0f;
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const float4 d = q.dinv != nullptr ? *reinterpret_cast<const float4*>(q.dinv + n0 + 32 * tn + (lane & 28))
+                                         : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+      ndinv[tn][0] = d.x;
+      ndinv[tn][1] = d.y;
+      ndinv[tn][2] = d.z;
+      ndinv[tn][3] = d.w;
+    }
+    if (n0 == 0 && g == 0 && lane < rows) q.r[m0 + lane] = ndelta / gain;
   }
   const int rf_bits = __float_as_int(rowf);
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
@@ -452,9 +475,13 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM, BN>::WGS_PER_CU)) void gemm
     quad_transpose(o, lane);
     const int row = tm * 32 + 8 * g + 4 * h + (lane & 3);
     const int n = n0 + 32 * tn + (lane & 28);
+    float grow = 0.0f;
+    if constexpr (kGelu) grow = __int_as_float(__builtin_amdgcn_ds_bpermute(row * 4, __float_as_int(gain)));
     if (row < rows) {
       const size_t m = static_cast<size_t>(m0 + row);
-      if (f32out) {
+      if constexpr (kGelu) {
+        *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(a.out) + m * N + n) = gelu_codes4(o, ndinv[tn], grow, ninv);
+      } else if (f32out) {
         *reinterpret_cast<float4*>(static_cast<float*>(a.out) + m * N + n) = make_float4(o[0], o[1], o[2], o[3]);
       } else {
         uint2 w;
@@ -513,7 +540,7 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
     y[2] = acc.z;
     y[3] = acc.w;
   }
-  if constexpr (EPI == kEpiOut) {
+  if constexpr (EPI == kEpiOut || EPI == kEpiGelu) {
     const float rowf = QX ? (a.clip[a.step] / 127.0f) / a.gamma[a.step * a.S + a.tok2stream[m]]
                           : ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
                                        : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
@@ -523,7 +550,18 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
       y[j] = __builtin_fmaf(y[j], rowf, b);
     }
   }
-  if (EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32) {
+  if constexpr (EPI == kEpiGelu) {  // the next layer's codes (and, from the first column, its row scale)
+    const NextQuant& q = a.nq;
+    const float ndelta = q.clip[q.step] / 127.0f;
+    float ninv = 1.0f / ndelta;
+    if (__builtin_isinf(ninv)) ninv = 0.0f;
+    const float gain = q.gamma[q.step * q.S + q.tok2stream[m]];
+    const float4 d4 = q.dinv != nullptr ? *reinterpret_cast<const float4*>(q.dinv + n) : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+    const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+    *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(a.out) + static_cast<size_t>(m) * a.N + n) =
+        gelu_codes4(y, dv, gain, ninv);
+    if (n == 0) q.r[m] = ndelta / gain;
+  } else if (EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32) {
     *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * a.N + n) =
         make_float4(y[0], y[1], y[2], y[3]);
   } else {
@@ -649,6 +687,9 @@ hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s
       case kEpiPartial:
         return pc ? launch_t<8, kEpiPartial, true>(a, s, partial, partial_bytes)
                   : launch_t<8, kEpiPartial, false>(a, s, partial, partial_bytes);
+      case kEpiGelu:
+        return pc ? launch_t<8, kEpiGelu, true>(a, s, partial, partial_bytes)
+                  : launch_t<8, kEpiGelu, false>(a, s, partial, partial_bytes);
     }
   } else {
     switch (epi) {

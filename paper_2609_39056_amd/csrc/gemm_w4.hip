@@ -1673,7 +1673,8 @@ size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t
 }
 
 hipError_t launch_gemm_gelu_quant(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
-  if (skinny_applies(8, a.M, a.K, a.w_group) || a.w_group != KT) return hipErrorInvalidValue;
+  if (skinny_applies(8, a.M, a.K, a.w_group)) return launch_skinny(8, kEpiGelu, a, s, partial, partial_bytes);
+  if (a.w_group != KT) return hipErrorInvalidValue;
   return launch_t<8, kEpiGelu, true>(a, s, partial, partial_bytes);
 }
 

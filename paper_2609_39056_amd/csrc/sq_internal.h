@@ -128,7 +128,8 @@ size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t
 // Compute units of the current device (256 when there is none), capped at 256.
 int device_cus();
 
-// Weight-streaming GEMM for M <= kSkinnyMaxM (epi kEpiOut or kEpiPartial):
+// Weight-streaming GEMM for M <= kSkinnyMaxM (epi kEpiOut, kEpiPartial, or
+// kEpiGelu with 8-bit activations):
 // 4-bit activations with any weight groups, 8-bit ones with 128-wide groups
 // or one step per output channel.  Splits K across workgroups when `partial`
 // holds skinny_partial_bytes(...) bytes.
@@ -168,8 +169,9 @@ hipError_t launch_pack_weights(const PackArgs& a, hipStream_t s);
 // every tile is then computed whole).
 hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial = nullptr,
                        size_t partial_bytes = 0);
-// The 8-bit GEMM with 128-wide weight groups on the pipelined kernel (more
-// than kSkinnyMaxM rows) and the kEpiGelu epilogue (a.nq set, a.out the codes).
+// The 8-bit GEMM with the kEpiGelu epilogue (a.nq set, a.out the codes): the
+// pipelined kernel with 128-wide weight groups (more than kSkinnyMaxM rows),
+// or the weight-streaming one (128-wide groups or one step per channel).
 hipError_t launch_gemm_gelu_quant(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes);
 // GELU of n bf16 values to bf16 (the fp32 sequence of gelu.h).
 hipError_t launch_gelu_bf16(const uint16_t* x, size_t n, uint16_t* y, hipStream_t s);

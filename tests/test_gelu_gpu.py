@@ -141,16 +141,39 @@ def test_gelu_quant_chain(name, M, K, N, counts):
         a = M // 6
         p = M // 10
         counts = (M - a - p, p, a)
+    chain_case(counts, K, N, 128)
+
+
+# At most 128 tokens the chain's up projection runs the weight-streaming GEMM
+# with the GELU epilogue: 64 x 32 blocks, 64-channel strips, 32-row blocks
+# with K split across workgroups (the epilogue then runs in the second
+# kernel), and one weight step per channel (int32 sums, also through a split).
+FEW = [  # name, stream counts, K, N, weight group
+    ("2B up 64 action tokens", (0, 0, 64), 2048, 8192, 128),
+    ("2B up 128 tokens 64-channel strips", (0, 64, 64), 2048, 8192, 128),
+    ("64x8192x2048 32-row blocks split along K", (0, 0, 64), 8192, 2048, 128),
+    ("100x2048x1024 one step per channel", (0, 36, 64), 2048, 1024, 2048),
+    ("64x8192x512 one step per channel split along K", (0, 0, 64), 8192, 512, 8192),
+    ("14B up 64 action tokens", (0, 0, 64), 5120, 13824, 128),
+]
+
+
+@pytest.mark.parametrize("name,counts,K,N,G", FEW, ids=[c[0] for c in FEW])
+def test_gelu_quant_chain_few_tokens(name, counts, K, N, G):
+    chain_case(counts, K, N, G)
+
+
+def chain_case(counts, K, N, G):
     L = synth.make_layer(K=K, N=N, stream_counts=counts, T=T, seed=[32, K, N], permute=True)
     M = L.M
-    pw, W = oracle_weight(L, 128)
+    pw, W = oracle_weight(L, G)
     rows = tile_rows(M, seed=[33, M]) if M > 600 else np.arange(M)
     x = u16_to_dev(L.x_bits, torch.bfloat16)
     t2s_dev = i32_to_dev(L.tok2stream)
     step = 4
     for up_mode in (B.SQ_RANGE_DYNAMIC, B.SQ_RANGE_STATIC):
         act = act_params(L, step, 8, up_mode)
-        res = O.linear(L.x_bits[rows], L.tok2stream[rows], L.gamma, step, pw["codes"], pw["w_scale"], 128,
+        res = O.linear(L.x_bits[rows], L.tok2stream[rows], L.gamma, step, pw["codes"], pw["w_scale"], G,
                        dinv=L.dinv, clip=L.clip, bias_bits=L.bias_bits, range_mode=up_mode, act_bits=8)
         h_or = O.f32_to_bf16_bits(res["y"])
         g_or = O.gelu_bf16(h_or)
@@ -167,7 +190,7 @@ def test_gelu_quant_chain(name, M, K, N, counts):
             del qn, rn, h_dev, qx_u, r_u
 
 
-EXACT = [(300, 2048, 1024), (4192, 2048, 8192), (1000, 384, 640)]
+EXACT = [(300, 2048, 1024), (4192, 2048, 8192), (1000, 384, 640), (64, 2048, 8192), (64, 8192, 2048)]
 
 
 @pytest.mark.parametrize("M,K,N", EXACT)

@@ -142,7 +142,8 @@ def test_graph_calibration_replays_match_eager(bits):
 
 def test_graph_chain_single_kernel_and_noalloc_replay():
     """The MLP chain with the producer-side fusion (up projection with the GELU
-    epilogue, then the down projection's GEMM on its codes), the bf16 GELU,
+    epilogue, then the down projection's GEMM on its codes; and at 64 tokens,
+    where the weight-streaming GEMM splits K), the bf16 GELU,
     the STATIC single-kernel linear (with and without a K split) and the
     allocation-free linear, captured as one HIP graph: every replay equals the
     eager calls bit for bit, with eager calls on other inputs in between."""
@@ -156,6 +157,7 @@ def test_graph_chain_single_kernel_and_noalloc_replay():
     Ls1 = synth.make_layer(K=Ks, N=Ns, stream_counts=(0, 0, Ms), T=3, seed=[21, 4])
     Ls2 = synth.make_layer(K=Ks, N=Ns, stream_counts=(0, 0, Ms), T=3, seed=[21, 5])
     _, Ws = oracle_weight(Ls1, 128)
+    Lsd = synth.make_layer(K=Ns, N=64, stream_counts=(0, 0, Ms), T=3, seed=[21, 6])  # the few-token chain's down
 
     def static_act(L, step, t2s=None):
         a = act_params(L, step, 8, B.SQ_RANGE_STATIC)
@@ -168,6 +170,8 @@ def test_graph_chain_single_kernel_and_noalloc_replay():
     au = [act_params(L, 1, 8, 0) for L in (Lu1, Lu2)]
     ad = [static_act(Ld, 1, au[0].tok2stream), static_act(Ld, 2, au[1].tok2stream)]
     as_ = [static_act(L, 1) for L in (Ls1, Ls2)]
+    asg = [act_params(L, 1, 8, 0) for L in (Ls1, Ls2)]  # few-token chain: dynamic up projection
+    asd = [static_act(Lsd, 1, asg[0].tok2stream), static_act(Lsd, 2, asg[1].tok2stream)]
     ws_u = B.alloc_workspace(B.SQ_VARIANT_FUSED, Mu, K, N, 8)
     ws_d = B.alloc_workspace(B.SQ_VARIANT_GEMM, Mu, N, N2, 8)
     ws_s = B.alloc_workspace(B.SQ_VARIANT_GEMM, Ms, Ks, Ns, 8)
@@ -178,6 +182,9 @@ def test_graph_chain_single_kernel_and_noalloc_replay():
     ys1 = torch.empty((Ms, Ns), dtype=torch.bfloat16, device="cuda")
     ys2 = torch.empty((Ms, Ns), dtype=torch.bfloat16, device="cuda")
     yn = torch.empty((Mu, N), dtype=torch.bfloat16, device="cuda")
+    ws_sg = B.alloc_workspace(B.SQ_VARIANT_FUSED, Ms, Ks, Ns, 8)
+    qs = torch.empty((Ms, Ns), dtype=torch.int8, device="cuda")
+    rs = torch.empty((Ms,), dtype=torch.float32, device="cuda")
 
     def call(i):
         B.sq_linear_w4a8_gelu_quant(xu[i], au[i], Wu, ad[i], qn, rn, ws_u)
@@ -186,8 +193,9 @@ def test_graph_chain_single_kernel_and_noalloc_replay():
         B.sq_linear_w4a8_static1(xs[i], as_[i], Ws, ys1, B.SQ_OUT_BF16)
         B.sq_linear_w4a8_static1(xs[i], as_[i], Ws, ys2, B.SQ_OUT_BF16, workspace=ws_s)
         B.sq_linear_w4a8_noalloc(xu[i], au[i], Wu, yn, B.SQ_OUT_BF16)
+        B.sq_linear_w4a8_gelu_quant(xs[i], asg[i], Ws, asd[i], qs, rs, ws_sg)  # few tokens, K split
 
-    outs = (qn, rn, yd, g_out, ys1, ys2, yn)
+    outs = (qn, rn, yd, g_out, ys1, ys2, yn, qs, rs)
 
     def snap():
         return [t.clone() for t in outs]
