@@ -63,6 +63,29 @@ def test_quantize_bitexact(bits, mode, K, M):
 
 
 @pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("K,M", [(2560, 2051), (5120, 2049), (8192, 2050), (10240, 2051), (13824, 2048)])
+def test_quantize_many_rows(bits, K, M):
+    """Thousands of rows of the lengths the layers use, with a ragged row
+    count (not a multiple of the rows per workgroup) and rows whose chunks
+    leave lanes idle (2560 channels): codes and scales bit-exact, DYNAMIC and
+    STATIC, with and without the channel scaling."""
+    L = layer(M, K, 64, seed=[2, K, M])
+    x = xdev(L)
+    for mode in (0, 1):
+        for use_dinv in (True, False):
+            act = act_params(L, 1, bits, mode, use_dinv=use_dinv)
+            qx, sc = B.act_buffers(M, K, bits)
+            B.sq_quantize_act(x, act, qx, sc)
+            ref = O.quantize_act(L.x_bits, L.tok2stream, L.gamma, 1, dinv=L.dinv if use_dinv else None,
+                                 clip=L.clip, range_mode=mode, act_bits=bits)
+            assert np.array_equal(qx.cpu().numpy().view(np.uint8), ref["qx"].view(np.uint8)), (mode, use_dinv)
+            if bits == 8:
+                assert np.array_equal(sc.cpu().numpy().view(np.uint32), ref["scale"].view(np.uint32))
+            else:
+                assert np.array_equal(bits16(sc), ref["scale"])
+
+
+@pytest.mark.parametrize("bits", [8, 4])
 def test_quantize_degenerate_rows(bits):
     """All-zero rows, a single non-zero element, bf16 subnormal magnitudes (the
     step underflows into fp32 subnormals and its reciprocal overflows), huge
