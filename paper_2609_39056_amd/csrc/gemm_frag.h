@@ -128,6 +128,42 @@ __device__ __forceinline__ float mul_step16(float cf, uint32_t pair) {
   return __builtin_fmaf(cf, static_cast<float>(__builtin_bit_cast(half2v, pair)[HI]), 0.0f);
 }
 
+// The sums of four adjacent outputs over the S ranges of a split K, range r
+// at P + r * stride (16-byte aligned), added in range order: fp32, or with
+// INT the raw bits of int32 sums (one weight step per channel).  The loads go
+// out eight at a time before any addition (a slot past S re-reads the last
+// range and is not added), so the sum waits about one memory latency per
+// eight ranges instead of one per range; the additions and their order are
+// those of a plain loop over r.
+template <bool INT>
+__device__ __forceinline__ float4 sum_ranges4(const float* P, size_t stride, int S) {
+  float4 f = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+  int4 q = make_int4(0, 0, 0, 0);
+  for (int s0 = 0; s0 < S; s0 += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] = *reinterpret_cast<const float4*>(P + static_cast<size_t>(min(s0 + i, S - 1)) * stride);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      if (s0 + i < S) {
+        if constexpr (INT) {
+          q.x += __float_as_int(v[i].x);
+          q.y += __float_as_int(v[i].y);
+          q.z += __float_as_int(v[i].z);
+          q.w += __float_as_int(v[i].w);
+        } else {
+          f.x += v[i].x;
+          f.y += v[i].y;
+          f.z += v[i].z;
+          f.w += v[i].w;
+        }
+      }
+    }
+  }
+  if constexpr (INT) return make_float4(__int_as_float(q.x), __int_as_float(q.y), __int_as_float(q.z), __int_as_float(q.w));
+  return f;
+}
+
 // Word 3 of a raw buffer resource (32-bit data format, no swizzle).
 constexpr int kBufWord3 = 0x00020000;
 

@@ -513,42 +513,31 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
   const int m = mb * BM + row, n = strip * BN + c;
   if (mb * BM >= a.M || m >= a.M) return;
   const float* P = a.partial + static_cast<size_t>(blk) * a.split * (BM * BN) + row * BN + c;
-  float y[4];
-  if constexpr (PC) {
-    int4 acc = make_int4(0, 0, 0, 0);
-    for (int sl = 0; sl < a.split; ++sl) {
-      const int4 v = *reinterpret_cast<const int4*>(P + static_cast<size_t>(sl) * (BM * BN));
-      acc.x += v.x;
-      acc.y += v.y;
-      acc.z += v.z;
-      acc.w += v.w;
-    }
-    const int ci[4] = {acc.x, acc.y, acc.z, acc.w};
+  // the epilogue's inputs first, so that their loads overlap the partial sums'
+  constexpr bool kOut = EPI == kEpiOut || EPI == kEpiGelu;
+  float rowf = 1.0f, bias[4] = {0.0f, 0.0f, 0.0f, 0.0f}, wpc[4];
+  if constexpr (kOut) {
+    rowf = QX ? (a.clip[a.step] / 127.0f) / a.gamma[a.step * a.S + a.tok2stream[m]]
+              : ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
+                           : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
+    if (a.bias != nullptr) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) y[j] = static_cast<float>(ci[j]) * (f16_to_f32(a.w_scale[n + j]) * 0.0625f);
-  } else {
-    float4 acc = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
-    for (int sl = 0; sl < a.split; ++sl) {
-      const float4 v = *reinterpret_cast<const float4*>(P + static_cast<size_t>(sl) * (BM * BN));
-      acc.x += v.x;
-      acc.y += v.y;
-      acc.z += v.z;
-      acc.w += v.w;
+      for (int j = 0; j < 4; ++j) bias[j] = bf16_to_f32(a.bias[n + j]);
     }
-    y[0] = acc.x;
-    y[1] = acc.y;
-    y[2] = acc.z;
-    y[3] = acc.w;
   }
-  if constexpr (EPI == kEpiOut || EPI == kEpiGelu) {
-    const float rowf = QX ? (a.clip[a.step] / 127.0f) / a.gamma[a.step * a.S + a.tok2stream[m]]
-                          : ABITS == 8 ? static_cast<const float*>(a.act_scale)[m]
-                                       : 1.0f / a.gamma[a.step * a.S + a.tok2stream[m]];
+  if constexpr (PC) {
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float b = a.bias != nullptr ? bf16_to_f32(a.bias[n + j]) : 0.0f;
-      y[j] = __builtin_fmaf(y[j], rowf, b);
-    }
+    for (int j = 0; j < 4; ++j) wpc[j] = f16_to_f32(a.w_scale[n + j]) * 0.0625f;
+  }
+  const float4 acc = sum_ranges4<PC>(P, static_cast<size_t>(BM) * BN, a.split);
+  float y[4] = {acc.x, acc.y, acc.z, acc.w};
+  if constexpr (PC) {  // the int32 sums, converted once with the column's step
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = static_cast<float>(__float_as_int(y[j])) * wpc[j];
+  }
+  if constexpr (kOut) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(y[j], rowf, bias[j]);
   }
   if constexpr (EPI == kEpiGelu) {  // the next layer's codes (and, from the first column, its row scale)
     const NextQuant& q = a.nq;
