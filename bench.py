@@ -76,6 +76,8 @@ def parse():
     p.add_argument("--headline-only", action="store_true",
                    help="only the headline line's own measurements (the 14B block's timed steps, the per-kernel "
                         "pass and the copy that calibrates the byte counters): for kernel traces and counters")
+    p.add_argument("--suite-summary", metavar="JSONL",
+                   help="print the markdown summary of a --suite run's records (no GPU needed)")
     p.add_argument("--cpu-video-rows", type=int, default=640,
                    help="video rows per layer in the oracle's stratified sample (all proprio / action rows too)")
     return p.parse_args()
@@ -186,6 +188,60 @@ def cpu_baseline(layers, video_rows):
                        f"TOPS = sum 2*rows*K*N / time")
 
 
+def suite_summary(path):
+    """Markdown tables of a --suite run: per layer, and the denoising sweeps."""
+    recs = [json.loads(line) for line in open(path) if line.strip()]
+    out = ["# Fused linear, every layer configuration and the denoising sweeps (W4A8 / W4A4)", "",
+           "Commands (repo root, one MI355X, ROCm 7.2):", "", "```",
+           "python3 bench.py --suite gpurun_out/suite/suite.jsonl",
+           "python3 bench.py --suite-summary gpurun_out/suite/suite.jsonl", "```", "",
+           "Per-layer times are HIP-event times of one replay of a HIP graph of back-to-back calls (400 for the "
+           "256x256 layer, 60 for the 2B layers and the action-only ones, 12 for the 14B layers; a quarter of that for "
+           "the unfused path), divided by the call count: device time including each launch's dispatch, not the "
+           "host's launch rate; the layer's weight is the same in every call (the denoising sweeps below stream "
+           "distinct weights).  K1 = `sq_quantize_act`, K2 = `sq_gemm_w4a*` (main kernel + split tail when there is "
+           "one), layer = the fused C-ABI call (K1 + K2), unfused = `sq_linear_unfused`.  With 4-bit activations and "
+           "more than 128 tokens the fused call runs its GEMM on the fp8 matrix cores (`gemm_a4f8_kernel`, first "
+           "kernel writing fp8 code bytes), while K2 is the stand-alone int8-path GEMM on packed codes.  Fractions: "
+           "int8-MFMA peak 5.0 POP/s, HBM 8 TB/s on the algorithmic bytes (bf16 X, int4 W, fp16 steps, bf16 Y, bias, "
+           "stream map).  CPU oracle = `oracle/sq_oracle.py` (`linear`, DYNAMIC, the layer's bit width) timed in the "
+           "same run on the host's cores: on every row of the small and action-only layers, else on every proprio "
+           "and action row plus 64 video rows with the time scaled to all rows (marked *).  Inputs are the seeded "
+           "synthetic layers of `synth.device_layer`.", ""]
+    for r in recs:
+        if r.get("group") == "dispatch cost":
+            out += [f"Dispatch cost of one HIP graph node (one-element kernel): **{r['us_per_node']} us**.", ""]
+    out += ["| layer | act | weight steps | M | K -> N | K1 us | K2 us | layer us | layer TOPS | K2 % int8 | "
+            "layer % HBM | unfused us | fused speedup | CPU oracle us | oracle TOPS | layer / oracle |",
+            "|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in recs:
+        if "linear" not in r:
+            continue
+        steps = "per channel" if r["w_group"] == r["K"] else f"groups of {r['w_group']}"
+        orc = ("—", "—", "—")
+        if "cpu_oracle_us" in r:
+            star = "*" if r["cpu_oracle_extrapolated"] else ""
+            orc = (f"{r['cpu_oracle_us']:.0f}{star}", f"{r['cpu_oracle_tops']:.4f}",
+                   f"{r['cpu_oracle_us'] / r['us_layer']:.0f}x")
+        out.append(f"| {r['group']} {r['linear']} | A{r['act_bits']} | {steps} | {r['M']} | {r['K']} -> {r['N']} | "
+                   f"{r['us_quant']:.2f} | {r['us_gemm']:.2f} | {r['us_layer']:.2f} | {r['tops_layer']:.1f} | "
+                   f"{100 * r['frac_int8_gemm']:.1f} | {100 * r['frac_hbm_layer']:.2f} | {r['us_unfused']:.2f} | "
+                   f"{r['fused_speedup']:.2f} | {orc[0]} | {orc[1]} | {orc[2]} |")
+    cores = {r["cpu_cores"] for r in recs if "cpu_cores" in r}
+    if cores:
+        out += ["", f"CPU oracle threads: {', '.join(str(c) for c in sorted(cores))}."]
+    out += ["", "Denoising sweep: 28 layers x 10 steps x {qkv, out, up, down} of the 2B class, each layer with its own "
+            "weights (0.7 GB packed, more than the 256 MB MALL), 1120 fused calls captured as one HIP graph:", "",
+            "| variant | act | graph ms | eager ms | us per call | TOPS | % int8 | GB/s | % HBM |",
+            "|---|---|---|---|---|---|---|---|---|"]
+    for r in recs:
+        if "variant" in r:
+            out.append(f"| {r['variant']} | A{r['act_bits']} | {r['ms_graph']:.2f} | {r['ms_eager']:.2f} | "
+                       f"{r['us_per_call']:.2f} | {r['tops']:.1f} | {100 * r['frac_int8']:.2f} | {r['gbs']:.0f} | "
+                       f"{100 * r['frac_hbm']:.2f} |")
+    print("\n".join(out))
+
+
 def run_suite(args):
     """Every layer configuration, one JSON record per measurement."""
     import torch
@@ -238,7 +294,35 @@ def run_suite(args):
     def alg_bytes(M, K, N, wg=W_GROUP):  # bf16 X, int4 W, fp16 steps, bf16 Y, bias, stream map
         return M * K * 2 + N * K // 2 + (K // wg) * N * 2 + M * N * 2 + 2 * N + 4 * M
 
-    def layer_record(group, name, L, W, bits, reps):
+    def oracle_record(L, w_host, G, bits, step):
+        """The oracle, as it stands, on the layer's stratified rows (every
+        proprio and action row plus SUITE_ORACLE_VIDEO_ROWS video rows: all
+        rows of the small and action-only layers), W4A8 / W4A4 DYNAMIC; time
+        extrapolated linearly to all M rows when sampled.  The weight packing
+        (offline) is not timed."""
+        from oracle import sq_oracle as O
+        M, K = L["x"].shape
+        N = w_host.shape[0]
+        t2s = L["tok2stream"].cpu().numpy()
+        rows = synth.stratified_rows(t2s, SUITE_ORACLE_VIDEO_ROWS, seed=0)
+        xr = L["x"][torch.as_tensor(rows, device=dev)].view(torch.int16).cpu().numpy().view(np.uint16)
+        pw = O.pack_weights(w_host, L["d"].cpu().numpy(), G)
+        gamma, dinv = L["gamma"].cpu().numpy(), L["dinv"].cpu().numpy()
+        bias = L["bias"].view(torch.int16).cpu().numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        O.linear(xr, t2s[rows], gamma, step, pw["codes"], pw["w_scale"], G, dinv=dinv, bias_bits=bias,
+                 act_bits=bits)
+        dt = time.perf_counter() - t0
+        us = dt * 1e6 * M / len(rows)
+        try:
+            cores = len(os.sched_getaffinity(0))
+        except AttributeError:
+            cores = os.cpu_count()
+        return dict(cpu_oracle_us=round(us, 1), cpu_oracle_tops=round(2.0 * M * K * N / us / 1e6, 5),
+                    cpu_oracle_rows=int(len(rows)), cpu_oracle_extrapolated=bool(len(rows) < M),
+                    cpu_cores=min(cores, int(os.environ.get("OMP_NUM_THREADS", cores))))
+
+    def layer_record(group, name, L, W, bits, reps, w_host=None):
         M, K = L["x"].shape
         N = W.N
         act = B.ActParams(tok2stream=L["tok2stream"], gamma=L["gamma"], step=min(3, L["gamma"].shape[0] - 1),
@@ -267,15 +351,19 @@ def run_suite(args):
                   frac_int8_gemm=round(ops / us_k2 / 1e6 / PEAK_INT8_TOPS, 4),
                   gbs_layer=round(ab / us_api / 1e3, 1), frac_hbm_layer=round(ab / us_api / 1e3 / PEAK_HBM_GBS, 4),
                   quant_gbs=round(k1b / us_k1 / 1e3, 1), us_unfused=round(us_unf, 2),
-                  fused_speedup=round(us_unf / us_api, 3)))
+                  fused_speedup=round(us_unf / us_api, 3),
+                  **(oracle_record(L, w_host, W.w_group, bits, act.step) if w_host is not None else {})))
         del qx, sc, wsg, wsf, wsu, y
 
     def layer_group(group, linears, tokens, bits_list, outl, reps, T=10, batch=1, per_channel=False):
         for li, (name, (K, N)) in enumerate(linears.items()):
             L = synth.device_layer(K, N, tokens, T=T, seed=1000 + li, outlier_frac=outl, batch=batch, device=dev)
-            W = B.prepare_weight(L.pop("w"), L["d"], K if per_channel else W_GROUP, bias=L["bias"])
+            w = L.pop("w")
+            w_host = None if args.no_cpu else w.cpu().numpy()
+            W = B.prepare_weight(w, L["d"], K if per_channel else W_GROUP, bias=L["bias"])
+            del w
             for bits in bits_list:
-                layer_record(group, name, L, W, bits, reps)
+                layer_record(group, name, L, W, bits, reps, w_host)
             del L, W
             torch.cuda.empty_cache()
 
@@ -303,6 +391,8 @@ def run_suite(args):
                 {"qkv/8": (5120, 1920), "up/8": (5120, 1728)}, synth.TOKENS_14B, (8, 4), 0.02, 24)
     layer_group("14B-class linears, W4A8, one weight step per output channel", synth.LINEARS_14B, synth.TOKENS_14B,
                 (8,), 0.02, 12, per_channel=True)
+    for M in (64, 128):  # the weight-streaming regime, one layer at a time (its weight stays cached across calls)
+        layer_group(f"2B-class linears, {M} action tokens only", synth.LINEARS_2B, (0, 0, M), (8, 4), 0.02, 60)
 
     # ---- denoising-loop sweep: 28 layers x 10 steps x {qkv, out, up, down} of
     # the 2B class, every layer with its own weights (0.7 GB packed: more than
@@ -368,6 +458,7 @@ def run_suite(args):
     fout.close()
 
 
+SUITE_ORACLE_VIDEO_ROWS = 64  # video rows per layer in the suite's oracle timing (plus every other row)
 PEAK_FP64_TFLOPS = 78.6     # MI355X fp64 (vector and matrix), 78.6 TFLOP/s
 CALIB_CANDIDATES = 16
 CALIB_ROUNDS = 8
@@ -666,6 +757,9 @@ def main():
         sys.exit(2)
     if args.action_only:
         run_action_only(args)
+        return
+    if args.suite_summary:
+        suite_summary(args.suite_summary)
         return
     if args.suite:
         run_suite(args)
