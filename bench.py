@@ -918,6 +918,8 @@ def main():
             del ly["ws_unf"]
         torch.cuda.empty_cache()
         chain14 = mlp_chain_figures(torch, B, dev, blk[2], blk[3])
+        chain14_pc = mlp_chain_figures(torch, B, dev, {**blk[2], "W": blk[2]["W_pc"]},
+                                       {**blk[3], "W": blk[3]["W_pc"]})
         for ly in blk:
             del ly["W_pc"], ly["ws_gemm"], ly["qx8"], ly["r8"]
         torch.cuda.empty_cache()
@@ -1034,7 +1036,8 @@ def main():
                                       "tops": round(mlp_ops / (ms_mlp8 * 1e-3) / 1e12, 2)},
                              "w4a4": {"ms_per_step": round(ms_mlp4, 5),
                                       "tops": round(mlp_ops / (ms_mlp4 * 1e-3) / 1e12, 2)}},
-            "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "2B_M4192": chain2, **chain_few},
+            "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "14B_M8384_per_channel_steps": chain14_pc,
+                                      "2B_M4192": chain2, **chain_few},
             "block_2B_batch4_M16768": {"workload": "2B-class block qkv/out/up/down, batch 4: M=16768",
                                        **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
                                                       "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}

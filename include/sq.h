@@ -245,8 +245,8 @@ sq_status sq_linear_w4a8_static1(const uint16_t* x, int32_t M, const sq_act_para
  * The epilogue runs in whichever GEMM the layer takes: the tiled one (more
  * than 128 tokens) or the weight-streaming one (at most 128 tokens), and in
  * the second kernel of a K split.
- * Requires act->act_bits == 8, w->w_group == 128 (or, for at most 128
- * tokens, w->w_group == K: one step per output channel),
+ * Requires act->act_bits == 8, w->w_group == 128 or K (one step per output
+ * channel, the paper's weight format),
  * act_next->act_bits == 8 and act_next->range_mode == SQ_RANGE_STATIC (a
  * dynamic range needs the whole row before any code): else
  * SQ_ERR_UNSUPPORTED. */

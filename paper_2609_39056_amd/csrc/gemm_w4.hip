@@ -188,15 +188,21 @@ __device__ __forceinline__ void dump_block(const GemmArgs& a, const v16i (&acc)[
 // Row factor of output row m0 + wm * 64 + lane (8-bit: r_i; 4-bit: the
 // inverse gain kappa_i; 1 for partial sums) and the bias of the lane's two
 // columns, loaded when a tile starts so that their latency hides under its
-// main loop.
+// main loop.  The GELU epilogue (8-bit) also loads the next layer's gain of
+// that row, its 1 / Delta and the D^-1 of the four columns the lane holds
+// after the quad transpose in each 32-wide tile.
 template <int ABITS, int EPI>
 struct EpiInputs {
+  static constexpr bool kOut = EPI == kEpiOut || EPI == kEpiGelu;
+  static constexpr bool kGelu = EPI == kEpiGelu;
   float rowf;
   float bias[TN];
+  float gain, inv;
+  float dinv[kGelu ? TN : 1][4];
   __device__ __forceinline__ void load(const GemmArgs& a, int m0, int n0, int wm, int wn, int lane) {
     const int m = min(m0 + wm * 64 + lane, a.M - 1);
     rowf = 1.0f;
-    if constexpr (EPI == kEpiOut) {
+    if constexpr (kOut) {
       if constexpr (ABITS == 8) {
         rowf = static_cast<const float*>(a.act_scale)[m];
       } else {
@@ -206,7 +212,23 @@ struct EpiInputs {
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
       const int n = min(n0 + wn * 64 + tn * 32 + (lane & 31), a.N - 1);
-      bias[tn] = (EPI == kEpiOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
+      bias[tn] = (kOut && a.bias != nullptr) ? bf16_to_f32(a.bias[n]) : 0.0f;
+    }
+    if constexpr (kGelu) {
+      const NextQuant& q = a.nq;
+      gain = q.gamma[q.step * q.S + q.tok2stream[m]];
+      inv = 1.0f / (q.clip[q.step] / 127.0f);
+      if (__builtin_isinf(inv)) inv = 0.0f;
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int n = min(n0 + wn * 64 + tn * 32 + (lane & 28), a.N - 4);
+        const float4 d = q.dinv != nullptr ? *reinterpret_cast<const float4*>(q.dinv + n)
+                                           : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+        dinv[tn][0] = d.x;
+        dinv[tn][1] = d.y;
+        dinv[tn][2] = d.z;
+        dinv[tn][3] = d.w;
+      }
     }
   }
 };
@@ -230,6 +252,10 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN]
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
   const int rf_bits = __float_as_int(in.rowf);
   const int half = (lane >> 5) * 16;  // lanes 32..63 hold rows 4 further down
+  if constexpr (EPI == kEpiGelu) {  // the next layer's row scales, from the waves of the first column tile
+    const int m = m0 + wm * 64 + lane;
+    if (n0 + wn * 64 == 0 && m < M) a.nq.r[m] = (a.nq.clip[a.nq.step] / 127.0f) / in.gain;
+  }
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
     float rowf[16];
@@ -249,8 +275,15 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN]
         quad_transpose(v, lane);
         const int m = m0 + wm * 64 + tm * 32 + g * 8 + (lane >> 5) * 4 + (lane & 3);
         const int n = n0 + wn * 64 + tn * 32 + (lane & 28);
+        float gain = 0.0f;  // the next layer's gain of the lane's row after the transpose
+        if constexpr (EPI == kEpiGelu)
+          gain = __int_as_float(__builtin_amdgcn_ds_bpermute(
+              (tm * 32 + g * 8 + (lane >> 5) * 4 + (lane & 3)) * 4, __float_as_int(in.gain)));
         if (m < M) {
-          if (f32out) {
+          if constexpr (EPI == kEpiGelu) {
+            *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(a.out) + static_cast<size_t>(m) * N + n) =
+                gelu_codes4(v, in.dinv[tn], gain, in.inv);
+          } else if (f32out) {
             *reinterpret_cast<float4*>(static_cast<float*>(a.out) + static_cast<size_t>(m) * N + n) =
                 make_float4(v[0], v[1], v[2], v[3]);
           } else {
@@ -446,7 +479,8 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
   constexpr int NDMA = LY::A_DMA + LY::B_DMA + (A4 ? 1 : 0) + (PC ? 0 : 1);
   constexpr int AHEAD = (CF::DIST - 1) * NDMA;  // loads issued after the stage waited for
   constexpr uint32_t RING = STAGES * LY::STAGE;
-  static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
+  static_assert(EPI == kEpiOut || EPI == kEpiPartial || (EPI == kEpiGelu && ABITS == 8),
+                "the pipelined path applies the weight steps");
 
   __shared__ __align__(1024) uint8_t smem[RING];
 
@@ -1660,6 +1694,7 @@ size_t gemm_partial_bytes(int act_bits, int32_t M, int32_t N, int32_t K, int32_t
 
 hipError_t launch_gemm_gelu_quant(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
   if (skinny_applies(8, a.M, a.K, a.w_group)) return launch_skinny(8, kEpiGelu, a, s, partial, partial_bytes);
+  if (a.w_group == a.K) return launch_t<8, kEpiGelu, true, true>(a, s, partial, partial_bytes);  // one step per channel
   if (a.w_group != KT) return hipErrorInvalidValue;
   return launch_t<8, kEpiGelu, true>(a, s, partial, partial_bytes);
 }

@@ -438,9 +438,9 @@ sq_status sq_linear_w4a8_gelu_quant(const uint16_t* x, int32_t M, const sq_act_p
   if (act->act_bits != 8 || act_next->act_bits != 8 || act_next->range_mode != SQ_RANGE_STATIC)
     return SQ_ERR_UNSUPPORTED;
   if (!valid_m(M)) return SQ_ERR_SHAPE;
-  // few tokens: the weight-streaming GEMM (128-wide groups or one step per
-  // channel); else the tiled one (128-wide groups)
-  if (!skinny_applies(8, M, w->K, w->w_group) && w->w_group != kKTile) return SQ_ERR_UNSUPPORTED;
+  // 128-wide weight groups or one step per output channel (the weight-streaming
+  // GEMM for few tokens, else the tiled ones)
+  if (w->w_group != kKTile && w->w_group != w->K) return SQ_ERR_UNSUPPORTED;
   if (!aligned(x, 16) || !aligned(workspace, 16) || !aligned(qx_next, 4) || !aligned(r_next, 4)) return SQ_ERR_ALIGN;
   if (ws_bytes < fused_ws_bytes(M, w->K, w->N, 8)) return SQ_ERR_WORKSPACE;
   FusedWs f = fused_ws(workspace, ws_bytes, M, w->K, 8, false);

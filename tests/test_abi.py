@@ -300,9 +300,8 @@ def test_static1_rejects(L):
 
 def test_gelu_quant_rejects(L):
     """The up projection with the GELU epilogue validates before launching:
-    8-bit activations, 128-wide weight groups (or, for at most 128 tokens, one
-    step per channel) and a STATIC 8-bit quantizer for the next layer, whose
-    K is this layer's N."""
+    8-bit activations, 128-wide weight groups or one step per channel, and a
+    STATIC 8-bit quantizer for the next layer, whose K is this layer's N."""
     big = 1 << 30
 
     def gq(x=A, M=300, a=None, w=None, an=None, qn=A, rn=A, ws=A, nbytes=big):
@@ -323,7 +322,6 @@ def test_gelu_quant_rejects(L):
     assert gq(M=100, w=wt(K=512, w_group=256)) == UNSUP     # few tokens: groups of 128 or one step per channel
     assert gq(M=0) == SHAPE
     assert gq(w=wt(K=512, w_group=256)) == UNSUP
-    assert gq(w=wt(K=512, w_group=512)) == UNSUP            # one step per channel
     assert gq(w=wt(N=192)) == SHAPE                         # next layer's K must be a multiple of 128
     assert gq(x=A + 2) == ALIGN
     assert gq(qn=A + 2) == ALIGN

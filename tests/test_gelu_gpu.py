@@ -163,6 +163,20 @@ def test_gelu_quant_chain_few_tokens(name, counts, K, N, G):
     chain_case(counts, K, N, G)
 
 
+# One weight step per output channel (the paper's weight format) on the tiled
+# kernel: int32 sums over each tile's K range, converted once; with few tiles
+# the ranges split and the second kernel applies the epilogue.
+PC_CHAIN = [  # name, stream counts, K, N
+    ("300x2048x1024 per channel, tiles split along K", (200, 40, 60), 2048, 1024),
+    ("2B up 4192x2048x8192 per channel", synth.TOKENS_2B, 2048, 8192),
+]
+
+
+@pytest.mark.parametrize("name,counts,K,N", PC_CHAIN, ids=[c[0] for c in PC_CHAIN])
+def test_gelu_quant_chain_per_channel(name, counts, K, N):
+    chain_case(counts, K, N, K)
+
+
 def chain_case(counts, K, N, G):
     L = synth.make_layer(K=K, N=N, stream_counts=counts, T=T, seed=[32, K, N], permute=True)
     M = L.M
