@@ -254,6 +254,46 @@ sq_status sq_linear_w4a8_gelu_quant(const uint16_t* x, int32_t M, const sq_act_p
                                     const sq_act_params* act_next, int8_t* qx_next, float* r_next, void* workspace,
                                     size_t ws_bytes, hipStream_t stream);
 
+/* The same producer-side fusion with 4-bit activations (the paper's W4A4
+ * mode): the fused W4A4 linear of the up projection (x, act, w, workspace as
+ * for sq_linear_w4a4) whose epilogue rounds Y to bf16, evaluates GELU as
+ * sq_gelu_bf16 does, rounds to bf16 and quantizes with the DOWN projection's
+ * STATIC 4-bit quantizer (act_next; Delta = fp16(clip[step] / 7), Eq. 1, 6
+ * and 8).  It writes the down projection's first-kernel output in the form
+ * that projection's GEMM takes at this token count:
+ *   M <= 128  qx_next    packed int4 [M][N/2] (the layout of sq_quantize_act)
+ *             scale_next fp16 sigma [M][N/64]; kc_next unused (may be NULL)
+ *             -> sq_gemm_w4a4; equal, bit for bit, to what
+ *             sq_quantize_act(act_next) writes for the bf16 output of
+ *             sq_gelu_bf16 applied to sq_linear_w4a4's bf16 output;
+ *   M > 128   qx_next    fp8 e4m3 code bytes [M][N] (code * 2^-9: sign and
+ *                        magnitude, |code| <= 7, a zero code of a negative
+ *                        value is -0)
+ *             scale_next fp32 sigma [M][N/64] (the fp16 step, widened)
+ *             kc_next    fp32 [M][N/64], -8 * S * sigma * 2^-18 with S the
+ *                        sum of the row's 64 codes of the group
+ *             -> sq_gemm_w4a4_fp8; the same codes and steps.
+ * qx_next, scale_next and kc_next 4-byte aligned (scale_next 2-byte for
+ * M <= 128).  The down layer's act_next->dinv must be NULL or 16-byte
+ * aligned.  Requires act->act_bits == 4, act_next->act_bits == 4 and
+ * act_next->range_mode == SQ_RANGE_STATIC (else SQ_ERR_UNSUPPORTED). */
+sq_status sq_linear_w4a4_gelu_quant(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                                    const sq_act_params* act_next, void* qx_next, void* scale_next, float* kc_next,
+                                    void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* The second kernel on 4-bit activations in the fp8 form that
+ * sq_linear_w4a4_gelu_quant writes for more than 128 tokens (Sec. 4.4 Eq.
+ * 10 with 64-wide activation groups): fp8 code bytes qx [M][K] (16-byte
+ * aligned), fp32 group steps sigma [M][K/64] and kc [M][K/64] (4-byte
+ * aligned), on the fp8 matrix cores; the outputs equal sq_gemm_w4a4's on the
+ * same codes and steps in the packed form.  act supplies the stream ids and
+ * gains (kappa = 1 / gamma_s(i)) and act->act_bits must be 4.  M <= 128
+ * returns SQ_ERR_UNSUPPORTED (sq_gemm_w4a4 takes the packed form there).
+ * workspace as for sq_gemm_w4a4. */
+sq_status sq_gemm_w4a4_fp8(const uint8_t* qx, const float* group_scale, const float* kc, int32_t M,
+                           const sq_act_params* act, const sq_weight* w, void* y, int32_t out_dtype, void* workspace,
+                           size_t ws_bytes, hipStream_t stream);
+
 /* GELU of n bf16 values (x, y device buffers of n uint16 bit patterns,
  * 16-byte aligned, y may equal x; n may be 0): y = bf16(0.5 x (1 + erf(x /
  * sqrt 2))) with erf by Abramowitz and Stegun 7.1.28 as one fixed sequence of

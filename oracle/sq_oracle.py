@@ -371,16 +371,17 @@ def gelu_bf16(h_bits):
     return f32_to_bf16_bits(gelu_f32(bf16_bits_to_f32(h_bits)))
 
 
-def mlp_chain_codes(y_up, tok2stream, gamma_down, step, dinv_down, clip_down):
-    """The down projection's 8-bit codes and row scales from the up
-    projection's fp32 output y_up [M, N_up]: cast to bf16 (the layer's output
-    format), GELU in bf16, then the STATIC quantizer of the down layer (its
-    gains, thresholds and D^-1; Eq. 1, 6, 8).  Returns (h, g, qa): the up
-    output in bf16, the GELU output in bf16 and quantize_act's result."""
+def mlp_chain_codes(y_up, tok2stream, gamma_down, step, dinv_down, clip_down, act_bits=8):
+    """The down projection's codes and scales (8-bit: row scales; 4-bit:
+    fp16 group steps) from the up projection's fp32 output y_up [M, N_up]:
+    cast to bf16 (the layer's output format), GELU in bf16, then the STATIC
+    quantizer of the down layer (its gains, thresholds and D^-1; Eq. 1, 6,
+    8).  Returns (h, g, qa): the up output in bf16, the GELU output in bf16
+    and quantize_act's result."""
     h = f32_to_bf16_bits(np.asarray(y_up, dtype=F32))
     g = gelu_bf16(h)
     qa = quantize_act(g, tok2stream, gamma_down, step, dinv=dinv_down, clip=clip_down,
-                      range_mode=RANGE_STATIC, act_bits=8)
+                      range_mode=RANGE_STATIC, act_bits=act_bits)
     return h, g, qa
 
 

@@ -93,6 +93,10 @@ _SIGS = {
                                     _P]),
     "sq_linear_w4a8_gelu_quant": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight),
                                        ctypes.POINTER(sq_act_params), _P, _P, _P, _S, _P]),
+    "sq_linear_w4a4_gelu_quant": (_I, [_P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight),
+                                       ctypes.POINTER(sq_act_params), _P, _P, _P, _P, _S, _P]),
+    "sq_gemm_w4a4_fp8": (_I, [_P, _P, _P, _I, ctypes.POINTER(sq_act_params), ctypes.POINTER(sq_weight), _P, _I, _P,
+                              _S, _P]),
     "sq_gelu_bf16": (_I, [_P, _S, _P, _P]),
     "sq_debug_block_acc_i32": (_I, [_P, _I, _I, ctypes.POINTER(sq_weight), _P, _P]),
     "sq_calib_reference": (_I, [_P, _I, _P, ctypes.POINTER(sq_weight), _P, _P]),
@@ -274,6 +278,32 @@ def sq_linear_w4a8_gelu_quant(x, act: ActParams, w: Weight, act_next: ActParams,
                                            _ptr(qx_next), _ptr(r_next), _ptr(workspace),
                                            workspace.numel() * workspace.element_size(), _stream(stream)),
            "sq_linear_w4a8_gelu_quant")
+
+
+def sq_linear_w4a4_gelu_quant(x, act: ActParams, w: Weight, act_next: ActParams, qx_next, scale_next, kc_next,
+                              workspace, stream=None) -> None:
+    """The W4A4 up projection with the GELU epilogue that writes the down
+    projection's STATIC 4-bit codes (include/sq.h): at most 128 tokens packed
+    int4 qx_next [M, N/2] and fp16 scale_next [M, N/64] (kc_next None);
+    more, fp8 code bytes qx_next [M, N] with fp32 scale_next and kc_next
+    [M, N/64].  workspace as for sq_linear_w4a4."""
+    M = x.shape[0]
+    s, ws, sn = act.struct(), w.struct(), act_next.struct()
+    _check(lib().sq_linear_w4a4_gelu_quant(_ptr(x), M, ctypes.byref(s), ctypes.byref(ws), ctypes.byref(sn),
+                                           _ptr(qx_next), _ptr(scale_next), _ptr(kc_next), _ptr(workspace),
+                                           workspace.numel() * workspace.element_size(), _stream(stream)),
+           "sq_linear_w4a4_gelu_quant")
+
+
+def sq_gemm_w4a4_fp8(qx, group_scale, kc, act: ActParams, w: Weight, y, out_dtype: int, workspace=None,
+                     stream=None) -> None:
+    """The 4-bit GEMM on fp8 code bytes [M, K] with fp32 group steps and kc
+    [M, K/64] (more than 128 tokens; include/sq.h)."""
+    M = qx.shape[0]
+    s, ws = act.struct(), w.struct()
+    wp, wb = _ws(workspace)
+    _check(lib().sq_gemm_w4a4_fp8(_ptr(qx), _ptr(group_scale), _ptr(kc), M, ctypes.byref(s), ctypes.byref(ws),
+                                  _ptr(y), out_dtype, wp, wb, _stream(stream)), "sq_gemm_w4a4_fp8")
 
 
 def sq_gelu_bf16(x, y, stream=None) -> None:

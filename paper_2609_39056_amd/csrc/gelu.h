@@ -80,5 +80,49 @@ __device__ __forceinline__ uint32_t gelu_codes4(const float (&y)[4], const float
   return w;
 }
 
+// The next linear's STATIC 4-bit step and its reciprocal (the first kernel's
+// arithmetic: Delta rounded to fp16 before use; an infinite 1 / Delta gives 0).
+__device__ __forceinline__ uint32_t static_step4(float clip, float& delta, float& inv) {
+  const uint32_t bits = f32_to_f16(clip / 7.0f);
+  delta = f16_to_f32(bits);
+  inv = 1.0f / delta;
+  if (__builtin_isinf(inv)) inv = 0.0f;
+  return bits;
+}
+
+// Four outputs y (fp32, one row, consecutive columns) of the up projection ->
+// bf16 -> GELU -> bf16 -> the next layer's STATIC 4-bit quantizer (t = ((g *
+// D^-1) * gain) * (1 / Delta) clamped to [-7, 7], rounded to even).  Returns
+// per element the bits of t + 1.5 * 2^23 (the low nibble is the two's
+// complement code) and in neg the sign bit of t (the fp8 form's sign: a code
+// 0 of negative t is -0).
+__device__ __forceinline__ void gelu_codes4_a4(const float (&y)[4], const float (&dinv)[4], float gain, float inv,
+                                               uint32_t (&bits)[4], uint32_t (&neg)[4]) {
+  float v[4] = {y[0], y[1], y[2], y[3]};
+  bf16_round2(v[0], v[1]);
+  bf16_round2(v[2], v[3]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = gelu_f32(v[j]);
+  bf16_round2(v[0], v[1]);
+  bf16_round2(v[2], v[3]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float t = ((v[j] * dinv[j]) * gain) * inv;
+    t = __builtin_fminf(__builtin_fmaxf(t, -7.0f), 7.0f);
+    bits[j] = __float_as_uint(t + 12582912.0f);
+    neg[j] = __float_as_uint(t) >> 31;
+  }
+}
+
+// The fp8 form of a code (e4m3 byte of code * 2^-9: sign and magnitude) and
+// the code's value, from gelu_codes4_a4's bits and sign: |code| = rne(|t|) =
+// |rne(t)|, the rounding being symmetric.
+__device__ __forceinline__ uint32_t fp8_code_byte(uint32_t bits, uint32_t neg, int& code) {
+  const int c = static_cast<int>(static_cast<int8_t>(static_cast<uint8_t>(bits & 0xFFu)));
+  const uint32_t mag = static_cast<uint32_t>(c < 0 ? -c : c);
+  code = c;
+  return mag | (neg << 7);
+}
+
 }  // namespace
 }  // namespace sq

@@ -442,14 +442,20 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM, BN>::WGS_PER_CU)) void gemm
   }
   // GELU epilogue: the next layer's gain of the lane's row, its 1 / Delta,
   // and the D^-1 of the four columns each lane holds after the transpose;
-  // the first strip's first wave writes the next layer's row scales
+  // 8-bit: the first strip's first wave writes the next layer's row scales
   float gain = 0.0f, ninv = 0.0f, ndinv[TN][4];
+  uint32_t nstep16 = 0;  // 4-bit: the next layer's fp16 step
   if constexpr (kGelu) {
     const NextQuant& q = a.nq;
     gain = q.gamma[q.step * q.S + q.tok2stream[m0 + min(lane, rows - 1)]];
-    const float ndelta = q.clip[q.step] / 127.0f;
-    ninv = 1.0f / ndelta;
-    if (__builtin_isinf(ninv)) ninv = 0.0f;
+    float ndelta;
+    if constexpr (ABITS == 8) {
+      ndelta = q.clip[q.step] / 127.0f;
+      ninv = 1.0f / ndelta;
+      if (__builtin_isinf(ninv)) ninv = 0.0f;
+    } else {
+      nstep16 = static_step4(q.clip[q.step], ndelta, ninv);
+    }
 #pragma unroll
     for (int tn = 0; tn < TN; ++tn) {
       const float4 d = q.dinv != nullptr ? *reinterpret_cast<const float4*>(q.dinv + n0 + 32 * tn + (lane & 28))
@@ -459,7 +465,9 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM, BN>::WGS_PER_CU)) void gemm
       ndinv[tn][2] = d.z;
       ndinv[tn][3] = d.w;
     }
-    if (n0 == 0 && g == 0 && lane < rows) q.r[m0 + lane] = ndelta / gain;
+    if constexpr (ABITS == 8) {
+      if (n0 == 0 && g == 0 && lane < rows) q.r[m0 + lane] = ndelta / gain;
+    }
   }
   const int rf_bits = __float_as_int(rowf);
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
@@ -477,6 +485,28 @@ __global__ __launch_bounds__(256, (Sk<ABITS, QX, BM, BN>::WGS_PER_CU)) void gemm
     const int n = n0 + 32 * tn + (lane & 28);
     float grow = 0.0f;
     if constexpr (kGelu) grow = __int_as_float(__builtin_amdgcn_ds_bpermute(row * 4, __float_as_int(gain)));
+    if constexpr (kGelu && ABITS == 4) {
+      // packed 4-bit codes: in a run of eight, codes 0-3 (this lane when
+      // n % 8 == 0) fill the low nibbles of four bytes and codes 4-7 (lane ^ 4)
+      // the high ones; one fp16 step per row and 64-group
+      uint32_t bits[4], neg[4];
+      gelu_codes4_a4(o, ndinv[tn], grow, ninv, bits, neg);
+      uint32_t nib = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) nib |= (bits[j] & 0xFu) << (4 * j);
+      const uint32_t other = static_cast<uint32_t>(__shfl_xor(static_cast<int>(nib), 4, 64));
+      if (row < rows) {
+        const size_t m = static_cast<size_t>(m0 + row);
+        if ((lane & 4) == 0) {
+          uint32_t w = 0;
+#pragma unroll
+          for (int j = 0; j < 4; ++j) w |= (((nib >> (4 * j)) & 0xFu) | (((other >> (4 * j)) & 0xFu) << 4)) << (8 * j);
+          *reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(a.out) + m * (N / 2) + n / 2) = w;
+        }
+        if ((n & 63) == 0) static_cast<uint16_t*>(a.nq.scale)[m * (N / 64) + n / 64] = static_cast<uint16_t>(nstep16);
+      }
+      continue;
+    }
     if (row < rows) {
       const size_t m = static_cast<size_t>(m0 + row);
       if constexpr (kGelu) {
@@ -539,7 +569,29 @@ __global__ __launch_bounds__(256) void gemm_skinny_tail_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(y[j], rowf, bias[j]);
   }
-  if constexpr (EPI == kEpiGelu) {  // the next layer's codes (and, from the first column, its row scale)
+  if constexpr (EPI == kEpiGelu && ABITS == 4) {  // packed codes (pairs of threads fill bytes) and fp16 steps
+    const NextQuant& q = a.nq;
+    float ndelta, ninv;
+    const uint32_t nstep16 = static_step4(q.clip[q.step], ndelta, ninv);
+    const float gain = q.gamma[q.step * q.S + q.tok2stream[m]];
+    const float4 d4 = q.dinv != nullptr ? *reinterpret_cast<const float4*>(q.dinv + n) : make_float4(1.0f, 1.0f, 1.0f, 1.0f);
+    const float dv[4] = {d4.x, d4.y, d4.z, d4.w};
+    uint32_t bits[4], neg[4];
+    gelu_codes4_a4(y, dv, gain, ninv, bits, neg);
+    uint32_t nib = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) nib |= (bits[j] & 0xFu) << (4 * j);
+    // the thread with the run's codes 4-7 is the next one (n + 4: lane ^ 1), on the same row
+    const uint32_t other = static_cast<uint32_t>(__shfl_xor(static_cast<int>(nib), 1, 64));
+    if ((n & 7) == 0) {
+      uint32_t w = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) w |= (((nib >> (4 * j)) & 0xFu) | (((other >> (4 * j)) & 0xFu) << 4)) << (8 * j);
+      *reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(a.out) + static_cast<size_t>(m) * (a.N / 2) + n / 2) = w;
+    }
+    if ((n & 63) == 0) static_cast<uint16_t*>(q.scale)[static_cast<size_t>(m) * (a.N / 64) + n / 64] =
+        static_cast<uint16_t>(nstep16);
+  } else if constexpr (EPI == kEpiGelu) {  // the next layer's codes (and, from the first column, its row scale)
     const NextQuant& q = a.nq;
     const float ndelta = q.clip[q.step] / 127.0f;
     float ninv = 1.0f / ndelta;
@@ -684,6 +736,7 @@ hipError_t launch_skinny(int act_bits, int epi, const GemmArgs& a, hipStream_t s
     switch (epi) {
       case kEpiOut: return launch_t<4, kEpiOut, false>(a, s, partial, partial_bytes);
       case kEpiPartial: return launch_t<4, kEpiPartial, false>(a, s, partial, partial_bytes);
+      case kEpiGelu: return launch_t<4, kEpiGelu, false>(a, s, partial, partial_bytes);
     }
   }
   return hipErrorInvalidValue;

@@ -197,7 +197,7 @@ struct EpiInputs {
   static constexpr bool kGelu = EPI == kEpiGelu;
   float rowf;
   float bias[TN];
-  float gain, inv;
+  float gain, inv, delta;  // the next layer's gain of the row, 1 / Delta and (4-bit) Delta
   float dinv[kGelu ? TN : 1][4];
   __device__ __forceinline__ void load(const GemmArgs& a, int m0, int n0, int wm, int wn, int lane) {
     const int m = min(m0 + wm * 64 + lane, a.M - 1);
@@ -217,8 +217,12 @@ struct EpiInputs {
     if constexpr (kGelu) {
       const NextQuant& q = a.nq;
       gain = q.gamma[q.step * q.S + q.tok2stream[m]];
-      inv = 1.0f / (q.clip[q.step] / 127.0f);
-      if (__builtin_isinf(inv)) inv = 0.0f;
+      if constexpr (ABITS == 8) {
+        inv = 1.0f / (q.clip[q.step] / 127.0f);
+        if (__builtin_isinf(inv)) inv = 0.0f;
+      } else {
+        static_step4(q.clip[q.step], delta, inv);
+      }
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int n = min(n0 + wn * 64 + tn * 32 + (lane & 28), a.N - 4);
@@ -252,9 +256,55 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN]
   const bool f32out = EPI == kEpiPartial || a.out_dtype == SQ_OUT_F32;
   const int rf_bits = __float_as_int(in.rowf);
   const int half = (lane >> 5) * 16;  // lanes 32..63 hold rows 4 further down
-  if constexpr (EPI == kEpiGelu) {  // the next layer's row scales, from the waves of the first column tile
+  if constexpr (EPI == kEpiGelu && ABITS == 8) {  // the next layer's row scales, from the waves of the first column tile
     const int m = m0 + wm * 64 + lane;
     if (n0 + wn * 64 == 0 && m < M) a.nq.r[m] = (a.nq.clip[a.nq.step] / 127.0f) / in.gain;
+  }
+  if constexpr (EPI == kEpiGelu && ABITS == 4) {
+    // the next layer's 4-bit codes as fp8 bytes, and per (row, 64-group) the
+    // step sigma (fp32) and kc = -8 S sigma 2^-18 (S: the group's code sum);
+    // the wave's 64 columns are one group, a row's codes sit in the lanes that
+    // differ in bits 2-4 (both 32-wide tiles)
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      float rowf[16];
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        rowf[r] = __int_as_float(__builtin_amdgcn_ds_bpermute(half + (tm * 32 + (r >> 2) * 8 + (r & 3)) * 4, rf_bits));
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int m = m0 + wm * 64 + tm * 32 + g * 8 + (lane >> 5) * 4 + (lane & 3);
+        const float gain = __int_as_float(__builtin_amdgcn_ds_bpermute(
+            (tm * 32 + g * 8 + (lane >> 5) * 4 + (lane & 3)) * 4, __float_as_int(in.gain)));
+        int csum = 0;
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          float v[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) v[q] = __builtin_fmaf(y[tm][tn][g * 4 + q], rowf[g * 4 + q], in.bias[tn]);
+          quad_transpose(v, lane);
+          uint32_t bits[4], neg[4], w = 0;
+          gelu_codes4_a4(v, in.dinv[tn], gain, in.inv, bits, neg);
+#pragma unroll
+          for (int j = 0; j < 4; ++j) {
+            int code;
+            w |= fp8_code_byte(bits[j], neg[j], code) << (8 * j);
+            csum += code;
+          }
+          const int n = n0 + wn * 64 + tn * 32 + (lane & 28);
+          if (m < M) *reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(a.out) + static_cast<size_t>(m) * N + n) = w;
+        }
+        csum += __shfl_xor(csum, 4, 64);
+        csum += __shfl_xor(csum, 8, 64);
+        csum += __shfl_xor(csum, 16, 64);
+        if (m < M && (lane & 28) == 0) {
+          const size_t gi = static_cast<size_t>(m) * (N / 64) + (n0 + wn * 64) / 64;
+          static_cast<float*>(a.nq.scale)[gi] = in.delta;
+          a.nq.kc[gi] = (static_cast<float>(-8 * csum) * in.delta) * 3.814697265625e-06f;  // * 2^-18
+        }
+      }
+    }
+    return;
   }
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
@@ -280,7 +330,7 @@ __device__ __forceinline__ void store_tile(const GemmArgs& a, float (&y)[TM][TN]
           gain = __int_as_float(__builtin_amdgcn_ds_bpermute(
               (tm * 32 + g * 8 + (lane >> 5) * 4 + (lane & 3)) * 4, __float_as_int(in.gain)));
         if (m < M) {
-          if constexpr (EPI == kEpiGelu) {
+          if constexpr (EPI == kEpiGelu && ABITS == 8) {
             *reinterpret_cast<uint32_t*>(static_cast<int8_t*>(a.out) + static_cast<size_t>(m) * N + n) =
                 gelu_codes4(v, in.dinv[tn], gain, in.inv);
           } else if (f32out) {
@@ -1217,7 +1267,7 @@ __global__ __launch_bounds__(256, 2) void gemm_a4f8_kernel(GemmArgs a) {
   using LY = F8Layout;
   constexpr int BM = LY::BM, BN = LY::BN;
   constexpr uint32_t RING = LY::STAGES * LY::STAGE;
-  static_assert(EPI == kEpiOut || EPI == kEpiPartial, "the pipelined path applies the weight steps");
+  static_assert(EPI == kEpiOut || EPI == kEpiPartial || EPI == kEpiGelu, "the pipelined path applies the weight steps");
   static_assert(2 * RING <= 160 * 1024, "two workgroups per CU");
 
   __shared__ __align__(1024) uint8_t smem[RING];
@@ -1525,6 +1575,42 @@ __global__ __launch_bounds__(256) void gemm_tail_kernel(GemmArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) y[j] = __builtin_fmaf(y[j], rowf, bias[j]);
   }
+  if constexpr (EPI == kEpiGelu && ABITS == 4) {
+    // fp8 code bytes; the 16 threads of a row's 64-group (lanes that differ in
+    // bits 0-3) add their code sums, and the first writes sigma and kc
+    const NextQuant& q = a.nq;
+    const float gain = q.gamma[q.step * q.S + q.tok2stream[m]];
+    float delta, inv;
+    static_step4(q.clip[q.step], delta, inv);
+    float d[4] = {1.0f, 1.0f, 1.0f, 1.0f};
+    if (q.dinv != nullptr) {
+      const float4 dv = *reinterpret_cast<const float4*>(q.dinv + n);
+      d[0] = dv.x;
+      d[1] = dv.y;
+      d[2] = dv.z;
+      d[3] = dv.w;
+    }
+    uint32_t bits[4], neg[4], w = 0;
+    gelu_codes4_a4(y, d, gain, inv, bits, neg);
+    int csum = 0;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      int code;
+      w |= fp8_code_byte(bits[j], neg[j], code) << (8 * j);
+      csum += code;
+    }
+    *reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(a.out) + static_cast<size_t>(m) * a.N + n) = w;
+    csum += __shfl_xor(csum, 1, 64);
+    csum += __shfl_xor(csum, 2, 64);
+    csum += __shfl_xor(csum, 4, 64);
+    csum += __shfl_xor(csum, 8, 64);
+    if ((n & 63) == 0) {
+      const size_t gi = static_cast<size_t>(m) * (a.N / 64) + n / 64;
+      static_cast<float*>(q.scale)[gi] = delta;
+      q.kc[gi] = (static_cast<float>(-8 * csum) * delta) * 3.814697265625e-06f;  // * 2^-18
+    }
+    return;
+  }
   if constexpr (EPI == kEpiGelu) {
     const NextQuant& q = a.nq;
     const float gain = q.gamma[q.step * q.S + q.tok2stream[m]];
@@ -1697,6 +1783,11 @@ hipError_t launch_gemm_gelu_quant(const GemmArgs& a, hipStream_t s, float* parti
   if (a.w_group == a.K) return launch_t<8, kEpiGelu, true, true>(a, s, partial, partial_bytes);  // one step per channel
   if (a.w_group != KT) return hipErrorInvalidValue;
   return launch_t<8, kEpiGelu, true>(a, s, partial, partial_bytes);
+}
+
+hipError_t launch_gemm_gelu_quant4(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes) {
+  if (skinny_applies(4, a.M, a.K, a.w_group)) return launch_skinny(4, kEpiGelu, a, s, partial, partial_bytes);
+  return launch_a4f8<kEpiGelu>(a, s, partial, partial_bytes);
 }
 
 hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, float* partial,

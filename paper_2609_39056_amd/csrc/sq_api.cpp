@@ -457,6 +457,62 @@ sq_status sq_linear_w4a8_gelu_quant(const uint16_t* x, int32_t M, const sq_act_p
   return hip_status(launch_gemm_gelu_quant(g, stream, f.partial, f.partial_bytes));
 }
 
+sq_status sq_linear_w4a4_gelu_quant(const uint16_t* x, int32_t M, const sq_act_params* act, const sq_weight* w,
+                                    const sq_act_params* act_next, void* qx_next, void* scale_next, float* kc_next,
+                                    void* workspace, size_t ws_bytes, hipStream_t stream) {
+  if (x == nullptr || qx_next == nullptr || scale_next == nullptr || workspace == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  st = check_act(act, w->K);
+  if (st != SQ_OK) return st;
+  st = check_act(act_next, w->N);  // the next layer's input channels are this layer's outputs
+  if (st != SQ_OK) return st;
+  if (act->act_bits != 4 || act_next->act_bits != 4 || act_next->range_mode != SQ_RANGE_STATIC)
+    return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  // more than 128 tokens: the fp8 tiled GEMM, and the next layer's codes in its form
+  const bool f8 = a4_fp8_path(M, w->K, w->w_group);
+  if (f8 && kc_next == nullptr) return SQ_ERR_NULL;
+  if (!aligned(x, 16) || !aligned(workspace, 16) || !aligned(qx_next, 4) || !aligned(scale_next, f8 ? 4 : 2) ||
+      (f8 && !aligned(kc_next, 4)))
+    return SQ_ERR_ALIGN;
+  if (ws_bytes < fused_ws_bytes(M, w->K, w->N, 4)) return SQ_ERR_WORKSPACE;
+  FusedWs f = fused_ws(workspace, ws_bytes, M, w->K, 4, f8);
+  st = quantize(x, M, w->K, act, f.qx, f.scale, stream, f.kc);
+  if (st != SQ_OK) return st;
+  GemmArgs g = gemm_args(f.qx, f.scale, M, act, w, qx_next, SQ_OUT_BF16);
+  g.kc = f.kc;
+  g.nq.tok2stream = act_next->tok2stream;
+  g.nq.gamma = act_next->gamma;
+  g.nq.dinv = act_next->dinv;
+  g.nq.clip = act_next->clip;
+  g.nq.S = act_next->num_streams;
+  g.nq.step = act_next->step;
+  g.nq.r = nullptr;
+  g.nq.scale = scale_next;
+  g.nq.kc = f8 ? kc_next : nullptr;
+  return hip_status(launch_gemm_gelu_quant4(g, stream, f.partial, f.partial_bytes));
+}
+
+sq_status sq_gemm_w4a4_fp8(const uint8_t* qx, const float* group_scale, const float* kc, int32_t M,
+                           const sq_act_params* act, const sq_weight* w, void* y, int32_t out_dtype, void* workspace,
+                           size_t ws_bytes, hipStream_t stream) {
+  if (qx == nullptr || group_scale == nullptr || kc == nullptr || y == nullptr) return SQ_ERR_NULL;
+  sq_status st = check_weight(w);
+  if (st != SQ_OK) return st;
+  st = check_act(act, w->K);
+  if (st != SQ_OK) return st;
+  if (act->act_bits != 4) return SQ_ERR_UNSUPPORTED;
+  if (!valid_m(M)) return SQ_ERR_SHAPE;
+  if (!a4_fp8_path(M, w->K, w->w_group)) return SQ_ERR_UNSUPPORTED;  // few tokens: packed codes, sq_gemm_w4a4
+  if (!valid_out(out_dtype)) return SQ_ERR_UNSUPPORTED;
+  if (!aligned(qx, 16) || !aligned(y, 16) || !aligned(group_scale, 4) || !aligned(kc, 4)) return SQ_ERR_ALIGN;
+  if (workspace != nullptr && !aligned(workspace, 16)) return SQ_ERR_ALIGN;
+  GemmArgs g = gemm_args(qx, group_scale, M, act, w, y, out_dtype);
+  g.kc = kc;
+  return hip_status(launch_gemm(4, kEpiOut, g, stream, static_cast<float*>(workspace), workspace ? ws_bytes : 0));
+}
+
 sq_status sq_gelu_bf16(const uint16_t* x, size_t n, uint16_t* y, hipStream_t stream) {
   if (n > 0 && (x == nullptr || y == nullptr)) return SQ_ERR_NULL;
   if (!aligned(x, 16) || !aligned(y, 16)) return SQ_ERR_ALIGN;

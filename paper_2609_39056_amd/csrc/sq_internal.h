@@ -79,19 +79,27 @@ enum EpiMode : int {
   kEpiPartial = 1,  // fp32 sum_b fp32(C^b) * s_b * Delta_W (no row factor / bias)
   kEpiInt32 = 2,    // int32 C (one block spanning K)
   kEpiDump = 3,     // int32 C^b of every block to acc_out[b][i][j]
-  kEpiGelu = 4,     // row factor, bias, bf16, GELU, bf16, the next layer's STATIC 8-bit codes to out
+  kEpiGelu = 4,     // row factor, bias, bf16, GELU, bf16, the next layer's STATIC codes to out
 };
 
-// The next linear's STATIC 8-bit quantizer, applied by the kEpiGelu epilogue
-// to GELU of this GEMM's bf16 output: codes int8 [M][N] go to GemmArgs::out,
-// the row scales r = Delta / gamma_s(i) to `r`.
+// The next linear's STATIC quantizer, applied by the kEpiGelu epilogue to
+// GELU of this GEMM's bf16 output (codes to GemmArgs::out).  8-bit
+// activations (this GEMM's and the next layer's): codes int8 [M][N], the row
+// scales r = Delta / gamma_s(i) to `r`.  4-bit activations (both): Delta =
+// fp16(clip / 7), and the codes in the form the next layer's GEMM takes:
+// packed int4 [M][N/2] with fp16 steps [M][N/64] in `scale` (the
+// weight-streaming GEMM, at most kSkinnyMaxM rows), or fp8 code bytes
+// [M][N] with fp32 steps and kc = -8 S sigma 2^-18 per (row, 64-group) in
+// `scale` and `kc` (the fp8 tiled GEMM).
 struct NextQuant {
   const int32_t* tok2stream;
   const float* gamma;  // [num_steps][S]
   const float* dinv;   // D^-1 [N] or NULL
-  const float* clip;   // [num_steps]: Delta = clip[step] / 127
+  const float* clip;   // [num_steps]: Delta = clip[step] / 127 (8-bit) or fp16(clip[step] / 7) (4-bit)
   int32_t S, step;
-  float* r;            // [M]
+  float* r;            // [M] (8-bit)
+  void* scale;         // 4-bit: fp16 [M][N/64] (packed codes) or fp32 [M][N/64] (fp8 code bytes)
+  float* kc;           // 4-bit fp8 code bytes: [M][N/64]
 };
 
 struct GemmArgs {
@@ -173,6 +181,11 @@ hipError_t launch_gemm(int act_bits, int epi, const GemmArgs& a, hipStream_t s, 
 // pipelined kernel with 128-wide weight groups (more than kSkinnyMaxM rows),
 // or the weight-streaming one (128-wide groups or one step per channel).
 hipError_t launch_gemm_gelu_quant(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes);
+// The same for 4-bit activations (this GEMM's and the next layer's): the
+// weight-streaming GEMM on packed codes (at most kSkinnyMaxM rows; next
+// layer's codes packed, fp16 steps) or the fp8 tiled GEMM (a.kc set; next
+// layer's codes as fp8 bytes, fp32 steps and kc).
+hipError_t launch_gemm_gelu_quant4(const GemmArgs& a, hipStream_t s, float* partial, size_t partial_bytes);
 // GELU of n bf16 values to bf16 (the fp32 sequence of gelu.h).
 hipError_t launch_gelu_bf16(const uint16_t* x, size_t n, uint16_t* y, hipStream_t s);
 

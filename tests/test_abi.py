@@ -331,6 +331,63 @@ def test_gelu_quant_rejects(L):
     assert gq(nbytes=1024) == WS
 
 
+def test_gelu_quant4_rejects(L):
+    """The W4A4 up projection with the GELU epilogue: 4-bit activations for
+    this layer and the next (STATIC), kc required for more than 128 tokens
+    (the fp8 form), alignments, the workspace size."""
+    big = 1 << 30
+
+    def gq(x=A, M=300, a=None, w=None, an=None, qn=A, sn=A, kn=A, ws=A, nbytes=big):
+        a = act(act_bits=4) if a is None else a
+        w = wt() if w is None else w
+        an = act(range_mode=1, act_bits=4) if an is None else an
+        return L.sq_linear_w4a4_gelu_quant(x, M, ctypes.byref(a), ctypes.byref(w), ctypes.byref(an), qn, sn, kn, ws,
+                                           nbytes, None)
+
+    assert gq(x=None) == NULL
+    assert gq(qn=None) == NULL
+    assert gq(sn=None) == NULL
+    assert gq(ws=None) == NULL
+    assert gq(kn=None) == NULL                              # more than 128 tokens: the fp8 form needs kc
+    assert gq(an=act(act_bits=4)) == UNSUP                  # next layer DYNAMIC
+    assert gq(an=act(range_mode=1, act_bits=8)) == UNSUP
+    assert gq(a=act(act_bits=8)) == UNSUP
+    assert gq(an=act(range_mode=1, act_bits=4, clip=None)) == NULL
+    assert gq(M=0) == SHAPE
+    assert gq(w=wt(N=192)) == SHAPE                         # next layer's K must be a multiple of 128
+    assert gq(x=A + 2) == ALIGN
+    assert gq(qn=A + 2) == ALIGN
+    assert gq(sn=A + 2) == ALIGN                            # fp32 steps
+    assert gq(kn=A + 2) == ALIGN
+    assert gq(M=100, kn=None, sn=A + 1) == ALIGN            # at most 128 tokens: fp16 steps, kc unused
+    assert gq(ws=A + 8) == ALIGN
+    assert gq(an=act(range_mode=1, act_bits=4, dinv=A + 4)) == ALIGN
+    assert gq(nbytes=1024) == WS
+
+
+def test_gemm_w4a4_fp8_rejects(L):
+    """The 4-bit GEMM on fp8 code bytes: more than 128 tokens only (the packed
+    form is sq_gemm_w4a4's), 4-bit activations, alignments."""
+    def g8(qx=A, sg=A, kc=A, M=300, a=None, w=None, y=A, out=1, ws=None, nbytes=0):
+        a = act(act_bits=4) if a is None else a
+        w = wt() if w is None else w
+        return L.sq_gemm_w4a4_fp8(qx, sg, kc, M, ctypes.byref(a), ctypes.byref(w), y, out, ws, nbytes, None)
+
+    assert g8(qx=None) == NULL
+    assert g8(sg=None) == NULL
+    assert g8(kc=None) == NULL
+    assert g8(y=None) == NULL
+    assert g8(M=100) == UNSUP                               # few tokens: packed codes, sq_gemm_w4a4
+    assert g8(a=act(act_bits=8)) == UNSUP
+    assert g8(out=3) == UNSUP
+    assert g8(M=0) == SHAPE
+    assert g8(qx=A + 8) == ALIGN
+    assert g8(sg=A + 2) == ALIGN
+    assert g8(kc=A + 2) == ALIGN
+    assert g8(y=A + 8) == ALIGN
+    assert g8(ws=A + 8, nbytes=1 << 20) == ALIGN
+
+
 def test_gelu_bf16_rejects(L):
     assert L.sq_gelu_bf16(None, 8, A, None) == NULL
     assert L.sq_gelu_bf16(A, 8, None, None) == NULL

@@ -26,7 +26,7 @@ import numpy as np
 import pytest
 import torch
 
-from gpu_util import act_params, bits16, f32_to_dev, i32_to_dev, oracle_weight, u16_to_dev
+from gpu_util import act_params, bits16, expected_kc, f32_to_dev, i32_to_dev, oracle_weight, u16_to_dev
 from oracle import sq_oracle as O
 from paper_2609_39056_amd import binding as B
 from paper_2609_39056_amd import synth
@@ -230,3 +230,159 @@ def test_gelu_quant_chain_exact(M, K, N):
     _, qx_u, r_u = run_unfused(x, act, W, act_next, M, N)
     assert torch.equal(qn, qx_u.view(torch.int8))
     assert torch.equal(rn.view(torch.int32), r_u.view(torch.int32))
+
+
+# ---------------------------------------------------------------- 4-bit activations (the W4A4 chain)
+def run_fused4(x, act, W, act_next, M, N):
+    """The W4A4 up projection with the GELU epilogue.  At most 128 tokens the
+    down projection's codes come packed with fp16 steps; above, as fp8 code
+    bytes with fp32 steps and kc."""
+    ws = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, W.K, N, 4)
+    if M <= 128:
+        qn = torch.full((M, N // 2), 0x99, dtype=torch.uint8, device="cuda")
+        sn = torch.full((M, N // 64), float("nan"), dtype=torch.float16, device="cuda")
+        kn = None
+    else:
+        qn = torch.full((M, N), 0x55, dtype=torch.uint8, device="cuda")
+        sn = torch.full((M, N // 64), float("nan"), dtype=torch.float32, device="cuda")
+        kn = torch.full((M, N // 64), float("nan"), dtype=torch.float32, device="cuda")
+    B.sq_linear_w4a4_gelu_quant(x, act, W, act_next, qn, sn, kn, ws)
+    return qn, sn, kn
+
+
+def run_unfused4(x, act, W, act_next, M, N):
+    """sq_linear_w4a4 into bf16, sq_gelu_bf16, the down projection's first
+    kernel (packed 4-bit codes, fp16 steps)."""
+    ws = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, W.K, N, 4)
+    h = torch.empty((M, N), dtype=torch.bfloat16, device="cuda")
+    B.sq_linear_w4a4(x, act, W, h, B.SQ_OUT_BF16, ws)
+    g = torch.empty_like(h)
+    B.sq_gelu_bf16(h, g)
+    qx, sc = B.act_buffers(M, N, 4)
+    B.sq_quantize_act(g, act_next, qx, sc)
+    return h, qx, sc
+
+
+def fp8_codes(b):
+    """Codes from fp8 code bytes (sign and magnitude)."""
+    b = b.astype(np.int64)
+    return np.where(b & 0x80, -(b & 0x7F), b & 0x7F)
+
+
+def check_chain4(qn, sn, kn, qx_u, sc_u, M, N):
+    """The fused 4-bit chain against the unfused GPU chain, every element:
+    packed form bit for bit; fp8 form the same codes, the fp16 steps widened,
+    kc = -8 S sigma 2^-18 from the codes.  Returns the codes [M, N]."""
+    codes_u = O.unpack_int4(qx_u.cpu().numpy())
+    if M <= 128:
+        assert torch.equal(qn, qx_u), "fused packed codes differ from the unfused chain"
+        assert torch.equal(sn.view(torch.int16), sc_u.view(torch.int16)), "fused steps differ"
+        return codes_u.astype(np.int64)
+    codes = fp8_codes(qn.cpu().numpy())
+    assert np.array_equal(codes, codes_u.astype(np.int64)), "fused fp8 codes differ from the unfused chain"
+    sig_bits = bits16(sc_u)
+    assert np.array_equal(sn.cpu().numpy(), sig_bits.view(np.float16).astype(np.float32)), "fused steps differ"
+    assert np.array_equal(kn.cpu().numpy(), expected_kc(codes, sig_bits)), "kc differs"
+    return codes
+
+
+def chain_case4(counts, K, N, G):
+    L = synth.make_layer(K=K, N=N, stream_counts=counts, T=T, seed=[34, K, N], permute=True)
+    M = L.M
+    pw, W = oracle_weight(L, G)
+    rows = tile_rows(M, seed=[35, M]) if M > 600 else np.arange(M)
+    x = u16_to_dev(L.x_bits, torch.bfloat16)
+    t2s_dev = i32_to_dev(L.tok2stream)
+    step = 6
+    for up_mode in (B.SQ_RANGE_DYNAMIC, B.SQ_RANGE_STATIC):
+        act = act_params(L, step, 4, up_mode)
+        res = O.linear(L.x_bits[rows], L.tok2stream[rows], L.gamma, step, pw["codes"], pw["w_scale"], G,
+                       dinv=L.dinv, clip=L.clip, bias_bits=L.bias_bits, range_mode=up_mode, act_bits=4)
+        h_or = O.f32_to_bf16_bits(res["y"])
+        g_or = O.gelu_bf16(h_or)
+        for use_dinv in (True, False):
+            dp = DownParams(N, L.S, seed=[K, N, up_mode, use_dinv, 4], g_or=g_or, use_dinv=use_dinv)
+            act_next = B.ActParams(tok2stream=t2s_dev, gamma=f32_to_dev(dp.gamma), step=step, act_bits=4,
+                                   range_mode=B.SQ_RANGE_STATIC, clip=f32_to_dev(dp.clip),
+                                   dinv=f32_to_dev(dp.dinv) if dp.dinv is not None else None)
+            _, _, qa = O.mlp_chain_codes(res["y"], L.tok2stream[rows], dp.gamma, step, dp.dinv, dp.clip, act_bits=4)
+            assert np.abs(qa["codes"].astype(np.int64)).max() >= 6, "threshold leaves the code range unused"
+            qn, sn, kn = run_fused4(x, act, W, act_next, M, N)
+            h_dev, qx_u, sc_u = run_unfused4(x, act, W, act_next, M, N)
+            codes = check_chain4(qn, sn, kn, qx_u, sc_u, M, N)
+            # against the oracle: steps exact; codes equal wherever the bf16 up
+            # output agrees, elsewhere within one code step
+            assert np.array_equal(bits16(sc_u)[rows], qa["scale"])
+            got = codes[rows]
+            want = qa["codes"].astype(np.int64)
+            same_h = bits16(h_dev)[rows] == h_or
+            assert np.array_equal(got[same_h], want[same_h]), "codes differ where the bf16 up output agrees"
+            assert np.abs(got - want)[~same_h].max(initial=0) <= 1
+            assert (~same_h).mean() < 0.01
+            del qn, sn, kn, h_dev, qx_u, sc_u
+
+
+CHAIN4 = [  # name, stream counts, K, N
+    ("64 action tokens 2048x8192 packed codes", (0, 0, 64), 2048, 8192),
+    ("128 tokens 2048x8192 packed codes", (0, 64, 64), 2048, 8192),
+    ("64 tokens 8192x2048 split along K, packed codes", (0, 0, 64), 8192, 2048),
+    ("300x2048x1024 fp8 codes, tiles split along K", (200, 40, 60), 2048, 1024),
+    ("2B up 4192x2048x8192 fp8 codes", synth.TOKENS_2B, 2048, 8192),
+]
+
+
+@pytest.mark.parametrize("name,counts,K,N", CHAIN4, ids=[c[0] for c in CHAIN4])
+def test_gelu_quant_chain_4bit(name, counts, K, N):
+    chain_case4(counts, K, N, 128)
+
+
+@pytest.mark.parametrize("M,K,N", [(300, 2048, 1024), (64, 2048, 8192), (1000, 384, 640)])
+def test_gelu_quant_chain_4bit_exact(M, K, N):
+    """Integer 4-bit activations and power-of-two steps: the up projection's
+    fp32 output is exact on both sides, so the chain's codes and steps equal
+    the oracle's on every checked row (packed form at 64 tokens, fp8 form
+    above 128)."""
+    E = ExactLayer(M, K, N, 128, 4, seed=[44], w_exp=(-9, -6))
+    x, act, W = E.device()
+    rows = tile_rows(M, seed=[45, M])
+    y = E.oracle(rows)["y"]
+    assert np.mean(np.abs(y) < 4) > 0.2, "outputs miss GELU's curved range"
+    dp = DownParams(N, 3, seed=[46, M], clip=np.linspace(2.0, 9.0, T))
+    act_next = B.ActParams(tok2stream=act.tok2stream, gamma=f32_to_dev(dp.gamma), step=E.step, act_bits=4,
+                           range_mode=B.SQ_RANGE_STATIC, clip=f32_to_dev(dp.clip), dinv=f32_to_dev(dp.dinv))
+    _, _, qa = O.mlp_chain_codes(y, E.t2s[rows], dp.gamma, E.step, dp.dinv, dp.clip, act_bits=4)
+    qn, sn, kn = run_fused4(x, act, W, act_next, M, N)
+    _, qx_u, sc_u = run_unfused4(x, act, W, act_next, M, N)
+    codes = check_chain4(qn, sn, kn, qx_u, sc_u, M, N)
+    assert np.array_equal(codes[rows], qa["codes"].astype(np.int64))
+    assert np.array_equal(bits16(sc_u)[rows], qa["scale"])
+
+
+@pytest.mark.parametrize("M,K,N", [(300, 1024, 512), (4192, 8192, 2048)])
+def test_gemm_w4a4_fp8_equals_packed(M, K, N):
+    """The down projection's GEMM on the chain's fp8 form (sq_gemm_w4a4_fp8)
+    equals sq_gemm_w4a4 on the same codes in the packed form, bit for bit
+    (fp32 and bf16 outputs), with K split over idle workgroups where the
+    tiles leave them (a workspace) and without."""
+    rng = np.random.default_rng([47, M, K, N])
+    counts = (M - M // 5, M // 10, M - (M - M // 5) - M // 10)
+    L = synth.make_layer(K=K, N=N, stream_counts=counts, T=T, seed=[48, M], permute=True)
+    _, W = oracle_weight(L, 128)
+    codes = rng.integers(-7, 8, (M, K)).astype(np.int8)
+    sig_bits = O.f32_to_f16_bits(rng.lognormal(-3.0, 0.5, (M, K // 64)).astype(np.float32))
+    act = act_params(L, 2, 4, B.SQ_RANGE_DYNAMIC)
+    packed = torch.from_numpy(O.pack_int4(codes)).cuda()
+    sig16 = torch.from_numpy(sig_bits.view(np.int16)).view(torch.float16).cuda()
+    f8 = np.where(codes < 0, 0x80 | (-codes.astype(np.int16)), codes.astype(np.int16)).astype(np.uint8)
+    qf8 = torch.from_numpy(f8).cuda()
+    sig32 = torch.from_numpy(sig_bits.view(np.float16).astype(np.float32)).cuda()
+    kc = torch.from_numpy(expected_kc(codes.astype(np.int64), sig_bits)).cuda()
+    for out, dt in ((B.SQ_OUT_F32, torch.float32), (B.SQ_OUT_BF16, torch.bfloat16)):
+        for with_ws in (False, True):
+            ws = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, K, N, 4) if with_ws else None
+            y0 = torch.full((M, N), float("nan"), dtype=dt, device="cuda")
+            y1 = torch.full((M, N), float("nan"), dtype=dt, device="cuda")
+            B.sq_gemm_w4a4(packed, sig16, act, W, y0, out, workspace=ws)
+            B.sq_gemm_w4a4_fp8(qf8, sig32, kc, act, W, y1, out, workspace=ws)
+            assert torch.equal(y0.view(torch.int16 if dt == torch.bfloat16 else torch.int32),
+                               y1.view(torch.int16 if dt == torch.bfloat16 else torch.int32)), (out, with_ws)

@@ -143,7 +143,8 @@ def test_graph_calibration_replays_match_eager(bits):
 def test_graph_chain_single_kernel_and_noalloc_replay():
     """The MLP chain with the producer-side fusion (up projection with the GELU
     epilogue, then the down projection's GEMM on its codes; and at 64 tokens,
-    where the weight-streaming GEMM splits K), the bf16 GELU,
+    where the weight-streaming GEMM splits K; and with 4-bit activations, fp8
+    and packed code forms), the bf16 GELU,
     the STATIC single-kernel linear (with and without a K split) and the
     allocation-free linear, captured as one HIP graph: every replay equals the
     eager calls bit for bit, with eager calls on other inputs in between."""
@@ -172,6 +173,17 @@ def test_graph_chain_single_kernel_and_noalloc_replay():
     as_ = [static_act(L, 1) for L in (Ls1, Ls2)]
     asg = [act_params(L, 1, 8, 0) for L in (Ls1, Ls2)]  # few-token chain: dynamic up projection
     asd = [static_act(Lsd, 1, asg[0].tok2stream), static_act(Lsd, 2, asg[1].tok2stream)]
+    # the 4-bit chains: 300 tokens (fp8 code bytes) and 64 tokens with K split (packed codes)
+
+    def static4(L, step, t2s):
+        a = act_params(L, step, 4, B.SQ_RANGE_STATIC)
+        a.tok2stream = t2s
+        return a
+
+    au4 = [act_params(L, 1, 4, 0) for L in (Lu1, Lu2)]
+    ad4 = [static4(Ld, 1, au4[0].tok2stream), static4(Ld, 2, au4[1].tok2stream)]
+    as4 = [act_params(L, 1, 4, 0) for L in (Ls1, Ls2)]
+    asd4 = [static4(Lsd, 1, as4[0].tok2stream), static4(Lsd, 2, as4[1].tok2stream)]
     ws_u = B.alloc_workspace(B.SQ_VARIANT_FUSED, Mu, K, N, 8)
     ws_d = B.alloc_workspace(B.SQ_VARIANT_GEMM, Mu, N, N2, 8)
     ws_s = B.alloc_workspace(B.SQ_VARIANT_GEMM, Ms, Ks, Ns, 8)
@@ -185,6 +197,13 @@ def test_graph_chain_single_kernel_and_noalloc_replay():
     ws_sg = B.alloc_workspace(B.SQ_VARIANT_FUSED, Ms, Ks, Ns, 8)
     qs = torch.empty((Ms, Ns), dtype=torch.int8, device="cuda")
     rs = torch.empty((Ms,), dtype=torch.float32, device="cuda")
+    ws_u4 = B.alloc_workspace(B.SQ_VARIANT_FUSED, Mu, K, N, 4)
+    q8f = torch.empty((Mu, N), dtype=torch.uint8, device="cuda")
+    s8f = torch.empty((Mu, N // 64), dtype=torch.float32, device="cuda")
+    k8f = torch.empty((Mu, N // 64), dtype=torch.float32, device="cuda")
+    ws_s4 = B.alloc_workspace(B.SQ_VARIANT_FUSED, Ms, Ks, Ns, 4)
+    q4p = torch.empty((Ms, Ns // 2), dtype=torch.uint8, device="cuda")
+    s4p = torch.empty((Ms, Ns // 64), dtype=torch.float16, device="cuda")
 
     def call(i):
         B.sq_linear_w4a8_gelu_quant(xu[i], au[i], Wu, ad[i], qn, rn, ws_u)
@@ -194,8 +213,10 @@ def test_graph_chain_single_kernel_and_noalloc_replay():
         B.sq_linear_w4a8_static1(xs[i], as_[i], Ws, ys2, B.SQ_OUT_BF16, workspace=ws_s)
         B.sq_linear_w4a8_noalloc(xu[i], au[i], Wu, yn, B.SQ_OUT_BF16)
         B.sq_linear_w4a8_gelu_quant(xs[i], asg[i], Ws, asd[i], qs, rs, ws_sg)  # few tokens, K split
+        B.sq_linear_w4a4_gelu_quant(xu[i], au4[i], Wu, ad4[i], q8f, s8f, k8f, ws_u4)
+        B.sq_linear_w4a4_gelu_quant(xs[i], as4[i], Ws, asd4[i], q4p, s4p, None, ws_s4)
 
-    outs = (qn, rn, yd, g_out, ys1, ys2, yn, qs, rs)
+    outs = (qn, rn, yd, g_out, ys1, ys2, yn, qs, rs, q8f, k8f, q4p)
 
     def snap():
         return [t.clone() for t in outs]

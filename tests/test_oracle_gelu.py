@@ -82,3 +82,23 @@ def test_mlp_chain_identity_case():
     _, _, qa2 = O.mlp_chain_codes(y, t2s, gamma, 1, None, clip)
     assert np.array_equal(qa2["codes"][1].astype(np.int64), np.minimum(2 * want, 127))
     assert qa2["scale"][1] == np.float32(0.5)
+
+
+def test_mlp_chain_identity_case_4bit():
+    """The same with the 4-bit quantizer: c = 7 (Delta = fp16(1) = 1), unit
+    gains, D = I: integer up outputs 6 and 7 come back as their own codes,
+    larger ones clip to 7, h <= -10 gives code 0; every group step is fp16 1.
+    A gain of 0.5 halves the codes (rounding to even)."""
+    h = np.concatenate([np.arange(6, 70), -np.arange(10, 74)]).astype(np.float32)  # 128 = two 64-groups
+    y = np.tile(h, (3, 1))
+    t2s = np.array([0, 1, 2], np.int32)
+    gamma = np.ones((2, 3), np.float32)
+    clip = np.full(2, 7.0, np.float32)
+    _, _, qa = O.mlp_chain_codes(y, t2s, gamma, 1, None, clip, act_bits=4)
+    want = np.where(h > 0, np.minimum(h, 7), 0).astype(np.int64)
+    assert np.array_equal(qa["codes"].astype(np.int64), np.tile(want, (3, 1)))
+    assert np.array_equal(qa["scale"], np.full((3, 2), 0x3C00, np.uint16))
+    gamma[1, 2] = 0.5
+    _, _, qa2 = O.mlp_chain_codes(y, t2s, gamma, 1, None, clip, act_bits=4)
+    half = np.where(h > 0, np.minimum(np.rint(h * 0.5), 7), 0).astype(np.int64)
+    assert np.array_equal(qa2["codes"][2].astype(np.int64), half)
