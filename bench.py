@@ -635,34 +635,54 @@ def hbm_copy_figure(torch, dev, stream):
     return {"bytes": 2 * (COPY_MIB << 20), "us": round(us, 1), "gbs": round(2 * (COPY_MIB << 20) / (us * 1e-6) / 1e9, 1)}
 
 
-def mlp_chain_figures(torch, B, dev, up, down, reps=20):
+def mlp_chain_figures(torch, B, dev, up, down, reps=20, bits=8):
     """The MLP's direct chain, up projection -> GELU -> down projection, with
     the down projection's STATIC quantizer (its per-step thresholds):
-    unfused as three calls (sq_linear_w4a8 to bf16, sq_gelu_bf16,
-    sq_linear_w4a8 of the down projection) against the producer-side fusion
-    (sq_linear_w4a8_gelu_quant writing the down projection's codes and row
-    scales, then sq_gemm_w4a8).  us per chain and per call, graph-replayed;
-    the same tokens feed both projections."""
+    unfused as three calls (the fused linear to bf16, sq_gelu_bf16, the fused
+    linear of the down projection) against the producer-side fusion (the
+    linear with the GELU epilogue writing the down projection's codes and
+    steps, then the down projection's GEMM on them).  bits 8: W4A8
+    (sq_linear_w4a8_gelu_quant, sq_gemm_w4a8); bits 4: W4A4
+    (sq_linear_w4a4_gelu_quant, then sq_gemm_w4a4 on packed codes up to 128
+    tokens, sq_gemm_w4a4_fp8 on fp8 code bytes above).  us per chain and per
+    call, graph-replayed; the same tokens feed both projections."""
     M, N, K2 = up["M"], up["N"], down["N"]
-    ua, da = up["acts"][8], down["acts"][8]
+    ua, da = up["acts"][bits], down["acts"][bits]
     ua.step = 1
-    clip = torch.full((T_STEPS,), 4.0, dtype=torch.float32, device=dev)
-    dact = B.ActParams(tok2stream=ua.tok2stream, gamma=da.gamma, step=1, act_bits=8, range_mode=B.SQ_RANGE_STATIC,
-                       clip=clip, dinv=da.dinv)
+    clip = torch.full((T_STEPS,), 4.0 if bits == 8 else 3.0, dtype=torch.float32, device=dev)
+    dact = B.ActParams(tok2stream=ua.tok2stream, gamma=da.gamma, step=1, act_bits=bits,
+                       range_mode=B.SQ_RANGE_STATIC, clip=clip, dinv=da.dinv)
     h = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
     g = torch.empty_like(h)
     yd = torch.empty((M, K2), dtype=torch.bfloat16, device=dev)
-    ws_up = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, up["K"], N, 8, dev)
-    ws_dn = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, N, K2, 8, dev)
-    ws_g = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, N, K2, 8, dev)
-    qn, rn = B.act_buffers(M, N, 8, dev)
+    ws_up = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, up["K"], N, bits, dev)
+    ws_dn = B.alloc_workspace(B.SQ_VARIANT_FUSED, M, N, K2, bits, dev)
+    ws_g = B.alloc_workspace(B.SQ_VARIANT_GEMM, M, N, K2, bits, dev)
+    kn = None
+    if bits == 8 or M <= 128:
+        qn, sn = B.act_buffers(M, N, bits, dev)
+    else:
+        qn = torch.empty((M, N), dtype=torch.uint8, device=dev)
+        sn = torch.empty((M, N // B.A4_GROUP), dtype=torch.float32, device=dev)
+        kn = torch.empty_like(sn)
     BF = B.SQ_OUT_BF16
+    if bits == 8:
+        linear = B.sq_linear_w4a8
+        gelu_quant = lambda: B.sq_linear_w4a8_gelu_quant(up["x"], ua, up["W"], dact, qn, sn, ws_up)
+        down_gemm = lambda: B.sq_gemm_w4a8(qn, sn, down["W"], yd, BF, workspace=ws_g)
+    else:
+        linear = B.sq_linear_w4a4
+        gelu_quant = lambda: B.sq_linear_w4a4_gelu_quant(up["x"], ua, up["W"], dact, qn, sn, kn, ws_up)
+        if kn is None:
+            down_gemm = lambda: B.sq_gemm_w4a4(qn, sn, dact, down["W"], yd, BF, workspace=ws_g)
+        else:
+            down_gemm = lambda: B.sq_gemm_w4a4_fp8(qn, sn, kn, dact, down["W"], yd, BF, workspace=ws_g)
     calls = {
-        "up_linear_bf16": lambda: B.sq_linear_w4a8(up["x"], ua, up["W"], h, BF, ws_up),
+        "up_linear_bf16": lambda: linear(up["x"], ua, up["W"], h, BF, ws_up),
         "gelu_bf16": lambda: B.sq_gelu_bf16(h, g),
-        "down_linear_static": lambda: B.sq_linear_w4a8(g, dact, down["W"], yd, BF, ws_dn),
-        "up_linear_gelu_quant": lambda: B.sq_linear_w4a8_gelu_quant(up["x"], ua, up["W"], dact, qn, rn, ws_up),
-        "down_gemm": lambda: B.sq_gemm_w4a8(qn, rn, down["W"], yd, BF, workspace=ws_g),
+        "down_linear_static": lambda: linear(g, dact, down["W"], yd, BF, ws_dn),
+        "up_linear_gelu_quant": gelu_quant,
+        "down_gemm": down_gemm,
     }
     per = {k: round(graph_us(torch, f, reps), 2) for k, f in calls.items()}
 
@@ -677,8 +697,8 @@ def mlp_chain_figures(torch, B, dev, up, down, reps=20):
     us_u = graph_us(torch, unfused, reps)
     us_f = graph_us(torch, fused, reps)
     ops = 2.0 * M * up["K"] * N + 2.0 * M * N * K2
-    del h, g, yd, ws_up, ws_dn, ws_g, qn, rn
-    return {"M": M, "up": [up["K"], N], "down": [N, K2], "per_call_us": per,
+    del h, g, yd, ws_up, ws_dn, ws_g, qn, sn, kn
+    return {"M": M, "act_bits": bits, "up": [up["K"], N], "down": [N, K2], "per_call_us": per,
             "unfused_us": round(us_u, 2), "fused_us": round(us_f, 2), "fused_speedup": round(us_u / us_f, 3),
             "fused_tops": round(ops / (us_f * 1e-6) / 1e12, 1), "unfused_tops": round(ops / (us_u * 1e-6) / 1e12, 1)}
 
@@ -920,6 +940,7 @@ def main():
         chain14 = mlp_chain_figures(torch, B, dev, blk[2], blk[3])
         chain14_pc = mlp_chain_figures(torch, B, dev, {**blk[2], "W": blk[2]["W_pc"]},
                                        {**blk[3], "W": blk[3]["W_pc"]})
+        chain14_a4 = mlp_chain_figures(torch, B, dev, blk[2], blk[3], bits=4)
         for ly in blk:
             del ly["W_pc"], ly["ws_gemm"], ly["qx8"], ly["r8"]
         torch.cuda.empty_cache()
@@ -931,6 +952,7 @@ def main():
         ms_mlp8 = timed_steps(lambda t: fused_step(mlp, t), args.steps, args.warmup)
         ms_mlp4 = timed_steps(lambda t: fused_step(mlp, t, bits=4), args.steps, 2)
         chain2 = mlp_chain_figures(torch, B, dev, mlp[0], mlp[1])
+        chain2_a4 = mlp_chain_figures(torch, B, dev, mlp[0], mlp[1], bits=4)
         b4 = device_block(torch, B, synth, dev, synth.LINEARS_2B, synth.TOKENS_2B, seed=6000, batch=4)
         buffers(b4)
         ms_b4 = {bits: timed_steps(lambda t, b=bits: fused_step(b4, t, bits=b), max(10, args.steps // 2), 3)
@@ -942,11 +964,12 @@ def main():
         single = static_single_kernel_figures(torch, B, synth, dev)
         # ---- the MLP chain at few tokens (the weight-streaming GEMM with the GELU epilogue)
         chain_few = {}
-        for tag, lins, M in (("2B_M64", synth.LINEARS_2B, 64), ("2B_M128", synth.LINEARS_2B, 128),
-                             ("14B_M64", synth.LINEARS_14B, 64)):
-            pair = device_block(torch, B, synth, dev, {"up": lins["up"], "down": lins["down"]}, (0, 0, M),
+        for tag, lins, Mf in (("2B_M64", synth.LINEARS_2B, 64), ("2B_M128", synth.LINEARS_2B, 128),
+                              ("14B_M64", synth.LINEARS_14B, 64)):
+            pair = device_block(torch, B, synth, dev, {"up": lins["up"], "down": lins["down"]}, (0, 0, Mf),
                                 seed=7100)
             chain_few[tag] = mlp_chain_figures(torch, B, dev, pair[0], pair[1], reps=50)
+            chain_few[tag + "_A4"] = mlp_chain_figures(torch, B, dev, pair[0], pair[1], reps=50, bits=4)
             del pair
         torch.cuda.empty_cache()
 
@@ -1037,7 +1060,8 @@ def main():
                              "w4a4": {"ms_per_step": round(ms_mlp4, 5),
                                       "tops": round(mlp_ops / (ms_mlp4 * 1e-3) / 1e12, 2)}},
             "mlp_chain_gelu_fusion": {"14B_M8384": chain14, "14B_M8384_per_channel_steps": chain14_pc,
-                                      "2B_M4192": chain2, **chain_few},
+                                      "14B_M8384_A4": chain14_a4, "2B_M4192": chain2, "2B_M4192_A4": chain2_a4,
+                                      **chain_few},
             "block_2B_batch4_M16768": {"workload": "2B-class block qkv/out/up/down, batch 4: M=16768",
                                        **{f"w4a{b}": {"ms_per_step": round(ms_b4[b], 5),
                                                       "tops": round(b4_ops / (ms_b4[b] * 1e-3) / 1e12, 2)}
