@@ -807,7 +807,10 @@ struct P16 {
   static constexpr int BM = 128, BN = 128;
   static constexpr int DIST = 2, STAGES = 3, WGS_PER_CU = 2;
   // one stage in LDS: A codes, packed weights, then each wave's 256-byte
-  // area of weight-step pairs (the Layout<8, false> arrangement)
+  // area of weight-step pairs (the Layout<8, false> arrangement, except that
+  // weight column n holds chunk c at position c ^ ((n >> 1) & 3): the 16
+  // columns of a fragment read then fill all 64 banks; with (n >> 2) & 3 the
+  // read took twice as long in an LDS probe, and the kernel gained 0.5 %)
   static constexpr int A_BYTES = BM * KT, B_BYTES = BN * KT / 2, W_BYTES = NWAVE * 256;
   static constexpr int STAGE = A_BYTES + B_BYTES + W_BYTES;
   static constexpr int A_DMA = A_BYTES / 1024 / NWAVE, B_DMA = B_BYTES / 1024 / NWAVE;
@@ -832,7 +835,7 @@ struct StageLoads16 {
 #pragma unroll
     for (int i = 0; i < P16::B_DMA; ++i) {
       const int col = 16 * (P16::B_DMA * wave + i) + (lane >> 2);
-      const int c = (lane & 3) ^ ((col >> 2) & 3);
+      const int c = (lane & 3) ^ ((col >> 1) & 3);
       voffB[i] = static_cast<uint32_t>(min(n0 + col, N - 1) - n0) * static_cast<uint32_t>(K / 2) + c * 16;
     }
     // N is even, so the pair is clamped inside the row
@@ -862,9 +865,9 @@ struct FragOffsets16 {
     const int bcol0 = wn * P16_WCOLS + (lane & 15);
 #pragma unroll
     for (int s = 0; s < 2; ++s) a0[s] = arow0 * KT + 16 * ((2 * g + s) ^ ((arow0 >> 1) & 7));
-    b0 = LY::A_BYTES + bcol0 * (KT / 2) + 16 * (g ^ ((bcol0 >> 2) & 3));
+    b0 = LY::A_BYTES + bcol0 * (KT / 2) + 16 * (g ^ ((bcol0 >> 1) & 3));
   }
-  // a 16-row step keeps the swizzle term ((row >> 1) & 7 and (col >> 2) & 3)
+  // a 16-row step keeps the swizzle term ((row >> 1) & 7 and (col >> 1) & 3)
   __device__ __forceinline__ int a(int tm, int s) const { return a0[s] + tm * 16 * KT; }
   __device__ __forceinline__ int b(int tn) const { return b0 + tn * 16 * (KT / 2); }
 };
