@@ -651,6 +651,7 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
             bfull[tn][2 * k2] = unpack_frag(pb.x, pb.y);
             bfull[tn][2 * k2 + 1] = unpack_frag(pb.z, pb.w);
           }
+        __builtin_amdgcn_s_setprio(1);  // the MFMA phase first at the arbiter (+2 %)
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm) {
           v4i af[4];
@@ -662,6 +663,7 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
             for (int ks = 0; ks < 4; ++ks)
               acc[tm][tn] = __builtin_amdgcn_mfma_i32_32x32x32_i8(af[ks], bfull[tn][ks], acc[tm][tn], 0, 0, 0);
         }
+        __builtin_amdgcn_s_setprio(0);
         wait_vm_and_barrier<AHEAD>();
         c_slot = next_slot(c_slot);
       }
@@ -1108,6 +1110,11 @@ __global__ __launch_bounds__(P16::NTHREADS, P16::WGS_PER_CU) void gemm_pipe16_ke
           bq[tn][0] = unpack_frag(pb.x, pb.y);
           bq[tn][1] = unpack_frag(pb.z, pb.w);
         }
+        // the MFMA phase at a raised wave priority: when both waves of a SIMD
+        // can issue, the one feeding the matrix cores goes first and the
+        // other's widening and folds fill the gaps (measured +8 % on the 14B
+        // block against equal priorities)
+        __builtin_amdgcn_s_setprio(1);
 #pragma unroll
         for (int tm = 0; tm < TM16; ++tm) {
           const v4i a0 = *reinterpret_cast<const v4i*>(st + off.a(tm, 0));
@@ -1126,6 +1133,7 @@ __global__ __launch_bounds__(P16::NTHREADS, P16::WGS_PER_CU) void gemm_pipe16_ke
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
           __builtin_amdgcn_sched_group_barrier(0x002, 5, 0);  // up to five VALU
         }
+        __builtin_amdgcn_s_setprio(0);
 #pragma unroll
         for (int tn = 0; tn < TN16; ++tn) wsv_prev[tn] = wsv[tn];
         wait_vm_and_barrier<AHEAD>();
@@ -1373,6 +1381,7 @@ __global__ __launch_bounds__(256, 2) void gemm_a4f8_kernel(GemmArgs a) {
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn)
           bf[tn] = unpack_offset_frag(*reinterpret_cast<const uint4*>(st + boff[hb] + tn * 32 * (KT / 2)));
+        __builtin_amdgcn_s_setprio(1);  // the MFMA phase first at the arbiter (+1 %)
 #pragma unroll
         for (int tm = 0; tm < TM; ++tm) {
           const uint4 a0 = *reinterpret_cast<const uint4*>(st + aoff[hb][0] + tm * 32 * KT);
@@ -1391,6 +1400,7 @@ __global__ __launch_bounds__(256, 2) void gemm_a4f8_kernel(GemmArgs a) {
             acc[tm][tn] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(af, bf[tn], (v16f)(0.0f), 0, 0, 0, 0, 0, 0);
         }
       }
+      __builtin_amdgcn_s_setprio(0);
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) wsv_prev[tn] = wsv[tn];
       wait_vm_and_barrier<0>();
