@@ -798,8 +798,9 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
 // Waves: P16_NWM across a tile's 128 rows and P16_NWN across its 128
 // columns, each computing P16_WROWS x P16_WCOLS outputs as TM16 x TN16 tiles
 // of 16 x 16.  Measured alternatives to 2 x 2 waves of 64 x 64: 2 x 4 waves of
-// 64 x 32 (121 VGPRs, four waves per SIMD) the same speed, 1 x 4 waves of
-// 128 x 32 (each weight fragment widened once per workgroup) 1-2 % slower.
+// 64 x 32 (four waves per SIMD) the same speed without the raised-priority
+// MFMA phase below and 1 % slower with it, 1 x 4 waves of 128 x 32 (each
+// weight fragment widened once per workgroup) 1-2 % slower.
 constexpr int P16_NWM = 2, P16_NWN = 2;
 constexpr int TM16 = 8 / P16_NWM, TN16 = 8 / P16_NWN;
 constexpr int P16_WROWS = 16 * TM16, P16_WCOLS = 16 * TN16;
