@@ -1024,7 +1024,7 @@ def main():
         },
         "roofline": {
             "bound": "mfma",
-            "kernel": "sq_gemm_w4a8: gemm_pipe16_kernel<0> (+ gemm_tail_kernel<8,0,false> where tiles split)",
+            "kernel": "sq_gemm_w4a8: gemm_pipe16_kernel<0, false> (+ gemm_tail_kernel<8,0,false> where tiles split)",
             "per": "the four GEMM calls of one step (qkv, out, up, down)",
             "launches": int(args.steps * len(blk)),
             "achieved": round(gemm_tops, 1), "peak": PEAK_INT8_TOPS, "unit": "TOPS",

@@ -784,9 +784,12 @@ __global__ __launch_bounds__(kPipeWide ? 512 : 256, kPipeWide ? 1 : 2) void gemm
 // loop with random int8 operands and the per-block fold this instruction
 // sustains about 1.5x the rate of the 32 x 32 x 32 one under the board's power
 // limit; in the GEMM it gains 0-5 % (2B up about equal, 2B and 14B down 2-5 %
-// faster).  With one weight step per channel (no fold) the 32 x 32 kernel
-// stays, which was as fast or faster there, and so it does for the fp32
-// partial sums of the unfused path, whose 16 x 16 stores cover half a line.
+// faster).  With one weight step per channel (PC: no fold, int32 sums over
+// all of K, converted once with the column's step) it was as fast as the
+// 32 x 32 kernel before the raised-priority MFMA phase and is 2 % faster with
+// it on the 14B block (equal on the 2B layers); the 32 x 32 kernel stays for
+// the fp32 partial sums of the unfused path, whose 16 x 16 stores cover half
+// a line.
 //
 // Lane (row or column lane & 15, g = lane >> 4) feeds k-step s (0, 1) of a
 // stage with the channels [32 g + 16 s, +16): for 8-bit activations the
@@ -845,6 +848,7 @@ struct StageLoads16 {
     wcol2 = static_cast<uint32_t>(min(n0 + wn * P16_WCOLS + 2 * (lane & (P16_WCOLS / 2 - 1)), N - 2));
   }
 
+  template <bool PC = false>
   __device__ __forceinline__ void issue(const GemmArgs& a, int m0, int n0, int kt, uint32_t st, int wave) const {
     const int K = a.K;
     const uint8_t* bA = static_cast<const uint8_t*>(a.qx) + static_cast<size_t>(m0) * K + kt * KT;
@@ -853,8 +857,10 @@ struct StageLoads16 {
     for (int i = 0; i < P16::A_DMA; ++i) dma<16>(bA, voffA[i], st + (P16::A_DMA * wave + i) * 1024);
 #pragma unroll
     for (int i = 0; i < P16::B_DMA; ++i) dma<16>(bB, voffB[i], st + P16::A_BYTES + (P16::B_DMA * wave + i) * 1024);
-    const uint32_t e = static_cast<uint32_t>(kt) * static_cast<uint32_t>(a.N) + wcol2;
-    dma<4>(a.w_scale, e * 2, st + P16::A_BYTES + P16::B_BYTES + wave * 256);
+    if constexpr (!PC) {  // one step per channel: read once, in the epilogue
+      const uint32_t e = static_cast<uint32_t>(kt) * static_cast<uint32_t>(a.N) + wcol2;
+      dma<4>(a.w_scale, e * 2, st + P16::A_BYTES + P16::B_BYTES + wave * 256);
+    }
   }
 };
 
@@ -1014,14 +1020,14 @@ __device__ __forceinline__ void write_partial16(const GemmArgs& a, const float (
       }
 }
 
-template <int EPI>
+template <int EPI, bool PC>
 __global__ __launch_bounds__(P16::NTHREADS, P16::WGS_PER_CU) void gemm_pipe16_kernel(GemmArgs a) {
   using LY = P16;
   using CF = P16;
   static_assert(EPI == kEpiOut || EPI == kEpiPartial || EPI == kEpiGelu,
                 "the pipelined path applies the weight steps");
   constexpr int BM = CF::BM, BN = CF::BN;
-  constexpr int NDMA = LY::A_DMA + LY::B_DMA + 1;
+  constexpr int NDMA = LY::A_DMA + LY::B_DMA + (PC ? 0 : 1);
   constexpr int AHEAD = (CF::DIST - 1) * NDMA;
   constexpr uint32_t RING = CF::STAGES * LY::STAGE;
 
@@ -1047,7 +1053,7 @@ __global__ __launch_bounds__(P16::NTHREADS, P16::WGS_PER_CU) void gemm_pipe16_ke
   StageLoads16 ld;
   ld.set(d.m0, d.n0, M, N, K, wave, wn, lane);
   auto issue = [&]() {
-    ld.issue(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
+    ld.template issue<PC>(a, d.m0, d.n0, d_kt, smem_lds + d_slot, wave);
     d_slot = d_slot + LY::STAGE == RING ? 0 : d_slot + LY::STAGE;
   };
   // past the last stage of the last item the same stage is loaded again (in
@@ -1089,7 +1095,49 @@ __global__ __launch_bounds__(P16::NTHREADS, P16::WGS_PER_CU) void gemm_pipe16_ke
     EpiInputs16<EPI> ein;
     ein.load(a, c.m0, c.n0, wm, wn, lane);
     float y[TM16][TN16][4];
-    {
+    if constexpr (PC) {
+      // int32 sums over all of K (|16 C| < 2^31 for K <= 2^17), converted once
+#pragma unroll
+      for (int tm = 0; tm < TM16; ++tm)
+#pragma unroll
+        for (int tn = 0; tn < TN16; ++tn) acc[tm][tn] = (v4i)(0);
+      for (int kt = c.kt0; kt < c.kt1; ++kt) {
+        issue();
+        advance();
+        const uint8_t* st = smem + c_slot;
+        v4i bq[TN16][2];
+#pragma unroll
+        for (int tn = 0; tn < TN16; ++tn) {
+          const uint4 pb = *reinterpret_cast<const uint4*>(st + off.b(tn));
+          bq[tn][0] = unpack_frag(pb.x, pb.y);
+          bq[tn][1] = unpack_frag(pb.z, pb.w);
+        }
+        __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+        for (int tm = 0; tm < TM16; ++tm) {
+          const v4i a0 = *reinterpret_cast<const v4i*>(st + off.a(tm, 0));
+          const v4i a1 = *reinterpret_cast<const v4i*>(st + off.a(tm, 1));
+#pragma unroll
+          for (int tn = 0; tn < TN16; ++tn) {
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a0, bq[tn][0], acc[tm][tn], 0, 0, 0);
+            acc[tm][tn] = __builtin_amdgcn_mfma_i32_16x16x64_i8(a1, bq[tn][1], acc[tm][tn], 0, 0, 0);
+          }
+        }
+        __builtin_amdgcn_s_setprio(0);
+        wait_vm_and_barrier<AHEAD>();
+        c_slot = next_slot(c_slot);
+      }
+#pragma unroll
+      for (int tn = 0; tn < TN16; ++tn) {
+        const int n = min(c.n0 + wn * P16_WCOLS + tn * 16 + (lane & 15), N - 1);
+        const float wpc = f16_to_f32(a.w_scale[n]) * 0.0625f;  // widened codes: factor 16
+#pragma unroll
+        for (int tm = 0; tm < TM16; ++tm)
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            y[tm][tn][j] = c.unit >= 0 ? __int_as_float(acc[tm][tn][j]) : static_cast<float>(acc[tm][tn][j]) * wpc;
+      }
+    } else {
       float wsv_prev[TN16], wsv[TN16];
 #pragma unroll
       for (int tm = 0; tm < TM16; ++tm)
@@ -1712,8 +1760,8 @@ hipError_t launch_t(const GemmArgs& a0, hipStream_t s, float* partial, size_t pa
     const int rest = p.ntiles - p.ndp;
     const int nitems = p.ndp + rest * p.split;
     const unsigned grid = static_cast<unsigned>(std::min(nitems, slots));
-    if constexpr (ABITS == 8 && !PC && (EPI == kEpiOut || EPI == kEpiGelu) && kPipe16) {
-      hipLaunchKernelGGL((gemm_pipe16_kernel<EPI>), dim3(grid), dim3(P16::NTHREADS), 0, s, a);
+    if constexpr (ABITS == 8 && (EPI == kEpiOut || EPI == kEpiGelu) && kPipe16) {
+      hipLaunchKernelGGL((gemm_pipe16_kernel<EPI, PC>), dim3(grid), dim3(P16::NTHREADS), 0, s, a);
     } else
       hipLaunchKernelGGL((gemm_pipe_kernel<ABITS, EPI, PC>), dim3(grid), dim3(CF::NTHREADS), 0, s, a);
     hipError_t e = hipGetLastError();
