@@ -1287,9 +1287,9 @@ __device__ __forceinline__ v8i unpack_offset_frag(const uint4& p) {
   v8i r;
 #pragma unroll
   for (int d = 0; d < 4; ++d) {
-    const uint32_t q = w[d] ^ 0x88888888u;  // each nibble: code + 8 (mod 16)
-    r[2 * d] = static_cast<int>(q & 0x0F0F0F0Fu);
-    r[2 * d + 1] = static_cast<int>((q >> 4) & 0x0F0F0F0Fu);
+    // each nibble XOR 8 = code + 8 (mod 16); (x & m) ^ c is one three-input op
+    r[2 * d] = static_cast<int>((w[d] & 0x0F0F0F0Fu) ^ 0x08080808u);
+    r[2 * d + 1] = static_cast<int>(((w[d] >> 4) & 0x0F0F0F0Fu) ^ 0x08080808u);
   }
   return r;
 }
