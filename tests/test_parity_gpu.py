@@ -265,7 +265,7 @@ def test_few_tokens(bits, M, K, N, out, per_channel):
 
 
 @pytest.mark.parametrize("M,K,N", [(4192, 1024, 2048), (300, 2048, 384), (1000, 8192, 256), (64, 2048, 512),
-                                   (129, 256, 128)])
+                                   (129, 256, 128), (200, 512, 64)])
 @pytest.mark.parametrize("out", [F32, BF16])
 def test_per_channel_weights(M, K, N, out):
     """One weight step per output channel (G = K, the paper's weight format)
