@@ -394,3 +394,33 @@ def test_gelu_bf16_rejects(L):
     assert L.sq_gelu_bf16(A + 2, 8, A, None) == ALIGN
     assert L.sq_gelu_bf16(A, 8, A + 2, None) == ALIGN
     assert L.sq_gelu_bf16(None, 0, None, None) == OK        # nothing to do: no launch
+
+
+def test_header_is_c_and_links(L, tmp_path):
+    """include/sq.h compiles as C11 (-Wall -Werror) and a C program links
+    libsq.so and calls two host-only entry points: the boundary is usable
+    from C, not only through the Python binding."""
+    import shutil
+    import subprocess
+
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no C compiler")
+    src = tmp_path / "use_sq.c"
+    src.write_text(
+        "#include <stdio.h>\n#include \"sq.h\"\n"
+        "int main(void) {\n"
+        "  size_t b = sq_workspace_bytes(SQ_VARIANT_FUSED, 300, 2048, 1024, 8);\n"
+        "  printf(\"%s %zu\\n\", sq_status_string(SQ_ERR_SHAPE), b);\n"
+        "  return b > 0 ? 0 : 1;\n}\n")
+    libdir = os.path.dirname(B.LIB_PATH)
+    exe = tmp_path / "use_sq"
+    r = subprocess.run([cc, "-std=c11", "-Wall", "-Werror", "-D__HIP_PLATFORM_AMD__", f"-I{ROOT}/include",
+                        "-I/opt/rocm/include", str(src), f"-L{libdir}", "-lsq", f"-Wl,-rpath,{libdir}",
+                        "-o", str(exe)], capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([str(exe)], capture_output=True, text=True, timeout=60)
+    assert r.returncode == 0, r.stderr
+    msg, nbytes = r.stdout.rsplit(" ", 1)
+    assert msg == B.status_string(SHAPE)
+    assert int(nbytes) == B.sq_workspace_bytes(B.SQ_VARIANT_FUSED, 300, 2048, 1024, 8)
