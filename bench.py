@@ -976,6 +976,23 @@ def main():
         # ---- the calibration path of Eq. (9) on the 2B up projection
         calib = calibration_figures(torch, B, mlp[0], stream, dev, None if args.no_cpu else 256)
 
+        # ---- the 4-bit path's matrix-core rate (sq_probe_mfma_f8f6: the fp8 W4A4
+        # GEMM's instruction on fp8 and on fp6 operands, with and without its
+        # two-fma fold per output and block)
+        sink6 = B.probe_sink(dev)
+        n_wg6 = sink6.numel() // 256
+        f8f6 = {}
+        for fmt, fname in ((8, "fp8"), (6, "fp6")):
+            for label, fold in (("random_operands", 0), ("random_operands_with_fold", 1)):
+                B.sq_probe_mfma_f8f6(fmt, 200, True, fold, sink6, stream)
+                q0, q1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                q0.record(stream)
+                B.sq_probe_mfma_f8f6(fmt, 10000, True, fold, sink6, stream)
+                q1.record(stream)
+                torch.cuda.synchronize()
+                f8f6[f"{fname}_{label}"] = round(n_wg6 * 4 * 10000 * 2.0 ** 20 / (q0.elapsed_time(q1) * 1e-3) / 1e12, 1)
+        del sink6
+
     # ---- the int8 matrix-core rate this GPU sustains (sq_probe_mfma_i8: back
     # to back MFMAs on register operands at the GEMM's occupancy) in both MFMA
     # forms: zero operands, random operands, and random operands with the
@@ -1035,6 +1052,7 @@ def main():
             "frac_of_measured_ceiling": round(gemm_tops / ceil_gemm, 4),
         },
         "mfma_i8_ceiling_tops": ceiling,
+        **({} if args.headline_only else {"mfma_f8f6_ceiling_tops": f8f6}),
         "per_layer": per_layer,
         "quant_kernel_gbs": round(sum(k1_bytes) / (k1.sum() * 1e-3) / 1e9, 1),
         "w4a8_as_k1_k2_calls": {"ms_per_step": round(ms_split, 5),

@@ -464,6 +464,18 @@ size_t sq_probe_mfma_i8_sink_bytes(void);
 sq_status sq_probe_mfma_i8(int32_t shape, int32_t iters, int32_t random_operands, int32_t fold, int32_t* sink,
                            size_t sink_bytes, hipStream_t stream);
 
+/* Measurement hook for the 4-bit path's matrix-core instruction,
+ * v_mfma_scale_f32_32x32x64_f8f6f4, with fp8 e4m3 (format 8) or fp6 e2m3
+ * (format 6) operands: the same grid as sq_probe_mfma_i8, each wave issuing
+ * iters * 8 MFMAs on register operands (2^20 operations per iteration: the
+ * eight MFMAs of one 128-channel stage of the fp8 W4A4 GEMM).  With fold != 0
+ * every block's fp32 sum is also folded by two fmas per output, as that GEMM
+ * does.  Operands all zero or pseudo-random (fp8 bytes without NaN codes).
+ * sink: int32 scratch of sq_probe_mfma_i8_sink_bytes() bytes; iters in
+ * [1, 2^24]; another format returns SQ_ERR_UNSUPPORTED. */
+sq_status sq_probe_mfma_f8f6(int32_t format, int32_t iters, int32_t random_operands, int32_t fold, int32_t* sink,
+                             size_t sink_bytes, hipStream_t stream);
+
 /* Test hook: writes every int32 block accumulator of Q_X Q_W instead of an
  * epilogue: acc_out[b][i][j] = sum over K-block b of q_ik * w_jk, with blocks
  * of w_group (8-bit) or 64 (4-bit).  It runs the library's non-pipelined GEMM

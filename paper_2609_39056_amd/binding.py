@@ -113,6 +113,7 @@ _SIGS = {
                              ctypes.POINTER(sq_calib_search_params), _P, _P, _P, _P, _S, _P]),
     "sq_probe_mfma_i8_sink_bytes": (_S, []),
     "sq_probe_mfma_i8": (_I, [_I, _I, _I, _I, _P, _S, _P]),
+    "sq_probe_mfma_f8f6": (_I, [_I, _I, _I, _I, _P, _S, _P]),
 }
 
 _lib = None
@@ -450,6 +451,15 @@ def sq_probe_mfma_i8(iters: int, random_operands: bool, fold: bool, sink: torch.
     sink is int32 scratch of sq_probe_mfma_i8_sink_bytes() bytes."""
     _check(lib().sq_probe_mfma_i8(shape, iters, int(random_operands), int(fold), _ptr(sink), sink.numel() * 4,
                                   _stream(stream)), "sq_probe_mfma_i8")
+
+
+def sq_probe_mfma_f8f6(fmt: int, iters: int, random_operands: bool, fold: bool, sink: torch.Tensor,
+                       stream=None) -> None:
+    """The 4-bit path's fp8 / fp6 matrix-core rate probe (include/sq.h): fmt 8
+    (e4m3) or 6 (e2m3), iters * 2^20 operations per wave; sink as for
+    sq_probe_mfma_i8."""
+    _check(lib().sq_probe_mfma_f8f6(fmt, iters, int(random_operands), int(fold), _ptr(sink), sink.numel() * 4,
+                                    _stream(stream)), "sq_probe_mfma_f8f6")
 
 
 def probe_sink(device="cuda") -> torch.Tensor:

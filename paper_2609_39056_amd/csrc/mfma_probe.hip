@@ -14,7 +14,7 @@
 //    biased fold.
 // Both issue 2^20 int8 operations per wave and iteration.  Operands all zero
 // or pseudo-random: the rate depends on the data (random operands draw more
-// power).
+// power).  A third probe runs the 4-bit path's fp8 / fp6 instruction.
 #include "sq_internal.h"
 
 namespace sq {
@@ -122,9 +122,91 @@ __global__ __launch_bounds__(256, 2) void mfma_probe16_kernel(int32_t* sink, int
   sink[blockIdx.x * 256 + threadIdx.x] = s;  // keeps the work live
 }
 
+// The 4-bit path's instruction, v_mfma_scale_f32_32x32x64_f8f6f4, on fp8
+// (e4m3) or fp6 (e2m3) operands: per iteration a wave issues the eight MFMAs
+// of one 128-channel stage of the fp8 W4A4 kernel (2 x 2 tiles of 32 x 32,
+// two 64-wide blocks), 2^20 operations.  With `fold`, each block's fp32 sum is
+// folded as that kernel does: two fmas per output (the group step with its
+// offset term, then the weight step).  fp6 operands take six of the eight
+// operand registers (32 six-bit codes per lane).
+template <int FMT, bool FOLD>
+__global__ __launch_bounds__(256, 2) void mfma_probe_f8f6_kernel(int32_t* sink, int32_t iters, int32_t random) {
+  typedef int v8i_p __attribute__((ext_vector_type(8)));
+  typedef float v16f_p __attribute__((ext_vector_type(16)));
+  const int l = threadIdx.x & 63;
+  v8i_p a[2], b[2];  // one operand per row tile and per column tile (both blocks reuse them)
+  {
+    uint32_t h = static_cast<uint32_t>(l) * 2654435761u + blockIdx.x * 97u;
+    // random bits; fp8 bytes masked to exponents below 15 (no NaN encodings)
+    const uint32_t m = random ? (FMT == 8 ? 0x6F6F6F6Fu : 0xFFFFFFFFu) : 0u;
+    auto next = [&]() {
+      h ^= h >> 13;
+      h *= 2246822519u;
+      h ^= h >> 16;
+      h += 0x9E3779B9u;
+      return static_cast<int>(h & m);
+    };
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      a[i] = (v8i_p){next(), next(), next(), next(), next(), next(), next(), next()};
+      b[i] = (v8i_p){next(), next(), next(), next(), next(), next(), next(), next()};
+    }
+  }
+  constexpr int kFmt = FMT == 8 ? 0 : 2;  // operand format: fp8 e4m3 or fp6 e2m3
+  v16f_p acc[4];
+  float y[4][16];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    acc[t] = (v16f_p)(0.0f);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) y[t][r] = 0.0f;
+  }
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int hb = 0; hb < 2; ++hb)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {
+        if constexpr (FOLD) {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float u = __builtin_fmaf(acc[t][r], 0.75f, -0.25f);
+            y[t][r] = __builtin_fmaf(u, 0.001f, y[t][r]);
+          }
+          acc[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[t >> 1], b[t & 1], (v16f_p)(0.0f), kFmt,
+                                                                    kFmt, 0, 0, 0, 0);
+        } else {
+          acc[t] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a[t >> 1], b[t & 1], acc[t], kFmt, kFmt,
+                                                                    0, 0, 0, 0);
+        }
+      }
+  }
+  float s = 0.0f;
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) s += acc[t][r] + y[t][r];
+  sink[blockIdx.x * 256 + threadIdx.x] = __float_as_int(s);  // keeps the work live
+}
+
 }  // namespace
 
 int mfma_probe_workgroups() { return device_cus() * 2; }
+
+hipError_t launch_mfma_probe_f8f6(int32_t* sink, int32_t fmt, int32_t iters, int32_t random, int32_t fold,
+                                  hipStream_t s) {
+  const dim3 grid(static_cast<unsigned>(mfma_probe_workgroups()));
+  if (fmt == 8) {
+    if (fold)
+      hipLaunchKernelGGL((mfma_probe_f8f6_kernel<8, true>), grid, dim3(256), 0, s, sink, iters, random);
+    else
+      hipLaunchKernelGGL((mfma_probe_f8f6_kernel<8, false>), grid, dim3(256), 0, s, sink, iters, random);
+  } else if (fold) {
+    hipLaunchKernelGGL((mfma_probe_f8f6_kernel<6, true>), grid, dim3(256), 0, s, sink, iters, random);
+  } else {
+    hipLaunchKernelGGL((mfma_probe_f8f6_kernel<6, false>), grid, dim3(256), 0, s, sink, iters, random);
+  }
+  return hipGetLastError();
+}
 
 hipError_t launch_mfma_probe(int32_t* sink, int32_t shape, int32_t iters, int32_t random, int32_t fold,
                              hipStream_t s) {

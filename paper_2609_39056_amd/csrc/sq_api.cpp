@@ -770,6 +770,16 @@ sq_status sq_probe_mfma_i8(int32_t shape, int32_t iters, int32_t random_operands
   return hip_status(launch_mfma_probe(sink, shape, iters, random_operands != 0, fold != 0, stream));
 }
 
+sq_status sq_probe_mfma_f8f6(int32_t format, int32_t iters, int32_t random_operands, int32_t fold, int32_t* sink,
+                             size_t sink_bytes, hipStream_t stream) {
+  if (sink == nullptr) return SQ_ERR_NULL;
+  if (format != 8 && format != 6) return SQ_ERR_UNSUPPORTED;
+  if (iters < 1 || iters > (1 << 24)) return SQ_ERR_SHAPE;
+  if (sink_bytes < sq_probe_mfma_i8_sink_bytes()) return SQ_ERR_WORKSPACE;
+  if (!aligned(sink, 4)) return SQ_ERR_ALIGN;
+  return hip_status(launch_mfma_probe_f8f6(sink, format, iters, random_operands != 0, fold != 0, stream));
+}
+
 sq_status sq_debug_block_acc_i32(const void* qx, int32_t M, int32_t act_bits, const sq_weight* w,
                                  int32_t* acc_out, hipStream_t stream) {
   if (qx == nullptr || acc_out == nullptr) return SQ_ERR_NULL;

@@ -257,5 +257,7 @@ hipError_t launch_calib_select(int32_t S, const double* cand_obj, const double* 
 // matrix-core rate probe (measurement hook)
 int mfma_probe_workgroups();
 hipError_t launch_mfma_probe(int32_t* sink, int32_t shape, int32_t iters, int32_t random, int32_t fold, hipStream_t s);
+hipError_t launch_mfma_probe_f8f6(int32_t* sink, int32_t fmt, int32_t iters, int32_t random, int32_t fold,
+                                  hipStream_t s);
 
 }  // namespace sq

@@ -165,6 +165,14 @@ def test_mfma_probe_checks(L):
         assert L.sq_probe_mfma_i8(shape, 10, 1, 0, ctypes.c_void_p((1 << 20) + 2), n, None) == ALIGN
     for shape in (0, 8, 64):
         assert L.sq_probe_mfma_i8(shape, 10, 1, 0, A, n, None) == UNSUP
+    for fmt in (8, 6):
+        assert L.sq_probe_mfma_f8f6(fmt, 10, 1, 0, None, n, None) == NULL
+        assert L.sq_probe_mfma_f8f6(fmt, 0, 1, 0, A, n, None) == SHAPE
+        assert L.sq_probe_mfma_f8f6(fmt, (1 << 24) + 1, 1, 0, A, n, None) == SHAPE
+        assert L.sq_probe_mfma_f8f6(fmt, 10, 1, 0, A, n - 4, None) == WS
+        assert L.sq_probe_mfma_f8f6(fmt, 10, 1, 0, ctypes.c_void_p((1 << 20) + 2), n, None) == ALIGN
+    for fmt in (0, 4, 16):
+        assert L.sq_probe_mfma_f8f6(fmt, 10, 1, 0, A, n, None) == UNSUP
 
 
 def calib(L, x=A, M=88, t2s=A, S=3, dinv=None, bits=8, w=None, ref=A, C=4, g=A, c=A, om=A, obj=A, ws=A,

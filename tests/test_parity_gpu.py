@@ -393,3 +393,18 @@ def test_mfma_probe_runs(shape):
         B.sq_probe_mfma_i8(3, True, fold, sink, shape=shape)
         torch.cuda.synchronize()
         assert int(sink.abs().max()) > 0
+
+
+@pytest.mark.parametrize("fmt", [8, 6])
+def test_mfma_probe_f8f6_runs(fmt):
+    """The 4-bit path's fp8 / fp6 matrix-core probe runs and writes its sink;
+    zero operands leave every accumulator zero (without the fold)."""
+    sink = B.probe_sink()
+    sink.fill_(7)
+    B.sq_probe_mfma_f8f6(fmt, 3, False, False, sink)
+    torch.cuda.synchronize()
+    assert int(sink.abs().max()) == 0
+    for fold in (False, True):
+        B.sq_probe_mfma_f8f6(fmt, 3, True, fold, sink)
+        torch.cuda.synchronize()
+        assert int(sink.abs().max()) > 0
